@@ -1,0 +1,184 @@
+"""NumPy front end of the fp64 CPU oracle (oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg.  Nothing in the HIP path imports it.
+
+Every function takes host numpy arrays, widens floating operands exactly to
+float64, and returns freshly allocated float64 (or integer) results.  The
+composite attention functions are the plain compositions of the operator
+definitions (edge softmax followed by aggregation; aggregation backward
+followed by edge-softmax backward), Sec. 4.3.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_p = C.c_void_p
+_i64 = C.c_int64
+_i32 = C.c_int
+_f64 = C.c_double
+
+_SIGS = {
+    "oracle_csr_offsets": (None, [_p, _i64, _p]),
+    "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
+    "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
+    "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
+    "oracle_edge_softmax_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _f64, _f64, _p, _p, _p]),
+    "oracle_aggregate_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _p]),
+    "oracle_aggregate_bwd": (None, [_p, _i64, _i32, _i32, _p, _p, _p, _p, _p]),
+    "oracle_edge_softmax_bwd": (None, [_p, _i64, _i32, _i32, _p, _p, _f64, _f64, _p, _p, _p, _p, _p]),
+}
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            from . import build as _b
+            _b.build()
+        L = C.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _f64(a):
+    """Exact widening of an fp32/bf16 (torch or numpy) operand to float64."""
+    try:
+        import torch
+        if isinstance(a, torch.Tensor):
+            return a.detach().to("cpu", torch.float64).contiguous().numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+# ------------------------------------------------------------------ integer ops
+def csr_offsets(counts):
+    counts = _c(counts, np.int32)
+    off = np.empty(counts.shape[0] + 1, dtype=np.int32)
+    lib().oracle_csr_offsets(_ptr(counts), counts.shape[0], _ptr(off))
+    return off
+
+
+def dedup(ids):
+    ids = _c(ids, np.int64)
+    n = ids.shape[0]
+    uni = np.empty(max(n, 1), dtype=np.int64)
+    inv = np.empty(max(n, 1), dtype=np.int32)
+    u = lib().oracle_dedup(_ptr(ids), n, _ptr(uni), _ptr(inv))
+    return uni[:u].copy(), inv[:n].copy()
+
+
+def gather(uni, table, slot_map=None):
+    """Returns (rows [u, row] same dtype as table, hit mask [u], miss int32 [m])."""
+    uni = _c(uni, np.int64)
+    table = np.ascontiguousarray(table)
+    u = uni.shape[0]
+    row_shape = table.shape[1:]
+    row_bytes = table.dtype.itemsize * int(np.prod(row_shape, dtype=np.int64))
+    rows = np.zeros((u,) + row_shape, dtype=table.dtype)
+    miss = np.empty(max(u, 1), dtype=np.int32)
+    sm = None if slot_map is None else _c(slot_map, np.int32)
+    nm = lib().oracle_gather(_ptr(uni), u, _ptr(table), table.shape[0], row_bytes,
+                             _ptr(sm), _ptr(rows), _ptr(miss))
+    miss = miss[:nm].copy()
+    hit = np.ones(u, dtype=bool)
+    hit[miss] = False
+    return rows, hit, miss
+
+
+# ------------------------------------------------------------------ time encoding
+def time_encode(off, t_dst, t_e, omega, phi):
+    off = _c(off, np.int32)
+    t_dst, t_e = _c(t_dst, np.float32), _c(t_e, np.float32)
+    omega, phi = _c(omega, np.float32), _c(phi, np.float32)
+    N, E, d_t = off.shape[0] - 1, t_e.shape[0], omega.shape[0]
+    te = np.zeros((E, d_t), dtype=np.float64)
+    lib().oracle_time_encode(_ptr(off), N, _ptr(t_dst), _ptr(t_e), _ptr(omega),
+                             _ptr(phi), d_t, _ptr(te))
+    return te
+
+
+# ------------------------------------------------------------------ attention
+def edge_softmax_fwd(off, Q, K, scale, slope):
+    """Returns (alpha [E,H], lse [N,H], pre [E,H])."""
+    off = _c(off, np.int32)
+    Q, K = _f64(Q), _f64(K)
+    N, H, dh = Q.shape
+    E = K.shape[0]
+    alpha = np.zeros((E, H))
+    lse = np.zeros((N, H))
+    pre = np.zeros((E, H))
+    lib().oracle_edge_softmax_fwd(_ptr(off), N, H, dh, _ptr(Q), _ptr(K), scale, slope,
+                                  _ptr(pre), _ptr(alpha), _ptr(lse))
+    return alpha, lse, pre
+
+
+def aggregate_fwd(off, alpha, V):
+    off = _c(off, np.int32)
+    alpha, V = _f64(alpha), _f64(V)
+    E, H, dh = V.shape
+    N = off.shape[0] - 1
+    out = np.zeros((N, H, dh))
+    lib().oracle_aggregate_fwd(_ptr(off), N, H, dh, _ptr(alpha), _ptr(V), _ptr(out))
+    return out
+
+
+def aggregate_bwd(off, alpha, V, dout):
+    off = _c(off, np.int32)
+    alpha, V, dout = _f64(alpha), _f64(V), _f64(dout)
+    E, H, dh = V.shape
+    N = off.shape[0] - 1
+    dalpha = np.zeros((E, H))
+    dV = np.zeros((E, H, dh))
+    lib().oracle_aggregate_bwd(_ptr(off), N, H, dh, _ptr(alpha), _ptr(V), _ptr(dout),
+                               _ptr(dalpha), _ptr(dV))
+    return dalpha, dV
+
+
+def edge_softmax_bwd(off, Q, K, scale, slope, alpha, dalpha, branch=None):
+    off = _c(off, np.int32)
+    Q, K, alpha, dalpha = _f64(Q), _f64(K), _f64(alpha), _f64(dalpha)
+    N, H, dh = Q.shape
+    E = K.shape[0]
+    dQ = np.zeros((N, H, dh))
+    dK = np.zeros((E, H, dh))
+    br = None if branch is None else _c(branch, np.int8)
+    lib().oracle_edge_softmax_bwd(_ptr(off), N, H, dh, _ptr(Q), _ptr(K), scale, slope,
+                                  _ptr(alpha), _ptr(dalpha), _ptr(br), _ptr(dQ), _ptr(dK))
+    return dQ, dK
+
+
+def edge_attention_fwd(off, Q, K, V, scale, slope):
+    """Fused operator = edge softmax then aggregation.  Returns (out, lse, alpha, pre)."""
+    alpha, lse, pre = edge_softmax_fwd(off, Q, K, scale, slope)
+    out = aggregate_fwd(off, alpha, V)
+    return out, lse, alpha, pre
+
+
+def edge_attention_bwd(off, Q, K, V, dout, scale, slope, branch=None):
+    """Backward of the fused operator = aggregation backward then edge-softmax
+    backward.  Returns (dQ, dK, dV)."""
+    alpha, _, _ = edge_softmax_fwd(off, Q, K, scale, slope)
+    dalpha, dV = aggregate_bwd(off, alpha, V, dout)
+    dQ, dK = edge_softmax_bwd(off, Q, K, scale, slope, alpha, dalpha, branch)
+    return dQ, dK, dV

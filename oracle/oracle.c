@@ -1,0 +1,168 @@
+/*
+ * oracle.c -- plain fp64 CPU reference of FAST's temporal-subgraph operators.
+ *
+ * TEST INFRASTRUCTURE ONLY (see oracle.h).  Written for a reader checking it
+ * against the paper by eye: one loop nest per definition, no blocking, no
+ * reordering, no fusion.  Build with -ffp-contract=off so that the only fused
+ * multiply-add is the explicit fmaf of the time-encoding argument.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---- CSR offsets (Sec. 5: CSR-style ind_ptr of the compression triple) ---- */
+void oracle_csr_offsets(const int32_t* counts, int64_t n, int32_t* off) {
+  off[0] = 0;
+  for (int64_t v = 0; v < n; ++v) off[v + 1] = off[v] + counts[v];
+}
+
+/* ---- within-batch dedup (Sec. 4.2 compression; Sec. 5 uni_ID / inv_Idx) ---- */
+static int cmp_i64(const void* a, const void* b) {
+  int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+  return (x > y) - (x < y);
+}
+
+int64_t oracle_dedup(const int64_t* ids, int64_t n, int64_t* uni, int32_t* inv) {
+  if (n == 0) return 0;
+  int64_t* sorted = (int64_t*)malloc((size_t)n * sizeof(int64_t));
+  memcpy(sorted, ids, (size_t)n * sizeof(int64_t));
+  qsort(sorted, (size_t)n, sizeof(int64_t), cmp_i64);
+  int64_t u = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (i == 0 || sorted[i] != sorted[i - 1]) uni[u++] = sorted[i];
+  free(sorted);
+  for (int64_t i = 0; i < n; ++i) {          /* lower_bound of ids[i] in uni */
+    int64_t lo = 0, hi = u;
+    while (lo < hi) {
+      int64_t mid = lo + (hi - lo) / 2;
+      if (uni[mid] < ids[i]) lo = mid + 1; else hi = mid;
+    }
+    inv[i] = (int32_t)lo;
+  }
+  return u;
+}
+
+/* ---- row reconstruction through the cache slot map (Sec. 4.2) ---- */
+int64_t oracle_gather(const int64_t* uni, int64_t u, const void* table,
+                      int64_t table_rows, int64_t row_bytes, const int32_t* slot_map,
+                      void* rows, int32_t* miss) {
+  int64_t nmiss = 0;
+  for (int64_t k = 0; k < u; ++k) {
+    int64_t slot = slot_map ? (int64_t)slot_map[uni[k]] : uni[k];
+    if (slot >= 0 && slot < table_rows) {
+      if (rows)
+        memcpy((char*)rows + k * row_bytes, (const char*)table + slot * row_bytes,
+               (size_t)row_bytes);
+    } else {
+      if (miss) miss[nmiss] = (int32_t)k;
+      ++nmiss;
+    }
+  }
+  return nmiss;
+}
+
+/* ---- time encoding (Sec. 6.1: TGAT random Fourier time features) ---- */
+void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
+                        const float* t_e, const float* omega, const float* phi,
+                        int d_t, double* te) {
+  for (int64_t v = 0; v < N; ++v) {
+    for (int64_t e = off[v]; e < off[v + 1]; ++e) {
+      float dt = t_dst[v] - t_e[e];
+      for (int j = 0; j < d_t; ++j) {
+        float arg = fmaf(omega[j], dt, phi[j]);
+        te[e * d_t + j] = cos((double)arg);
+      }
+    }
+  }
+}
+
+/* ---- edge softmax forward (Sec. 4.3 "Edge Softmax": max, sum, divide) ---- */
+void oracle_edge_softmax_fwd(const int32_t* off, int64_t N, int H, int dh,
+                             const double* Q, const double* K, double scale,
+                             double slope, double* pre, double* alpha, double* lse) {
+  for (int64_t v = 0; v < N; ++v) {
+    int64_t e0 = off[v], e1 = off[v + 1];
+    for (int h = 0; h < H; ++h) {
+      if (e0 == e1) {
+        if (lse) lse[v * H + h] = -INFINITY;
+        continue;
+      }
+      /* logits, kept in alpha until normalised */
+      for (int64_t e = e0; e < e1; ++e) {
+        double dot = 0.0;
+        for (int i = 0; i < dh; ++i)
+          dot += Q[(v * H + h) * dh + i] * K[(e * H + h) * dh + i];
+        double p = scale * dot;
+        if (pre) pre[e * H + h] = p;
+        alpha[e * H + h] = p > 0.0 ? p : slope * p;
+      }
+      double m = -INFINITY;
+      for (int64_t e = e0; e < e1; ++e)
+        if (alpha[e * H + h] > m) m = alpha[e * H + h];
+      double Z = 0.0;
+      for (int64_t e = e0; e < e1; ++e) Z += exp(alpha[e * H + h] - m);
+      for (int64_t e = e0; e < e1; ++e)
+        alpha[e * H + h] = exp(alpha[e * H + h] - m) / Z;
+      if (lse) lse[v * H + h] = m + log(Z);
+    }
+  }
+}
+
+/* ---- aggregation forward (Sec. 4.3 "Balanced Aggregate"; Eq. 1) ---- */
+void oracle_aggregate_fwd(const int32_t* off, int64_t N, int H, int dh,
+                          const double* alpha, const double* V, double* out) {
+  for (int64_t v = 0; v < N; ++v)
+    for (int h = 0; h < H; ++h)
+      for (int i = 0; i < dh; ++i) {
+        double acc = 0.0;
+        for (int64_t e = off[v]; e < off[v + 1]; ++e)
+          acc += alpha[e * H + h] * V[(e * H + h) * dh + i];
+        out[(v * H + h) * dh + i] = acc;
+      }
+}
+
+/* ---- aggregation backward ---- */
+void oracle_aggregate_bwd(const int32_t* off, int64_t N, int H, int dh,
+                          const double* alpha, const double* V, const double* dout,
+                          double* dalpha, double* dV) {
+  for (int64_t v = 0; v < N; ++v)
+    for (int64_t e = off[v]; e < off[v + 1]; ++e)
+      for (int h = 0; h < H; ++h) {
+        double dot = 0.0;
+        for (int i = 0; i < dh; ++i)
+          dot += dout[(v * H + h) * dh + i] * V[(e * H + h) * dh + i];
+        dalpha[e * H + h] = dot;
+        for (int i = 0; i < dh; ++i)
+          dV[(e * H + h) * dh + i] = alpha[e * H + h] * dout[(v * H + h) * dh + i];
+      }
+}
+
+/* ---- edge softmax and logit backward ---- */
+void oracle_edge_softmax_bwd(const int32_t* off, int64_t N, int H, int dh,
+                             const double* Q, const double* K, double scale,
+                             double slope, const double* alpha, const double* dalpha,
+                             const int8_t* branch, double* dQ, double* dK) {
+  for (int64_t v = 0; v < N; ++v) {
+    int64_t e0 = off[v], e1 = off[v + 1];
+    for (int h = 0; h < H; ++h) {
+      double D = 0.0;
+      for (int64_t e = e0; e < e1; ++e) D += alpha[e * H + h] * dalpha[e * H + h];
+      for (int i = 0; i < dh; ++i) dQ[(v * H + h) * dh + i] = 0.0;
+      for (int64_t e = e0; e < e1; ++e) {
+        double dot = 0.0;
+        for (int i = 0; i < dh; ++i)
+          dot += Q[(v * H + h) * dh + i] * K[(e * H + h) * dh + i];
+        double p = scale * dot;
+        int b = branch ? branch[e * H + h] : 0;
+        double r = (b == 1) ? 1.0 : (b == 2) ? slope : (p > 0.0 ? 1.0 : slope);
+        double g = alpha[e * H + h] * (dalpha[e * H + h] - D) * r * scale;
+        for (int i = 0; i < dh; ++i) {
+          dQ[(v * H + h) * dh + i] += g * K[(e * H + h) * dh + i];
+          dK[(e * H + h) * dh + i] = g * Q[(v * H + h) * dh + i];
+        }
+      }
+    }
+  }
+}

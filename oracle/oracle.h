@@ -1,0 +1,79 @@
+/*
+ * oracle.h -- plain, slow CPU reference of FAST's temporal-subgraph operators.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists to check the HIP operators;
+ * only the test-suite, the smoke check and the CPU-baseline leg of the
+ * benchmark load it.  It shares no code, header or constant with the HIP
+ * library.  Floating point is accumulated in fp64 (inputs are widened
+ * exactly); the time encoding forms its argument in fp32 as stated below.
+ *
+ * Data model (all arrays row-major, host memory):
+ *   sampled CSR temporal subgraph of one layer block (Sec. 4.3, Sec. 5: the
+ *   compression engine's `ind_ptr`): off[N+1], edges of destination v are
+ *   e in [off[v], off[v+1]); per-edge rows [E,H,dh], per-destination rows
+ *   [N,H,dh], per-(edge,head) scalars [E,H], per-(destination,head) [N,H].
+ */
+#ifndef FAST_ORACLE_H
+#define FAST_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* CSR offsets: off[0] = 0, off[v+1] = off[v] + counts[v]. */
+void oracle_csr_offsets(const int32_t* counts, int64_t n, int32_t* off);
+
+/* Within-batch compression (Sec. 4.2, Sec. 5): uni = ascending distinct ids,
+ * inv[i] = position of ids[i] in uni.  Returns u = |uni|. */
+int64_t oracle_dedup(const int64_t* ids, int64_t n, int64_t* uni, int32_t* inv);
+
+/* Row reconstruction from the compressed ids: slot = slot_map ? slot_map[uni[k]]
+ * : uni[k]; a slot in [0, table_rows) copies row_bytes bytes to rows[k], any
+ * other slot appends k to miss (ascending).  Returns the number of misses. */
+int64_t oracle_gather(const int64_t* uni, int64_t u, const void* table,
+                      int64_t table_rows, int64_t row_bytes, const int32_t* slot_map,
+                      void* rows, int32_t* miss);
+
+/* Time encoding cos(omega_j * dt + phi_j), dt = t_dst[v] - t_e[e] for e in
+ * segment v.  dt and the argument are formed in fp32 (one subtraction, one
+ * fused multiply-add); the cosine itself is evaluated in fp64.  te[E*d_t]. */
+void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
+                        const float* t_e, const float* omega, const float* phi,
+                        int d_t, double* te);
+
+/* Edge softmax forward with per-edge multi-head logits:
+ *   pre[e,h]   = scale * <Q[v,h,:], K[e,h,:]>
+ *   s[e,h]     = pre > 0 ? pre : slope * pre            (LeakyReLU)
+ *   alpha[e,h] = exp(s - m) / Z,  m = max_e s,  Z = sum_e exp(s - m)
+ *   lse[v,h]   = m + log Z   (-inf for an empty segment)
+ * pre may be NULL. */
+void oracle_edge_softmax_fwd(const int32_t* off, int64_t N, int H, int dh,
+                             const double* Q, const double* K, double scale,
+                             double slope, double* pre, double* alpha, double* lse);
+
+/* Aggregation forward: out[v,h,:] = sum_e alpha[e,h] * V[e,h,:] (0 if empty). */
+void oracle_aggregate_fwd(const int32_t* off, int64_t N, int H, int dh,
+                          const double* alpha, const double* V, double* out);
+
+/* Aggregation backward for dOut:
+ *   dalpha[e,h] = <dOut[v,h,:], V[e,h,:]>,  dV[e,h,:] = alpha[e,h] * dOut[v,h,:] */
+void oracle_aggregate_bwd(const int32_t* off, int64_t N, int H, int dh,
+                          const double* alpha, const double* V, const double* dout,
+                          double* dalpha, double* dV);
+
+/* Edge softmax (and logit) backward:
+ *   D[v,h] = sum_e alpha*dalpha,  ds = alpha*(dalpha - D),
+ *   g = ds * r * scale with r = 1 if pre > 0 else slope,
+ *   dQ[v,h,:] = sum_e g * K[e,h,:],  dK[e,h,:] = g * Q[v,h,:].
+ * branch (may be NULL) overrides r per (e,h): 0 = by the sign of pre,
+ * 1 = take r = 1, 2 = take r = slope. */
+void oracle_edge_softmax_bwd(const int32_t* off, int64_t N, int H, int dh,
+                             const double* Q, const double* K, double scale,
+                             double slope, const double* alpha, const double* dalpha,
+                             const int8_t* branch, double* dQ, double* dK);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,100 @@
+"""Strength of the oracle pins: plant a plausible mistake in a copy of the
+oracle source (on the CPU), rebuild it, and check that at least one pin in
+test_oracle_pins.py fails against the planted copy."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+MUTATIONS = {
+    "offsets_shifted": ("off[v + 1] = off[v] + counts[v];",
+                        "off[v + 1] = off[v] + counts[v + 1 < n ? v + 1 : v];"),
+    "dedup_upper_bound": ("if (uni[mid] < ids[i]) lo = mid + 1;",
+                          "if (uni[mid] <= ids[i]) lo = mid + 1;"),
+    "gather_slot0_miss": ("if (slot >= 0 && slot < table_rows)",
+                          "if (slot > 0 && slot < table_rows)"),
+    "te_fp64_argument": ("float arg = fmaf(omega[j], dt, phi[j]);",
+                         "double arg = (double)omega[j] * ((double)t_dst[v] - (double)t_e[e]) + phi[j];"),
+    "te_wrong_segment": ("float dt = t_dst[v] - t_e[e];",
+                         "float dt = t_dst[v > 0 ? v - 1 : 0] - t_e[e];"),
+    "te_transposed_out": ("te[e * d_t + j] =", "te[(j * 0 + e) * d_t + (d_t - 1 - j)] ="),
+    "lrelu_swapped": ("alpha[e * H + h] = p > 0.0 ? p : slope * p;",
+                      "alpha[e * H + h] = p > 0.0 ? slope * p : p;"),
+    "no_max_shift": ("Z += exp(alpha[e * H + h] - m);", "Z += exp(alpha[e * H + h]);"),
+    "no_normalise": ("alpha[e * H + h] = exp(alpha[e * H + h] - m) / Z;",
+                     "alpha[e * H + h] = exp(alpha[e * H + h] - m);"),
+    "lse_missing_log": ("m + log(Z)", "m + Z"),
+    "agg_wrong_head": ("acc += alpha[e * H + h] * V[(e * H + h) * dh + i];",
+                       "acc += alpha[e * H + h] * V[(e * H + (H - 1 - h)) * dh + i];"),
+    "aggbwd_drop_alpha": ("dV[(e * H + h) * dh + i] = alpha[e * H + h] * dout[(v * H + h) * dh + i];",
+                          "dV[(e * H + h) * dh + i] = dout[(v * H + h) * dh + i];"),
+    "smbwd_drop_D": ("(dalpha[e * H + h] - D)", "(dalpha[e * H + h])"),
+    "smbwd_branch_swapped": ("(p > 0.0 ? 1.0 : slope)", "(p > 0.0 ? slope : 1.0)"),
+    "smbwd_drop_scale": ("* r * scale;", "* r;"),
+    "smbwd_dK_uses_K": ("dK[(e * H + h) * dh + i] = g * Q[(v * H + h) * dh + i];",
+                        "dK[(e * H + h) * dh + i] = g * K[(e * H + h) * dh + i];"),
+}
+
+PINS = [
+    (P.test_offsets_vs_cumsum, dict(n=1000)),
+    (P.test_offsets_vs_cumsum, dict(n=7)),
+    (P.test_dedup_vs_numpy_unique, dict(case="random")),
+    (P.test_dedup_vs_numpy_unique, dict(case="zipf")),
+    (P.test_gather_identity_slots, dict(dtype=P.np.float32)),
+    (P.test_gather_slot_map_and_miss_list, {}),
+    (P.test_time_encode_zero_dt_and_segment_mapping, {}),
+    (P.test_time_encode_closed_forms, {}),
+    (P.test_time_encode_double_angle_columns, {}),
+    (P.test_time_encode_fp32_difference, {}),
+    (P.test_fwd_vs_torch_sdpa, {}),
+    (P.test_fwd_vs_dense_masked_attention, dict(slope=0.2)),
+    (P.test_softmax_invariants, {}),
+    (P.test_huge_logits_stay_finite, {}),
+    (P.test_bwd_vs_torch_autograd_sdpa, {}),
+    (P.test_bwd_finite_differences_leaky, {}),
+    (P.test_softmax_bwd_vs_jacobian_matrix, {}),
+    (P.test_aggregate_bwd_is_the_transpose, {}),
+]
+
+
+def _build_mutant(tmp_path, name):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation site for {name} not found"
+    mutated = src.replace(old, new)
+    c_path = tmp_path / f"{name}.c"
+    c_path.write_text(mutated)
+    so = tmp_path / f"lib{name}.so"
+    hdr_dir = os.path.dirname(SRC)
+    subprocess.run(["gcc", "-std=c11", "-O1", "-ffp-contract=off", "-fPIC", "-shared",
+                    "-I", hdr_dir, "-o", str(so), str(c_path), "-lm"], check=True)
+    L = ctypes.CDLL(str(so))
+    for fn, (res, args) in oracle._SIGS.items():
+        f = getattr(L, fn)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    good = oracle.lib()
+    mutant = _build_mutant(tmp_path, name)
+    caught = []
+    oracle._lib = mutant
+    try:
+        for fn, kw in PINS:
+            try:
+                with P.np.errstate(all="ignore"):
+                    fn(**kw)
+            except (AssertionError, ValueError, IndexError, FloatingPointError):
+                caught.append(fn.__name__)
+    finally:
+        oracle._lib = good
+    assert caught, f"no pin detects the planted mistake {name!r}"

@@ -1,0 +1,389 @@
+"""Pins of the fp64 CPU oracle against facts that do not come from the oracle.
+
+Each check is independent of the oracle's own loops: library routines that
+compute the same quantity (np.cumsum, np.unique, numpy fancy indexing,
+torch's scaled-dot-product attention and its autograd, scipy's softmax and
+logsumexp), dense padded textbook attention, closed forms of the cosine,
+softmax invariants, the softmax Jacobian written as a matrix, and central
+finite differences.  Together they fail on a dropped term, a wrong sign, a
+wrong index or a transposed operand anywhere in the oracle (see
+test_oracle_mutations.py, which plants such mistakes and checks that a pin
+here catches each one).
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+from synth import make_batch, omega_phi, tiny_graph
+
+SLOPE = 0.2
+
+
+def _csr(counts):
+    counts = np.asarray(counts, dtype=np.int32)
+    return np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+
+
+def _rand_qkv(N, E, H, dh, seed):
+    r = np.random.default_rng(seed)
+    return (r.standard_normal((N, H, dh)), r.standard_normal((E, H, dh)),
+            r.standard_normal((E, H, dh)), r.standard_normal((N, H, dh)))
+
+
+def _dense(off, X):
+    """Pad per-edge rows [E,H,dh] into [N,Dmax,H,dh] plus a validity mask."""
+    N = off.shape[0] - 1
+    deg = np.diff(off)
+    Dm = max(int(deg.max()) if N else 0, 1)
+    out = np.zeros((N, Dm) + X.shape[1:])
+    mask = np.zeros((N, Dm), dtype=bool)
+    for v in range(N):
+        out[v, :deg[v]] = X[off[v]:off[v + 1]]
+        mask[v, :deg[v]] = True
+    return out, mask
+
+
+def _dense_attention(off, Q, K, V, scale, slope):
+    """Textbook masked attention on padded neighbour tiles (numpy + scipy)."""
+    Kd, mask = _dense(off, K)
+    Vd, _ = _dense(off, V)
+    S = scale * np.einsum("nhd,nkhd->nhk", Q, Kd)
+    S = np.where(S > 0, S, slope * S)
+    S = np.where(mask[:, None, :], S, -np.inf)
+    A = scipy.special.softmax(S, axis=2)
+    out = np.einsum("nhk,nkhd->nhd", A, Vd)
+    lse = scipy.special.logsumexp(S, axis=2)
+    return out, A, lse, mask
+
+
+# ---------------------------------------------------------------- offsets (a1)
+@pytest.mark.parametrize("n", [0, 1, 7, 1000])
+def test_offsets_vs_cumsum(n):
+    r = np.random.default_rng(n)
+    counts = r.integers(0, 25, n).astype(np.int32)
+    off = oracle.csr_offsets(counts)
+    ref = np.concatenate([[0], np.cumsum(counts)])
+    assert off.dtype == np.int32 and np.array_equal(off, ref)
+    assert off[-1] == counts.sum() and np.all(np.diff(off) >= 0)
+
+
+# ---------------------------------------------------------------- dedup (a2)
+@pytest.mark.parametrize("case", ["random", "empty", "single", "allsame", "sorted", "zipf"])
+def test_dedup_vs_numpy_unique(case):
+    r = np.random.default_rng(3)
+    ids = {
+        "random": r.integers(0, 500, 3000),
+        "empty": np.zeros(0, dtype=np.int64),
+        "single": np.array([42]),
+        "allsame": np.full(1000, 7),
+        "sorted": np.arange(0, 2000, 3),
+        "zipf": make_batch(2).node_ids,
+    }[case].astype(np.int64)
+    uni, inv = oracle.dedup(ids)
+    ref_u, ref_inv = np.unique(ids, return_inverse=True)
+    assert np.array_equal(uni, ref_u)
+    assert np.array_equal(inv, ref_inv.reshape(-1))
+    assert inv.dtype == np.int32
+    if ids.size:
+        assert np.array_equal(uni[inv], ids)
+        assert np.all(np.diff(uni) > 0)
+
+
+def test_repetition_rate_definition():
+    # Sec. 3.1: R = 1 - N_u / N_i; 12 ids with 7 distinct transfer 7 rows, not 12.
+    ids = np.array([5, 9, 5, 2, 9, 9, 11, 2, 40, 41, 5, 3], dtype=np.int64)
+    uni, _ = oracle.dedup(ids)
+    assert uni.size == 7
+    assert math.isclose(1 - uni.size / ids.size, 5 / 12)
+
+
+# ---------------------------------------------------------------- gather (a3)
+@pytest.mark.parametrize("dtype", [np.float32, np.uint16])
+def test_gather_identity_slots(dtype):
+    r = np.random.default_rng(5)
+    table = r.standard_normal((300, 172)).astype(np.float32)
+    if dtype == np.uint16:
+        table = (table.view(np.uint32) >> 16).astype(np.uint16)   # a bf16 bit table
+    ids = r.integers(0, 300, 2000).astype(np.int64)
+    uni, inv = oracle.dedup(ids)
+    rows, hit, miss = oracle.gather(uni, table)
+    assert hit.all() and miss.size == 0
+    assert rows.tobytes() == table[uni].tobytes()
+    # reconstruction through the inverse index returns every original row
+    assert rows[inv].tobytes() == table[ids].tobytes()
+
+
+def test_gather_slot_map_and_miss_list():
+    r = np.random.default_rng(6)
+    bound, C = 5000, 700
+    cache = r.standard_normal((C, 16)).astype(np.float32)
+    slot_map = np.full(bound, -1, dtype=np.int32)
+    cached = r.choice(bound, C, replace=False)
+    slot_map[cached] = np.arange(C, dtype=np.int32)
+    ids = r.integers(0, bound, 4000).astype(np.int64)
+    uni, _ = oracle.dedup(ids)
+    rows, hit, miss = oracle.gather(uni, cache, slot_map)
+    ref_miss = np.flatnonzero(slot_map[uni] < 0)
+    assert np.array_equal(miss, ref_miss)
+    assert np.array_equal(hit, slot_map[uni] >= 0)
+    assert rows[hit].tobytes() == cache[slot_map[uni[hit]]].tobytes()
+
+
+# ---------------------------------------------------------------- time encoding (a4)
+def test_time_encode_zero_dt_and_segment_mapping():
+    blk = tiny_graph([3, 0, 5, 1, 4])
+    off = _csr(blk.counts)
+    t_e = blk.edge_t.copy()
+    # edges 1 and 6 get their own destination's time: dt = 0 -> cos(phi) = 1 exactly
+    seg = np.repeat(np.arange(blk.num_dst), blk.counts)
+    for e in (1, 6):
+        t_e[e] = blk.dst_t[seg[e]]
+    om, ph = omega_phi(16)
+    te = oracle.time_encode(off, blk.dst_t, t_e, om, ph)
+    assert np.all(te[[1, 6]] == 1.0)
+    others = np.setdiff1d(np.arange(blk.num_edges), [1, 6])
+    assert np.all(te[others, 0] != 1.0)
+
+
+def test_time_encode_closed_forms():
+    off = np.array([0, 3], dtype=np.int32)
+    t_dst = np.array([1.0], dtype=np.float32)
+    t_e = np.array([0.0, 0.0, 1.0], dtype=np.float32)        # dt = 1, 1, 0
+    pi32, half32 = np.float32(np.pi), np.float32(np.pi / 2)
+    om = np.array([pi32, half32, 0.0], dtype=np.float32)
+    ph = np.array([0.0, 0.0, half32], dtype=np.float32)
+    te = oracle.time_encode(off, t_dst, t_e, om, ph)
+    # cos(pi + d) = -cos(d),  cos(pi/2 + d) = -sin(d), d = fl32(x) - x (known exactly)
+    d_pi = float(pi32) - math.pi
+    d_half = float(half32) - math.pi / 2
+    assert abs(te[0, 0] - (-math.cos(d_pi))) < 1e-15
+    assert abs(te[0, 1] - (-math.sin(d_half))) < 1e-15
+    assert abs(te[0, 1] + 4.371139e-8) < 1e-13
+    assert np.all(np.abs(te[:, 2] - (-math.sin(d_half))) < 1e-15)   # omega = 0 -> cos(phi)
+    assert te[2, 0] == 1.0 and te[2, 1] == 1.0                      # dt = 0, phi = 0
+
+
+def test_time_encode_double_angle_columns():
+    # omega_j = 2^j * omega_0 makes every argument exactly twice the previous
+    # one, so cos(2x) = 2 cos(x)^2 - 1 links column j+1 to column j.
+    blk = tiny_graph([4, 2, 6], seed=11)
+    off = _csr(blk.counts)
+    om = (np.float32(1.7e-3) * (2.0 ** np.arange(10))).astype(np.float32)
+    ph = np.zeros(10, dtype=np.float32)
+    te = oracle.time_encode(off, blk.dst_t, blk.edge_t, om, ph)
+    np.testing.assert_allclose(te[:, 1:], 2 * te[:, :-1] ** 2 - 1, atol=1e-9)
+    assert np.abs(te).max() <= 1.0
+
+
+def test_time_encode_fp32_difference():
+    # dt is one fp32 subtraction: 2^25 - 1 rounds to 2^25 (ties to even), so
+    # t_e = 1 and t_e = 0 give the same row, while an fp64 dt would differ.
+    off = np.array([0, 2], dtype=np.int32)
+    t_dst = np.array([2.0 ** 25], dtype=np.float32)
+    t_e = np.array([1.0, 0.0], dtype=np.float32)
+    om, ph = np.array([1.0, 0.25], dtype=np.float32), np.zeros(2, dtype=np.float32)
+    te = oracle.time_encode(off, t_dst, t_e, om, ph)
+    assert np.array_equal(te[0], te[1])
+    assert abs(math.cos(2.0 ** 25 - 1) - math.cos(2.0 ** 25)) > 1e-2
+
+
+# ---------------------------------------------------------------- attention forward (a5-a7)
+def test_fwd_vs_torch_sdpa():
+    # slope = 1 removes the LeakyReLU: the operator is masked scaled-dot-product attention
+    counts = [1, 4, 7, 2, 10, 3]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), off[-1], 3, 5
+    Q, K, V, _ = _rand_qkv(N, E, H, dh, 1)
+    scale = 0.37
+    out, lse, alpha, _ = oracle.edge_attention_fwd(off, Q, K, V, scale, 1.0)
+    Kd, mask = _dense(off, K)
+    Vd, _ = _dense(off, V)
+    q = torch.tensor(Q)[:, :, None, :]                    # [N,H,1,dh]
+    k = torch.tensor(Kd).permute(0, 2, 1, 3)              # [N,H,Dm,dh]
+    v = torch.tensor(Vd).permute(0, 2, 1, 3)
+    m = torch.tensor(mask)[:, None, None, :]
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v, attn_mask=m, scale=scale)
+    np.testing.assert_allclose(out, ref[:, :, 0, :].numpy(), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("slope", [0.2, 1.0, 0.0])
+def test_fwd_vs_dense_masked_attention(slope):
+    counts = [5, 0, 1, 3, 8, 2, 0, 6]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), off[-1], 2, 6
+    Q, K, V, _ = _rand_qkv(N, E, H, dh, 2)
+    out, lse, alpha, pre = oracle.edge_attention_fwd(off, Q, K, V, 0.5, slope)
+    ref_out, A, ref_lse, mask = _dense_attention(off, Q, K, V, 0.5, slope)
+    nz = np.diff(off) > 0
+    np.testing.assert_allclose(out[nz], ref_out[nz], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(lse[nz], ref_lse[nz], rtol=1e-12, atol=1e-12)
+    # alpha per edge equals the dense weights at the edge's slot
+    for v in np.flatnonzero(nz):
+        np.testing.assert_allclose(alpha[off[v]:off[v + 1]].T, A[v][:, :counts[v]], rtol=1e-12)
+    # empty segments: zero output, lse = -inf
+    assert np.all(out[~nz] == 0.0) and np.all(np.isneginf(lse[~nz]))
+
+
+def test_softmax_invariants():
+    counts = [1, 2, 9, 1, 5, 13]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), off[-1], 4, 3
+    Q, K, V, _ = _rand_qkv(N, E, H, dh, 4)
+    out, lse, alpha, _ = oracle.edge_attention_fwd(off, Q, K, V, 0.8, SLOPE)
+    seg = np.repeat(np.arange(N), counts)
+    sums = np.zeros((N, H))
+    np.add.at(sums, seg, alpha)
+    np.testing.assert_allclose(sums, 1.0, atol=1e-14)
+    # a single-neighbour segment returns its value row exactly
+    for v in (0, 3):
+        assert np.all(alpha[off[v]] == 1.0)
+        assert np.array_equal(out[v], V[off[v]])
+    # Q = 0: uniform weights and the mean of V
+    out0, _, alpha0, _ = oracle.edge_attention_fwd(off, np.zeros_like(Q), K, V, 0.8, SLOPE)
+    np.testing.assert_allclose(alpha0, (1.0 / np.asarray(counts))[seg][:, None] * np.ones(H), rtol=1e-15)
+    for v in range(N):
+        np.testing.assert_allclose(out0[v], V[off[v]:off[v + 1]].mean(axis=0), rtol=1e-13, atol=1e-15)
+
+
+def test_permutation_invariance_within_segment():
+    counts = [6, 3, 8]
+    off = _csr(counts)
+    N, E, H, dh = 3, off[-1], 2, 5
+    Q, K, V, dO = _rand_qkv(N, E, H, dh, 5)
+    r = np.random.default_rng(9)
+    perm = np.concatenate([off[v] + r.permutation(counts[v]) for v in range(N)])
+    out, lse, alpha, _ = oracle.edge_attention_fwd(off, Q, K, V, 0.6, SLOPE)
+    out_p, lse_p, alpha_p, _ = oracle.edge_attention_fwd(off, Q, K[perm], V[perm], 0.6, SLOPE)
+    np.testing.assert_allclose(out_p, out, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(alpha_p, alpha[perm], rtol=1e-13)
+    dQ, dK, dV = oracle.edge_attention_bwd(off, Q, K, V, dO, 0.6, SLOPE)
+    dQp, dKp, dVp = oracle.edge_attention_bwd(off, Q, K[perm], V[perm], dO, 0.6, SLOPE)
+    np.testing.assert_allclose(dQp, dQ, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dKp, dK[perm], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dVp, dV[perm], rtol=1e-12, atol=1e-13)
+
+
+def test_huge_logits_stay_finite():
+    # the max subtraction (safe softmax, Sec. 4.3) keeps exp() in range
+    counts = [4, 7]
+    off = _csr(counts)
+    Q, K, V, _ = _rand_qkv(2, 11, 2, 8, 6)
+    out, lse, alpha, _ = oracle.edge_attention_fwd(off, Q, K, V, 1.0e4, SLOPE)
+    assert np.isfinite(out).all() and np.isfinite(lse).all() and np.isfinite(alpha).all()
+    ref_out, _, _, _ = _dense_attention(off, Q, K, V, 1.0e4, SLOPE)
+    np.testing.assert_allclose(out, ref_out, rtol=1e-10, atol=1e-10)
+
+
+# ---------------------------------------------------------------- backward (a8, a9)
+def test_bwd_vs_torch_autograd_sdpa():
+    counts = [2, 5, 1, 9, 4]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), off[-1], 2, 7
+    Q, K, V, dO = _rand_qkv(N, E, H, dh, 7)
+    scale = 0.45
+    dQ, dK, dV = oracle.edge_attention_bwd(off, Q, K, V, dO, scale, 1.0)
+    Kd, mask = _dense(off, K)
+    Vd, _ = _dense(off, V)
+    q = torch.tensor(Q)[:, :, None, :].requires_grad_()
+    k = torch.tensor(Kd).permute(0, 2, 1, 3).contiguous().requires_grad_()
+    v = torch.tensor(Vd).permute(0, 2, 1, 3).contiguous().requires_grad_()
+    m = torch.tensor(mask)[:, None, None, :]
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, attn_mask=m, scale=scale)
+    (o * torch.tensor(dO)[:, :, None, :]).sum().backward()
+    np.testing.assert_allclose(dQ, q.grad[:, :, 0, :].numpy(), rtol=1e-11, atol=1e-12)
+    gk = k.grad.permute(0, 2, 1, 3).numpy()
+    gv = v.grad.permute(0, 2, 1, 3).numpy()
+    np.testing.assert_allclose(dK, gk[mask], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dV, gv[mask], rtol=1e-11, atol=1e-12)
+
+
+def _loss(off, Q, K, V, dO, scale, slope):
+    out, _, _, _ = oracle.edge_attention_fwd(off, Q, K, V, scale, slope)
+    return float((out * dO).sum())
+
+
+def test_bwd_finite_differences_leaky():
+    counts = [3, 1, 6, 0, 4]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), off[-1], 2, 4
+    Q, K, V, dO = _rand_qkv(N, E, H, dh, 8)
+    scale = 0.9
+    _, _, _, pre = oracle.edge_attention_fwd(off, Q, K, V, scale, SLOPE)
+    assert np.abs(pre).min() > 1e-3        # away from the LeakyReLU kink
+    dQ, dK, dV = oracle.edge_attention_bwd(off, Q, K, V, dO, scale, SLOPE)
+    h = 1e-6
+    for name, X, G in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
+        fd = np.zeros_like(X)
+        for idx in np.ndindex(X.shape):
+            Xp, Xm = X.copy(), X.copy()
+            Xp[idx] += h
+            Xm[idx] -= h
+            args = {"Q": Q, "K": K, "V": V}
+            args[name] = Xp
+            lp = _loss(off, args["Q"], args["K"], args["V"], dO, scale, SLOPE)
+            args[name] = Xm
+            lm = _loss(off, args["Q"], args["K"], args["V"], dO, scale, SLOPE)
+            fd[idx] = (lp - lm) / (2 * h)
+        np.testing.assert_allclose(G, fd, rtol=1e-6, atol=1e-7, err_msg=name)
+    assert np.all(dQ[3] == 0.0)             # empty segment
+
+
+def test_softmax_bwd_vs_jacobian_matrix():
+    counts = [5, 2, 7]
+    off = _csr(counts)
+    N, E, H, dh = 3, off[-1], 2, 3
+    Q, K, _, _ = _rand_qkv(N, E, H, dh, 10)
+    r = np.random.default_rng(11)
+    dalpha = r.standard_normal((E, H))
+    scale = 0.7
+    alpha, _, pre = oracle.edge_softmax_fwd(off, Q, K, scale, SLOPE)
+    dQ, dK = oracle.edge_softmax_bwd(off, Q, K, scale, SLOPE, alpha, dalpha)
+    for v in range(N):
+        sl = slice(off[v], off[v + 1])
+        for h in range(H):
+            a = alpha[sl, h]
+            J = np.diag(a) - np.outer(a, a)          # d alpha / d s
+            ds = J.T @ dalpha[sl, h]
+            dpre = ds * np.where(pre[sl, h] > 0, 1.0, SLOPE)
+            g = dpre * scale
+            np.testing.assert_allclose(dQ[v, h], g @ K[sl, h, :], rtol=1e-12, atol=1e-13)
+            np.testing.assert_allclose(dK[sl, h, :], np.outer(g, Q[v, h]), rtol=1e-12, atol=1e-13)
+
+
+def test_aggregate_bwd_is_the_transpose():
+    # aggregation is bilinear in (alpha, V): its backward is the exact adjoint
+    counts = [4, 0, 2, 5]
+    off = _csr(counts)
+    N, E, H, dh = 4, off[-1], 3, 5
+    r = np.random.default_rng(12)
+    alpha = r.random((E, H))
+    V = r.standard_normal((E, H, dh))
+    dO = r.standard_normal((N, H, dh))
+    da, dV = oracle.aggregate_bwd(off, alpha, V, dO)
+    a2 = r.random((E, H))
+    V2 = r.standard_normal((E, H, dh))
+    # <dO, agg(a2, V)> = <da, a2> and <dO, agg(alpha, V2)> = <dV, V2>
+    np.testing.assert_allclose((dO * oracle.aggregate_fwd(off, a2, V)).sum(), (da * a2).sum(), rtol=1e-12)
+    np.testing.assert_allclose((dO * oracle.aggregate_fwd(off, alpha, V2)).sum(), (dV * V2).sum(), rtol=1e-12)
+
+
+def test_branch_override():
+    counts = [3, 4]
+    off = _csr(counts)
+    Q, K, V, dO = _rand_qkv(2, 7, 2, 4, 13)
+    alpha, _, pre = oracle.edge_softmax_fwd(off, Q, K, 0.5, SLOPE)
+    assert (pre > 0).any() and (pre < 0).any()
+    da = np.random.default_rng(1).standard_normal(alpha.shape)
+    ones = np.ones(alpha.shape, np.int8)
+    twos = np.full(alpha.shape, 2, np.int8)
+    dQ1, dK1 = oracle.edge_softmax_bwd(off, Q, K, 0.5, SLOPE, alpha, da, ones)
+    dQr, dKr = oracle.edge_softmax_bwd(off, Q, K, 0.5, 1.0, alpha, da)
+    np.testing.assert_allclose(dQ1, dQr, rtol=1e-14, atol=1e-15)
+    dQ2, _ = oracle.edge_softmax_bwd(off, Q, K, 0.5, SLOPE, alpha, da, twos)
+    dQs, _ = oracle.edge_softmax_bwd(off, Q, K, 0.5 * SLOPE, 1.0, alpha, da)
+    # r = slope everywhere equals (scale*slope) with r = 1, since g = ds*r*scale
+    np.testing.assert_allclose(dQ2, dQs, rtol=1e-13, atol=1e-15)
