@@ -1,0 +1,331 @@
+"""Benchmark of the FAST temporal-subgraph hot path on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic batch, with
+every input already resident in HBM:
+  1. CSR offsets of both layer blocks              (fast_csr_offsets)
+  2. within-batch dedup + row gather, node ids     (fast_dedup_gather)
+  3. within-batch dedup + cache gather, edge ids   (fast_dedup_gather, slot map)
+  4. time encoding of both blocks                  (fast_time_encode)
+  5. fused edge softmax + aggregation: forward of layer 1 and layer 2, then
+     backward of layer 2 and layer 1               (fast_edge_attention_fwd/bwd)
+value = sampled edges per step / step time.  The roofline entry covers the
+dominant kernel, the fused backward of the layer-1 block, timed with HIP
+events on the stream it runs on.
+
+    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+SLOPE = 0.2
+WORKLOADS = {"bigdedup": 4, "large": 3}
+METRIC = "sampled edges/sec, fused edge-softmax+aggregation fwd+bwd; % HBM roofline"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_bwd.json")
+KERNEL_SOURCES = ["paper_2607_05095_amd/csrc/attention.hip", "paper_2607_05095_amd/csrc/common.h"]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def describe(b):
+    n1, e1 = b.blocks[0].num_dst, b.blocks[0].num_edges
+    return {
+        "workload": f"{b.name}: {b.blocks[1].num_dst} roots, 2 layers fan-out "
+                    f"{b.blocks[0].counts.max()}x{b.blocks[0].counts.max()}, "
+                    f"{b.sampled_edges} sampled edges per step",
+        "layer_blocks": [[blk.num_dst, blk.num_edges] for blk in b.blocks],
+        "heads": b.H, "head_dim": b.dh, "time_dim": b.d_t, "storage": b.dtype,
+        "node_ids": int(b.node_ids.size), "node_id_bound": b.node_bound, "node_dim": b.node_D,
+        "edge_ids": int(b.edge_ids.size), "edge_id_bound": b.edge_bound, "edge_dim": b.edge_D,
+        "edge_cache_rows": b.edge_cache_rows,
+    }
+
+
+class Step:
+    """All device buffers of one batch and the launch sequence of one step."""
+
+    def __init__(self, b, torch, fast):
+        from synth import make_block_operands, make_slot_map, make_table, omega_phi
+        self.b, self.torch, self.fast = b, torch, fast
+        dev = "cuda"
+        tdt = torch.float32 if b.dtype == "f32" else torch.bfloat16
+        self.DT = fast.F32 if b.dtype == "f32" else fast.BF16
+        self.blocks = []
+        for i, blk in enumerate(b.blocks):
+            N, E = blk.num_dst, blk.num_edges
+            d = dict(N=N, E=E)
+            d["counts"] = torch.from_numpy(blk.counts).to(dev)
+            d["off"] = torch.empty(N + 1, dtype=torch.int32, device=dev)
+            d["ws_off"] = torch.empty(fast.fast_csr_offsets_workspace(N), dtype=torch.uint8, device=dev)
+            d["dst_t"] = torch.from_numpy(blk.dst_t).to(dev)
+            d["edge_t"] = torch.from_numpy(blk.edge_t).to(dev)
+            d.update(make_block_operands(b, i, device=dev))
+            d["out"] = torch.empty((N, b.H, b.dh), dtype=tdt, device=dev)
+            d["lse"] = torch.empty((N, b.H), dtype=torch.float32, device=dev)
+            d["dQ"] = torch.empty((N, b.H, b.dh), dtype=tdt, device=dev)
+            d["dK"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
+            d["dV"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
+            d["te"] = torch.empty((E, b.d_t), dtype=tdt, device=dev)
+            d["g"] = fast.tcsr(d["off"], E, edge_t=d["edge_t"], dst_t=d["dst_t"])
+            self.blocks.append(d)
+        om, ph = omega_phi(b.d_t)
+        self.omega = torch.from_numpy(om).to(dev)
+        self.phi = torch.from_numpy(ph).to(dev)
+        self.scale = float(np.float32(1.0 / np.sqrt(b.dh)))
+        # node ids: table indexed by id
+        log(f"node table {b.node_bound} x {b.node_D} {b.dtype}")
+        self.node = self._dedup_bufs(b.node_ids, b.node_bound,
+                                     make_table(b.node_bound, b.node_D, b.dtype, dev, b.seed, 3), None)
+        # edge ids: a cache with a slot map, or a table indexed by id
+        if b.edge_cache_rows:
+            log(f"edge cache {b.edge_cache_rows} x {b.edge_D}, slot map over {b.edge_bound}")
+            table = make_table(b.edge_cache_rows, b.edge_D, b.dtype, dev, b.seed, 4)
+            slot = make_slot_map(b, device=dev)
+        else:
+            table = make_table(b.edge_bound, b.edge_D, b.dtype, dev, b.seed, 4)
+            slot = None
+        self.edge = self._dedup_bufs(b.edge_ids, b.edge_bound, table, slot)
+        self.events = None
+
+    def _dedup_bufs(self, ids_np, bound, table, slot):
+        torch, fast = self.torch, self.fast
+        n = ids_np.shape[0]
+        d = dict(n=n, bound=bound, table=table, slot=slot)
+        d["ids"] = torch.from_numpy(ids_np).cuda()
+        d["uni"] = torch.empty(n, dtype=torch.int64, device="cuda")
+        d["inv"] = torch.empty(n, dtype=torch.int32, device="cuda")
+        d["nu"] = torch.empty(1, dtype=torch.int64, device="cuda")
+        d["rows"] = torch.empty((n, table.shape[1]), dtype=table.dtype, device="cuda")
+        d["miss"] = torch.empty(n, dtype=torch.int32, device="cuda")
+        d["nm"] = torch.empty(1, dtype=torch.int64, device="cuda")
+        d["wsb"] = fast.fast_dedup_gather_workspace(n, bound)
+        d["ws"] = torch.empty(d["wsb"], dtype=torch.uint8, device="cuda")
+        return d
+
+    def _dedup(self, d):
+        f = self.fast
+        f.fast_dedup_gather(d["ids"], d["n"], d["bound"], d["table"], d["table"].shape[0],
+                            d["table"].shape[1], self.DT, d["slot"], d["uni"], d["inv"], d["nu"],
+                            d["rows"], d["miss"], d["nm"], d["ws"], d["wsb"])
+
+    def run(self, rec=None):
+        """Enqueue one step.  rec: optional dict name -> list of (start, end) events."""
+        torch, f, b = self.torch, self.fast, self.b
+        st = torch.cuda.current_stream()
+
+        def mark(name, fn):
+            if rec is None:
+                fn()
+                return
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record(st)
+            fn()
+            e.record(st)
+            rec.setdefault(name, []).append((s, e))
+
+        for i, d in enumerate(self.blocks):
+            mark(f"offsets_L{i + 1}", lambda d=d: f.fast_csr_offsets(d["counts"], d["N"], d["off"],
+                                                                      d["ws_off"], d["ws_off"].numel()))
+        mark("dedup_gather_nodes", lambda: self._dedup(self.node))
+        mark("dedup_gather_edges", lambda: self._dedup(self.edge))
+        for i, d in enumerate(self.blocks):
+            mark(f"time_encode_L{i + 1}", lambda d=d: f.fast_time_encode(
+                d["g"], self.omega, self.phi, b.d_t, d["te"], self.DT))
+        for i, d in enumerate(self.blocks):           # forward: layer 1 then layer 2
+            mark(f"attn_fwd_L{i + 1}", lambda d=d: f.fast_edge_attention_fwd(
+                d["g"], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                d["out"], d["lse"]))
+        for i in reversed(range(len(self.blocks))):  # backward: layer 2 then layer 1
+            d = self.blocks[i]
+            mark(f"attn_bwd_L{i + 1}", lambda d=d: f.fast_edge_attention_bwd(
+                d["g"], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                d["lse"], d["dO"], d["dQ"], d["dK"], d["dV"]))
+
+
+def attn_bwd_bytes(N, E, F, esz, H):
+    """Algorithmic bytes of one fused backward launch: read Q, dOut (N rows),
+    K, V (E rows), lse, offsets; write dQ (N rows), dK, dV (E rows)."""
+    return (4 * E + 3 * N) * F * esz + 4 * N * H + 4 * (N + 1)
+
+
+def attn_fwd_bytes(N, E, F, esz, H):
+    """Read Q (N rows), K, V (E rows), offsets; write out (N rows) and lse."""
+    return (2 * E + 2 * N) * F * esz + 4 * N * H + 4 * (N + 1)
+
+
+def cpu_baseline(b, step, torch, frac):
+    """The fp64 oracle, single-threaded, on a bounded sample of the same batch:
+    the first `frac` of the segments of each layer block and the matching
+    share of node and edge ids, through the same sequence of operators."""
+    import oracle
+    from synth import omega_phi
+    om, ph = omega_phi(b.d_t)
+    sample_edges = 0
+    # inputs for the sample (host copies, outside the timed region)
+    blocks = []
+    for i, blk in enumerate(b.blocks):
+        ns = max(1, int(blk.num_dst * frac))
+        counts = blk.counts[:ns]
+        es = int(counts.sum())
+        d = step.blocks[i]
+        blocks.append(dict(counts=counts, dst_t=blk.dst_t[:ns], edge_t=blk.edge_t[:es],
+                           Q=d["Q"][:ns].cpu(), K=d["K"][:es].cpu(), V=d["V"][:es].cpu(),
+                           dO=d["dO"][:ns].cpu()))
+        sample_edges += es
+    nn, ne = int(b.node_ids.size * frac), int(b.edge_ids.size * frac)
+    node_ids, edge_ids = b.node_ids[:nn], b.edge_ids[:ne]
+    bits = torch.int16 if b.dtype == "bf16" else torch.int32
+    node_table = step.node["table"].view(bits).cpu().numpy()
+    edge_table = step.edge["table"].view(bits).cpu().numpy()
+    slot = None if step.edge["slot"] is None else step.edge["slot"].cpu().numpy()
+    scale = step.scale
+    t0 = time.perf_counter()
+    offs = [oracle.csr_offsets(x["counts"]) for x in blocks]
+    uni, _ = oracle.dedup(node_ids)
+    oracle.gather(uni, node_table)
+    uni, _ = oracle.dedup(edge_ids)
+    oracle.gather(uni, edge_table, slot)
+    for x, off in zip(blocks, offs):
+        oracle.time_encode(off, x["dst_t"], x["edge_t"], om, ph)
+    for x, off in zip(blocks, offs):
+        oracle.edge_attention_fwd(off, x["Q"], x["K"], x["V"], scale, SLOPE)
+    for x, off in reversed(list(zip(blocks, offs))):
+        oracle.edge_attention_bwd(off, x["Q"], x["K"], x["V"], x["dO"], scale, SLOPE)
+    dt = time.perf_counter() - t0
+    return {
+        "value": sample_edges / dt, "unit": "sampled edges/s", "cores": 1, "kind": "oracle",
+        "sample": f"first {frac:.0%} of the segments of each layer block ({sample_edges} sampled "
+                  f"edges) and of the node/edge ids; offsets, dedup+gather, time encoding, "
+                  f"fused attention fwd+bwd in fp64; {dt:.1f} s",
+        "seconds": dt,
+    }
+
+
+def read_traffic(n_launch_bytes):
+    """HBM traffic of the dominant kernel from the committed rocprofv3 counter
+    summary, or None when it is absent or the kernel source changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="bigdedup")
+    ap.add_argument("--cpu-frac", type=float, default=0.25)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding "
+                                   "design is described but not built", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2607_05095_amd as fast
+
+    if args.copy_calibration:
+        x = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_each_way": x.numel() * 4, "copies": 5}))
+        return
+
+    from synth import make_batch
+    b = make_batch(WORKLOADS[args.workload])
+    log(f"workload {b.name}: blocks {[(x.num_dst, x.num_edges) for x in b.blocks]}")
+    step = Step(b, torch, fast)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    # timed region: K whole steps
+    rec = {}
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for _ in range(args.steps):
+        step.run(rec)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / args.steps
+    breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec.items()}
+    log(f"{ms:.3f} ms/step")
+
+    esz = 4 if b.dtype == "f32" else 2
+    F = b.H * b.dh
+    L1 = b.blocks[0]
+    bwd_ms = breakdown["attn_bwd_L1"]
+    bwd_bytes = attn_bwd_bytes(L1.num_dst, L1.num_edges, F, esz, b.H)
+    achieved = bwd_bytes / (bwd_ms * 1e-3) / 1e9
+    fused_ms = sum(v for k, v in breakdown.items() if k.startswith("attn_"))
+    fused_bytes = sum(attn_fwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) +
+                      attn_bwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) for x in b.blocks)
+    roofline = {
+        "kernel": "k_attn_bwd (fused ESM+AGG backward, layer-1 block)",
+        "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(bwd_bytes),
+        "algorithmic_bytes_per_launch": bwd_bytes, "avg_launch_ms": round(bwd_ms, 4),
+    }
+    result = {
+        "metric": METRIC,
+        "value": b.sampled_edges / (ms * 1e-3),
+        "unit": "sampled edges/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": b.dtype, "data": "synthetic",
+        "config": describe(b),
+        "roofline": roofline,
+        "fused_attention": {
+            "edges_per_s": b.sampled_edges / (fused_ms * 1e-3), "ms": round(fused_ms, 4),
+            "algorithmic_bytes": fused_bytes,
+            "hbm_frac": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
+        "kernel_source_sha": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(b, step, torch, args.cpu_frac)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,197 @@
+/*
+ * fast.h -- C ABI of the MI355X (gfx950) temporal-subgraph operators of FAST
+ * (arXiv 2607.05095): the GPU hot path of one temporal-GNN training step.
+ *
+ *   fast_csr_offsets          CSR ind_ptr of a sampled block          (Sec. 5)
+ *   fast_dedup_gather         uni_ID / inv_Idx + row reconstruction   (Sec. 4.2, Sec. 5)
+ *   fast_time_encode          cos(omega * dt + phi) time features     (Sec. 6.1, TGAT)
+ *   fast_edge_softmax_fwd/bwd per-edge multi-head logits + ESM        (Sec. 4.3)
+ *   fast_temporal_aggregate_fwd/bwd  attention-weighted AGG           (Sec. 4.3, Eq. 1)
+ *   fast_edge_attention_fwd/bwd      ESM and AGG fused in one kernel  (Sec. 4.3)
+ *
+ * Conventions shared by every entry point
+ *   - Memory: every array argument is a DEVICE pointer into HBM owned by the
+ *     caller.  The library allocates nothing, frees nothing, never
+ *     synchronises the stream and keeps no state other than a thread-local
+ *     error message.  Scratch memory, where needed, is a caller-provided
+ *     workspace whose size the matching *_workspace() query returns.
+ *   - Streams: `stream` is a hipStream_t passed as void* (NULL = the null
+ *     stream).  Work is enqueued asynchronously; results are valid once the
+ *     stream reaches that point.  Calls on one stream run in order.
+ *   - Layout: row-major and contiguous.  Per-edge rows [E,H,dh] follow the
+ *     CSR edge order; per-destination rows are [N,H,dh].  Per-(edge,head)
+ *     scalars (alpha, dalpha) are fp32 [E,H]; per-(destination,head) lse is
+ *     fp32 [N,H].  Row storage is FAST_F32 or FAST_BF16 (bfloat16, stored
+ *     as round-to-nearest-even; all arithmetic is fp32).
+ *   - Errors: problems the host can see (a NULL required pointer, a negative
+ *     size, an unsupported shape or dtype, a misaligned pointer, a workspace
+ *     that is too small) return a non-zero status BEFORE anything is
+ *     enqueued; a failed launch returns FAST_ERR_HIP.  fast_last_error()
+ *     then describes the failure.  No C++ exception crosses this boundary.
+ *   - Device-data contract: offsets are non-decreasing with off[0] = 0 and
+ *     off[N] = E.  Kernels clamp every offset to [0, E], so a malformed
+ *     offsets array gives wrong numbers but never an out-of-bounds access.
+ *   - Empty inputs (N = 0, E = 0, n = 0) are valid and write the
+ *     documented empty-segment values.
+ */
+#ifndef FAST_H
+#define FAST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FAST_OK = 0,
+  FAST_ERR_INVALID_ARG = 1,  /* NULL required pointer, negative size, bad enum */
+  FAST_ERR_UNSUPPORTED = 2,  /* shape/dtype/alignment this build does not handle */
+  FAST_ERR_WORKSPACE = 3,    /* ws NULL or ws_bytes smaller than the query */
+  FAST_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+} fast_status_t;
+
+typedef enum { FAST_F32 = 0, FAST_BF16 = 1 } fast_dtype_t;
+
+typedef void* fast_stream_t; /* hipStream_t */
+
+/* A sampled temporal subgraph of one layer block in CSR-by-destination form
+ * (Sec. 4.3: CSR for ESM; Sec. 5: the compression triple's ind_ptr).  Edges
+ * of destination v are e in [dst_offsets[v], dst_offsets[v+1]).  All
+ * pointers are DEVICE pointers; an operator states which fields it reads and
+ * the others may be NULL. */
+typedef struct fast_tcsr {
+  int64_t num_dst;            /* N >= 0 destination segments                   */
+  int64_t num_edges;          /* E >= 0 edges, E < 2^31                        */
+  const int32_t* dst_offsets; /* [N+1] int32                                   */
+  const int64_t* src_ids;     /* [E] source node id per edge (dedup input)     */
+  const float* edge_t;        /* [E] edge timestamps                           */
+  const int64_t* edge_ids;    /* [E] edge id per edge (dedup input)            */
+  const float* dst_t;         /* [N] destination (query) timestamps            */
+} fast_tcsr_t;
+
+/* Message for the last non-OK status returned on the calling thread ("" if
+ * none).  The string stays valid until the next failing call on that thread. */
+const char* fast_last_error(void);
+
+/* Library version string, e.g. "fast-mi355x 0.1 gfx950". */
+const char* fast_version(void);
+
+/* ------------------------------------------------------------------------
+ * CSR offsets (Sec. 5: the compression engine's CSR-style ind_ptr).
+ *   offsets[0] = 0, offsets[v+1] = offsets[v] + counts[v]   for v < n
+ * counts: [n] int32 >= 0, sum < 2^31.  offsets: [n+1] int32.
+ * Workspace: fast_csr_offsets_workspace(n) bytes (never 0).
+ * ------------------------------------------------------------------------ */
+size_t fast_csr_offsets_workspace(int64_t n);
+fast_status_t fast_csr_offsets(const int32_t* counts, int64_t n, int32_t* offsets,
+                               void* ws, size_t ws_bytes, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Within-batch de-duplication and row reconstruction (Sec. 4.2 SlimCache
+ * compression; Sec. 5 uni_ID / inv_Idx).
+ *   uni[0..u)   = the distinct values of ids[0..n), ascending
+ *   inv[i]      = the k with uni[k] == ids[i]
+ *   *num_unique = u                                  (device int64 scalar)
+ *   rows[k]     = table[slot(uni[k])] (D elements, bit-exact copy) where
+ *                 slot(x) = slot_map ? slot_map[x] : x
+ *   miss[0..m)  = ascending k with slot outside [0, table_rows); rows[k] of a
+ *                 missed k is left untouched; *num_miss = m (device int64)
+ * ids: [n] int64 in [0, id_bound).  An id outside that range is skipped:
+ *   it gets inv = -1 and does not enter uni.
+ * table: [table_rows, D] of dtype.  slot_map: NULL or [id_bound] int32.
+ *   When rows are requested without a slot_map, id_bound must be <= table_rows.
+ * Outputs: uni cap n, inv [n], rows cap n*D (or NULL: dedup only, then
+ *   table may be NULL), miss cap n (or NULL; *num_miss is still written
+ *   when num_miss != NULL).
+ * Limits: n < 2^31, id_bound <= 2^35.
+ * Workspace: fast_dedup_gather_workspace(n, id_bound) bytes.
+ * ------------------------------------------------------------------------ */
+size_t fast_dedup_gather_workspace(int64_t n, int64_t id_bound);
+fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
+                                const void* table, int64_t table_rows, int D,
+                                fast_dtype_t dtype, const int32_t* slot_map,
+                                int64_t* uni, int32_t* inv, int64_t* num_unique,
+                                void* rows, int32_t* miss, int64_t* num_miss,
+                                void* ws, size_t ws_bytes, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Time encoding (Sec. 6.1: TGAT's random Fourier time features).
+ *   te[e, j] = cos(fmaf(omega[j], dt_e, phi[j])),  dt_e = dst_t[v] - edge_t[e]
+ * for e in segment v.  dt and the argument are fp32 (one subtraction, one
+ * fused multiply-add); cos is the accurate device-library cosine.
+ * Reads g->dst_offsets, g->dst_t, g->edge_t.  omega, phi: [d_t] fp32 device.
+ * te: [E, d_t] of te_dtype.  d_t >= 1.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega, const float* phi,
+                               int d_t, void* te, fast_dtype_t te_dtype,
+                               fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Edge softmax with per-edge multi-head attention logits (Sec. 4.3 "Edge
+ * Softmax": a numerically stable max / sum / divide per destination).
+ *   pre[e,h]   = scale * <Q[v,h,:], K[e,h,:]>,  s = pre > 0 ? pre : neg_slope*pre
+ *   alpha[e,h] = exp(s - m) / Z,  m = max_{e in v} s,  Z = sum_{e in v} exp(s - m)
+ *   lse[v,h]   = m + log Z  (-inf for an empty segment; lse may be NULL)
+ * Q: [N,H,dh], K: [E,H,dh] of dtype.  alpha: [E,H] fp32.  Reads g->dst_offsets.
+ * Supported: 1 <= H, 1 <= dh, H*dh <= 4096, dh <= 256 * (16 / element size).
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_edge_softmax_fwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
+                                    const void* Q, const void* K, float scale,
+                                    float neg_slope, float* alpha, float* lse,
+                                    fast_stream_t stream);
+
+/* Backward of fast_edge_softmax_fwd for an upstream gradient dalpha [E,H]:
+ *   D[v,h] = sum_e alpha*dalpha,  g = alpha*(dalpha - D) * (pre > 0 ? 1 : neg_slope) * scale
+ *   dQ[v,h,:] = sum_e g*K[e,h,:]  (0 for an empty segment),  dK[e,h,:] = g*Q[v,h,:]
+ * alpha: the forward's output.  dQ: [N,H,dh], dK: [E,H,dh] of dtype. */
+fast_status_t fast_edge_softmax_bwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
+                                    const void* Q, const void* K, float scale,
+                                    float neg_slope, const float* alpha,
+                                    const float* dalpha, void* dQ, void* dK,
+                                    fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Attention-weighted temporal aggregation (Sec. 4.3 "Balanced Aggregate";
+ * Eq. 1 with AGG = sum of alpha-weighted neighbour messages).
+ *   out[v,h,:] = sum_{e in v} alpha[e,h] * V[e,h,:]   (0 for an empty segment)
+ * Deterministic: each destination row is reduced by one sub-wavefront, no
+ * atomics.  alpha: [E,H] fp32; V: [E,H,dh], out: [N,H,dh] of dtype.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_temporal_aggregate_fwd(const fast_tcsr_t* g, int H, int dh,
+                                          fast_dtype_t dtype, const float* alpha,
+                                          const void* V, void* out, fast_stream_t stream);
+
+/* Backward: dalpha[e,h] = <dout[v,h,:], V[e,h,:]>,  dV[e,h,:] = alpha[e,h]*dout[v,h,:].
+ * dalpha: [E,H] fp32; dV: [E,H,dh] of dtype. */
+fast_status_t fast_temporal_aggregate_bwd(const fast_tcsr_t* g, int H, int dh,
+                                          fast_dtype_t dtype, const float* alpha,
+                                          const void* V, const void* dout, float* dalpha,
+                                          void* dV, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Fused edge softmax + aggregation (Sec. 4.3 operators in one pass; alpha is
+ * never written to memory).  Equals fast_edge_softmax_fwd followed by
+ * fast_temporal_aggregate_fwd: out = AGG(ESM(Q,K), V); lse as in ESM (may be
+ * NULL).  Q,out: [N,H,dh]; K,V: [E,H,dh] of dtype.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_edge_attention_fwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
+                                      const void* Q, const void* K, const void* V,
+                                      float scale, float neg_slope, void* out, float* lse,
+                                      fast_stream_t stream);
+
+/* Backward of the fused operator for dout [N,H,dh]: equals
+ * fast_temporal_aggregate_bwd followed by fast_edge_softmax_bwd, with alpha
+ * recomputed from Q and K.  lse: the forward's lse, or NULL to recompute the
+ * softmax normaliser.  dQ: [N,H,dh]; dK, dV: [E,H,dh] of dtype. */
+fast_status_t fast_edge_attention_bwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
+                                      const void* Q, const void* K, const void* V,
+                                      float scale, float neg_slope, const float* lse,
+                                      const void* dout, void* dQ, void* dK, void* dV,
+                                      fast_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FAST_H */

@@ -1,0 +1,194 @@
+"""Thin Python binding of libfast.so, the gfx950 temporal-subgraph operators.
+
+Every function has the name and argument order of the C entry point in
+include/fast.h.  Arguments are torch tensors resident on the GPU (or None
+for optional pointers); the binding only marshals pointers, sizes and the
+current HIP stream, and raises FastError for a non-OK status.  All
+computation happens in the HIP kernels; there is no fallback path: if the
+library is missing the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+__all__ = [
+    "FastError", "lib", "TCSR", "tcsr", "F32", "BF16", "dtype_of",
+    "fast_version", "fast_last_error",
+    "fast_csr_offsets_workspace", "fast_csr_offsets",
+    "fast_dedup_gather_workspace", "fast_dedup_gather",
+    "fast_time_encode",
+    "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
+    "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
+    "fast_edge_attention_fwd", "fast_edge_attention_bwd",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfast.so")
+
+F32, BF16 = 0, 1
+_STATUS = {0: "FAST_OK", 1: "FAST_ERR_INVALID_ARG", 2: "FAST_ERR_UNSUPPORTED",
+           3: "FAST_ERR_WORKSPACE", 4: "FAST_ERR_HIP"}
+
+
+class FastError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class TCSR(C.Structure):
+    """fast_tcsr_t: a sampled temporal subgraph of one layer block (device pointers)."""
+    _fields_ = [
+        ("num_dst", C.c_int64),
+        ("num_edges", C.c_int64),
+        ("dst_offsets", C.c_void_p),
+        ("src_ids", C.c_void_p),
+        ("edge_t", C.c_void_p),
+        ("edge_ids", C.c_void_p),
+        ("dst_t", C.c_void_p),
+    ]
+
+
+_p, _i64, _i32, _f32, _sz = C.c_void_p, C.c_int64, C.c_int, C.c_float, C.c_size_t
+_G = C.POINTER(TCSR)
+_SIGS = {
+    "fast_last_error": (C.c_char_p, []),
+    "fast_version": (C.c_char_p, []),
+    "fast_csr_offsets_workspace": (_sz, [_i64]),
+    "fast_csr_offsets": (_i32, [_p, _i64, _p, _p, _sz, _p]),
+    "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
+    "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
+                                 _p, _p, _p, _p, _sz, _p]),
+    "fast_time_encode": (_i32, [_G, _p, _p, _i32, _p, _i32, _p]),
+    "fast_edge_softmax_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p]),
+    "fast_edge_softmax_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p]),
+    "fast_temporal_aggregate_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _p]),
+    "fast_temporal_aggregate_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p]),
+    "fast_edge_attention_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p, _p]),
+    "fast_edge_attention_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p,
+                                       _p, _p, _p, _p]),
+}
+
+_lib = None
+
+
+def lib():
+    """Load libfast.so (built in-tree by build.py); raises if it is absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FastError(-1, f"{LIB_PATH} is not built; run python -m paper_2607_05095_amd.build")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(st: int):
+    if st != 0:
+        raise FastError(st, fast_last_error())
+
+
+def dtype_of(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise FastError(2, f"unsupported tensor dtype {t.dtype}")
+
+
+def tcsr(dst_offsets, num_edges: int, src_ids=None, edge_t=None, edge_ids=None, dst_t=None) -> TCSR:
+    """Builds a fast_tcsr_t over device tensors.  The tensors must stay alive
+    while the struct is in use."""
+    return TCSR(dst_offsets.shape[0] - 1, int(num_edges), _ptr(dst_offsets), _ptr(src_ids),
+                _ptr(edge_t), _ptr(edge_ids), _ptr(dst_t))
+
+
+# ------------------------------------------------------------------ entry points
+def fast_last_error() -> str:
+    return lib().fast_last_error().decode()
+
+
+def fast_version() -> str:
+    return lib().fast_version().decode()
+
+
+def fast_csr_offsets_workspace(n: int) -> int:
+    return lib().fast_csr_offsets_workspace(n)
+
+
+def fast_csr_offsets(counts, n, offsets, ws, ws_bytes, stream=None):
+    _check(lib().fast_csr_offsets(_ptr(counts), n, _ptr(offsets), _ptr(ws), ws_bytes,
+                                  _stream(stream)))
+
+
+def fast_dedup_gather_workspace(n: int, id_bound: int) -> int:
+    return lib().fast_dedup_gather_workspace(n, id_bound)
+
+
+def fast_dedup_gather(ids, n, id_bound, table, table_rows, D, dtype, slot_map, uni, inv,
+                      num_unique, rows, miss, num_miss, ws, ws_bytes, stream=None):
+    _check(lib().fast_dedup_gather(_ptr(ids), n, id_bound, _ptr(table), table_rows, D, dtype,
+                                   _ptr(slot_map), _ptr(uni), _ptr(inv), _ptr(num_unique),
+                                   _ptr(rows), _ptr(miss), _ptr(num_miss), _ptr(ws), ws_bytes,
+                                   _stream(stream)))
+
+
+def fast_time_encode(g: TCSR, omega, phi, d_t, te, te_dtype, stream=None):
+    _check(lib().fast_time_encode(C.byref(g), _ptr(omega), _ptr(phi), d_t, _ptr(te), te_dtype,
+                                  _stream(stream)))
+
+
+def fast_edge_softmax_fwd(g: TCSR, H, dh, dtype, Q, K, scale, neg_slope, alpha, lse, stream=None):
+    _check(lib().fast_edge_softmax_fwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), scale,
+                                       neg_slope, _ptr(alpha), _ptr(lse), _stream(stream)))
+
+
+def fast_edge_softmax_bwd(g: TCSR, H, dh, dtype, Q, K, scale, neg_slope, alpha, dalpha, dQ, dK,
+                          stream=None):
+    _check(lib().fast_edge_softmax_bwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), scale,
+                                       neg_slope, _ptr(alpha), _ptr(dalpha), _ptr(dQ), _ptr(dK),
+                                       _stream(stream)))
+
+
+def fast_temporal_aggregate_fwd(g: TCSR, H, dh, dtype, alpha, V, out, stream=None):
+    _check(lib().fast_temporal_aggregate_fwd(C.byref(g), H, dh, dtype, _ptr(alpha), _ptr(V),
+                                             _ptr(out), _stream(stream)))
+
+
+def fast_temporal_aggregate_bwd(g: TCSR, H, dh, dtype, alpha, V, dout, dalpha, dV, stream=None):
+    _check(lib().fast_temporal_aggregate_bwd(C.byref(g), H, dh, dtype, _ptr(alpha), _ptr(V),
+                                             _ptr(dout), _ptr(dalpha), _ptr(dV), _stream(stream)))
+
+
+def fast_edge_attention_fwd(g: TCSR, H, dh, dtype, Q, K, V, scale, neg_slope, out, lse,
+                            stream=None):
+    _check(lib().fast_edge_attention_fwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), _ptr(V),
+                                         scale, neg_slope, _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def fast_edge_attention_bwd(g: TCSR, H, dh, dtype, Q, K, V, scale, neg_slope, lse, dout, dQ, dK,
+                            dV, stream=None):
+    _check(lib().fast_edge_attention_bwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), _ptr(V),
+                                         scale, neg_slope, _ptr(lse), _ptr(dout), _ptr(dQ),
+                                         _ptr(dK), _ptr(dV), _stream(stream)))

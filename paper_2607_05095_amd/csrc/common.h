@@ -1,0 +1,150 @@
+// common.h -- shared device helpers and host-side status handling of the
+// gfx950 operator library.  Wave64 only (CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fast.h"
+
+namespace fast {
+
+// ------------------------------------------------------------------ host side
+// Records a formatted message for fast_last_error() and returns `st`.
+fast_status_t fail(fast_status_t st, const char* fmt, ...)
+    __attribute__((format(printf, 2, 3)));
+// FAST_ERR_HIP with the runtime's message if the last launch failed.
+fast_status_t check_launch(const char* what);
+// Clears the thread's error message (successful call).
+fast_status_t ok();
+
+inline bool aligned(const void* p, size_t a) {
+  return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int elem_size(fast_dtype_t dt) { return dt == FAST_BF16 ? 2 : 4; }
+
+// Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD
+// b % 8).  This bijection hands every XCD a contiguous range of logical
+// tiles, so neighbouring tiles -- which share the partial cache lines at
+// their boundaries -- meet in the same 4 MB L2.
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t nb) {
+  const uint32_t q = nb >> 3, r = nb & 7u, x = b & 7u;
+  return x * q + (x < r ? x : r) + (b >> 3);
+}
+
+// ------------------------------------------------------------------ bf16
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
+  return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
+// ------------------------------------------------------------------ vectors
+// VecIO<T,VE>: VE consecutive elements of storage type T (float, or uint16_t
+// holding bf16) moved as one aligned global access and widened to fp32.
+template <typename T, int VE> struct VecIO;
+
+template <> struct VecIO<float, 1> {
+  __device__ static void load(const float* p, float* x) { x[0] = *p; }
+  __device__ static void store(float* p, const float* x) { *p = x[0]; }
+};
+template <> struct VecIO<float, 2> {
+  __device__ static void load(const float* p, float* x) {
+    float2 v = *reinterpret_cast<const float2*>(p);
+    x[0] = v.x; x[1] = v.y;
+  }
+  __device__ static void store(float* p, const float* x) {
+    *reinterpret_cast<float2*>(p) = make_float2(x[0], x[1]);
+  }
+};
+template <> struct VecIO<float, 4> {
+  __device__ static void load(const float* p, float* x) {
+    float4 v = *reinterpret_cast<const float4*>(p);
+    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+  }
+  __device__ static void store(float* p, const float* x) {
+    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  }
+};
+template <> struct VecIO<uint16_t, 1> {
+  __device__ static void load(const uint16_t* p, float* x) { x[0] = __uint_as_float(uint32_t(*p) << 16); }
+  __device__ static void store(uint16_t* p, const float* x) { *p = uint16_t(bf16_rne(x[0])); }
+};
+template <> struct VecIO<uint16_t, 2> {
+  __device__ static void load(const uint16_t* p, float* x) {
+    uint32_t w = *reinterpret_cast<const uint32_t*>(p);
+    x[0] = bf16_lo(w); x[1] = bf16_hi(w);
+  }
+  __device__ static void store(uint16_t* p, const float* x) {
+    *reinterpret_cast<uint32_t*>(p) = bf16_pack(x[0], x[1]);
+  }
+};
+template <> struct VecIO<uint16_t, 4> {
+  __device__ static void load(const uint16_t* p, float* x) {
+    uint2 w = *reinterpret_cast<const uint2*>(p);
+    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x); x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
+  }
+  __device__ static void store(uint16_t* p, const float* x) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(bf16_pack(x[0], x[1]), bf16_pack(x[2], x[3]));
+  }
+};
+template <> struct VecIO<uint16_t, 8> {
+  __device__ static void load(const uint16_t* p, float* x) {
+    uint4 w = *reinterpret_cast<const uint4*>(p);
+    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x); x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
+    x[4] = bf16_lo(w.z); x[5] = bf16_hi(w.z); x[6] = bf16_lo(w.w); x[7] = bf16_hi(w.w);
+  }
+  __device__ static void store(uint16_t* p, const float* x) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(bf16_pack(x[0], x[1]), bf16_pack(x[2], x[3]),
+                                              bf16_pack(x[4], x[5]), bf16_pack(x[6], x[7]));
+  }
+};
+
+// ------------------------------------------------------------------ cross-lane sums
+// All-reduce (sum) over aligned groups of `lanes` lanes (a power of two <= 64)
+// with DPP row operations and the gfx950 permlane swaps, no LDS traffic.
+// Every lane of a group ends with the bitwise-identical sum: each step adds
+// a lane's value to its partner's, and x + y == y + x exactly.
+__device__ __forceinline__ float dpp_quad_xor1(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float dpp_quad_xor2(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float dpp_row_half_mirror(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float dpp_row_mirror(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float sum_rows16(float x) {  // lanes l and l^16
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_halves32(float x) {  // lanes l and l^32
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float group_sum(float x, int lanes) {
+  if (lanes >= 2) x += dpp_quad_xor1(x);
+  if (lanes >= 4) x += dpp_quad_xor2(x);
+  if (lanes >= 8) x += dpp_row_half_mirror(x);
+  if (lanes >= 16) x += dpp_row_mirror(x);
+  if (lanes >= 32) x = sum_rows16(x);
+  if (lanes >= 64) x = sum_halves32(x);
+  return x;
+}
+
+__device__ __forceinline__ int64_t clamp64(int64_t x, int64_t lo, int64_t hi) {
+  return x < lo ? lo : (x > hi ? hi : x);
+}
+
+}  // namespace fast

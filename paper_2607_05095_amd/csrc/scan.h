@@ -1,0 +1,134 @@
+// scan.h -- device-wide exclusive scan over uint32 items (three launches:
+// per-tile reduce, one-block scan of the tile sums, per-tile down-sweep).
+// Item producers and prefix consumers are functors, so callers fuse their
+// own load (counts, bitmap popcounts, miss flags) and store (offsets, word
+// ranks, compaction scatter) into the scan's two passes over the data.
+#pragma once
+
+#include "common.h"
+
+namespace fast {
+
+constexpr int SCAN_THREADS = 256;
+constexpr int SCAN_ITEMS = 8;
+constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+
+inline int64_t scan_tiles(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE; }
+// Workspace of one scan over n items: the tile sums plus the total.
+inline size_t scan_workspace(int64_t n) {
+  return align_up(size_t(scan_tiles(n) + 1) * sizeof(uint32_t), 256);
+}
+
+// Exclusive prefix of a 256-thread block; returns the thread's exclusive
+// prefix and writes the block total.  Uses 4 words of LDS.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* lds4,
+                                                         uint32_t& total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) lds4[wid] = inc;
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < SCAN_THREADS / 64; ++w) {
+    uint32_t v = lds4[w];
+    before += (w < wid) ? v : 0u;
+    tot += v;
+  }
+  __syncthreads();
+  total = tot;
+  return before + inc - x;
+}
+
+template <class In>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(In in, int64_t n, uint32_t* tsum) {
+  __shared__ uint32_t lds4[4];
+  const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int64_t i = base + k * SCAN_THREADS + threadIdx.x;
+    if (i < n) s += in(i);
+  }
+  uint32_t total;
+  block_exclusive_scan(s, lds4, total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+
+// One 256-thread block scans the nt tile sums in place (exclusive) and
+// stores the grand total at tsum[nt] and into the optional outputs.
+template <int UNUSED = 0>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(uint32_t* tsum, int64_t nt,
+                                                           int64_t* total_i64,
+                                                           int32_t* total_i32) {
+  __shared__ uint32_t lds4[4];
+  uint32_t carry = 0;
+  for (int64_t b0 = 0; b0 < nt; b0 += SCAN_THREADS) {
+    const int64_t i = b0 + threadIdx.x;
+    const uint32_t x = (i < nt) ? tsum[i] : 0u;
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan(x, lds4, total);
+    if (i < nt) tsum[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) {
+    tsum[nt] = carry;
+    if (total_i64) *total_i64 = int64_t(carry);
+    if (total_i32) *total_i32 = int32_t(carry);
+  }
+}
+
+template <class In, class Out>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
+                                                            const uint32_t* tsum, Out out) {
+  __shared__ uint32_t tile[SCAN_TILE + SCAN_TILE / 32];
+  __shared__ uint32_t lds4[4];
+  const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
+  // striped, coalesced load into LDS (padded every 32 words against bank conflicts)
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int j = k * SCAN_THREADS + threadIdx.x;
+    const int64_t i = base + j;
+    tile[j + (j >> 5)] = (i < n) ? in(i) : 0u;
+  }
+  __syncthreads();
+  uint32_t v[SCAN_ITEMS], s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int j = threadIdx.x * SCAN_ITEMS + k;
+    v[k] = tile[j + (j >> 5)];
+    s += v[k];
+  }
+  uint32_t total;
+  uint32_t run = block_exclusive_scan(s, lds4, total) + tsum[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int64_t i = base + threadIdx.x * SCAN_ITEMS + k;
+    if (i < n) out(i, run, v[k]);
+    run += v[k];
+  }
+}
+
+// Enqueues the three launches.  ws must hold scan_workspace(n) bytes.
+// total_i64 / total_i32 (device, optional) receive the sum of all items.
+template <class In, class Out>
+hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
+                       int32_t* total_i32, hipStream_t st) {
+  uint32_t* tsum = static_cast<uint32_t*>(ws);
+  const int64_t nt = scan_tiles(n);
+  if (nt > 0) {
+    hipLaunchKernelGGL(k_scan_reduce<In>, dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n, tsum);
+  }
+  hipLaunchKernelGGL(k_scan_top<0>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, nt, total_i64, total_i32);
+  if (nt > 0) {
+    hipLaunchKernelGGL((k_scan_down<In, Out>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
+                       in, n, tsum, out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fast

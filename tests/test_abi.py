@@ -1,0 +1,134 @@
+"""The C ABI without a GPU: libfast.so loads, exports every function that
+include/fast.h declares, and rejects bad arguments on the host (before any
+launch) with the documented status codes and a message."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2607_05095_amd as fast
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fast.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = 0x10000  # a 256-byte aligned stand-in address; never dereferenced on these paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fast_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_operator_set():
+    names = declared_functions()
+    for n in ["fast_csr_offsets", "fast_dedup_gather", "fast_time_encode",
+              "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
+              "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
+              "fast_edge_attention_fwd", "fast_edge_attention_bwd", "fast_last_error"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = fast.lib()
+    missing = [n for n in declared_functions() if not hasattr(L, n)]
+    assert not missing, missing
+    out = subprocess.run(["nm", "-D", "--defined-only", fast.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (fast_[a-z0-9_]+)\b", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_library_is_built_for_gfx950_only():
+    out = subprocess.run(["/opt/rocm/bin/roc-obj-ls", fast.LIB_PATH], capture_output=True, text=True)
+    if out.returncode != 0:
+        pytest.skip("roc-obj-ls unavailable")
+    archs = set(re.findall(r"gfx\d+\w*", out.stdout))
+    assert archs == {"gfx950"}, archs
+
+
+def test_version():
+    assert "gfx950" in fast.fast_version()
+
+
+def _g(N=4, E=40, off=FAKE):
+    return fast.TCSR(N, E, off, None, FAKE, None, FAKE)
+
+
+def _attn_fwd(g, H=2, dh=50, dt=0, Q=FAKE, K=FAKE, V=FAKE, out=FAKE, lse=None):
+    gp = ctypes.byref(g) if g is not None else None
+    return fast.lib().fast_edge_attention_fwd(gp, H, dh, dt, Q, K, V, 1.0, 0.2, out, lse, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(g=None), INVALID),
+    (dict(g="negN"), INVALID),
+    (dict(H=0), INVALID),
+    (dict(dh=0), INVALID),
+    (dict(dt=7), INVALID),
+    (dict(Q=None), INVALID),
+    (dict(K=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(H=64, dh=128), UNSUPPORTED),        # H*dh > 4096
+    (dict(Q=FAKE + 2), UNSUPPORTED),          # fp32 row not 4-byte aligned
+    (dict(g="hugeE"), UNSUPPORTED),
+    (dict(g="edges_no_dst"), INVALID),
+    (dict(g="nullofs"), INVALID),
+])
+def test_attention_fwd_validation(kw, status):
+    g = kw.pop("g", "ok")
+    graph = {"ok": _g(), "negN": _g(N=-1), "hugeE": _g(E=1 << 31),
+             "edges_no_dst": _g(N=0, E=5), "nullofs": _g(off=None), None: None}[g]
+    st = _attn_fwd(graph, **kw)
+    assert st == status
+    assert fast.fast_last_error() != ""
+
+
+def test_empty_graph_is_a_no_op_without_launch():
+    # N = 0 returns before any HIP call, so it succeeds even with no GPU
+    assert _attn_fwd(_g(N=0, E=0), Q=None, K=None, V=None, out=None) == OK
+    assert fast.fast_last_error() == ""
+    L = fast.lib()
+    g = _g(N=0, E=0)
+    assert L.fast_time_encode(ctypes.byref(g), FAKE, FAKE, 100, FAKE, 0, None) == OK
+
+
+def test_other_entry_points_validate():
+    L = fast.lib()
+    g = _g()
+    gp = ctypes.byref(g)
+    assert L.fast_edge_attention_bwd(gp, 2, 50, 0, FAKE, FAKE, FAKE, 1.0, 0.2, None, FAKE,
+                                     FAKE, None, FAKE, None) == INVALID   # dK NULL
+    assert L.fast_edge_softmax_fwd(gp, 2, 50, 0, FAKE, FAKE, 1.0, 0.2, None, None, None) == INVALID
+    assert L.fast_edge_softmax_bwd(gp, 2, 50, 0, FAKE, FAKE, 1.0, 0.2, FAKE, None, FAKE, FAKE,
+                                   None) == INVALID
+    assert L.fast_temporal_aggregate_fwd(gp, 2, 50, 0, None, FAKE, FAKE, None) == INVALID
+    assert L.fast_temporal_aggregate_bwd(gp, 2, 50, 0, FAKE, FAKE, FAKE, None, FAKE, None) == INVALID
+    assert L.fast_time_encode(gp, FAKE, FAKE, 0, FAKE, 0, None) == INVALID       # d_t = 0
+    assert L.fast_time_encode(gp, None, FAKE, 100, FAKE, 0, None) == INVALID     # omega NULL
+    assert L.fast_time_encode(gp, FAKE, FAKE, 100, FAKE, 5, None) == INVALID     # dtype
+    assert L.fast_csr_offsets(FAKE, -1, FAKE, FAKE, 1 << 20, None) == INVALID
+    assert L.fast_csr_offsets(FAKE, 10, FAKE, FAKE, 4, None) == WORKSPACE
+    assert L.fast_csr_offsets(FAKE, 10, None, FAKE, 1 << 20, None) == INVALID
+
+
+def test_dedup_validation_and_workspace_query():
+    L = fast.lib()
+    ws = L.fast_dedup_gather_workspace(1000, 1 << 20)
+    assert ws >= (1 << 20) // 8 * 2          # bitmap + word ranks
+    assert L.fast_dedup_gather_workspace(1000, 1 << 36) == 0
+    args = lambda **k: [k.get("ids", FAKE), k.get("n", 1000), k.get("bound", 1 << 20),
+                        k.get("table", FAKE), k.get("rows_n", 1 << 20), 100, k.get("dt", 0),
+                        k.get("slot", None), FAKE, FAKE, k.get("nu", FAKE), k.get("rows", FAKE),
+                        None, None, FAKE, k.get("ws", ws), None]
+    assert L.fast_dedup_gather(*args(ws=ws - 1)) == WORKSPACE
+    assert L.fast_dedup_gather(*args(n=-1)) == INVALID
+    assert L.fast_dedup_gather(*args(nu=None)) == INVALID
+    assert L.fast_dedup_gather(*args(ids=None)) == INVALID
+    assert L.fast_dedup_gather(*args(dt=3)) == INVALID
+    assert L.fast_dedup_gather(*args(bound=1 << 36)) == UNSUPPORTED
+    assert L.fast_dedup_gather(*args(rows_n=10)) == INVALID      # no slot map, bound > rows
+    assert L.fast_dedup_gather(*args(table=None)) == INVALID     # rows wanted, no table

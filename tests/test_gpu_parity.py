@@ -1,0 +1,400 @@
+"""GPU parity: every operator through the C ABI against the fp64 CPU oracle.
+
+Workloads 0-2 are compared in full (they span many workgroups and end in a
+ragged tail); workloads 3 and 4 run at their full size in the launch
+configuration the benchmark times and are compared on sampled segments.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05095_amd as fast
+from synth import make_batch, make_block_operands, make_slot_map, make_table, omega_phi, tiny_graph
+from tests.parity import (SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks,
+                          sample_segments, sub_csr, tdtype, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+DT = {"f32": fast.F32, "bf16": fast.BF16}
+
+
+def _announce(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+# ------------------------------------------------------------------ device block
+class DevBlock:
+    """A layer block on the GPU: offsets from the oracle, timestamps, operands."""
+
+    def __init__(self, counts, dst_t, edge_t, ops, H, dh, dt):
+        self.counts = np.asarray(counts, dtype=np.int32)
+        self.off = oracle.csr_offsets(self.counts)
+        self.N, self.E = self.counts.shape[0], int(self.off[-1])
+        self.H, self.dh, self.dt = H, dh, dt
+        self.d_off = to_dev(self.off)
+        self.d_dst_t = to_dev(np.asarray(dst_t, dtype=np.float32))
+        self.d_edge_t = to_dev(np.asarray(edge_t, dtype=np.float32))
+        self.ops = {k: v.cuda() for k, v in ops.items()}
+        self.g = fast.tcsr(self.d_off, self.E, edge_t=self.d_edge_t, dst_t=self.d_dst_t)
+        self.scale = float(np.float32(1.0 / np.sqrt(dh)))
+
+    def empty(self, rows, dtype=None):
+        return torch.empty((rows, self.H, self.dh), dtype=dtype or tdtype(self.dt), device="cuda")
+
+    def scalars(self, rows):
+        return torch.empty((rows, self.H), dtype=torch.float32, device="cuda")
+
+
+def _block_from_batch(b, i):
+    blk = b.blocks[i]
+    ops = make_block_operands(b, i, device="cuda")
+    return DevBlock(blk.counts, blk.dst_t, blk.edge_t, ops, b.H, b.dh, b.dtype)
+
+
+def _host(t):
+    return t.detach().float().cpu().double().numpy()
+
+
+def _run_fused(d, with_lse=True):
+    o = d.ops
+    out = d.empty(d.N)
+    lse = d.scalars(d.N)
+    fast.fast_edge_attention_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, SLOPE,
+                                 out, lse)
+    dQ, dK, dV = d.empty(d.N), d.empty(d.E), d.empty(d.E)
+    fast.fast_edge_attention_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, SLOPE,
+                                 lse if with_lse else None, o["dO"], dQ, dK, dV)
+    return out, lse, dQ, dK, dV
+
+
+def _run_unfused(d):
+    o = d.ops
+    alpha, lse = d.scalars(d.E), d.scalars(d.N)
+    fast.fast_edge_softmax_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, SLOPE, alpha, lse)
+    out = d.empty(d.N)
+    fast.fast_temporal_aggregate_fwd(d.g, d.H, d.dh, DT[d.dt], alpha, o["V"], out)
+    dalpha, dV = d.scalars(d.E), d.empty(d.E)
+    fast.fast_temporal_aggregate_bwd(d.g, d.H, d.dh, DT[d.dt], alpha, o["V"], o["dO"], dalpha, dV)
+    dQ, dK = d.empty(d.N), d.empty(d.E)
+    fast.fast_edge_softmax_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, SLOPE, alpha,
+                               dalpha, dQ, dK)
+    return alpha, lse, out, dalpha, dV, dQ, dK
+
+
+def _check_block(d, segs=None, what=""):
+    """Fused and unfused operators vs the oracle on all (segs=None) or the
+    sampled segments."""
+    torch.cuda.synchronize()
+    fused = _run_fused(d, with_lse=True)
+    fused_nolse = _run_fused(d, with_lse=False)
+    unf = _run_unfused(d)
+    torch.cuda.synchronize()
+    if segs is None:
+        segs = np.arange(d.N, dtype=np.int64)
+    sub_off, eidx = sub_csr(d.off, segs)
+    Q = _host(d.ops["Q"][torch.as_tensor(segs, device="cuda")])
+    dO = _host(d.ops["dO"][torch.as_tensor(segs, device="cuda")])
+    ei = torch.as_tensor(eidx, device="cuda")
+    K = _host(d.ops["K"][ei])
+    V = _host(d.ops["V"][ei])
+    out, lse, alpha, _ = oracle.edge_attention_fwd(sub_off, Q, K, V, d.scale, SLOPE)
+    dalpha, _ = oracle.aggregate_bwd(sub_off, alpha, V, dO)
+    dQ, dK, dV, alts = bwd_reference_with_kinks(sub_off, Q, K, V, dO, d.scale, SLOPE)
+    sg = torch.as_tensor(segs, device="cuda")
+    nz = np.diff(sub_off) > 0
+    # forward
+    g_out, g_lse, g_dQ, g_dK, g_dV = fused
+    assert_close(g_out[sg], out, d.dt, what + " fused out")
+    assert_close(_host(g_lse[sg])[nz], lse[nz], "f32", what + " fused lse")
+    assert np.all(np.isneginf(_host(g_lse[sg])[~nz])), "empty segment lse must be -inf"
+    # fused backward, with and without the saved lse
+    for tag, (_, _, bdQ, bdK, bdV) in (("lse", fused), ("nolse", fused_nolse)):
+        assert_close(bdV[ei], dV, d.dt, f"{what} fused[{tag}] dV")
+        assert_bwd_close(bdQ[sg], bdK[ei], sub_off, dQ, dK, alts, d.dt, f"{what} fused[{tag}]")
+    # unfused chain
+    u_alpha, u_lse, u_out, u_dalpha, u_dV, u_dQ, u_dK = unf
+    assert_close(u_alpha[ei], alpha, "f32", what + " ESM alpha")
+    assert_close(_host(u_lse[sg])[nz], lse[nz], "f32", what + " ESM lse")
+    assert_close(u_out[sg], out, d.dt, what + " AGG out")
+    assert_close(u_dalpha[ei], dalpha, "f32", what + " AGG dalpha")
+    assert_close(u_dV[ei], dV, d.dt, what + " AGG dV")
+    assert_bwd_close(u_dQ[sg], u_dK[ei], sub_off, dQ, dK, alts, d.dt, what + " ESM-bwd")
+    return fused, unf
+
+
+# ------------------------------------------------------------------ attention: workloads
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_attention_small_workloads_full(cfg):
+    b = make_batch(cfg)
+    for i in range(len(b.blocks)):
+        _announce(f"attention cfg={cfg} block={i}")
+        d = _block_from_batch(b, i)
+        _check_block(d, None, f"cfg{cfg}/L{i + 1}")
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_attention_large_workloads_sampled(cfg):
+    b = make_batch(cfg)
+    for i in range(len(b.blocks)):
+        _announce(f"attention cfg={cfg} block={i} (full size, sampled segments)")
+        d = _block_from_batch(b, i)
+        segs = sample_segments(d.N, 1500, seed=cfg * 10 + i, include=[0, d.N - 1])
+        _check_block(d, segs, f"cfg{cfg}/L{i + 1}")
+        del d
+        torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ attention: edge cases
+def _synthetic_block(counts, H, dh, dt, seed=0):
+    blk = tiny_graph(counts, H=H, dh=dh, seed=seed + 1)
+    ops = make_block_operands((blk.num_dst, blk.num_edges), device="cuda", seed=seed,
+                              dtype=dt, H=H, dh=dh)
+    return DevBlock(blk.counts, blk.dst_t, blk.edge_t, ops, H, dh, dt)
+
+
+@pytest.mark.parametrize("name,counts,H,dh,dt", [
+    ("single_edge", [1], 2, 50, "f32"),
+    ("deg1_everywhere", [1] * 300, 2, 50, "f32"),
+    ("all_empty", [0] * 40, 2, 50, "f32"),
+    ("empties_mixed", [0, 3, 0, 0, 7, 1, 0, 12, 0], 2, 50, "f32"),
+    ("long_segments", [1000, 3, 25, 24, 23, 40, 8, 9, 17], 2, 50, "f32"),
+    ("long_bf16", [333, 20, 21, 1, 0, 64], 4, 32, "bf16"),
+    ("one_head", [5, 9, 2, 30], 1, 64, "f32"),
+    ("odd_dh", [4, 7, 11, 2], 3, 13, "f32"),
+    ("wide_dh_P4", [6, 3, 10], 2, 130, "f32"),
+    ("wide_dh_P2_bf16", [6, 3, 10], 2, 100, "bf16"),
+    ("many_heads", [8, 8, 3, 15], 16, 16, "f32"),
+    ("bf16_vec4", [5, 12, 1], 2, 36, "bf16"),
+    ("big_block_G", [4, 9], 8, 64, "f32"),
+])
+def test_attention_edge_cases(name, counts, H, dh, dt):
+    _announce(f"attention edge case {name}")
+    d = _synthetic_block(counts, H, dh, dt, seed=len(counts))
+    fused, unf = _check_block(d, None, name)
+    if name == "deg1_everywhere":
+        # a single-neighbour segment returns its value row exactly
+        assert torch.equal(fused[0], d.ops["V"])
+        assert torch.equal(unf[0], torch.ones_like(unf[0]))
+    if name == "all_empty":
+        assert torch.count_nonzero(fused[0]) == 0 and torch.count_nonzero(fused[2]) == 0
+
+
+def test_attention_empty_graph_and_zero_edges():
+    _announce("attention N=0")
+    d0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = fast.tcsr(d0, 0)
+    fast.fast_edge_attention_fwd(g, 2, 50, fast.F32, None, None, None, 0.1, SLOPE, None, None)
+    fast.fast_edge_attention_bwd(g, 2, 50, fast.F32, None, None, None, 0.1, SLOPE, None, None,
+                                 None, None, None)
+    torch.cuda.synchronize()
+
+
+def test_attention_run_to_run_bitwise_determinism():
+    _announce("attention determinism cfg=2")
+    b = make_batch(2)
+    d = _block_from_batch(b, 0)
+    r1 = _run_fused(d)
+    r2 = _run_fused(d)
+    torch.cuda.synchronize()
+    for x, y in zip(r1, r2):
+        assert torch.equal(x, y)
+
+
+def test_fused_equals_unfused_composition():
+    _announce("fused vs unfused cfg=1")
+    b = make_batch(1)
+    d = _block_from_batch(b, 0)
+    out, lse, dQ, dK, dV = _run_fused(d)
+    _, u_lse, u_out, _, u_dV, u_dQ, u_dK = _run_unfused(d)
+    torch.cuda.synchronize()
+    for a_, b_, n in ((out, u_out, "out"), (dV, u_dV, "dV"), (dQ, u_dQ, "dQ"), (dK, u_dK, "dK")):
+        assert_close(a_, _host(b_), "f32", f"fused vs unfused {n}")
+
+
+# ------------------------------------------------------------------ offsets (a1)
+@pytest.mark.parametrize("case", ["cfg0", "cfg2", "cfg3", "cfg4", "empty", "zeros", "ragged", "big"])
+def test_csr_offsets_bit_exact(case):
+    _announce(f"offsets {case}")
+    r = np.random.default_rng(1)
+    counts = {
+        "cfg0": lambda: make_batch(0).blocks[0].counts,
+        "cfg2": lambda: make_batch(2).blocks[0].counts,
+        "cfg3": lambda: make_batch(3).blocks[0].counts,
+        "cfg4": lambda: make_batch(4).blocks[0].counts,
+        "empty": lambda: np.zeros(0, np.int32),
+        "zeros": lambda: np.zeros(5000, np.int32),
+        "ragged": lambda: r.integers(0, 30, 2049 * 3 + 7).astype(np.int32),
+        "big": lambda: r.integers(0, 3, 3_000_001).astype(np.int32),
+    }[case]()
+    n = counts.shape[0]
+    d_counts = to_dev(counts) if n else torch.zeros(1, dtype=torch.int32, device="cuda")
+    off = torch.full((n + 1,), -7, dtype=torch.int32, device="cuda")
+    wsb = fast.fast_csr_offsets_workspace(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_csr_offsets(d_counts, n, off, ws, wsb)
+    assert np.array_equal(off.cpu().numpy(), oracle.csr_offsets(counts))
+
+
+# ------------------------------------------------------------------ dedup + gather (a2, a3)
+def _dedup(ids_np, id_bound, table=None, slot_map=None, want_miss=True):
+    n = ids_np.shape[0]
+    ids = to_dev(ids_np) if n else torch.zeros(1, dtype=torch.int64, device="cuda")
+    cap = max(n, 1)
+    uni = torch.full((cap,), -5, dtype=torch.int64, device="cuda")
+    inv = torch.full((cap,), -5, dtype=torch.int32, device="cuda")
+    nu = torch.full((1,), -1, dtype=torch.int64, device="cuda")
+    rows = None
+    D = 0
+    dt = fast.F32
+    if table is not None:
+        D = table.shape[1]
+        dt = fast.dtype_of(table)
+        rows = torch.zeros((cap, D), dtype=table.dtype, device="cuda")
+    miss = torch.full((cap,), -5, dtype=torch.int32, device="cuda") if want_miss else None
+    nm = torch.full((1,), -1, dtype=torch.int64, device="cuda")
+    wsb = fast.fast_dedup_gather_workspace(n, id_bound)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_dedup_gather(ids, n, id_bound, table, table.shape[0] if table is not None else 0, D,
+                           dt, slot_map, uni, inv, nu, rows, miss, nm, ws, wsb)
+    torch.cuda.synchronize()
+    u = int(nu.item())
+    return (uni[:u].cpu().numpy(), inv[:n].cpu().numpy(), u,
+            None if rows is None else rows[:u], None if miss is None else miss, int(nm.item()))
+
+
+def _bits(t):
+    """Raw bits of a device float tensor (bf16 via int16 view) as numpy."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy()
+    return t.view(torch.int32).cpu().numpy()
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_dedup_gather_workloads(cfg):
+    b = make_batch(cfg)
+    for kind, ids, bound, D, stream in (("node", b.node_ids, b.node_bound, b.node_D, 3),
+                                        ("edge", b.edge_ids, b.edge_bound, b.edge_D, 4)):
+        _announce(f"dedup cfg={cfg} {kind} n={ids.size} bound={bound}")
+        table = make_table(bound, D, b.dtype, device="cuda", seed=b.seed, stream=stream)
+        uni, inv, u, rows, miss, nm = _dedup(ids, bound, table)
+        ref_uni, ref_inv = oracle.dedup(ids)
+        assert u == ref_uni.size
+        assert np.array_equal(uni, ref_uni) and np.array_equal(inv, ref_inv)
+        assert nm == 0
+        ref_rows, hit, _ = oracle.gather(ref_uni, _bits(table))
+        assert hit.all()
+        assert np.array_equal(_bits(rows), ref_rows), "gathered rows differ"
+        del table
+        torch.cuda.empty_cache()
+
+
+def test_dedup_gather_bigdedup_slot_map():
+    b = make_batch(4)
+    _announce("dedup cfg=4 node ids over 1e7 with a 4 GB table")
+    table = make_table(b.node_bound, b.node_D, "f32", device="cuda", seed=b.seed, stream=3)
+    uni, inv, u, rows, miss, nm = _dedup(b.node_ids, b.node_bound, table)
+    ref_uni, ref_inv = oracle.dedup(b.node_ids)
+    assert u == ref_uni.size and np.array_equal(uni, ref_uni) and np.array_equal(inv, ref_inv)
+    ref_rows, _, _ = oracle.gather(ref_uni, _bits(table))
+    assert np.array_equal(_bits(rows), ref_rows)
+    del table, rows
+    torch.cuda.empty_cache()
+    _announce("dedup cfg=4 edge ids over 2e8 through a 2e6-row cache")
+    cache = make_table(b.edge_cache_rows, b.edge_D, "f32", device="cuda", seed=b.seed, stream=4)
+    sm = make_slot_map(b, device="cuda")
+    uni, inv, u, rows, miss, nm = _dedup(b.edge_ids, b.edge_bound, cache, slot_map=sm)
+    ref_uni, ref_inv = oracle.dedup(b.edge_ids)
+    assert u == ref_uni.size and np.array_equal(uni, ref_uni) and np.array_equal(inv, ref_inv)
+    ref_rows, hit, ref_miss = oracle.gather(ref_uni, _bits(cache), sm.cpu().numpy())
+    assert nm == ref_miss.size and np.array_equal(miss[:nm].cpu().numpy(), ref_miss)
+    assert 0 < nm < u
+    assert np.array_equal(_bits(rows)[hit], ref_rows[hit])
+
+
+@pytest.mark.parametrize("case", ["empty", "single", "allsame", "top_id", "bound_not_x32",
+                                  "bf16_odd_D", "dedup_only", "negative_and_oob"])
+def test_dedup_edge_cases(case):
+    _announce(f"dedup edge case {case}")
+    r = np.random.default_rng(2)
+    bound = 1000
+    ids = {
+        "empty": np.zeros(0, np.int64),
+        "single": np.array([17], np.int64),
+        "allsame": np.full(5000, 999, np.int64),
+        "top_id": np.array([999, 0, 999, 998, 31, 32, 33], np.int64),
+        "bound_not_x32": r.integers(0, 1000, 777).astype(np.int64),
+        "bf16_odd_D": r.integers(0, 1000, 3000).astype(np.int64),
+        "dedup_only": r.integers(0, 1000, 3000).astype(np.int64),
+        "negative_and_oob": np.array([5, -1, 7, 1000, 5, 123456, 7], np.int64),
+    }[case]
+    table = None
+    if case == "bf16_odd_D":
+        table = make_table(bound, 7, "bf16", device="cuda", seed=9)
+    elif case != "dedup_only":
+        table = make_table(bound, 12, "f32", device="cuda", seed=9)
+    uni, inv, u, rows, miss, nm = _dedup(ids, bound, table)
+    valid = (ids >= 0) & (ids < bound)
+    ref_uni, ref_inv = oracle.dedup(ids[valid])
+    assert u == ref_uni.size and np.array_equal(uni, ref_uni)
+    assert np.array_equal(inv[valid], ref_inv) and np.all(inv[~valid] == -1)
+    if table is not None:
+        ref_rows, _, _ = oracle.gather(ref_uni, _bits(table))
+        assert np.array_equal(_bits(rows), ref_rows)
+        assert nm == 0
+    else:
+        # no table: every distinct id is a miss (slot = id lies outside zero table rows)
+        assert nm == u and np.array_equal(miss[:nm].cpu().numpy(), np.arange(u))
+
+
+# ------------------------------------------------------------------ time encoding (a4)
+def _te_gpu(blk_off, dst_t, edge_t, omega, phi, dt="f32"):
+    E = edge_t.shape[0]
+    d_off, d_dst, d_e = to_dev(blk_off), to_dev(dst_t), to_dev(edge_t)
+    g = fast.tcsr(d_off, E, edge_t=d_e, dst_t=d_dst)
+    te = torch.empty((max(E, 1), omega.shape[0]), dtype=tdtype(dt), device="cuda")
+    fast.fast_time_encode(g, to_dev(omega), to_dev(phi), omega.shape[0], te, DT[dt])
+    torch.cuda.synchronize()
+    return te[:E]
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_time_encode_workloads(cfg):
+    b = make_batch(cfg)
+    om, ph = omega_phi(b.d_t)
+    for i, blk in enumerate(b.blocks):
+        _announce(f"time encode cfg={cfg} block={i} E={blk.num_edges} d_t={b.d_t} {b.dtype}")
+        off = oracle.csr_offsets(blk.counts)
+        te = _te_gpu(off, blk.dst_t, blk.edge_t, om, ph, b.dtype)
+        if blk.num_edges <= 200_000:
+            ref = oracle.time_encode(off, blk.dst_t, blk.edge_t, om, ph)
+            assert_close(te, ref, b.dtype, f"te cfg{cfg}/L{i + 1}")
+        else:
+            segs = sample_segments(blk.counts.shape[0], 3000, seed=cfg, include=[0, blk.counts.shape[0] - 1])
+            sub_off, eidx = sub_csr(off, segs)
+            ref = oracle.time_encode(sub_off, blk.dst_t[segs], blk.edge_t[eidx], om, ph)
+            assert_close(te[torch.as_tensor(eidx, device="cuda")], ref, b.dtype, f"te cfg{cfg}/L{i + 1}")
+
+
+@pytest.mark.parametrize("d_t,dt", [(1, "f32"), (7, "f32"), (6, "f32"), (100, "bf16"),
+                                    (3, "bf16"), (6, "bf16"), (128, "f32")])
+def test_time_encode_shapes_and_zero_dt(d_t, dt):
+    _announce(f"time encode d_t={d_t} {dt}")
+    blk = tiny_graph([0, 3, 0, 70, 1, 0, 130, 2], seed=d_t)
+    off = oracle.csr_offsets(blk.counts)
+    edge_t = blk.edge_t.copy()
+    seg = np.repeat(np.arange(blk.num_dst), blk.counts)
+    edge_t[::9] = blk.dst_t[seg[::9]]                  # dt = 0 rows
+    om, ph = omega_phi(d_t)
+    te = _te_gpu(off, blk.dst_t, edge_t, om, ph, dt)
+    ref = oracle.time_encode(off, blk.dst_t, edge_t, om, ph)
+    assert_close(te, ref, dt, f"te d_t={d_t}")
+    assert torch.all(te[::9].float() == 1.0)
+
+
+def test_time_encode_no_edges():
+    off = np.zeros(6, np.int32)
+    te = _te_gpu(off, np.ones(5, np.float32), np.zeros(0, np.float32), *omega_phi(10))
+    assert te.shape[0] == 0
