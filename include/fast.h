@@ -120,7 +120,8 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
  * Time encoding (Sec. 6.1: TGAT's random Fourier time features).
  *   te[e, j] = cos(fmaf(omega[j], dt_e, phi[j])),  dt_e = dst_t[v] - edge_t[e]
  * for e in segment v.  dt and the argument are fp32 (one subtraction, one
- * fused multiply-add); cos is the accurate device-library cosine.
+ * fused multiply-add); the cosine of that fp32 argument is accurate to about
+ * 1e-7 absolute (Cody-Waite reduction; library cosf beyond |arg| = 2^16).
  * Reads g->dst_offsets, g->dst_t, g->edge_t.  omega, phi: [d_t] fp32 device.
  * te: [E, d_t] of te_dtype.  d_t >= 1.
  * ------------------------------------------------------------------------ */
@@ -135,7 +136,8 @@ fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega, const f
  *   alpha[e,h] = exp(s - m) / Z,  m = max_{e in v} s,  Z = sum_{e in v} exp(s - m)
  *   lse[v,h]   = m + log Z  (-inf for an empty segment; lse may be NULL)
  * Q: [N,H,dh], K: [E,H,dh] of dtype.  alpha: [E,H] fp32.  Reads g->dst_offsets.
- * Supported: 1 <= H, 1 <= dh, H*dh <= 4096, dh <= 256 * (16 / element size).
+ * Supported: H >= 1, 1 <= dh <= 256, H*dh <= 4096; larger shapes return
+ * FAST_ERR_UNSUPPORTED.  Row pointers must be aligned to the element size.
  * ------------------------------------------------------------------------ */
 fast_status_t fast_edge_softmax_fwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
                                     const void* Q, const void* K, float scale,

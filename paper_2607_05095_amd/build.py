@@ -35,7 +35,8 @@ def sources():
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + COMMON + ["-c", src, "-o", obj]
+    extra = os.environ.get("FAST_HIPCC_FLAGS", "").split()   # e.g. -DFAST_ATT_CH=10
+    cmd = [HIPCC] + COMMON + extra + ["-c", src, "-o", obj]
     if src.endswith(".cpp"):
         cmd = [HIPCC, "-O2", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC, "-c", src, "-o", obj]
     if verbose:

@@ -1,0 +1,190 @@
+// attention_fused.hip -- fused edge softmax + aggregation forward/backward
+// (Sec. 4.3 operators in one pass; alpha never reaches memory), and the
+// host-side layout choice and validation shared with the unfused operators.
+#include <cstdlib>
+#include <type_traits>
+
+#include "attention.h"
+
+namespace fast {
+
+static int next_pow2(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Optional tuning override of the lanes per head (FAST_ATTN_LANES_PER_HEAD,
+// a power of two <= 64), read once; 0 = use the default rule.
+static int lanes_override() {
+  static const int v = [] {
+    const char* e = std::getenv("FAST_ATTN_LANES_PER_HEAD");
+    const int x = e ? std::atoi(e) : 0;
+    return (x > 0 && x <= 64 && (x & (x - 1)) == 0) ? x : 0;
+  }();
+  return v;
+}
+
+fast_status_t attn_layout(const char* fn, int H, int dh, fast_dtype_t dt, const void* const* rows,
+                          int nrows, AttnLayout& L) {
+  if (H < 1 || dh < 1) return fail(FAST_ERR_INVALID_ARG, "%s: H = %d, dh = %d", fn, H, dh);
+  if (int64_t(H) * dh > 4096) return fail(FAST_ERR_UNSUPPORTED, "%s: H*dh > 4096", fn);
+  const int esz = elem_size(dt);
+  for (int k = 0; k < nrows; ++k)
+    if (rows[k] && !aligned(rows[k], size_t(esz)))
+      return fail(FAST_ERR_UNSUPPORTED, "%s: operand %d is not %d-byte aligned", fn, k, esz);
+  const int cands_f32[] = {4, 2, 1};
+  const int cands_bf16[] = {8, 4, 2, 1};
+  const int* cands = dt == FAST_BF16 ? cands_bf16 : cands_f32;
+  const int nc = dt == FAST_BF16 ? 4 : 3;
+  int VE = 1;
+  for (int i = 0; i < nc; ++i) {
+    const int ve = cands[i];
+    if (dh % ve) continue;
+    bool al = true;
+    for (int k = 0; k < nrows; ++k)
+      if (rows[k] && !aligned(rows[k], size_t(ve) * esz)) al = false;
+    if (!al) continue;
+    if (ve > 1 && dh / ve > 64) continue;
+    VE = ve;
+    break;
+  }
+  const int CPH = dh / VE;
+  // Default: at most 16 lanes per head (fewer reduction steps and less
+  // per-lane repetition of the scalar softmax work), more chunks per lane;
+  // wider heads spread over up to 64 lanes with at most 4 chunks each.
+  int LPH = next_pow2(CPH < 16 ? CPH : 16);
+  int P = (CPH + LPH - 1) / LPH;
+  if (P > 2 && VE >= 4) {          // wide vectors: keep P <= 2, widen the group instead
+    LPH = next_pow2((CPH + 1) / 2);
+    P = (CPH + LPH - 1) / LPH;
+  }
+  while (P > 4 && LPH < 64) {
+    LPH *= 2;
+    P = (CPH + LPH - 1) / LPH;
+  }
+  if (P > 4) return fail(FAST_ERR_UNSUPPORTED, "%s: dh = %d too large for this dtype", fn, dh);
+  if (P == 3) P = 4;
+  if (const int o = lanes_override()) {
+    int p = (CPH + o - 1) / o;
+    if (p == 3) p = 4;
+    const bool have = p == 1 || ((p == 2 || p == 4) && VE <= 2) || (p == 2 && VE >= 4);
+    if (p <= 4 && have) {
+      LPH = o;
+      P = p;
+    }
+  }
+  const int G = H * LPH;
+  if (G > 1024) return fail(FAST_ERR_UNSUPPORTED, "%s: H * lanes-per-head = %d > 1024", fn, G);
+  L.H = H;
+  L.dh = dh;
+  L.F = H * dh;
+  L.VE = VE;
+  L.P = P;
+  L.CPH = CPH;
+  L.LPH = LPH;
+  L.G = G;
+  if (G <= ATT_BLOCK) {
+    L.block = ATT_BLOCK;
+    L.SPB = ATT_BLOCK / G;
+  } else {
+    L.block = (G + 63) / 64 * 64;
+    L.SPB = 1;
+  }
+  return FAST_OK;
+}
+
+fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int dh, fast_dtype_t dt,
+                       AttnArgs a, const void* const* rows, int nrows, fast_stream_t stream) {
+  if (!g) return fail(FAST_ERR_INVALID_ARG, "%s: graph is NULL", fn);
+  if (g->num_dst < 0 || g->num_edges < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
+  if (g->num_edges >= (int64_t(1) << 31)) return fail(FAST_ERR_UNSUPPORTED, "%s: E >= 2^31", fn);
+  if (g->num_dst >= (int64_t(1) << 31)) return fail(FAST_ERR_UNSUPPORTED, "%s: N >= 2^31", fn);
+  if (dt != FAST_F32 && dt != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
+  if (!(a.slope == a.slope) || !(a.scale == a.scale))
+    return fail(FAST_ERR_INVALID_ARG, "%s: NaN scale/slope", fn);
+  if (g->num_dst == 0 && g->num_edges > 0)
+    return fail(FAST_ERR_INVALID_ARG, "%s: E > 0 edges but no destination", fn);
+  fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, a.L);
+  if (s != FAST_OK) return s;
+  if (g->num_dst == 0) return ok();
+  if (!g->dst_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: dst_offsets is NULL", fn);
+  a.N = g->num_dst;
+  a.E = g->num_edges;
+  a.off = g->dst_offsets;
+  const int64_t nb = (a.N + a.L.SPB - 1) / a.L.SPB;
+  const dim3 grid{uint32_t(nb)}, block{uint32_t(a.L.block)};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool fused = op == Op::kAttnFwd || op == Op::kAttnBwd;
+  const bool done = fused ? attn_launch_fused(op, dt, a, grid, block, st)
+                          : attn_launch_unfused(op, dt, a, grid, block, st);
+  if (!done)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: no kernel for VE=%d P=%d LPH=%d", fn, a.L.VE, a.L.P, a.L.LPH);
+  return check_launch(fn);
+}
+
+template <typename T, int VE, int P, int LPH>
+static void launch_fused(Op op, const AttnArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+  if (op == Op::kAttnFwd) hipLaunchKernelGGL((k_attn_fwd<T, VE, P, LPH>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((k_attn_bwd<T, VE, P, LPH>), grid, block, 0, st, a);
+}
+
+bool attn_launch_fused(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
+                       hipStream_t st) {
+  const bool bf = dt == FAST_BF16;
+  const int VE = a.L.VE, P = a.L.P, LPH = a.L.LPH;
+#define FAST_TRY(T_, VE_, P_, L_)                                                     \
+  if (bf == std::is_same<T_, uint16_t>::value && VE == VE_ && P == P_ &&              \
+      (L_ == 0 || LPH == L_)) {                                                       \
+    launch_fused<T_, VE_, P_, L_>(op, a, grid, block, st);                            \
+    return true;                                                                      \
+  }
+  FAST_ATTN_FAST_SET(FAST_TRY)
+  FAST_ATTN_GENERIC_SET(FAST_TRY)
+#undef FAST_TRY
+  return false;
+}
+
+}  // namespace fast
+
+using namespace fast;
+
+#define FAST_NEED(ptr, fn)                                                               \
+  do {                                                                                   \
+    if (!(ptr)) return fail(FAST_ERR_INVALID_ARG, "%s: " #ptr " is NULL", fn);           \
+  } while (0)
+
+static bool has_work(const fast_tcsr_t* g) { return g && g->num_dst > 0; }
+
+extern "C" fast_status_t fast_edge_attention_fwd(const fast_tcsr_t* g, int H, int dh,
+                                                 fast_dtype_t dtype, const void* Q, const void* K,
+                                                 const void* V, float scale, float neg_slope,
+                                                 void* out, float* lse, fast_stream_t stream) {
+  const char* fn = "fast_edge_attention_fwd";
+  if (has_work(g)) {
+    FAST_NEED(Q, fn); FAST_NEED(out, fn);
+    if (g->num_edges > 0) { FAST_NEED(K, fn); FAST_NEED(V, fn); }
+  }
+  AttnArgs a = {};
+  a.scale = scale; a.slope = neg_slope;
+  a.Q = Q; a.K = K; a.V = V; a.out = out; a.lse_out = lse;
+  const void* rows[] = {Q, K, V, out};
+  return attn_run(fn, Op::kAttnFwd, g, H, dh, dtype, a, rows, 4, stream);
+}
+
+extern "C" fast_status_t fast_edge_attention_bwd(const fast_tcsr_t* g, int H, int dh,
+                                                 fast_dtype_t dtype, const void* Q, const void* K,
+                                                 const void* V, float scale, float neg_slope,
+                                                 const float* lse, const void* dout, void* dQ,
+                                                 void* dK, void* dV, fast_stream_t stream) {
+  const char* fn = "fast_edge_attention_bwd";
+  if (has_work(g)) {
+    FAST_NEED(Q, fn); FAST_NEED(dout, fn); FAST_NEED(dQ, fn);
+    if (g->num_edges > 0) { FAST_NEED(K, fn); FAST_NEED(V, fn); FAST_NEED(dK, fn); FAST_NEED(dV, fn); }
+  }
+  AttnArgs a = {};
+  a.scale = scale; a.slope = neg_slope;
+  a.Q = Q; a.K = K; a.V = V; a.dO = dout; a.lse_in = lse; a.dQ = dQ; a.dK = dK; a.dV = dV;
+  const void* rows[] = {Q, K, V, dout, dQ, dK, dV};
+  return attn_run(fn, Op::kAttnBwd, g, H, dh, dtype, a, rows, 7, stream);
+}

@@ -107,6 +107,55 @@ template <> struct VecIO<uint16_t, 8> {
   }
 };
 
+// Raw<T,VE>: the same VE elements kept packed in registers (bf16 pairs in one
+// 32-bit register) between the load and their first use, so that a chunk of
+// in-flight rows costs VE*sizeof(T)/4 registers per row, not VE.
+template <typename T, int VE> struct Raw;
+template <int VE> struct Raw<float, VE> {
+  float v[VE];
+  __device__ void load(const float* p) { VecIO<float, VE>::load(p, v); }
+  __device__ void unpack(float* x) const {
+#pragma unroll
+    for (int j = 0; j < VE; ++j) x[j] = v[j];
+  }
+  __device__ void zero() {
+#pragma unroll
+    for (int j = 0; j < VE; ++j) v[j] = 0.f;
+  }
+};
+template <> struct Raw<uint16_t, 1> {
+  uint32_t w;
+  __device__ void load(const uint16_t* p) { w = uint32_t(*p) << 16; }
+  __device__ void unpack(float* x) const { x[0] = __uint_as_float(w); }
+  __device__ void zero() { w = 0u; }
+};
+template <int VE> struct Raw<uint16_t, VE> {
+  static_assert(VE == 2 || VE == 4 || VE == 8, "bf16 vector of 2, 4 or 8");
+  uint32_t w[VE / 2];
+  __device__ void load(const uint16_t* p) {
+    if constexpr (VE == 2) {
+      w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (VE == 4) {
+      const uint2 t = *reinterpret_cast<const uint2*>(p);
+      w[0] = t.x; w[1] = t.y;
+    } else {
+      const uint4 t = *reinterpret_cast<const uint4*>(p);
+      w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
+    }
+  }
+  __device__ void unpack(float* x) const {
+#pragma unroll
+    for (int k = 0; k < VE / 2; ++k) {
+      x[2 * k] = bf16_lo(w[k]);
+      x[2 * k + 1] = bf16_hi(w[k]);
+    }
+  }
+  __device__ void zero() {
+#pragma unroll
+    for (int k = 0; k < VE / 2; ++k) w[k] = 0u;
+  }
+};
+
 // ------------------------------------------------------------------ cross-lane sums
 // All-reduce (sum) over aligned groups of `lanes` lanes (a power of two <= 64)
 // with DPP row operations and the gfx950 permlane swaps, no LDS traffic.

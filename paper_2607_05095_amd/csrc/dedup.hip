@@ -3,20 +3,43 @@
 // uni_ID / inv_Idx triple).
 //
 // MI355X design: ids live in a bounded universe [0, id_bound), so the sorted
-// distinct set is a bitmap over that universe.  Marking is one (checked)
-// atomicOr per id; the rank of an id is the exclusive popcount prefix of the
-// bitmap words below it plus a popcount inside its word.  This is exact and
-// deterministic whatever the id order or thread interleaving, costs
-// O(n + id_bound/32) work, and needs no sort.  Rows are then copied with
+// distinct set is a bitmap over that universe; the rank of an id is the
+// exclusive popcount prefix of the bitmap words below it plus a popcount
+// inside its word.  This is exact and deterministic whatever the id order or
+// thread interleaving, and needs no sort.  The bitmap is built one of two
+// ways, chosen from (n, id_bound) alone:
+//   * byte map (id_bound <= 32 n): every id stores 1 into its own byte with a
+//     plain store (racing stores of the same value are benign), then one
+//     pass packs 32 bytes into each bitmap word -- O(n + id_bound) bytes,
+//     no atomics at all;
+//   * hashed atomics (sparse universes): ids are merged per workgroup in an
+//     LDS hash table and each touched word gets one global atomicOr.  Rows are then copied with
 // 16/8/4-byte vector moves, one thread per vector of a row, from the table
 // slot that the optional cache slot map names.
+#include <cstdlib>
+#include <cstring>
+
 #include "scan.h"
 
 namespace fast {
 
 constexpr int DD_THREADS = 256;
 
+// Byte-map marking when the universe is at most this many times the batch.
+constexpr int64_t BYTEMAP_RATIO = 32;
+
+static bool use_bytemap(int64_t n, int64_t id_bound) {
+  static const int mode = [] {
+    const char* e = std::getenv("FAST_DEDUP_MARK");   // tuning override: bytemap | hash
+    if (!e) return 0;
+    return std::strcmp(e, "bytemap") == 0 ? 1 : std::strcmp(e, "hash") == 0 ? 2 : 0;
+  }();
+  if (mode) return mode == 1;
+  return id_bound <= BYTEMAP_RATIO * (n > 0 ? n : 1);
+}
+
 struct DedupWs {
+  uint8_t* bytemap;   // [32 W] (byte-map marking only)
   uint32_t* bitmap;   // [W]
   uint32_t* prefix;   // [W] exclusive popcount prefix per word
   void* scan_w;       // scan workspace over W words
@@ -32,12 +55,14 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     off += align_up(bytes, 256);
     return base ? base + o : nullptr;
   };
+  char* by = take(use_bytemap(n, id_bound) ? size_t(W) * 32 : 0);
   char* bm = take(size_t(W) * 4);
   char* pf = take(size_t(W) * 4);
   char* sw = take(scan_workspace(W));
   char* fl = take(size_t(n));
   char* sn = take(scan_workspace(n));
   if (ws) {
+    ws->bytemap = reinterpret_cast<uint8_t*>(by);
     ws->bitmap = reinterpret_cast<uint32_t*>(bm);
     ws->prefix = reinterpret_cast<uint32_t*>(pf);
     ws->scan_w = sw;
@@ -53,18 +78,83 @@ __global__ void __launch_bounds__(DD_THREADS) k_fill_u32(uint32_t* p, int64_t n,
     p[i] = v;
 }
 
-__global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __restrict__ ids,
-                                                           int64_t n, int64_t id_bound,
-                                                           uint32_t* bitmap) {
+__global__ void __launch_bounds__(DD_THREADS) k_fill_u128(uint4* p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * DD_THREADS)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+__global__ void __launch_bounds__(DD_THREADS) k_dedup_mark_bytes(const int64_t* __restrict__ ids,
+                                                                 int64_t n, int64_t id_bound,
+                                                                 uint8_t* bytemap) {
   const int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (i >= n) return;
   const int64_t id = ids[i];
-  if (id < 0 || id >= id_bound) return;
-  uint32_t* w = bitmap + (id >> 5);
-  const uint32_t bit = 1u << (id & 31);
-  // Zipf-hot ids repeat thousands of times: read first so that only the
-  // first few occurrences pay for an atomic on the hot word.
-  if ((__atomic_load_n(w, __ATOMIC_RELAXED) & bit) == 0) atomicOr(w, bit);
+  if (id >= 0 && id < id_bound) bytemap[id] = 1;
+}
+
+// bitmap word w <- bytes 32w .. 32w+31 of the byte map (each 0 or 1).
+__global__ void __launch_bounds__(DD_THREADS) k_dedup_pack(const uint4* __restrict__ bytemap,
+                                                           int64_t W, uint32_t* __restrict__ bitmap) {
+  const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
+  if (w >= W) return;
+  const uint4 a = bytemap[2 * w], b = bytemap[2 * w + 1];
+  const uint32_t q[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  uint32_t word = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    // bytes b0..b3 in {0,1} at bits 0,8,16,24 -> b0 | b1<<1 | b2<<2 | b3<<3 at bit 24
+    const uint32_t nib = ((q[k] & 0x01010101u) * 0x01020408u) >> 24;
+    word |= (nib & 0xfu) << (4 * k);
+  }
+  bitmap[w] = word;
+}
+
+// Marking: each workgroup takes MARK_ITEMS ids per thread and first merges
+// them in an LDS hash table keyed by bitmap word (open addressing, LDS
+// atomics), so a word receives at most one global atomicOr per workgroup.
+// Zipf-hot ids (the hottest is ~12% of a batch) would otherwise serialise
+// hundreds of thousands of atomics on one L2 address.
+constexpr int MARK_ITEMS = 8;
+constexpr int MARK_IDS = DD_THREADS * MARK_ITEMS;
+constexpr int MARK_SLOTS = 2 * MARK_IDS;        // load factor <= 1/2: probing always ends
+static_assert(MARK_SLOTS == 4096, "the hash below yields 12 bits");
+constexpr uint32_t MARK_EMPTY = 0xffffffffu;     // never a word index (W <= 2^30)
+
+__global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __restrict__ ids,
+                                                           int64_t n, int64_t id_bound,
+                                                           uint32_t* bitmap) {
+  __shared__ uint32_t keys[MARK_SLOTS];
+  __shared__ uint32_t bits[MARK_SLOTS];
+  for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
+    keys[s] = MARK_EMPTY;
+    bits[s] = 0u;
+  }
+  __syncthreads();
+  const int64_t base = int64_t(blockIdx.x) * MARK_IDS;
+#pragma unroll
+  for (int k = 0; k < MARK_ITEMS; ++k) {
+    const int64_t i = base + k * DD_THREADS + threadIdx.x;
+    if (i >= n) break;
+    const int64_t id = ids[i];
+    if (id < 0 || id >= id_bound) continue;
+    const uint32_t w = uint32_t(id >> 5);
+    const uint32_t bit = 1u << (id & 31);
+    uint32_t h = (w * 2654435761u) >> (32 - 12);     // Fibonacci hashing into 4096 slots
+    for (;;) {
+      const uint32_t prev = atomicCAS(&keys[h], MARK_EMPTY, w);
+      if (prev == MARK_EMPTY || prev == w) {
+        atomicOr(&bits[h], bit);
+        break;
+      }
+      h = (h + 1) & (MARK_SLOTS - 1);
+    }
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
+    const uint32_t w = keys[s];
+    if (w != MARK_EMPTY) atomicOr(bitmap + w, bits[s]);
+  }
 }
 
 struct InPopc {
@@ -109,8 +199,9 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restr
 }
 
 // Row copy: thread t of a block moves vector c of row k; a block covers
-// `rpb` consecutive rows of `cpr` vectors each.  Rows k >= *num_unique are
-// idle.  A slot outside [0, table_rows) flags k as a miss.
+// `rpb` consecutive rows of `cpr` vectors each and strides over row groups,
+// so the grid is sized for the machine, not for the worst-case n.  Rows
+// k >= *num_unique are idle.  A slot outside [0, table_rows) flags a miss.
 template <typename V>
 __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __restrict__ uni,
                                                             const int64_t* __restrict__ num_unique,
@@ -123,14 +214,13 @@ __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __res
   const int r = threadIdx.x / cpr;
   const int c = threadIdx.x - r * cpr;
   if (r >= rpb) return;
-  const int64_t k = int64_t(blockIdx.x) * rpb + r;
-  if (k >= u) return;
-  const int64_t id = uni[k];
-  const int64_t slot = slot_map ? int64_t(slot_map[id]) : id;
-  const bool hit = slot >= 0 && slot < table_rows;
-  if (c == 0 && flags) flags[k] = hit ? 0 : 1;
-  if (!hit || !rows) return;
-  rows[k * cpr + c] = table[slot * cpr + c];
+  for (int64_t k = int64_t(blockIdx.x) * rpb + r; k < u; k += int64_t(gridDim.x) * rpb) {
+    const int64_t id = uni[k];
+    const int64_t slot = slot_map ? int64_t(slot_map[id]) : id;
+    const bool hit = slot >= 0 && slot < table_rows;
+    if (c == 0 && flags) flags[k] = hit ? 0 : 1;
+    if (hit && rows) rows[k * cpr + c] = table[slot * cpr + c];
+  }
 }
 
 struct InFlags {
@@ -151,7 +241,8 @@ static void launch_gather(const int64_t* uni, const int64_t* num_unique, const v
                           void* rows, uint8_t* flags, int64_t cap, hipStream_t st) {
   const int cpr = int(row_bytes / int64_t(sizeof(V)));
   const int rpb = cpr >= DD_THREADS ? 1 : DD_THREADS / cpr;
-  const int64_t nb = (cap + rpb - 1) / rpb;
+  int64_t nb = (cap + rpb - 1) / rpb;
+  if (nb > 8192) nb = 8192;           // 32 workgroups per CU, striding over the rest
   if (nb == 0) return;
   if (cpr <= DD_THREADS) {
     hipLaunchKernelGGL(k_gather_rows<V>, dim3(uint32_t(nb)), dim3(DD_THREADS), 0, st, uni,
@@ -198,15 +289,31 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
   dedup_layout(n, id_bound, static_cast<char*>(ws), &w);
   const int64_t W = (id_bound + 31) / 32;
 
-  // 1. clear the bitmap, 2. mark ids
-  if (W > 0) {
-    const int64_t nb = (W + DD_THREADS - 1) / DD_THREADS;
-    hipLaunchKernelGGL(k_fill_u32, dim3(uint32_t(nb < 4096 ? nb : 4096)), dim3(DD_THREADS), 0, st,
-                       w.bitmap, W, 0u);
+  // 1. clear, 2. mark ids
+  if (use_bytemap(n, id_bound)) {
+    if (W > 0) {
+      const int64_t n16 = W * 2;        // 32 W bytes as 16-byte vectors
+      const int64_t nb = (n16 + DD_THREADS - 1) / DD_THREADS;
+      hipLaunchKernelGGL(k_fill_u128, dim3(uint32_t(nb < 8192 ? nb : 8192)), dim3(DD_THREADS), 0,
+                         st, reinterpret_cast<uint4*>(w.bytemap), n16);
+    }
+    if (n > 0)
+      hipLaunchKernelGGL(k_dedup_mark_bytes, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
+                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bytemap);
+    if (W > 0)
+      hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
+                         dim3(DD_THREADS), 0, st, reinterpret_cast<const uint4*>(w.bytemap), W,
+                         w.bitmap);
+  } else {
+    if (W > 0) {
+      const int64_t nb = (W + DD_THREADS - 1) / DD_THREADS;
+      hipLaunchKernelGGL(k_fill_u32, dim3(uint32_t(nb < 4096 ? nb : 4096)), dim3(DD_THREADS), 0,
+                         st, w.bitmap, W, 0u);
+    }
+    if (n > 0)
+      hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + MARK_IDS - 1) / MARK_IDS)),
+                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bitmap);
   }
-  if (n > 0)
-    hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bitmap);
   // 3. word ranks (exclusive popcount prefix) and u
   hipError_t e = scan_launch(InPopc{w.bitmap}, OutPrefix{w.prefix}, W, w.scan_w, num_unique,
                              nullptr, st);

@@ -2,70 +2,126 @@
 //   te[e, j] = cos(fmaf(omega[j], dst_t[v] - edge_t[e], phi[j])),  e in segment v.
 //
 // The op writes E*d_t values from 8 bytes of input per edge, so it is bound by
-// HBM writes and by the cosine.  A workgroup owns TE_ROWS consecutive edges:
-// it locates their segments with two binary searches over the offsets (one
-// per block end) and a short search per row inside that range, stages the
-// per-edge dt in LDS, and then streams the [TE_ROWS, d_t] tile out with
-// 16-byte stores.  The cosine is the accurate device-library cosf (its
-// argument reaches |omega*dt| ~ 1e4 rad, where a hardware sine without a
-// full range reduction would lose the 1e-5 target).
+// HBM writes and by the cosine.  A workgroup owns TE_SEGS consecutive
+// destination segments: it loads their offsets and times into LDS with one
+// coalesced access, then walks the segments' edges in tiles of rows: each
+// row finds its segment by a short binary search in LDS and stages dt in LDS,
+// and the [rows, d_t] tile is streamed out with 16-byte stores.
+//
+// The argument reaches |omega*dt| ~ 1e4 rad, where the hardware sine (no
+// full range reduction) would lose the 1e-5 target and the device library's
+// general cosf spends most of the op's time.  cos_cw below is a Cody-Waite
+// reduction (W. J. Cody and W. Waite, "Software Manual for the Elementary
+// Functions", 1980): x = k*pi/2 + r with pi/2 split into three fp32 parts
+// C1 + C2 + C3 (each the fp32 rounding of what remained of pi/2, derived
+// exactly from Machin's formula for pi), every step one fused multiply-add,
+// followed by the Taylor polynomials of cos and sin on |r| <= pi/4 (truncation
+// below 3e-8).  Absolute error is about 1e-7 for |x| <= 2^16; larger
+// arguments take the library cosf.
 #include "common.h"
 
 namespace fast {
 
 constexpr int TE_THREADS = 256;
-constexpr int TE_ROWS = 64;
+constexpr int TE_SEGS = 32;      // destination segments per workgroup
+constexpr int TE_TILE_MAX = 256; // rows staged per tile (at most)
 
-// Largest s in [lo, hi] with off[s] <= e (the segment holding edge e).
-__device__ __forceinline__ int64_t seg_of(const int32_t* __restrict__ off, int64_t e,
-                                          int64_t lo, int64_t hi) {
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (int64_t(off[mid]) <= e) lo = mid; else hi = mid - 1;
-  }
-  return lo;
+__device__ __forceinline__ float cos_cw(float x) {
+  if (!(fabsf(x) <= 65536.f)) return cosf(x);     // also NaN and +-inf
+  const float C1 = 0x1.921fb6p+0f, C2 = -0x1.777a5cp-25f, C3 = -0x1.ee59dap-50f;
+  const float TWO_OVER_PI = 0x1.45f306p-1f;
+  const float k = rintf(x * TWO_OVER_PI);
+  float r = fmaf(-k, C1, x);
+  r = fmaf(-k, C2, r);
+  r = fmaf(-k, C3, r);
+  const float r2 = r * r;
+  // cos r = 1 - r^2/2! + r^4/4! - r^6/6! + r^8/8!
+  float c = fmaf(r2, 1.f / 40320.f, -1.f / 720.f);
+  c = fmaf(c, r2, 1.f / 24.f);
+  c = fmaf(c, r2, -0.5f);
+  c = fmaf(c, r2, 1.f);
+  // sin r = r - r^3/3! + r^5/5! - r^7/7! + r^9/9!
+  float p = fmaf(r2, 1.f / 362880.f, -1.f / 5040.f);
+  p = fmaf(p, r2, 1.f / 120.f);
+  p = fmaf(p, r2, -1.f / 6.f);
+  const float s = fmaf(r * r2, p, r);
+  const int q = int(k) & 3;                         // quadrant of x
+  const float v = (q & 1) ? s : c;                  // q: 0 cos r, 1 -sin r, 2 -cos r, 3 sin r
+  return ((q + 1) & 2) ? -v : v;
 }
 
+// Thread t owns the column chunk t % cpr of rows t / cpr, t / cpr + rpp, ...
+// (rpp = rows per pass), so omega and phi of its columns stay in registers.
 template <typename TO, int VEC>
 __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
     const int32_t* __restrict__ off, int64_t N, int64_t E, const float* __restrict__ dst_t,
     const float* __restrict__ edge_t, const float* __restrict__ omega,
     const float* __restrict__ phi, int d_t, TO* __restrict__ te) {
-  __shared__ float s_dt[TE_ROWS];
-  __shared__ int64_t s_rng[2];
-  const int64_t r0 = int64_t(blockIdx.x) * TE_ROWS;
-  const int nrows = int(E - r0 < TE_ROWS ? E - r0 : TE_ROWS);
-  if (threadIdx.x < 2) {
-    const int64_t e = r0 + (threadIdx.x == 0 ? 0 : nrows - 1);
-    s_rng[threadIdx.x] = seg_of(off, e, 0, N - 1);
-  }
+  __shared__ int64_t s_off[TE_SEGS + 1];
+  __shared__ float s_tdst[TE_SEGS];
+  __shared__ float s_dt[TE_TILE_MAX];
+  const int64_t s0 = int64_t(blockIdx.x) * TE_SEGS;
+  const int ns = int(N - s0 < TE_SEGS ? N - s0 : TE_SEGS);
+  if (threadIdx.x <= ns) s_off[threadIdx.x] = clamp64(off[s0 + threadIdx.x], 0, E);
+  if (threadIdx.x < ns) s_tdst[threadIdx.x] = dst_t[s0 + threadIdx.x];
   __syncthreads();
-  if (threadIdx.x < nrows) {
-    const int64_t e = r0 + threadIdx.x;
-    const int64_t s = seg_of(off, e, s_rng[0], s_rng[1] < s_rng[0] ? s_rng[0] : s_rng[1]);
-    s_dt[threadIdx.x] = dst_t[s] - edge_t[e];
-  }
-  __syncthreads();
-  const int cpr = d_t / VEC;
-  const int total = nrows * cpr;
-  for (int idx = threadIdx.x; idx < total; idx += TE_THREADS) {
-    const int row = idx / cpr;
-    const int c = idx - row * cpr;
-    const float dt = s_dt[row];
-    float o[VEC];
+  const int64_t r0 = s_off[0], r1 = s_off[ns];
+
+  const int cpr = d_t / VEC;                       // vector chunks per row
+  const bool narrow = cpr <= TE_THREADS;
+  const int rpp = narrow ? TE_THREADS / cpr : 1;   // rows per pass
+  const int rsub = narrow ? int(threadIdx.x) / cpr : 0;
+  const int c0 = narrow ? int(threadIdx.x) - rsub * cpr : int(threadIdx.x);
+  const int tile = rpp * 8 < TE_TILE_MAX ? rpp * 8 : TE_TILE_MAX;
+  float om[VEC], ph[VEC];
+  if (narrow && rsub < rpp) {
 #pragma unroll
     for (int k = 0; k < VEC; ++k) {
-      const int j = c * VEC + k;
-      o[k] = cosf(fmaf(omega[j], dt, phi[j]));
+      om[k] = omega[c0 * VEC + k];
+      ph[k] = phi[c0 * VEC + k];
     }
-    VecIO<TO, VEC>::store(te + (r0 + row) * d_t + c * VEC, o);
+  }
+  for (int64_t t0 = r0; t0 < r1; t0 += tile) {
+    const int nrows = int(r1 - t0 < tile ? r1 - t0 : tile);
+    if (threadIdx.x < nrows) {
+      const int64_t e = t0 + threadIdx.x;
+      int lo = 0, hi = ns - 1;          // last local segment with s_off <= e
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_off[mid] <= e) lo = mid; else hi = mid - 1;
+      }
+      s_dt[threadIdx.x] = s_tdst[lo] - edge_t[e];
+    }
+    __syncthreads();
+    if (narrow) {
+      if (rsub < rpp) {
+        for (int row = rsub; row < nrows; row += rpp) {
+          const float dt = s_dt[row];
+          float o[VEC];
+#pragma unroll
+          for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(om[k], dt, ph[k]));
+          VecIO<TO, VEC>::store(te + (t0 + row) * d_t + c0 * VEC, o);
+        }
+      }
+    } else {                            // very wide rows: stride over the columns
+      for (int row = 0; row < nrows; ++row) {
+        const float dt = s_dt[row];
+        for (int c = c0; c < cpr; c += TE_THREADS) {
+          float o[VEC];
+#pragma unroll
+          for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(omega[c * VEC + k], dt, phi[c * VEC + k]));
+          VecIO<TO, VEC>::store(te + (t0 + row) * d_t + c * VEC, o);
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
 template <typename TO, int VEC>
 static void launch_te(const fast_tcsr_t* g, const float* omega, const float* phi, int d_t,
                       void* te, hipStream_t st) {
-  const int64_t nb = (g->num_edges + TE_ROWS - 1) / TE_ROWS;
+  const int64_t nb = (g->num_dst + TE_SEGS - 1) / TE_SEGS;
   hipLaunchKernelGGL((k_time_encode<TO, VEC>), dim3(uint32_t(nb)), dim3(TE_THREADS), 0, st,
                      g->dst_offsets, g->num_dst, g->num_edges, g->dst_t, g->edge_t, omega, phi,
                      d_t, static_cast<TO*>(te));

@@ -398,3 +398,20 @@ def test_time_encode_no_edges():
     off = np.zeros(6, np.int32)
     te = _te_gpu(off, np.ones(5, np.float32), np.zeros(0, np.float32), *omega_phi(10))
     assert te.shape[0] == 0
+
+
+def test_time_encode_cosine_accuracy_sweep():
+    # one destination per edge with dst_t = dt and edge_t = 0, so dt is exact;
+    # omega = 1 makes the argument dt itself (plus a phase-shifted column)
+    _announce("time encode cosine sweep")
+    r = np.random.default_rng(5)
+    n = 400_000
+    dt = np.concatenate([r.uniform(0, 1e4, n // 2), r.uniform(1e4, 2e5, n // 4),
+                         np.linspace(0, 20, n // 8), r.uniform(65000, 66000, n // 8)]).astype(np.float32)
+    off = np.arange(dt.size + 1, dtype=np.int32)
+    om = np.array([1.0, 1.0, 0.37], dtype=np.float32)
+    ph = np.array([0.0, np.float32(np.pi / 2), -1.25], dtype=np.float32)
+    te = _te_gpu(off, dt, np.zeros(dt.size, np.float32), om, ph)
+    ref = oracle.time_encode(off, dt, np.zeros(dt.size, np.float32), om, ph)
+    err = np.abs(te.cpu().numpy().astype(np.float64) - ref)
+    assert err.max() <= 3e-7, f"max cosine error {err.max():.3g}"
