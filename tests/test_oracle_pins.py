@@ -387,3 +387,16 @@ def test_branch_override():
     dQs, _ = oracle.edge_softmax_bwd(off, Q, K, 0.5 * SLOPE, 1.0, alpha, da)
     # r = slope everywhere equals (scale*slope) with r = 1, since g = ds*r*scale
     np.testing.assert_allclose(dQ2, dQs, rtol=1e-13, atol=1e-15)
+
+
+# ---------------------------------------------------------------- regression fixture
+def test_oracle_matches_stored_regression_fixture():
+    import json, os
+    from tests.golden import make_golden as mg
+    with open(os.path.join(os.path.dirname(mg.__file__), "tiny_oracle.json")) as f:
+        stored = json.load(f)
+    got = mg.outputs(mg.inputs())
+    for k, v in stored.items():
+        a, b = np.asarray(got[k], dtype=np.float64), np.asarray(v, dtype=np.float64)
+        assert a.shape == b.shape, k
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-14, err_msg=k)
