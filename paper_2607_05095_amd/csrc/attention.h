@@ -60,6 +60,7 @@ struct AttnLayout {
   int G;          // lanes per segment = H * LPH
   int SPB;        // segments per workgroup
   int block;      // workgroup size
+  bool nt;        // streamed rows cover whole cache lines: non-temporal policy
 };
 
 struct AttnArgs {
@@ -127,12 +128,12 @@ __device__ __forceinline__ void load_row(const T* __restrict__ base, int64_t row
   }
 }
 
-template <typename T, int VE, int P>
+template <typename T, int VE, int P, bool NT>
 __device__ __forceinline__ void load_raw(const T* __restrict__ base, int64_t row, int F,
                                          const LaneMap<P>& m, Raw<T, VE> (&x)[P]) {
 #pragma unroll
   for (int p = 0; p < P; ++p) {
-    if (m.cok[p]) x[p].load(base + row * F + m.foff[p]);
+    if (m.cok[p]) x[p].template load<NT>(base + row * F + m.foff[p]);
     else x[p].zero();
   }
 }
@@ -149,6 +150,14 @@ __device__ __forceinline__ void store_row(T* __restrict__ base, int64_t row, int
 #pragma unroll
   for (int p = 0; p < P; ++p)
     if (m.cok[p]) VecIO<T, VE>::store(base + row * F + m.foff[p], x[p]);
+}
+
+template <typename T, int VE, int P, bool NT>
+__device__ __forceinline__ void store_row_stream(T* __restrict__ base, int64_t row, int F,
+                                                 const LaneMap<P>& m, const float (&x)[P][VE]) {
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (m.cok[p]) StreamIO<T, VE, NT>::store(base + row * F + m.foff[p], x[p]);
 }
 
 template <int LPH>
@@ -196,7 +205,7 @@ __device__ __forceinline__ int64_t slot_row(int64_t base, int i, int64_t e1) {
       _Pragma("unroll") for (int j_ = 0; j_ < VE; ++j_) arr[p_][j_] = 0.f
 
 // ============================================================ fused forward
-template <typename T, int VE, int P, int LPH_CT>
+template <typename T, int VE, int P, int LPH_CT, bool NT>
 __global__ void __launch_bounds__(ATT_BLOCK) k_attn_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
@@ -216,8 +225,8 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_attn_fwd(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < ATT_CH_FWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      load_raw<T, VE, P>(K, e, F, m, kr[i]);
-      load_raw<T, VE, P>(V, e, F, m, vr[i]);
+      load_raw<T, VE, P, NT>(K, e, F, m, kr[i]);
+      load_raw<T, VE, P, NT>(V, e, F, m, vr[i]);
     }
     float t[ATT_CH_FWD];
     float cm = -INFINITY;
@@ -269,7 +278,7 @@ struct BwdState {
 
 // Edges [base, min(base+CH, e1)): loads K and V, forms t (log2-unit logit)
 // and dalpha = <dOut, V>, and folds them into the running sums.
-template <typename T, int VE, int P, int LPH_CT>
+template <typename T, int VE, int P, int LPH_CT, bool NT>
 __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m, int64_t base,
                                           int64_t e1, bool has_lse, float sl2,
                                           BwdState<VE, P>& S, float (&t)[ATT_CH_BWD],
@@ -281,8 +290,8 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
 #pragma unroll
   for (int i = 0; i < ATT_CH_BWD; ++i) {
     const int64_t e = slot_row(base, i, e1);
-    load_raw<T, VE, P>(K, e, F, m, kr[i]);
-    load_raw<T, VE, P>(V, e, F, m, vr[i]);
+    load_raw<T, VE, P, NT>(K, e, F, m, kr[i]);
+    load_raw<T, VE, P, NT>(V, e, F, m, vr[i]);
   }
   float cm = -INFINITY;
 #pragma unroll
@@ -328,7 +337,7 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
   }
 }
 
-template <typename T, int VE, int P>
+template <typename T, int VE, int P, bool NT>
 __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m, int64_t e, float t,
                                          float da, float invZ, float D, const BwdState<VE, P>& S) {
   const float al = exp2_hw(t - S.mx) * invZ;
@@ -341,11 +350,11 @@ __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m,
       dk[p][j] = g * S.q[p][j];
       dv[p][j] = al * S.go[p][j];
     }
-  store_row<T, VE, P>(static_cast<T*>(a.dK), e, a.L.F, m, dk);
-  store_row<T, VE, P>(static_cast<T*>(a.dV), e, a.L.F, m, dv);
+  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dK), e, a.L.F, m, dk);
+  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dV), e, a.L.F, m, dv);
 }
 
-template <typename T, int VE, int P, int LPH_CT>
+template <typename T, int VE, int P, int LPH_CT, bool NT>
 __global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
@@ -369,11 +378,11 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < ATT_NSAVE; ++c) {
     const int64_t base = e0 + c * ATT_CH_BWD;
-    if (base < e1) bwd_chunk<T, VE, P, LPH_CT>(a, m, base, e1, has_lse, sl2, S, st[c], sda[c]);
+    if (base < e1) bwd_chunk<T, VE, P, LPH_CT, NT>(a, m, base, e1, has_lse, sl2, S, st[c], sda[c]);
   }
   for (int64_t base = e0 + ATT_NSAVE * ATT_CH_BWD; base < e1; base += ATT_CH_BWD) {
     float tt[ATT_CH_BWD], td[ATT_CH_BWD];
-    bwd_chunk<T, VE, P, LPH_CT>(a, m, base, e1, has_lse, sl2, S, tt, td);
+    bwd_chunk<T, VE, P, LPH_CT, NT>(a, m, base, e1, has_lse, sl2, S, tt, td);
   }
 
   // dQ = scale/Z * (A - D B)
@@ -393,7 +402,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
     const int64_t base = e0 + c * ATT_CH_BWD;
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i)
-      if (base + i < e1) bwd_emit<T, VE, P>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
+      if (base + i < e1) bwd_emit<T, VE, P, NT>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
   }
   // long segments: re-read K and V for the edges past the register window
   for (int64_t base = e0 + ATT_NSAVE * ATT_CH_BWD; base < e1; base += ATT_CH_BWD) {
@@ -408,7 +417,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
     for (int i = 0; i < ATT_CH_BWD; ++i) {
       const float t = lrelu(head_dot<VE, P, LPH_CT>(S.q, kx[i], m.lph) * sl2, a.slope);
       const float da = head_dot<VE, P, LPH_CT>(S.go, vx[i], m.lph);
-      if (base + i < e1) bwd_emit<T, VE, P>(a, m, base + i, t, da, invZ, D, S);
+      if (base + i < e1) bwd_emit<T, VE, P, NT>(a, m, base + i, t, da, invZ, D, S);
     }
   }
 }

@@ -107,6 +107,11 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
     return fail(FAST_ERR_INVALID_ARG, "%s: E > 0 edges but no destination", fn);
   fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, a.L);
   if (s != FAST_OK) return s;
+  // Non-temporal streaming only when every per-edge row starts and ends on a
+  // cache line, so no two rows share a line.
+  a.L.nt = (size_t(a.L.F) * elem_size(dt)) % CACHE_LINE == 0;
+  for (const void* p : {a.K, a.V, static_cast<const void*>(a.dK), static_cast<const void*>(a.dV)})
+    if (p && !aligned(p, CACHE_LINE)) a.L.nt = false;
   if (g->num_dst == 0) return ok();
   if (!g->dst_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: dst_offsets is NULL", fn);
   a.N = g->num_dst;
@@ -123,10 +128,16 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
   return check_launch(fn);
 }
 
+template <typename T, int VE, int P, int LPH, bool NT>
+static void launch_fused_nt(Op op, const AttnArgs& a, dim3 grid, dim3 block, hipStream_t st) {
+  if (op == Op::kAttnFwd) hipLaunchKernelGGL((k_attn_fwd<T, VE, P, LPH, NT>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((k_attn_bwd<T, VE, P, LPH, NT>), grid, block, 0, st, a);
+}
+
 template <typename T, int VE, int P, int LPH>
 static void launch_fused(Op op, const AttnArgs& a, dim3 grid, dim3 block, hipStream_t st) {
-  if (op == Op::kAttnFwd) hipLaunchKernelGGL((k_attn_fwd<T, VE, P, LPH>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((k_attn_bwd<T, VE, P, LPH>), grid, block, 0, st, a);
+  if (a.L.nt) launch_fused_nt<T, VE, P, LPH, true>(op, a, grid, block, st);
+  else launch_fused_nt<T, VE, P, LPH, false>(op, a, grid, block, st);
 }
 
 bool attn_launch_fused(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,

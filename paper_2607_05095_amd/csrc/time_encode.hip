@@ -52,7 +52,7 @@ __device__ __forceinline__ float cos_cw(float x) {
 
 // Thread t owns the column chunk t % cpr of rows t / cpr, t / cpr + rpp, ...
 // (rpp = rows per pass), so omega and phi of its columns stay in registers.
-template <typename TO, int VEC>
+template <typename TO, int VEC, bool NT>
 __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
     const int32_t* __restrict__ off, int64_t N, int64_t E, const float* __restrict__ dst_t,
     const float* __restrict__ edge_t, const float* __restrict__ omega,
@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
           float o[VEC];
 #pragma unroll
           for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(om[k], dt, ph[k]));
-          VecIO<TO, VEC>::store(te + (t0 + row) * d_t + c0 * VEC, o);
+          StreamIO<TO, VEC, NT>::store(te + (t0 + row) * d_t + c0 * VEC, o);
         }
       }
     } else {                            // very wide rows: stride over the columns
@@ -110,7 +110,7 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
           float o[VEC];
 #pragma unroll
           for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(omega[c * VEC + k], dt, phi[c * VEC + k]));
-          VecIO<TO, VEC>::store(te + (t0 + row) * d_t + c * VEC, o);
+          StreamIO<TO, VEC, NT>::store(te + (t0 + row) * d_t + c * VEC, o);
         }
       }
     }
@@ -122,9 +122,16 @@ template <typename TO, int VEC>
 static void launch_te(const fast_tcsr_t* g, const float* omega, const float* phi, int d_t,
                       void* te, hipStream_t st) {
   const int64_t nb = (g->num_dst + TE_SEGS - 1) / TE_SEGS;
-  hipLaunchKernelGGL((k_time_encode<TO, VEC>), dim3(uint32_t(nb)), dim3(TE_THREADS), 0, st,
-                     g->dst_offsets, g->num_dst, g->num_edges, g->dst_t, g->edge_t, omega, phi,
-                     d_t, static_cast<TO*>(te));
+  // streaming stores only when each output row covers whole cache lines
+  const bool nt = (size_t(d_t) * sizeof(TO)) % CACHE_LINE == 0 && aligned(te, CACHE_LINE);
+  if (nt)
+    hipLaunchKernelGGL((k_time_encode<TO, VEC, true>), dim3(uint32_t(nb)), dim3(TE_THREADS), 0, st,
+                       g->dst_offsets, g->num_dst, g->num_edges, g->dst_t, g->edge_t, omega, phi,
+                       d_t, static_cast<TO*>(te));
+  else
+    hipLaunchKernelGGL((k_time_encode<TO, VEC, false>), dim3(uint32_t(nb)), dim3(TE_THREADS), 0, st,
+                       g->dst_offsets, g->num_dst, g->num_edges, g->dst_t, g->edge_t, omega, phi,
+                       d_t, static_cast<TO*>(te));
 }
 
 }  // namespace fast
