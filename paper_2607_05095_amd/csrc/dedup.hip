@@ -38,10 +38,12 @@ static bool use_bytemap(int64_t n, int64_t id_bound) {
   return id_bound <= BYTEMAP_RATIO * (n > 0 ? n : 1);
 }
 
+// Word record w: .x = bits of ids 32w .. 32w+31, .y = number of set bits in
+// all words before w (the rank of the word's first id).  Keeping both in one
+// 8-byte record makes the inverse lookup of an id a single random load.
 struct DedupWs {
   uint8_t* bytemap;   // [32 W] (byte-map marking only)
-  uint32_t* bitmap;   // [W]
-  uint32_t* prefix;   // [W] exclusive popcount prefix per word
+  uint2* words;       // [W] word records
   void* scan_w;       // scan workspace over W words
   uint8_t* flags;     // [n] miss flags
   void* scan_n;       // scan workspace over n flags
@@ -56,15 +58,13 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     return base ? base + o : nullptr;
   };
   char* by = take(use_bytemap(n, id_bound) ? size_t(W) * 32 : 0);
-  char* bm = take(size_t(W) * 4);
-  char* pf = take(size_t(W) * 4);
+  char* wr = take(size_t(W) * 8);
   char* sw = take(scan_workspace(W));
   char* fl = take(size_t(n));
   char* sn = take(scan_workspace(n));
   if (ws) {
     ws->bytemap = reinterpret_cast<uint8_t*>(by);
-    ws->bitmap = reinterpret_cast<uint32_t*>(bm);
-    ws->prefix = reinterpret_cast<uint32_t*>(pf);
+    ws->words = reinterpret_cast<uint2*>(wr);
     ws->scan_w = sw;
     ws->flags = reinterpret_cast<uint8_t*>(fl);
     ws->scan_n = sn;
@@ -95,7 +95,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark_bytes(const int64_t* 
 
 // bitmap word w <- bytes 32w .. 32w+31 of the byte map (each 0 or 1).
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_pack(const uint4* __restrict__ bytemap,
-                                                           int64_t W, uint32_t* __restrict__ bitmap) {
+                                                           int64_t W, uint2* __restrict__ words) {
   const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (w >= W) return;
   const uint4 a = bytemap[2 * w], b = bytemap[2 * w + 1];
@@ -107,7 +107,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_pack(const uint4* __restri
     const uint32_t nib = ((q[k] & 0x01010101u) * 0x01020408u) >> 24;
     word |= (nib & 0xfu) << (4 * k);
   }
-  bitmap[w] = word;
+  words[w].x = word;
 }
 
 // Marking: each workgroup takes MARK_ITEMS ids per thread and first merges
@@ -123,7 +123,7 @@ constexpr uint32_t MARK_EMPTY = 0xffffffffu;     // never a word index (W <= 2^3
 
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __restrict__ ids,
                                                            int64_t n, int64_t id_bound,
-                                                           uint32_t* bitmap) {
+                                                           uint2* words) {
   __shared__ uint32_t keys[MARK_SLOTS];
   __shared__ uint32_t bits[MARK_SLOTS];
   for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
@@ -153,27 +153,29 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __rest
   __syncthreads();
   for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
     const uint32_t w = keys[s];
-    if (w != MARK_EMPTY) atomicOr(bitmap + w, bits[s]);
+    if (w != MARK_EMPTY) atomicOr(&words[w].x, bits[s]);
   }
 }
 
 struct InPopc {
-  const uint32_t* bm;
-  __device__ uint32_t operator()(int64_t i) const { return __popc(bm[i]); }
+  const uint2* wr;
+  __device__ uint32_t operator()(int64_t i) const { return __popc(wr[i].x); }
 };
-struct OutPrefix {
-  uint32_t* pf;
-  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { pf[i] = prefix; }
+struct OutPrefix {   // rewrites the whole record: contiguous 8-byte stores
+  uint2* wr;
+  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const {
+    wr[i] = make_uint2(wr[i].x, prefix);
+  }
 };
 
 // uni: every set bit of word w is written at its rank.
-__global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint32_t* __restrict__ bitmap,
-                                                          const uint32_t* __restrict__ prefix,
+__global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint2* __restrict__ words,
                                                           int64_t W, int64_t* __restrict__ uni) {
   const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (w >= W) return;
-  uint32_t bits = bitmap[w];
-  uint32_t r = prefix[w];
+  const uint2 rec = words[w];
+  uint32_t bits = rec.x;
+  uint32_t r = rec.y;
   while (bits) {
     const int b = __ffs(bits) - 1;
     uni[r++] = (w << 5) + b;
@@ -183,8 +185,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint32_t* __rest
 
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restrict__ ids, int64_t n,
                                                           int64_t id_bound,
-                                                          const uint32_t* __restrict__ bitmap,
-                                                          const uint32_t* __restrict__ prefix,
+                                                          const uint2* __restrict__ words,
                                                           int32_t* __restrict__ inv) {
   const int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (i >= n) return;
@@ -193,15 +194,18 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restr
     inv[i] = -1;
     return;
   }
-  const int64_t w = id >> 5;
-  const uint32_t below = bitmap[w] & ((1u << (id & 31)) - 1u);
-  inv[i] = int32_t(prefix[w] + __popc(below));
+  const uint2 rec = words[id >> 5];
+  const uint32_t below = rec.x & ((1u << (id & 31)) - 1u);
+  inv[i] = int32_t(rec.y + __popc(below));
 }
 
 // Row copy: thread t of a block moves vector c of row k; a block covers
 // `rpb` consecutive rows of `cpr` vectors each and strides over row groups,
 // so the grid is sized for the machine, not for the worst-case n.  Rows
 // k >= *num_unique are idle.  A slot outside [0, table_rows) flags a miss.
+// (Several row groups per iteration measured slower than one.)
+constexpr int GATHER_U = 1;
+
 template <typename V>
 __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __restrict__ uni,
                                                             const int64_t* __restrict__ num_unique,
@@ -214,12 +218,32 @@ __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __res
   const int r = threadIdx.x / cpr;
   const int c = threadIdx.x - r * cpr;
   if (r >= rpb) return;
-  for (int64_t k = int64_t(blockIdx.x) * rpb + r; k < u; k += int64_t(gridDim.x) * rpb) {
-    const int64_t id = uni[k];
-    const int64_t slot = slot_map ? int64_t(slot_map[id]) : id;
-    const bool hit = slot >= 0 && slot < table_rows;
-    if (c == 0 && flags) flags[k] = hit ? 0 : 1;
-    if (hit && rows) rows[k * cpr + c] = table[slot * cpr + c];
+  const int64_t step = int64_t(gridDim.x) * rpb;
+  for (int64_t k0 = int64_t(blockIdx.x) * rpb + r; k0 < u; k0 += step * GATHER_U) {
+    int64_t slot[GATHER_U];
+#pragma unroll
+    for (int j = 0; j < GATHER_U; ++j) {
+      const int64_t k = k0 + j * step;
+      slot[j] = -1;
+      if (k < u) {
+        const int64_t id = uni[k];
+        slot[j] = slot_map ? int64_t(slot_map[id]) : id;
+      }
+    }
+    V val[GATHER_U];
+#pragma unroll
+    for (int j = 0; j < GATHER_U; ++j) {
+      const bool hit = slot[j] >= 0 && slot[j] < table_rows;
+      if (hit && rows) val[j] = table[slot[j] * cpr + c];
+    }
+#pragma unroll
+    for (int j = 0; j < GATHER_U; ++j) {
+      const int64_t k = k0 + j * step;
+      if (k >= u) break;
+      const bool hit = slot[j] >= 0 && slot[j] < table_rows;
+      if (c == 0 && flags) flags[k] = hit ? 0 : 1;
+      if (hit && rows) rows[k * cpr + c] = val[j];
+    }
   }
 }
 
@@ -303,28 +327,28 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
     if (W > 0)
       hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
                          dim3(DD_THREADS), 0, st, reinterpret_cast<const uint4*>(w.bytemap), W,
-                         w.bitmap);
+                         w.words);
   } else {
     if (W > 0) {
-      const int64_t nb = (W + DD_THREADS - 1) / DD_THREADS;
+      const int64_t nb = (2 * W + DD_THREADS - 1) / DD_THREADS;
       hipLaunchKernelGGL(k_fill_u32, dim3(uint32_t(nb < 4096 ? nb : 4096)), dim3(DD_THREADS), 0,
-                         st, w.bitmap, W, 0u);
+                         st, reinterpret_cast<uint32_t*>(w.words), 2 * W, 0u);
     }
     if (n > 0)
       hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + MARK_IDS - 1) / MARK_IDS)),
-                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bitmap);
+                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words);
   }
   // 3. word ranks (exclusive popcount prefix) and u
-  hipError_t e = scan_launch(InPopc{w.bitmap}, OutPrefix{w.prefix}, W, w.scan_w, num_unique,
+  hipError_t e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique,
                              nullptr, st);
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   // 4. uni, 5. inv
   if (W > 0)
     hipLaunchKernelGGL(k_dedup_uni, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, w.bitmap, w.prefix, W, uni);
+                       dim3(DD_THREADS), 0, st, w.words, W, uni);
   if (n > 0)
     hipLaunchKernelGGL(k_dedup_inv, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bitmap, w.prefix, inv);
+                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words, inv);
 
   // 6. rows through the slot map, miss flags, 7. ordered miss list
   const bool want_miss = miss || num_miss;
