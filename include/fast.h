@@ -136,8 +136,9 @@ fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega, const f
  *   alpha[e,h] = exp(s - m) / Z,  m = max_{e in v} s,  Z = sum_{e in v} exp(s - m)
  *   lse[v,h]   = m + log Z  (-inf for an empty segment; lse may be NULL)
  * Q: [N,H,dh], K: [E,H,dh] of dtype.  alpha: [E,H] fp32.  Reads g->dst_offsets.
- * Supported: H >= 1, 1 <= dh <= 256, H*dh <= 4096; larger shapes return
- * FAST_ERR_UNSUPPORTED.  Row pointers must be aligned to the element size.
+ * Supported: every shape with H <= 64, dh <= 256 and H*dh <= 1024; larger
+ * shapes return FAST_ERR_UNSUPPORTED when no lane layout fits.  Row pointers
+ * must be aligned to the element size.
  * ------------------------------------------------------------------------ */
 fast_status_t fast_edge_softmax_fwd(const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype,
                                     const void* Q, const void* K, float scale,

@@ -44,9 +44,30 @@
 #define FAST_ATT_SAVE_EDGES 24
 #endif
 
+// Workgroup sizes: 256 threads for the forward and unfused kernels, 512 for
+// the fused backward (measured faster on MI355X for the backward's mixed
+// read/write stream); a segment wider than the workgroup (many heads) gets a
+// 512-thread workgroup.  A segment never exceeds ATT_MAX_GROUP lanes.
+#ifndef FAST_ATT_BLOCK
+#define FAST_ATT_BLOCK 256
+#endif
+#ifndef FAST_ATT_BLOCK_BWD
+#define FAST_ATT_BLOCK_BWD 512
+#endif
+// Occupancy target of the fused kernels in waves per SIMD (the register
+// budget follows from it: 512 / waves).
+#ifdef FAST_ATT_WAVES_PER_EU
+#define FAST_ATT_OCC __attribute__((amdgpu_waves_per_eu(FAST_ATT_WAVES_PER_EU)))
+#else
+#define FAST_ATT_OCC
+#endif
+
 namespace fast {
 
-constexpr int ATT_BLOCK = 256;
+constexpr int ATT_BLOCK = FAST_ATT_BLOCK;
+constexpr int ATT_BLOCK_BWD = FAST_ATT_BLOCK_BWD;
+constexpr int ATT_MAX_GROUP = 512;   // lanes per destination segment, at most
+constexpr int ATT_MAX_BLOCK = 512;   // launch bound of every attention kernel
 constexpr int ATT_CH_FWD = FAST_ATT_CH_FWD;
 constexpr int ATT_CH_BWD = FAST_ATT_CH_BWD;
 constexpr int ATT_NSAVE = (FAST_ATT_SAVE_EDGES + ATT_CH_BWD - 1) / ATT_CH_BWD;
@@ -206,7 +227,7 @@ __device__ __forceinline__ int64_t slot_row(int64_t base, int i, int64_t e1) {
 
 // ============================================================ fused forward
 template <typename T, int VE, int P, int LPH_CT, bool NT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_attn_fwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F;
@@ -355,7 +376,7 @@ __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m,
 }
 
 template <typename T, int VE, int P, int LPH_CT, bool NT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F;
@@ -424,7 +445,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_attn_bwd(AttnArgs a) {
 
 // ============================================================ edge softmax fwd
 template <typename T, int VE, int P, int LPH_CT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_softmax_fwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) k_softmax_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F, H = a.L.H;
@@ -470,7 +491,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_softmax_fwd(AttnArgs a) {
 
 // ============================================================ edge softmax bwd
 template <typename T, int VE, int P, int LPH_CT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_softmax_bwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) k_softmax_bwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F, H = a.L.H;
@@ -510,7 +531,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_softmax_bwd(AttnArgs a) {
 
 // ============================================================ aggregation fwd
 template <typename T, int VE, int P, int LPH_CT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_agg_fwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) k_agg_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F, H = a.L.H;
@@ -539,7 +560,7 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_agg_fwd(AttnArgs a) {
 
 // ============================================================ aggregation bwd
 template <typename T, int VE, int P, int LPH_CT>
-__global__ void __launch_bounds__(ATT_BLOCK) k_agg_bwd(AttnArgs a) {
+__global__ void __launch_bounds__(ATT_MAX_BLOCK) k_agg_bwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
   const int F = a.L.F, H = a.L.H;
@@ -576,9 +597,10 @@ __global__ void __launch_bounds__(ATT_BLOCK) k_agg_bwd(AttnArgs a) {
 enum class Op { kAttnFwd, kAttnBwd, kSoftmaxFwd, kSoftmaxBwd, kAggFwd, kAggBwd };
 
 // Picks the vector width and lane mapping for (H, dh, dtype) given every row
-// pointer the op touches (all must be aligned to the vector access).
+// pointer the op touches (all must be aligned to the vector access), for
+// workgroups of `block` threads.
 fast_status_t attn_layout(const char* fn, int H, int dh, fast_dtype_t dt, const void* const* rows,
-                          int nrows, AttnLayout& L);
+                          int nrows, int block, AttnLayout& L);
 
 // Validates the graph and launches `op` with the chosen layout.
 fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int dh, fast_dtype_t dt,

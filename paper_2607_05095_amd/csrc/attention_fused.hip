@@ -25,8 +25,15 @@ static int lanes_override() {
   return v;
 }
 
+// Kernels exist for these (vector width, chunks per lane) pairs.
+static bool have_kernel(fast_dtype_t dt, int VE, int P) {
+  if (P == 1) return true;
+  if (VE <= 2) return P == 2 || P == 4;
+  return P == 2;   // 16-byte (fp32 x4, bf16 x8) and bf16 x4 vectors
+}
+
 fast_status_t attn_layout(const char* fn, int H, int dh, fast_dtype_t dt, const void* const* rows,
-                          int nrows, AttnLayout& L) {
+                          int nrows, int block, AttnLayout& L) {
   if (H < 1 || dh < 1) return fail(FAST_ERR_INVALID_ARG, "%s: H = %d, dh = %d", fn, H, dh);
   if (int64_t(H) * dh > 4096) return fail(FAST_ERR_UNSUPPORTED, "%s: H*dh > 4096", fn);
   const int esz = elem_size(dt);
@@ -68,14 +75,19 @@ fast_status_t attn_layout(const char* fn, int H, int dh, fast_dtype_t dt, const 
   if (const int o = lanes_override()) {
     int p = (CPH + o - 1) / o;
     if (p == 3) p = 4;
-    const bool have = p == 1 || ((p == 2 || p == 4) && VE <= 2) || (p == 2 && VE >= 4);
-    if (p <= 4 && have) {
+    if (p <= 4 && have_kernel(dt, VE, p)) {
       LPH = o;
       P = p;
     }
   }
-  const int G = H * LPH;
-  if (G > 1024) return fail(FAST_ERR_UNSUPPORTED, "%s: H * lanes-per-head = %d > 1024", fn, G);
+  // many heads: narrow the head groups until a segment fits ATT_MAX_GROUP lanes
+  while (H * LPH > ATT_MAX_GROUP && LPH > 1) {
+    LPH >>= 1;
+    P = (CPH + LPH - 1) / LPH;
+    if (P == 3) P = 4;
+  }
+  if (int64_t(H) * LPH > ATT_MAX_GROUP || P > 4 || !have_kernel(dt, VE, P))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: no lane layout for H = %d, dh = %d", fn, H, dh);
   L.H = H;
   L.dh = dh;
   L.F = H * dh;
@@ -83,14 +95,9 @@ fast_status_t attn_layout(const char* fn, int H, int dh, fast_dtype_t dt, const 
   L.P = P;
   L.CPH = CPH;
   L.LPH = LPH;
-  L.G = G;
-  if (G <= ATT_BLOCK) {
-    L.block = ATT_BLOCK;
-    L.SPB = ATT_BLOCK / G;
-  } else {
-    L.block = (G + 63) / 64 * 64;
-    L.SPB = 1;
-  }
+  L.G = H * LPH;
+  L.block = L.G <= block ? block : ATT_MAX_BLOCK;
+  L.SPB = L.block / L.G;
   return FAST_OK;
 }
 
@@ -105,7 +112,8 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
     return fail(FAST_ERR_INVALID_ARG, "%s: NaN scale/slope", fn);
   if (g->num_dst == 0 && g->num_edges > 0)
     return fail(FAST_ERR_INVALID_ARG, "%s: E > 0 edges but no destination", fn);
-  fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, a.L);
+  const int wg = op == Op::kAttnBwd ? ATT_BLOCK_BWD : ATT_BLOCK;
+  fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, wg, a.L);
   if (s != FAST_OK) return s;
   // Non-temporal streaming only when every per-edge row starts and ends on a
   // cache line, so no two rows share a line.

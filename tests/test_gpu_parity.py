@@ -169,6 +169,8 @@ def _synthetic_block(counts, H, dh, dt, seed=0):
     ("many_heads", [8, 8, 3, 15], 16, 16, "f32"),
     ("bf16_vec4", [5, 12, 1], 2, 36, "bf16"),
     ("big_block_G", [4, 9], 8, 64, "f32"),
+    ("wide_group_512", [3, 7, 1, 12], 5, 130, "f32"),
+    ("many_heads_bf16", [6, 2, 9], 64, 16, "bf16"),
 ])
 def test_attention_edge_cases(name, counts, H, dh, dt):
     _announce(f"attention edge case {name}")
