@@ -120,8 +120,9 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
  * Time encoding (Sec. 6.1: TGAT's random Fourier time features).
  *   te[e, j] = cos(fmaf(omega[j], dt_e, phi[j])),  dt_e = dst_t[v] - edge_t[e]
  * for e in segment v.  dt and the argument are fp32 (one subtraction, one
- * fused multiply-add); the cosine of that fp32 argument is accurate to about
- * 1e-7 absolute (Cody-Waite reduction; library cosf beyond |arg| = 2^16).
+ * fused multiply-add); the cosine of that fp32 argument is accurate to better
+ * than 1e-6 absolute (exact Cody-Waite reduction, then the hardware cosine on
+ * the reduced angle; library cosf beyond |arg| = 2^16).
  * Reads g->dst_offsets, g->dst_t, g->edge_t.  omega, phi: [d_t] fp32 device.
  * te: [E, d_t] of te_dtype.  d_t >= 1.
  * ------------------------------------------------------------------------ */

@@ -8,47 +8,48 @@
 // row finds its segment by a short binary search in LDS and stages dt in LDS,
 // and the [rows, d_t] tile is streamed out with 16-byte stores.
 //
-// The argument reaches |omega*dt| ~ 1e4 rad, where the hardware sine (no
-// full range reduction) would lose the 1e-5 target and the device library's
-// general cosf spends most of the op's time.  cos_cw below is a Cody-Waite
+// The argument reaches |omega*dt| ~ 1e4 rad, where the hardware cosine
+// (argument in revolutions, no range reduction worth the name) would lose
+// the 1e-5 target on its own, and the device library's general cosf costs
+// most of the op's time.  cos_rr below first reduces exactly: a Cody-Waite
 // reduction (W. J. Cody and W. Waite, "Software Manual for the Elementary
-// Functions", 1980): x = k*pi/2 + r with pi/2 split into three fp32 parts
+// Functions", 1980) x = k*pi/2 + r with pi/2 split into three fp32 parts
 // C1 + C2 + C3 (each the fp32 rounding of what remained of pi/2, derived
 // exactly from Machin's formula for pi), every step one fused multiply-add,
-// followed by the Taylor polynomials of cos and sin on |r| <= pi/4 (truncation
-// below 3e-8).  Absolute error is about 1e-7 for |x| <= 2^16; larger
-// arguments take the library cosf.
+// so |r| <= pi/4 carries about 1e-7 absolute error for |x| <= 2^16.  The
+// reduced angle r + q*pi/2 (q = k mod 4) is then handed to v_cos_f32 in
+// revolutions, r/(2 pi) + q/4, a value below one revolution, where the
+// hardware cosine measured 3e-7 worst-case absolute error against fp64 on
+// MI355X.  Larger arguments take the library cosf.
 #include "common.h"
 
 namespace fast {
 
+#ifndef FAST_TE_SEGS
+#define FAST_TE_SEGS 32
+#endif
+#ifndef FAST_TE_PASSES
+#define FAST_TE_PASSES 25
+#endif
 constexpr int TE_THREADS = 256;
-constexpr int TE_SEGS = 32;      // destination segments per workgroup
-constexpr int TE_TILE_MAX = 256; // rows staged per tile (at most)
+constexpr int TE_SEGS = FAST_TE_SEGS;    // destination segments per workgroup
+constexpr int TE_TILE_MAX = 256;         // rows staged per tile (at most)
+constexpr int TE_PASSES = FAST_TE_PASSES;  // row passes per tile
 
-__device__ __forceinline__ float cos_cw(float x) {
-  if (!(fabsf(x) <= 65536.f)) return cosf(x);     // also NaN and +-inf
+// Branch-free: valid (about 3e-7 absolute) for |x| <= 2^16, finite beyond.
+__device__ __forceinline__ float cos_rr(float x) {
   const float C1 = 0x1.921fb6p+0f, C2 = -0x1.777a5cp-25f, C3 = -0x1.ee59dap-50f;
-  const float TWO_OVER_PI = 0x1.45f306p-1f;
+  const float TWO_OVER_PI = 0x1.45f306p-1f, INV_TWO_PI = 0x1.45f306p-3f;
   const float k = rintf(x * TWO_OVER_PI);
   float r = fmaf(-k, C1, x);
   r = fmaf(-k, C2, r);
   r = fmaf(-k, C3, r);
-  const float r2 = r * r;
-  // cos r = 1 - r^2/2! + r^4/4! - r^6/6! + r^8/8!
-  float c = fmaf(r2, 1.f / 40320.f, -1.f / 720.f);
-  c = fmaf(c, r2, 1.f / 24.f);
-  c = fmaf(c, r2, -0.5f);
-  c = fmaf(c, r2, 1.f);
-  // sin r = r - r^3/3! + r^5/5! - r^7/7! + r^9/9!
-  float p = fmaf(r2, 1.f / 362880.f, -1.f / 5040.f);
-  p = fmaf(p, r2, 1.f / 120.f);
-  p = fmaf(p, r2, -1.f / 6.f);
-  const float s = fmaf(r * r2, p, r);
-  const int q = int(k) & 3;                         // quadrant of x
-  const float v = (q & 1) ? s : c;                  // q: 0 cos r, 1 -sin r, 2 -cos r, 3 sin r
-  return ((q + 1) & 2) ? -v : v;
+  const float q = float(int32_t(k) & 3);        // quadrant, exact
+  return __builtin_amdgcn_cosf(fmaf(r, INV_TWO_PI, 0.25f * q));
 }
+
+// Large arguments (|x| > 2^16, or not finite) take the library cosf.
+__device__ __forceinline__ bool cos_cw_ok(float x) { return fabsf(x) <= 65536.f; }
 
 // Thread t owns the column chunk t % cpr of rows t / cpr, t / cpr + rpp, ...
 // (rpp = rows per pass), so omega and phi of its columns stay in registers.
@@ -72,7 +73,7 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
   const int rpp = narrow ? TE_THREADS / cpr : 1;   // rows per pass
   const int rsub = narrow ? int(threadIdx.x) / cpr : 0;
   const int c0 = narrow ? int(threadIdx.x) - rsub * cpr : int(threadIdx.x);
-  const int tile = rpp * 8 < TE_TILE_MAX ? rpp * 8 : TE_TILE_MAX;
+  const int tile = rpp * TE_PASSES < TE_TILE_MAX ? rpp * TE_PASSES : (TE_TILE_MAX / rpp) * rpp;
   float om[VEC], ph[VEC];
   if (narrow && rsub < rpp) {
 #pragma unroll
@@ -97,9 +98,19 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
       if (rsub < rpp) {
         for (int row = rsub; row < nrows; row += rpp) {
           const float dt = s_dt[row];
-          float o[VEC];
+          float x[VEC], o[VEC];
+          bool big = false;
 #pragma unroll
-          for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(om[k], dt, ph[k]));
+          for (int k = 0; k < VEC; ++k) {
+            x[k] = fmaf(om[k], dt, ph[k]);
+            o[k] = cos_rr(x[k]);
+            big |= !cos_cw_ok(x[k]);
+          }
+          if (__builtin_expect(big, 0)) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+              if (!cos_cw_ok(x[k])) o[k] = cosf(x[k]);
+          }
           StreamIO<TO, VEC, NT>::store(te + (t0 + row) * d_t + c0 * VEC, o);
         }
       }
@@ -109,7 +120,10 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
         for (int c = c0; c < cpr; c += TE_THREADS) {
           float o[VEC];
 #pragma unroll
-          for (int k = 0; k < VEC; ++k) o[k] = cos_cw(fmaf(omega[c * VEC + k], dt, phi[c * VEC + k]));
+          for (int k = 0; k < VEC; ++k) {
+            const float x = fmaf(omega[c * VEC + k], dt, phi[c * VEC + k]);
+            o[k] = cos_cw_ok(x) ? cos_rr(x) : cosf(x);
+          }
           StreamIO<TO, VEC, NT>::store(te + (t0 + row) * d_t + c * VEC, o);
         }
       }
@@ -123,7 +137,11 @@ static void launch_te(const fast_tcsr_t* g, const float* omega, const float* phi
                       void* te, hipStream_t st) {
   const int64_t nb = (g->num_dst + TE_SEGS - 1) / TE_SEGS;
   // streaming stores only when each output row covers whole cache lines
+#ifdef FAST_TE_FORCE_NT
+  const bool nt = true;
+#else
   const bool nt = (size_t(d_t) * sizeof(TO)) % CACHE_LINE == 0 && aligned(te, CACHE_LINE);
+#endif
   if (nt)
     hipLaunchKernelGGL((k_time_encode<TO, VEC, true>), dim3(uint32_t(nb)), dim3(TE_THREADS), 0, st,
                        g->dst_offsets, g->num_dst, g->num_edges, g->dst_t, g->edge_t, omega, phi,
