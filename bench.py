@@ -12,7 +12,11 @@ value = sampled edges per step / step time.  The roofline entry covers the
 dominant kernel, the fused backward of the layer-1 block, timed with HIP
 events on the stream it runs on.
 
-    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large]
+    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large] [--pipelined]
+
+The timed steps run serially on one stream (prep, then attention).  With
+--pipelined the line also reports the same steps software-pipelined: prep of
+batch i+1 on a second stream overlaps attention of batch i.
 """
 from __future__ import annotations
 
@@ -64,11 +68,17 @@ def describe(b):
 
 
 class Step:
-    """All device buffers of one batch and the launch sequence of one step."""
+    """Device buffers of a batch and the launch sequences of one step.
 
-    def __init__(self, b, torch, fast):
+    The step is split in two parts: prep (CSR offsets, dedup + gather of node
+    and edge rows, time encoding) and attention (fused forward of both layer
+    blocks, then fused backward).  Prep outputs live in `slots` buffer sets,
+    so that prep of the next batch can run while attention of the current
+    batch still reads its own offsets (software pipelining on two streams)."""
+
+    def __init__(self, b, torch, fast, slots=2):
         from synth import make_block_operands, make_slot_map, make_table, omega_phi
-        self.b, self.torch, self.fast = b, torch, fast
+        self.b, self.torch, self.fast, self.slots = b, torch, fast, slots
         dev = "cuda"
         tdt = torch.float32 if b.dtype == "f32" else torch.bfloat16
         self.DT = fast.F32 if b.dtype == "f32" else fast.BF16
@@ -77,8 +87,6 @@ class Step:
             N, E = blk.num_dst, blk.num_edges
             d = dict(N=N, E=E)
             d["counts"] = torch.from_numpy(blk.counts).to(dev)
-            d["off"] = torch.empty(N + 1, dtype=torch.int32, device=dev)
-            d["ws_off"] = torch.empty(fast.fast_csr_offsets_workspace(N), dtype=torch.uint8, device=dev)
             d["dst_t"] = torch.from_numpy(blk.dst_t).to(dev)
             d["edge_t"] = torch.from_numpy(blk.edge_t).to(dev)
             d.update(make_block_operands(b, i, device=dev))
@@ -87,8 +95,14 @@ class Step:
             d["dQ"] = torch.empty((N, b.H, b.dh), dtype=tdt, device=dev)
             d["dK"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
             d["dV"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
-            d["te"] = torch.empty((E, b.d_t), dtype=tdt, device=dev)
-            d["g"] = fast.tcsr(d["off"], E, edge_t=d["edge_t"], dst_t=d["dst_t"])
+            d["off"], d["ws_off"], d["te"], d["g"] = [], [], [], []
+            for _ in range(slots):
+                off = torch.empty(N + 1, dtype=torch.int32, device=dev)
+                d["off"].append(off)
+                d["ws_off"].append(torch.empty(fast.fast_csr_offsets_workspace(N), dtype=torch.uint8,
+                                               device=dev))
+                d["te"].append(torch.empty((E, b.d_t), dtype=tdt, device=dev))
+                d["g"].append(fast.tcsr(off, E, edge_t=d["edge_t"], dst_t=d["dst_t"]))
             self.blocks.append(d)
         om, ph = omega_phi(b.d_t)
         self.omega = torch.from_numpy(om).to(dev)
@@ -96,18 +110,17 @@ class Step:
         self.scale = float(np.float32(1.0 / np.sqrt(b.dh)))
         # node ids: table indexed by id
         log(f"node table {b.node_bound} x {b.node_D} {b.dtype}")
-        self.node = self._dedup_bufs(b.node_ids, b.node_bound,
-                                     make_table(b.node_bound, b.node_D, b.dtype, dev, b.seed, 3), None)
+        node_table = make_table(b.node_bound, b.node_D, b.dtype, dev, b.seed, 3)
         # edge ids: a cache with a slot map, or a table indexed by id
         if b.edge_cache_rows:
             log(f"edge cache {b.edge_cache_rows} x {b.edge_D}, slot map over {b.edge_bound}")
-            table = make_table(b.edge_cache_rows, b.edge_D, b.dtype, dev, b.seed, 4)
-            slot = make_slot_map(b, device=dev)
+            edge_table = make_table(b.edge_cache_rows, b.edge_D, b.dtype, dev, b.seed, 4)
+            slot_map = make_slot_map(b, device=dev)
         else:
-            table = make_table(b.edge_bound, b.edge_D, b.dtype, dev, b.seed, 4)
-            slot = None
-        self.edge = self._dedup_bufs(b.edge_ids, b.edge_bound, table, slot)
-        self.events = None
+            edge_table = make_table(b.edge_bound, b.edge_D, b.dtype, dev, b.seed, 4)
+            slot_map = None
+        self.node = [self._dedup_bufs(b.node_ids, b.node_bound, node_table, None) for _ in range(slots)]
+        self.edge = [self._dedup_bufs(b.edge_ids, b.edge_bound, edge_table, slot_map) for _ in range(slots)]
 
     def _dedup_bufs(self, ids_np, bound, table, slot):
         torch, fast = self.torch, self.fast
@@ -130,13 +143,12 @@ class Step:
                             d["table"].shape[1], self.DT, d["slot"], d["uni"], d["inv"], d["nu"],
                             d["rows"], d["miss"], d["nm"], d["ws"], d["wsb"])
 
-    def run(self, rec=None):
-        """Enqueue one step.  rec: optional dict name -> list of (start, end) events."""
-        torch, f, b = self.torch, self.fast, self.b
+    @staticmethod
+    def _marker(torch, rec, names):
         st = torch.cuda.current_stream()
 
         def mark(name, fn):
-            if rec is None:
+            if rec is None or (names is not None and name not in names):
                 fn()
                 return
             s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -144,24 +156,69 @@ class Step:
             fn()
             e.record(st)
             rec.setdefault(name, []).append((s, e))
+        return mark
 
+    def prep(self, slot, rec=None, names=None):
+        """Offsets, dedup + gather (nodes, edges), time encoding into `slot`."""
+        f, b = self.fast, self.b
+        mark = self._marker(self.torch, rec, names)
         for i, d in enumerate(self.blocks):
-            mark(f"offsets_L{i + 1}", lambda d=d: f.fast_csr_offsets(d["counts"], d["N"], d["off"],
-                                                                      d["ws_off"], d["ws_off"].numel()))
-        mark("dedup_gather_nodes", lambda: self._dedup(self.node))
-        mark("dedup_gather_edges", lambda: self._dedup(self.edge))
+            mark(f"offsets_L{i + 1}", lambda d=d: f.fast_csr_offsets(
+                d["counts"], d["N"], d["off"][slot], d["ws_off"][slot], d["ws_off"][slot].numel()))
+        mark("dedup_gather_nodes", lambda: self._dedup(self.node[slot]))
+        mark("dedup_gather_edges", lambda: self._dedup(self.edge[slot]))
         for i, d in enumerate(self.blocks):
             mark(f"time_encode_L{i + 1}", lambda d=d: f.fast_time_encode(
-                d["g"], self.omega, self.phi, b.d_t, d["te"], self.DT))
-        for i, d in enumerate(self.blocks):           # forward: layer 1 then layer 2
+                d["g"][slot], self.omega, self.phi, b.d_t, d["te"][slot], self.DT))
+
+    def attn(self, slot, rec=None, names=None):
+        """Fused forward of layer 1 then layer 2, fused backward of layer 2 then
+        layer 1, on the offsets of `slot`."""
+        f, b = self.fast, self.b
+        mark = self._marker(self.torch, rec, names)
+        for i, d in enumerate(self.blocks):
             mark(f"attn_fwd_L{i + 1}", lambda d=d: f.fast_edge_attention_fwd(
-                d["g"], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
                 d["out"], d["lse"]))
-        for i in reversed(range(len(self.blocks))):  # backward: layer 2 then layer 1
+        for i in reversed(range(len(self.blocks))):
             d = self.blocks[i]
             mark(f"attn_bwd_L{i + 1}", lambda d=d: f.fast_edge_attention_bwd(
-                d["g"], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
                 d["lse"], d["dO"], d["dQ"], d["dK"], d["dV"]))
+
+    def run_serial(self, rec=None, names=None):
+        self.prep(0, rec, names)
+        self.attn(0, rec, names)
+
+    def run_pipelined(self, K, side, rec=None, names=None):
+        """K steps; prep of batch i+1 runs on stream `side` while attention of
+        batch i runs on the current stream.  Dependencies: attention(i) waits
+        for prep(i); prep(i+2) reuses slot i % 2 only after attention(i)."""
+        torch = self.torch
+        main = torch.cuda.current_stream()
+        ready = [torch.cuda.Event() for _ in range(self.slots)]
+        free = [None] * self.slots
+        side.wait_stream(main)
+
+        def enqueue_prep(i):
+            s = i % self.slots
+            with torch.cuda.stream(side):
+                if free[s] is not None:
+                    side.wait_event(free[s])
+                self.prep(s)
+                ready[s].record(side)
+
+        enqueue_prep(0)
+        for i in range(K):
+            if i + 1 < K:
+                enqueue_prep(i + 1)
+            s = i % self.slots
+            main.wait_event(ready[s])
+            self.attn(s, rec, names)
+            ev = torch.cuda.Event()
+            ev.record(main)
+            free[s] = ev
+        main.wait_stream(side)
 
 
 def attn_bwd_bytes(N, E, F, esz, H):
@@ -198,9 +255,9 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     nn, ne = int(b.node_ids.size * frac), int(b.edge_ids.size * frac)
     node_ids, edge_ids = b.node_ids[:nn], b.edge_ids[:ne]
     bits = torch.int16 if b.dtype == "bf16" else torch.int32
-    node_table = step.node["table"].view(bits).cpu().numpy()
-    edge_table = step.edge["table"].view(bits).cpu().numpy()
-    slot = None if step.edge["slot"] is None else step.edge["slot"].cpu().numpy()
+    node_table = step.node[0]["table"].view(bits).cpu().numpy()
+    edge_table = step.edge[0]["table"].view(bits).cpu().numpy()
+    slot = None if step.edge[0]["slot"] is None else step.edge[0]["slot"].cpu().numpy()
     scale = step.scale
 
     def one_pass():
@@ -253,6 +310,8 @@ def main():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="bigdedup")
     ap.add_argument("--cpu-frac", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pipelined", action="store_true",
+                    help="also time the steps software-pipelined over two streams")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -278,33 +337,54 @@ def main():
     b = make_batch(WORKLOADS[args.workload])
     log(f"workload {b.name}: blocks {[(x.num_dst, x.num_edges) for x in b.blocks]}")
     step = Step(b, torch, fast)
+    side = torch.cuda.Stream()
     torch.cuda.synchronize()
     for _ in range(args.warmup):
-        step.run()
+        step.run_serial()
+    if args.pipelined:
+        step.run_pipelined(max(args.warmup, 1), side)
     torch.cuda.synchronize()
     log("warmup done")
 
-    # timed region: K whole steps
+    def timed(fn):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / args.steps
+
+    # timed region: K whole steps, serial schedule; HIP events only around the
+    # dominant kernel, on the stream it is launched on
     rec = {}
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    dominant = ["attn_bwd_L1"]
+
+    def serial_steps():
+        for _ in range(args.steps):
+            step.run_serial(rec, dominant)
+    ms = timed(serial_steps)
+    bwd_ms = float(np.mean([s.elapsed_time(e) for s, e in rec["attn_bwd_L1"]]))
+    log(f"{ms:.3f} ms/step (serial)")
+    # optionally, the same K steps software-pipelined over two streams
+    ms_pipe = None
+    if args.pipelined:
+        ms_pipe = timed(lambda: step.run_pipelined(args.steps, side))
+        log(f"{ms_pipe:.3f} ms/step (pipelined)")
+
+    # per-operator breakdown: separate serial steps, every operator timed
+    rec_all = {}
+    for _ in range(3):
+        step.run_serial(rec_all)
     torch.cuda.synchronize()
-    t_start.record()
-    for _ in range(args.steps):
-        step.run(rec)
-    t_end.record()
-    torch.cuda.synchronize()
-    ms = t_start.elapsed_time(t_end) / args.steps
-    breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec.items()}
-    log(f"{ms:.3f} ms/step")
+    breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec_all.items()}
 
     esz = 4 if b.dtype == "f32" else 2
     F = b.H * b.dh
     L1 = b.blocks[0]
-    bwd_ms = breakdown["attn_bwd_L1"]
     bwd_bytes = attn_bwd_bytes(L1.num_dst, L1.num_edges, F, esz, b.H)
     achieved = bwd_bytes / (bwd_ms * 1e-3) / 1e9
-    fused_ms = sum(v for k, v in breakdown.items() if k.startswith("attn_"))
+    fused_ms = sum(v for k, v in breakdown.items() if k.startswith("attn_"))   # serial pass
     fused_bytes = sum(attn_fwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) +
                       attn_bwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) for x in b.blocks)
     roofline = {
@@ -328,9 +408,20 @@ def main():
             "algorithmic_bytes": fused_bytes,
             "hbm_frac": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
+        "schedule": "serial: prep (offsets, dedup+gather, time encoding) then attention of each "
+                    "batch on one stream",
+
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
+        "breakdown_note": "operators timed one by one in 3 extra serial steps outside the timed region",
         "kernel_source_sha": kernel_source_hash(),
     }
+    if ms_pipe is not None:
+        result["pipelined"] = {
+            "ms_per_step": round(ms_pipe, 4),
+            "value": b.sampled_edges / (ms_pipe * 1e-3),
+            "schedule": "prep of batch i+1 on a second stream overlaps attention of batch i; "
+                        "attention(i) waits for prep(i); double-buffered prep outputs",
+        }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(b, step, torch, args.cpu_frac)
