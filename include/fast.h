@@ -89,6 +89,21 @@ fast_status_t fast_csr_offsets(const int32_t* counts, int64_t n, int32_t* offset
                                void* ws, size_t ws_bytes, fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Contract check of a sampled subgraph (the device-data contract above).
+ * Counts, into violations[0..5) (device int64, overwritten):
+ *   [0] v with off[v+1] < off[v]             (non-monotone offsets)
+ *   [1] off[0] != 0 or off[N] != E            (0, 1 or 2)
+ *   [2] e with src_ids[e] outside [0, src_bound)    (0 if src_ids is NULL)
+ *   [3] e with edge_ids[e] outside [0, edge_bound)  (0 if edge_ids is NULL)
+ *   [4] e with edge_t[e] > dst_t[v] for its segment v, i.e. dt < 0, counted
+ *       only where the offsets are monotone     (0 if a time array is NULL)
+ * Reads every field of g that is not NULL; dst_offsets is required.  Any
+ * offsets, even malformed ones, are read in bounds.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_check_tcsr(const fast_tcsr_t* g, int64_t src_bound, int64_t edge_bound,
+                              int64_t* violations, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
  * Within-batch de-duplication and row reconstruction (Sec. 4.2 SlimCache
  * compression; Sec. 5 uni_ID / inv_Idx).
  *   uni[0..u)   = the distinct values of ids[0..n), ascending

@@ -27,6 +27,7 @@ _f64 = C.c_double
 
 _SIGS = {
     "oracle_csr_offsets": (None, [_p, _i64, _p]),
+    "oracle_check_tcsr": (None, [_p, _i64, _i64, _p, _i64, _p, _i64, _p, _p, _p]),
     "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
     "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
@@ -77,6 +78,18 @@ def csr_offsets(counts):
     off = np.empty(counts.shape[0] + 1, dtype=np.int32)
     lib().oracle_csr_offsets(_ptr(counts), counts.shape[0], _ptr(off))
     return off
+
+
+def check_tcsr(off, E, src_ids=None, src_bound=0, edge_ids=None, edge_bound=0,
+               edge_t=None, dst_t=None):
+    off = _c(off, np.int32)
+    c = lambda a, t: None if a is None else _c(a, t)
+    src_ids, edge_ids = c(src_ids, np.int64), c(edge_ids, np.int64)
+    edge_t, dst_t = c(edge_t, np.float32), c(dst_t, np.float32)
+    v = np.zeros(5, dtype=np.int64)
+    lib().oracle_check_tcsr(_ptr(off), off.shape[0] - 1, E, _ptr(src_ids), src_bound,
+                            _ptr(edge_ids), edge_bound, _ptr(edge_t), _ptr(dst_t), _ptr(v))
+    return v
 
 
 def dedup(ids):

@@ -18,6 +18,27 @@ void oracle_csr_offsets(const int32_t* counts, int64_t n, int32_t* off) {
   for (int64_t v = 0; v < n; ++v) off[v + 1] = off[v] + counts[v];
 }
 
+/* ---- contract check of a sampled subgraph ---- */
+void oracle_check_tcsr(const int32_t* off, int64_t N, int64_t E, const int64_t* src_ids,
+                       int64_t src_bound, const int64_t* edge_ids, int64_t edge_bound,
+                       const float* edge_t, const float* dst_t, int64_t* violations) {
+  for (int k = 0; k < 5; ++k) violations[k] = 0;
+  for (int64_t v = 0; v < N; ++v)
+    if (off[v + 1] < off[v]) violations[0] += 1;
+  if (off[0] != 0) violations[1] += 1;
+  if (off[N] != E) violations[1] += 1;
+  for (int64_t e = 0; e < E; ++e) {
+    if (src_ids && (src_ids[e] < 0 || src_ids[e] >= src_bound)) violations[2] += 1;
+    if (edge_ids && (edge_ids[e] < 0 || edge_ids[e] >= edge_bound)) violations[3] += 1;
+  }
+  if (edge_t && dst_t)
+    for (int64_t v = 0; v < N; ++v) {
+      if (off[v + 1] < off[v]) continue;
+      for (int64_t e = off[v]; e < off[v + 1]; ++e)
+        if (e >= 0 && e < E && edge_t[e] > dst_t[v]) violations[4] += 1;
+    }
+}
+
 /* ---- within-batch dedup (Sec. 4.2 compression; Sec. 5 uni_ID / inv_Idx) ---- */
 static int cmp_i64(const void* a, const void* b) {
   int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;

@@ -24,6 +24,14 @@ extern "C" {
 /* CSR offsets: off[0] = 0, off[v+1] = off[v] + counts[v]. */
 void oracle_csr_offsets(const int32_t* counts, int64_t n, int32_t* off);
 
+/* Contract check of a sampled subgraph: violations[5] as documented for
+ * fast_check_tcsr (non-monotone offsets; wrong first/last offset; src ids
+ * and edge ids outside their bounds; edge times after their destination's
+ * time where the offsets are monotone).  NULL arrays count 0. */
+void oracle_check_tcsr(const int32_t* off, int64_t N, int64_t E, const int64_t* src_ids,
+                       int64_t src_bound, const int64_t* edge_ids, int64_t edge_bound,
+                       const float* edge_t, const float* dst_t, int64_t* violations);
+
 /* Within-batch compression (Sec. 4.2, Sec. 5): uni = ascending distinct ids,
  * inv[i] = position of ids[i] in uni.  Returns u = |uni|. */
 int64_t oracle_dedup(const int64_t* ids, int64_t n, int64_t* uni, int32_t* inv);

@@ -15,7 +15,7 @@ import os
 __all__ = [
     "FastError", "lib", "TCSR", "tcsr", "F32", "BF16", "dtype_of",
     "fast_version", "fast_last_error",
-    "fast_csr_offsets_workspace", "fast_csr_offsets",
+    "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
     "fast_dedup_gather_workspace", "fast_dedup_gather",
     "fast_time_encode",
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
@@ -57,6 +57,7 @@ _SIGS = {
     "fast_version": (C.c_char_p, []),
     "fast_csr_offsets_workspace": (_sz, [_i64]),
     "fast_csr_offsets": (_i32, [_p, _i64, _p, _p, _sz, _p]),
+    "fast_check_tcsr": (_i32, [_G, _i64, _i64, _p, _p]),
     "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
                                  _p, _p, _p, _p, _sz, _p]),
@@ -140,6 +141,11 @@ def fast_csr_offsets_workspace(n: int) -> int:
 def fast_csr_offsets(counts, n, offsets, ws, ws_bytes, stream=None):
     _check(lib().fast_csr_offsets(_ptr(counts), n, _ptr(offsets), _ptr(ws), ws_bytes,
                                   _stream(stream)))
+
+
+def fast_check_tcsr(g: TCSR, src_bound, edge_bound, violations, stream=None):
+    _check(lib().fast_check_tcsr(C.byref(g), src_bound, edge_bound, _ptr(violations),
+                                 _stream(stream)))
 
 
 def fast_dedup_gather_workspace(n: int, id_bound: int) -> int:

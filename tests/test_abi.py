@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_header_declares_the_operator_set():
     names = declared_functions()
-    for n in ["fast_csr_offsets", "fast_dedup_gather", "fast_time_encode",
+    for n in ["fast_csr_offsets", "fast_check_tcsr", "fast_dedup_gather", "fast_time_encode",
               "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
               "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
               "fast_edge_attention_fwd", "fast_edge_attention_bwd", "fast_last_error"]:
@@ -113,6 +113,14 @@ def test_other_entry_points_validate():
     assert L.fast_csr_offsets(FAKE, -1, FAKE, FAKE, 1 << 20, None) == INVALID
     assert L.fast_csr_offsets(FAKE, 10, FAKE, FAKE, 4, None) == WORKSPACE
     assert L.fast_csr_offsets(FAKE, 10, None, FAKE, 1 << 20, None) == INVALID
+    assert L.fast_check_tcsr(None, 0, 0, FAKE, None) == INVALID
+    assert L.fast_check_tcsr(gp, 0, 0, None, None) == INVALID              # violations NULL
+    assert L.fast_check_tcsr(ctypes.byref(_g(off=None)), 0, 0, FAKE, None) == INVALID
+    assert L.fast_check_tcsr(ctypes.byref(_g(N=-1)), 0, 0, FAKE, None) == INVALID
+    assert L.fast_check_tcsr(ctypes.byref(_g(E=1 << 31)), 0, 0, FAKE, None) == UNSUPPORTED
+    gs = fast.TCSR(4, 40, FAKE, FAKE, None, FAKE, None)
+    assert L.fast_check_tcsr(ctypes.byref(gs), -1, 10, FAKE, None) == INVALID  # src_bound
+    assert L.fast_check_tcsr(ctypes.byref(gs), 10, -1, FAKE, None) == INVALID  # edge_bound
 
 
 def test_dedup_validation_and_workspace_query():

@@ -240,6 +240,60 @@ def test_csr_offsets_bit_exact(case):
     assert np.array_equal(off.cpu().numpy(), oracle.csr_offsets(counts))
 
 
+# ------------------------------------------------------------------ subgraph contract check
+def _check_gpu(off, E, src=None, src_bound=0, eid=None, edge_bound=0, et=None, dt=None):
+    d = lambda a, t: None if a is None else to_dev(np.asarray(a, dtype=t))
+    d_off = to_dev(np.asarray(off, np.int32))
+    d_src, d_eid = d(src, np.int64), d(eid, np.int64)
+    d_et, d_dt = d(et, np.float32), d(dt, np.float32)
+    g = fast.tcsr(d_off, E, src_ids=d_src, edge_t=d_et, edge_ids=d_eid, dst_t=d_dt)
+    v = torch.full((5,), -3, dtype=torch.int64, device="cuda")
+    fast.fast_check_tcsr(g, src_bound, edge_bound, v)
+    return v.cpu().numpy()
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_check_tcsr_workloads_clean(cfg):
+    _announce(f"check_tcsr cfg{cfg}")
+    b = make_batch(cfg)
+    for blk in b.blocks:
+        off = oracle.csr_offsets(blk.counts)
+        args = (off, blk.num_edges, blk.src_ids, b.node_bound, blk.edge_ids, b.edge_bound,
+                blk.edge_t, blk.dst_t)
+        got = _check_gpu(*args)
+        assert np.array_equal(got, oracle.check_tcsr(*args))
+        assert got.tolist() == [0, 0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_check_tcsr_malformed_bit_exact(seed):
+    _announce(f"check_tcsr malformed seed {seed}")
+    r = np.random.default_rng(100 + seed)
+    N, E = 3001 + 517 * seed, 4099 + 1031 * seed
+    # offsets mostly increasing with random faults, some below 0 or above E
+    off = np.sort(r.integers(0, E + 1, N + 1)).astype(np.int32)
+    off[0], off[-1] = 0, E
+    bad = r.choice(N + 1, 40, replace=False)
+    off[bad] = r.integers(-100, E + 100, 40)
+    src = r.integers(-5, 1000, E)
+    eid = r.integers(0, 2000, E)
+    dt = r.uniform(0, 100, N).astype(np.float32)
+    et = r.uniform(0, 110, E).astype(np.float32)
+    args = (off, E, src, 995, eid, 1990, et, dt)
+    want = oracle.check_tcsr(*args)
+    assert want.min() >= 0 and want[[0, 2, 3, 4]].min() > 0
+    assert np.array_equal(_check_gpu(*args), want)
+    # optional arrays absent
+    assert np.array_equal(_check_gpu(off, E), oracle.check_tcsr(off, E))
+
+
+def test_check_tcsr_empty_and_single_offset():
+    _announce("check_tcsr empty")
+    assert _check_gpu([0], 0).tolist() == [0, 0, 0, 0, 0]
+    assert _check_gpu([3], 0).tolist() == [0, 2, 0, 0, 0]
+    assert _check_gpu([0, 0, 0], 0, et=[], dt=[1.0, 2.0]).tolist() == [0, 0, 0, 0, 0]
+
+
 # ------------------------------------------------------------------ dedup + gather (a2, a3)
 def _dedup(ids_np, id_bound, table=None, slot_map=None, want_miss=True):
     n = ids_np.shape[0]

@@ -389,6 +389,64 @@ def test_branch_override():
     np.testing.assert_allclose(dQ2, dQs, rtol=1e-13, atol=1e-15)
 
 
+# ---------------------------------------------------------------- subgraph contract check
+def test_check_tcsr_hand_counted_case():
+    # off = [0, 3, 2, 5] with E = 4: segment 1 runs backwards, off[N] != E.
+    # src ids -1 and 10 fall outside [0, 10).  dt < 0 where an edge is later
+    # than its destination: segment 0 holds edges 0..2 (edge 1: 6 > 5),
+    # segment 1 is skipped, segment 2 is [2, 5) cut to [2, 4) (edge 3: 2 > 1).
+    off = np.array([0, 3, 2, 5], np.int32)
+    v = oracle.check_tcsr(off, 4, src_ids=[-1, 0, 9, 10], src_bound=10,
+                          edge_t=[4.0, 6.0, 0.0, 2.0], dst_t=[5.0, 5.0, 1.0])
+    assert v.tolist() == [1, 1, 2, 0, 2]
+    # every optional array absent: only the offset counters remain
+    assert oracle.check_tcsr(off, 4).tolist() == [1, 1, 0, 0, 0]
+    # N = 0: the single offset is both first and last
+    assert oracle.check_tcsr(np.array([0], np.int32), 0).tolist() == [0, 0, 0, 0, 0]
+    assert oracle.check_tcsr(np.array([3], np.int32), 0).tolist() == [0, 2, 0, 0, 0]
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_check_tcsr_generated_batches_are_clean(cfg):
+    b = make_batch(cfg)
+    for blk in b.blocks:
+        off = oracle.csr_offsets(blk.counts)
+        v = oracle.check_tcsr(off, blk.num_edges, blk.src_ids, b.node_bound, blk.edge_ids,
+                              b.edge_bound, blk.edge_t, blk.dst_t)
+        assert v.tolist() == [0, 0, 0, 0, 0]
+
+
+def test_check_tcsr_each_planted_fault_hits_its_counter():
+    b = make_batch(0)
+    blk = b.blocks[0]
+    off = oracle.csr_offsets(blk.counts)
+    E, N = blk.num_edges, blk.num_dst
+    base = dict(src_ids=blk.src_ids.copy(), src_bound=b.node_bound,
+                edge_ids=blk.edge_ids.copy(), edge_bound=b.edge_bound,
+                edge_t=blk.edge_t.copy(), dst_t=blk.dst_t.copy())
+    v = [k for k in range(N) if blk.counts[k] > 0][3]
+    e = int(off[v])
+    cases = []
+    a = dict(base); a["src_ids"] = a["src_ids"].copy(); a["src_ids"][e] = b.node_bound
+    cases.append((off, a, 2))
+    a = dict(base); a["edge_ids"] = a["edge_ids"].copy(); a["edge_ids"][e] = -1
+    cases.append((off, a, 3))
+    a = dict(base); a["edge_t"] = a["edge_t"].copy(); a["edge_t"][e] = a["dst_t"][v] + 1.0
+    cases.append((off, a, 4))
+    o = off.copy(); o[-1] += 1
+    cases.append((o, base, 1))
+    for o, a, k in cases:
+        got = oracle.check_tcsr(o, E, **a)
+        want = [0] * 5
+        want[k] = 1
+        assert got.tolist() == want, (k, got)
+    # swapping two adjacent interior offsets with a gap breaks monotonicity once
+    o = off.copy()
+    i = next(i for i in range(1, N) if o[i + 1] > o[i])
+    o[i], o[i + 1] = o[i + 1], o[i]
+    assert oracle.check_tcsr(o, E)[0] == 1
+
+
 # ---------------------------------------------------------------- regression fixture
 def test_oracle_matches_stored_regression_fixture():
     import json, os
