@@ -119,10 +119,14 @@ def dtype_of(t) -> int:
 
 
 def tcsr(dst_offsets, num_edges: int, src_ids=None, edge_t=None, edge_ids=None, dst_t=None) -> TCSR:
-    """Builds a fast_tcsr_t over device tensors.  The tensors must stay alive
-    while the struct is in use."""
-    return TCSR(dst_offsets.shape[0] - 1, int(num_edges), _ptr(dst_offsets), _ptr(src_ids),
-                _ptr(edge_t), _ptr(edge_ids), _ptr(dst_t))
+    """Builds a fast_tcsr_t over device tensors.  The struct keeps a reference
+    to each tensor, so a temporary passed here (`x.cuda()`) is not returned to
+    torch's caching allocator, and reused, while the struct is alive."""
+    g = TCSR(dst_offsets.shape[0] - 1, int(num_edges), _ptr(dst_offsets), _ptr(src_ids),
+             _ptr(edge_t), _ptr(edge_ids), _ptr(dst_t))
+    g._keep = tuple(t for t in (dst_offsets, src_ids, edge_t, edge_ids, dst_t)
+                    if t is not None and not isinstance(t, int))
+    return g
 
 
 # ------------------------------------------------------------------ entry points

@@ -140,3 +140,23 @@ def test_dedup_validation_and_workspace_query():
     assert L.fast_dedup_gather(*args(bound=1 << 36)) == UNSUPPORTED
     assert L.fast_dedup_gather(*args(rows_n=10)) == INVALID      # no slot map, bound > rows
     assert L.fast_dedup_gather(*args(table=None)) == INVALID     # rows wanted, no table
+
+
+def test_tcsr_keeps_its_tensors_alive():
+    # Regression: the struct holds raw device addresses, so a temporary tensor
+    # passed to tcsr() must not be freed (and its memory reused by torch's
+    # caching allocator) while the struct is in use.
+    import gc
+    import weakref
+
+    import torch
+    t = torch.arange(3, dtype=torch.float32)
+    ref = weakref.ref(t)
+    g = fast.tcsr(torch.zeros(5, dtype=torch.int32), 3, edge_t=t)
+    del t
+    gc.collect()
+    assert ref() is not None and g.edge_t == ref().data_ptr()
+    assert g.num_dst == 4 and g.num_edges == 3 and g.src_ids is None
+    del g
+    gc.collect()
+    assert ref() is None
