@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0
 SLOPE = 0.2
 WORKLOADS = {"bigdedup": 4, "large": 3}
 METRIC = "sampled edges/sec, fused edge-softmax+aggregation fwd+bwd; % HBM roofline"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_bwd.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_bwd_{workload}.json")
 KERNEL_SOURCES = ["paper_2607_05095_amd/csrc/attention.h", "paper_2607_05095_amd/csrc/attention_fused.hip",
                   "paper_2607_05095_amd/csrc/common.h"]
 
@@ -289,15 +289,16 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     }
 
 
-def read_traffic(n_launch_bytes):
-    """HBM traffic of the dominant kernel from the committed rocprofv3 counter
-    summary, or None when it is absent or the kernel source changed since."""
+def read_traffic(workload):
+    """HBM traffic of the dominant kernel on this workload, from the committed
+    rocprofv3 counter summary, or None when there is none for this workload or
+    the kernel source changed since the counters were taken."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(TRAFFIC_FILE.format(workload=workload)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha") != kernel_source_hash():
+    if t.get("kernel_source_sha") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("bytes_per_launch")
 
@@ -390,7 +391,7 @@ def main():
     roofline = {
         "kernel": "k_attn_bwd (fused ESM+AGG backward, layer-1 block)",
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(bwd_bytes),
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(args.workload),
         "algorithmic_bytes_per_launch": bwd_bytes, "avg_launch_ms": round(bwd_ms, 4),
     }
     result = {

@@ -31,6 +31,7 @@ _SIGS = {
     "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
     "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
+    "oracle_time_encode_bwd": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p, _p, _p]),
     "oracle_edge_softmax_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _f64, _f64, _p, _p, _p]),
     "oracle_aggregate_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _p]),
     "oracle_aggregate_bwd": (None, [_p, _i64, _i32, _i32, _p, _p, _p, _p, _p]),
@@ -129,6 +130,21 @@ def time_encode(off, t_dst, t_e, omega, phi):
     lib().oracle_time_encode(_ptr(off), N, _ptr(t_dst), _ptr(t_e), _ptr(omega),
                              _ptr(phi), d_t, _ptr(te))
     return te
+
+
+def time_encode_bwd(off, t_dst, t_e, omega, phi, dte):
+    """Returns (domega [d_t], dphi [d_t]) in float64 for the upstream gradient dte [E, d_t]."""
+    off = _c(off, np.int32)
+    t_dst, t_e = _c(t_dst, np.float32), _c(t_e, np.float32)
+    omega, phi = _c(omega, np.float32), _c(phi, np.float32)
+    dte = _f64(dte)
+    N, d_t = off.shape[0] - 1, omega.shape[0]
+    assert dte.shape == (t_e.shape[0], d_t)
+    domega = np.zeros(d_t, dtype=np.float64)
+    dphi = np.zeros(d_t, dtype=np.float64)
+    lib().oracle_time_encode_bwd(_ptr(off), N, _ptr(t_dst), _ptr(t_e), _ptr(omega), _ptr(phi),
+                                 d_t, _ptr(dte), _ptr(domega), _ptr(dphi))
+    return domega, dphi
 
 
 # ------------------------------------------------------------------ attention

@@ -99,6 +99,29 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
   }
 }
 
+/* ---- time-encoding backward (the Sec. 6.1 time features are trainable):
+ * the gradient of cos(omega_j * dt + phi_j) taken at the forward's fp32
+ * argument, summed over every edge in fp64 ---- */
+void oracle_time_encode_bwd(const int32_t* off, int64_t N, const float* t_dst,
+                            const float* t_e, const float* omega, const float* phi,
+                            int d_t, const double* dte, double* domega, double* dphi) {
+  for (int j = 0; j < d_t; ++j) {
+    domega[j] = 0.0;
+    dphi[j] = 0.0;
+  }
+  for (int64_t v = 0; v < N; ++v) {
+    for (int64_t e = off[v]; e < off[v + 1]; ++e) {
+      float dt = t_dst[v] - t_e[e];
+      for (int j = 0; j < d_t; ++j) {
+        float arg = fmaf(omega[j], dt, phi[j]);
+        double dcos = -sin((double)arg);          /* d cos(a) / da */
+        dphi[j] += dte[e * d_t + j] * dcos;
+        domega[j] += dte[e * d_t + j] * dcos * (double)dt;
+      }
+    }
+  }
+}
+
 /* ---- edge softmax forward (Sec. 4.3 "Edge Softmax": max, sum, divide) ---- */
 void oracle_edge_softmax_fwd(const int32_t* off, int64_t N, int H, int dh,
                              const double* Q, const double* K, double scale,

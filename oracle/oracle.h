@@ -50,6 +50,15 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
                         const float* t_e, const float* omega, const float* phi,
                         int d_t, double* te);
 
+/* Backward of the time encoding for an upstream gradient dte [E, d_t]:
+ *   a = fmaf(omega[j], dt_e, phi[j])  (the forward's fp32 argument)
+ *   dphi[j]   = sum_e dte[e,j] * (-sin a)
+ *   domega[j] = sum_e dte[e,j] * (-sin a) * dt_e
+ * summed in fp64 over every edge of every segment. */
+void oracle_time_encode_bwd(const int32_t* off, int64_t N, const float* t_dst,
+                            const float* t_e, const float* omega, const float* phi,
+                            int d_t, const double* dte, double* domega, double* dphi);
+
 /* Edge softmax forward with per-edge multi-head logits:
  *   pre[e,h]   = scale * <Q[v,h,:], K[e,h,:]>
  *   s[e,h]     = pre > 0 ? pre : slope * pre            (LeakyReLU)

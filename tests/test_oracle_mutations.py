@@ -24,6 +24,16 @@ MUTATIONS = {
     "te_wrong_segment": ("float dt = t_dst[v] - t_e[e];",
                          "float dt = t_dst[v > 0 ? v - 1 : 0] - t_e[e];"),
     "te_transposed_out": ("te[e * d_t + j] =", "te[(j * 0 + e) * d_t + (d_t - 1 - j)] ="),
+    "tebwd_cos_for_sin": ("double dcos = -sin((double)arg);", "double dcos = -cos((double)arg);"),
+    "tebwd_sign": ("double dcos = -sin((double)arg);", "double dcos = sin((double)arg);"),
+    "tebwd_fp64_argument": ("double dcos = -sin((double)arg);",
+                            "double dcos = -sin((double)omega[j] * ((double)t_dst[v] - (double)t_e[e]) + phi[j]);"),
+    "tebwd_no_dt": ("domega[j] += dte[e * d_t + j] * dcos * (double)dt;",
+                    "domega[j] += dte[e * d_t + j] * dcos;"),
+    "tebwd_wrong_row": ("dphi[j] += dte[e * d_t + j] * dcos;",
+                        "dphi[j] += dte[(e > 0 ? e - 1 : 0) * d_t + j] * dcos;"),
+    "tebwd_column_swap": ("float arg = fmaf(omega[j], dt, phi[j]);\n        double dcos",
+                          "float arg = fmaf(omega[d_t - 1 - j], dt, phi[j]);\n        double dcos"),
     "lrelu_swapped": ("alpha[e * H + h] = p > 0.0 ? p : slope * p;",
                       "alpha[e * H + h] = p > 0.0 ? slope * p : p;"),
     "no_max_shift": ("Z += exp(alpha[e * H + h] - m);", "Z += exp(alpha[e * H + h]);"),
@@ -52,6 +62,8 @@ PINS = [
     (P.test_time_encode_closed_forms, {}),
     (P.test_time_encode_double_angle_columns, {}),
     (P.test_time_encode_fp32_difference, {}),
+    (P.test_time_encode_bwd_finite_differences, {}),
+    (P.test_time_encode_bwd_pythagorean_with_the_forward, {}),
     (P.test_fwd_vs_torch_sdpa, {}),
     (P.test_fwd_vs_dense_masked_attention, dict(slope=0.2)),
     (P.test_softmax_invariants, {}),

@@ -191,6 +191,82 @@ def test_time_encode_fp32_difference():
     assert abs(math.cos(2.0 ** 25 - 1) - math.cos(2.0 ** 25)) > 1e-2
 
 
+# ---------------------------------------------------------------- time-encoding backward
+def _dyadic_time_block(seed):
+    """A block whose fp32 time arguments are exact: dt = k/8 (k <= 32),
+    omega_j = m/256 in [0.25, 2], phi_j = n/64 in [-1, 1].  omega*dt + phi
+    then needs at most 18 significant bits, so it stays exact in fp32 even
+    after a perturbation of omega or phi by a multiple of 2^-12."""
+    r = np.random.default_rng(seed)
+    counts = np.array([3, 0, 5, 1, 4, 2], dtype=np.int32)
+    off = _csr(counts)
+    N, E, d_t = counts.size, int(off[-1]), 9
+    t_dst = (4.0 + r.integers(0, 5, N)).astype(np.float32)
+    seg = np.repeat(np.arange(N), counts)
+    t_e = (t_dst[seg] - r.integers(0, 33, E) / 8.0).astype(np.float32)
+    om = (r.integers(64, 513, d_t) / 256.0).astype(np.float32)
+    ph = (r.integers(-64, 65, d_t) / 64.0).astype(np.float32)
+    dte = r.standard_normal((E, d_t))
+    return off, t_dst, t_e, om, ph, dte
+
+
+def _te_loss(off, t_dst, t_e, om, ph, dte):
+    return float(np.sum(dte * oracle.time_encode(off, t_dst, t_e, om, ph)))
+
+
+def test_time_encode_bwd_finite_differences():
+    # central differences of L = sum(dte * te) through the forward oracle,
+    # Richardson-extrapolated from steps 2^-11 and 2^-12 (error O(h^4))
+    off, t_dst, t_e, om, ph, dte = _dyadic_time_block(5)
+    domega, dphi = oracle.time_encode_bwd(off, t_dst, t_e, om, ph, dte)
+
+    def central(which, j, h):
+        lo, hi = [a.copy() for a in (om, ph)], [a.copy() for a in (om, ph)]
+        lo[which][j] -= np.float32(h)
+        hi[which][j] += np.float32(h)
+        return (_te_loss(off, t_dst, t_e, *hi, dte) - _te_loss(off, t_dst, t_e, *lo, dte)) / (2 * h)
+
+    for j in range(om.size):
+        for which, got in ((0, domega[j]), (1, dphi[j])):
+            d1, d2 = central(which, j, 2.0 ** -11), central(which, j, 2.0 ** -12)
+            fd = (4 * d2 - d1) / 3
+            assert abs(got - fd) <= 1e-8 * (1 + abs(fd)), (which, j, got, fd)
+
+
+def test_time_encode_bwd_pythagorean_with_the_forward():
+    # one edge per destination and dte = 1: dphi_j = -sin(a_j) and the
+    # forward gives cos(a_j) at the same fp32 argument, so dphi^2 + te^2 = 1;
+    # domega_j = dphi_j * dt.  Large dt makes a_j ~ 1e4 rad, where an
+    # argument not rounded to fp32 as in the forward breaks the identity.
+    om, ph = omega_phi(12)
+    ph = np.linspace(-1, 1, 12).astype(np.float32)
+    for dt in (0.0, 0.75, 3.1e3, 9.87654e3):
+        off = np.array([0, 1], dtype=np.int32)
+        t_dst = np.array([1e4], dtype=np.float32)
+        t_e = np.array([np.float32(1e4) - np.float32(dt)], dtype=np.float32)
+        dt32 = float(t_dst[0] - t_e[0])
+        te = oracle.time_encode(off, t_dst, t_e, om, ph)[0]
+        domega, dphi = oracle.time_encode_bwd(off, t_dst, t_e, om, ph, np.ones((1, 12)))
+        np.testing.assert_allclose(dphi ** 2 + te ** 2, 1.0, atol=1e-14)
+        np.testing.assert_array_equal(domega, dphi * dt32)
+
+
+def test_time_encode_bwd_sums_over_edges():
+    # the gradient of a block is the sum of the gradients of its edges taken
+    # one at a time (each edge as a one-edge block of its own destination)
+    off, t_dst, t_e, om, ph, dte = _dyadic_time_block(9)
+    domega, dphi = oracle.time_encode_bwd(off, t_dst, t_e, om, ph, dte)
+    seg = np.repeat(np.arange(off.size - 1), np.diff(off))
+    acc_w, acc_p = np.zeros(om.size), np.zeros(om.size)
+    for e in range(t_e.size):
+        w, p = oracle.time_encode_bwd(np.array([0, 1], np.int32), t_dst[seg[e]:seg[e] + 1],
+                                      t_e[e:e + 1], om, ph, dte[e:e + 1])
+        acc_w += w
+        acc_p += p
+    np.testing.assert_allclose(domega, acc_w, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dphi, acc_p, rtol=1e-12, atol=1e-12)
+
+
 # ---------------------------------------------------------------- attention forward (a5-a7)
 def test_fwd_vs_torch_sdpa():
     # slope = 1 removes the LeakyReLU: the operator is masked scaled-dot-product attention
