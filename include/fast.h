@@ -5,6 +5,7 @@
  *   fast_csr_offsets          CSR ind_ptr of a sampled block          (Sec. 5)
  *   fast_dedup_gather         uni_ID / inv_Idx + row reconstruction   (Sec. 4.2, Sec. 5)
  *   fast_time_encode          cos(omega * dt + phi) time features     (Sec. 6.1, TGAT)
+ *   fast_time_encode_bwd      gradients of omega and phi              (Sec. 6.1)
  *   fast_edge_softmax_fwd/bwd per-edge multi-head logits + ESM        (Sec. 4.3)
  *   fast_temporal_aggregate_fwd/bwd  attention-weighted AGG           (Sec. 4.3, Eq. 1)
  *   fast_edge_attention_fwd/bwd      ESM and AGG fused in one kernel  (Sec. 4.3)
@@ -144,6 +145,30 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
 fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega, const float* phi,
                                int d_t, void* te, fast_dtype_t te_dtype,
                                fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Backward of the time encoding (Sec. 6.1: the encoder's frequencies and
+ * phases are trained with the model).  For an upstream gradient dte [E, d_t]:
+ *   a_ej      = fmaf(omega[j], dt_e, phi[j])       (the forward's fp32 argument)
+ *   domega[j] = sum_e dte[e,j] * (-sin a_ej) * dt_e
+ *   dphi[j]   = sum_e dte[e,j] * (-sin a_ej)
+ * summed over every edge of the block.  The sine of the fp32 argument, the
+ * products and the sums are fp64 (results rounded once to fp32), so a column
+ * whose terms nearly cancel keeps its accuracy.  Deterministic: the order of
+ * the sums depends only on N and d_t, and repeated calls give bitwise-equal
+ * results.  domega, dphi: [d_t] fp32 device, overwritten (zeros when E = 0).
+ * Reads g->dst_offsets, g->dst_t, g->edge_t.  dte: [E, d_t] of dte_dtype.
+ * Limits: 1 <= d_t, and d_t / v <= 256 for the widest v in {8 (bf16 only),
+ * 4, 2, 1} that divides d_t and matches dte's alignment (so d_t <= 256
+ * always works, and up to 1024 fp32 / 2048 bf16 when divisible by 4 / 8);
+ * otherwise FAST_ERR_UNSUPPORTED.
+ * Workspace: fast_time_encode_bwd_workspace(N, d_t) bytes, 8-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t fast_time_encode_bwd_workspace(int64_t num_dst, int d_t);
+fast_status_t fast_time_encode_bwd(const fast_tcsr_t* g, const float* omega, const float* phi,
+                                   int d_t, const void* dte, fast_dtype_t dte_dtype,
+                                   float* domega, float* dphi, void* ws, size_t ws_bytes,
+                                   fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Edge softmax with per-edge multi-head attention logits (Sec. 4.3 "Edge

@@ -17,7 +17,7 @@ __all__ = [
     "fast_version", "fast_last_error",
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
     "fast_dedup_gather_workspace", "fast_dedup_gather",
-    "fast_time_encode",
+    "fast_time_encode", "fast_time_encode_bwd_workspace", "fast_time_encode_bwd",
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
     "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
     "fast_edge_attention_fwd", "fast_edge_attention_bwd",
@@ -62,6 +62,8 @@ _SIGS = {
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
                                  _p, _p, _p, _p, _sz, _p]),
     "fast_time_encode": (_i32, [_G, _p, _p, _i32, _p, _i32, _p]),
+    "fast_time_encode_bwd_workspace": (_sz, [_i64, _i32]),
+    "fast_time_encode_bwd": (_i32, [_G, _p, _p, _i32, _p, _i32, _p, _p, _p, _sz, _p]),
     "fast_edge_softmax_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p]),
     "fast_edge_softmax_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p]),
     "fast_temporal_aggregate_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _p]),
@@ -167,6 +169,17 @@ def fast_dedup_gather(ids, n, id_bound, table, table_rows, D, dtype, slot_map, u
 def fast_time_encode(g: TCSR, omega, phi, d_t, te, te_dtype, stream=None):
     _check(lib().fast_time_encode(C.byref(g), _ptr(omega), _ptr(phi), d_t, _ptr(te), te_dtype,
                                   _stream(stream)))
+
+
+def fast_time_encode_bwd_workspace(num_dst: int, d_t: int) -> int:
+    return lib().fast_time_encode_bwd_workspace(num_dst, d_t)
+
+
+def fast_time_encode_bwd(g: TCSR, omega, phi, d_t, dte, dte_dtype, domega, dphi, ws, ws_bytes,
+                         stream=None):
+    _check(lib().fast_time_encode_bwd(C.byref(g), _ptr(omega), _ptr(phi), d_t, _ptr(dte),
+                                      dte_dtype, _ptr(domega), _ptr(dphi), _ptr(ws), ws_bytes,
+                                      _stream(stream)))
 
 
 def fast_edge_softmax_fwd(g: TCSR, H, dh, dtype, Q, K, scale, neg_slope, alpha, lse, stream=None):

@@ -160,3 +160,38 @@ def test_tcsr_keeps_its_tensors_alive():
     del g
     gc.collect()
     assert ref() is None
+
+
+def test_time_encode_bwd_validation_and_workspace_query():
+    L = fast.lib()
+    g = _g(N=64, E=640)
+    gp = ctypes.byref(g)
+    ws = L.fast_time_encode_bwd_workspace(64, 100)
+    assert ws >= 2 * 100 * 2 * 8                      # two groups of 32 segments
+    assert L.fast_time_encode_bwd_workspace(-1, 100) == 0
+    assert L.fast_time_encode_bwd_workspace(64, 0) == 0
+    # one partial per workgroup, at most 2048 workgroups whatever N is
+    assert L.fast_time_encode_bwd_workspace(10 ** 9, 128) == L.fast_time_encode_bwd_workspace(
+        2048 * 32, 128)
+
+    def call(**k):
+        return L.fast_time_encode_bwd(
+            k.get("g", gp), k.get("om", FAKE), k.get("ph", FAKE), k.get("d_t", 100),
+            k.get("dte", FAKE), k.get("dt", 0), k.get("dw", FAKE), k.get("dp", FAKE),
+            k.get("ws", FAKE), k.get("wsb", ws), None)
+
+    assert call(g=None) == INVALID
+    assert call(d_t=0) == INVALID
+    assert call(dt=5) == INVALID
+    assert call(dw=None) == INVALID
+    assert call(dp=None) == INVALID
+    assert call(om=None) == INVALID
+    assert call(dte=None) == INVALID
+    assert call(wsb=ws - 1) == WORKSPACE
+    assert call(ws=None) == WORKSPACE
+    assert call(dw=FAKE + 2) == UNSUPPORTED                      # misaligned output
+    assert call(d_t=257, wsb=1 << 20) == UNSUPPORTED             # 257 chunks of one column
+    assert call(g=ctypes.byref(_g(N=0, E=5))) == INVALID
+    assert call(g=ctypes.byref(_g(N=-1))) == INVALID
+    assert call(g=ctypes.byref(_g(E=1 << 31))) == UNSUPPORTED
+    assert fast.fast_last_error() != ""
