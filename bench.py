@@ -232,6 +232,50 @@ def attn_fwd_bytes(N, E, F, esz, H):
     return (2 * E + 2 * N) * F * esz + 4 * N * H + 4 * (N + 1)
 
 
+def time_encode_bwd_bytes(N, E, d_t, esz):
+    """Read dte [E, d_t], edge times, destination times and offsets, omega and
+    phi; write domega and dphi."""
+    return E * (4 + d_t * esz) + 8 * N + 4 + 16 * d_t
+
+
+def widened_ops(b, step, torch, fast, reps=10):
+    """Operators beyond the timed step, each timed alone with HIP events on
+    its launch stream (mean of `reps` launches after one warm-up): the
+    time-encoding backward of each layer block, on a seeded upstream gradient."""
+    from synth import _randn
+    esz = 4 if b.dtype == "f32" else 2
+    res = {}
+    for i, d in enumerate(step.blocks):
+        N, E = d["N"], d["E"]
+        dte = _randn((E, b.d_t), b.dtype, "cuda", 4242 + i)
+        dw = torch.empty(b.d_t, device="cuda")
+        dp = torch.empty(b.d_t, device="cuda")
+        wsb = fast.fast_time_encode_bwd_workspace(N, b.d_t)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        g = d["g"][0]
+
+        def call():
+            fast.fast_time_encode_bwd(g, step.omega, step.phi, b.d_t, dte, step.DT, dw, dp, ws, wsb)
+        call()
+        st = torch.cuda.current_stream()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record(st)
+        for _ in range(reps):
+            call()
+        e.record(st)
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / reps
+        nbytes = time_encode_bwd_bytes(N, E, b.d_t, esz)
+        res[f"time_encode_bwd_L{i + 1}"] = {
+            "ms": round(ms, 4), "algorithmic_bytes": nbytes, "bound": "alu (fp64 sine per element)",
+            "achieved_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+        del dte, ws
+    return res
+
+
 def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     """The fp64 oracle, single-threaded, on a bounded sample of the same batch:
     the first `frac` of the segments of each layer block and the matching
@@ -380,6 +424,9 @@ def main():
     torch.cuda.synchronize()
     breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec_all.items()}
 
+    widened = widened_ops(b, step, torch, fast)
+    log(f"widened ops: {widened}")
+
     esz = 4 if b.dtype == "f32" else 2
     F = b.H * b.dh
     L1 = b.blocks[0]
@@ -413,6 +460,8 @@ def main():
                     "batch on one stream",
 
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
+        "widened_ops": widened,
+        "widened_note": "operators beyond the timed step, timed alone outside the timed region",
         "breakdown_note": "operators timed one by one in 3 extra serial steps outside the timed region",
         "kernel_source_sha": kernel_source_hash(),
     }

@@ -12,7 +12,8 @@
 // split into its fp64 rounding and the fp64 rounding of the remainder, each
 // step one fused multiply-add) and the Taylor series of sin(r)/r in r^2
 // through r^14, whose truncation error is below 6e-12 for |r| <= pi/2.
-// Arguments beyond 2^30 rad (or not finite) take the library sine.
+// Arguments beyond 2^30 rad (or not finite) take the library sine in a cold
+// second pass of the workgroups that met one.
 //
 // Determinism: the reduction order depends only on N and d_t.  A workgroup
 // owns the segment groups b, b + nblk, b + 2*nblk, ... (TB_SEGS segments
@@ -36,19 +37,20 @@ __host__ __device__ inline int64_t tb_blocks(int64_t N) {
   return g < TB_MAX_BLOCKS ? g : TB_MAX_BLOCKS;
 }
 
-// Library sine for the rare |x| > 2^30 or non-finite x, kept out of line so
-// that its registers do not weigh on the streaming loop.
-__device__ __attribute__((noinline)) double sin_big(double x) { return sin(x); }
-
-// sin(x) for an fp32 x, in fp64.  For |x| <= 2^30, k <= 2^29: k * PI_HI is
-// exact inside the first fma, and k * (pi - PI_HI - PI_LO) stays below 1e-24,
-// so r carries an absolute error of about 1e-16.
-__device__ __forceinline__ double sin_f64(float xf) {
+// sin(x) for an fp32 x with |x| <= 2^30, in fp64, returned as (-1)^k sin r
+// where x = k*pi + r: the value is sin(r), and bit 31 of `flip` is set when
+// k is odd (sin x = -sin r).  k comes from the magic-number rounding
+// fma(x, 1/pi, 1.5*2^52), whose low word holds k in two's complement.  For
+// |x| <= 2^30, k <= 2^29: k * PI_HI is exact inside the first fma and
+// k * (pi - PI_HI - PI_LO) stays below 1e-24, so r carries an absolute error
+// of about 1e-16.
+__device__ __forceinline__ double sin_reduced(float xf, uint32_t& flip) {
   const double x = double(xf);
-  if (__builtin_expect(!(fabs(x) <= 0x1p30), 0)) return sin_big(x);
   const double PI_HI = 0x1.921fb54442d18p+1, PI_LO = 0x1.1a62633145c07p-53;
-  const double INV_PI = 0x1.45f306dc9c883p-2;
-  const double k = rint(x * INV_PI);
+  const double INV_PI = 0x1.45f306dc9c883p-2, MAGIC = 0x1.8p52;
+  const double t = fma(x, INV_PI, MAGIC);
+  const double k = t - MAGIC;
+  flip = uint32_t(__double2loint(t)) << 31;
   double r = fma(-k, PI_HI, x);
   r = fma(-k, PI_LO, r);
   const double r2 = r * r;
@@ -59,9 +61,13 @@ __device__ __forceinline__ double sin_f64(float xf) {
   p = fma(p, r2, -0x1.a01a01a01a01ap-13);     // -1/7!
   p = fma(p, r2, 0x1.1111111111111p-7);       //  1/5!
   p = fma(p, r2, -0x1.5555555555555p-3);      // -1/3!
-  const double s = fma(r * r2, p, r);         // r + r^3 * (...)
-  return (int64_t(k) & 1) ? -s : s;           // sin(r + k pi) = (-1)^k sin r
+  return fma(r * r2, p, r);                   // r + r^3 * (...)
 }
+
+// Arguments beyond this (or not finite) are left to the library sine, called
+// out of line so that its registers do not weigh on the streaming loop.
+__device__ __forceinline__ bool sin_reduced_ok(float x) { return fabsf(x) <= 0x1p30f; }
+__device__ __attribute__((noinline)) double sin_library(double x) { return sin(x); }
 
 // Grid: tb_blocks(N) workgroups.  Thread t owns the column chunk t % cpr of
 // the rows t / cpr, t / cpr + rpp, ... of every tile, as in the forward.
@@ -87,6 +93,7 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
 
   float om[VEC], ph[VEC];
   double acc_w[VEC], acc_p[VEC];
+  bool big = false;                        // an argument beyond the reduction's range
 #pragma unroll
   for (int k = 0; k < VEC; ++k) {
     om[k] = active ? omega[c0 * VEC + k] : 0.f;
@@ -123,13 +130,66 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
           raw.unpack(g);
 #pragma unroll
           for (int k = 0; k < VEC; ++k) {
-            const double gs = -double(g[k]) * sin_f64(fmaf(om[k], dt, ph[k]));
+            const float x = fmaf(om[k], dt, ph[k]);
+            uint32_t flip;
+            const double s = sin_reduced(x, flip);
+            const bool ok = sin_reduced_ok(x);
+            big |= !ok;
+            // -g * sin x, the sign folded into g; 0 for an argument left to
+            // the cold pass
+            const float gn = ok ? __uint_as_float(__float_as_uint(g[k]) ^ flip ^ 0x80000000u) : 0.f;
+            const double gs = double(gn) * s;
             acc_p[k] += gs;
             acc_w[k] = fma(gs, double(dt), acc_w[k]);
           }
         }
       }
       __syncthreads();
+    }
+  }
+
+  // Cold pass, only in a workgroup that met an argument beyond 2^30 rad (or
+  // not finite): the same rows again, adding just those elements with the
+  // library sine.  The order stays a fixed function of the inputs.
+  if (__syncthreads_or(big)) {
+    for (int64_t grp = blockIdx.x; grp < ngroups; grp += nblk) {
+      const int64_t s0 = grp * TB_SEGS;
+      const int ns = int(N - s0 < TB_SEGS ? N - s0 : TB_SEGS);
+      if (threadIdx.x <= ns) s_off[threadIdx.x] = clamp64(off[s0 + threadIdx.x], 0, E);
+      if (threadIdx.x < ns) s_tdst[threadIdx.x] = dst_t[s0 + threadIdx.x];
+      __syncthreads();
+      const int64_t r0 = s_off[0], r1 = s_off[ns] > r0 ? s_off[ns] : r0;
+      for (int64_t t0 = r0; t0 < r1; t0 += tile) {
+        const int nrows = int(r1 - t0 < tile ? r1 - t0 : tile);
+        if (threadIdx.x < nrows) {
+          const int64_t e = t0 + threadIdx.x;
+          int lo = 0, hi = ns - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_off[mid] <= e) lo = mid; else hi = mid - 1;
+          }
+          s_dt[threadIdx.x] = s_tdst[lo] - edge_t[e];
+        }
+        __syncthreads();
+        if (active && big) {
+          for (int row = rsub; row < nrows; row += rpp) {
+            const float dt = s_dt[row];
+            Raw<TG, VEC> raw;
+            raw.template load<false>(dte + (t0 + row) * d_t + c0 * VEC);
+            float g[VEC];
+            raw.unpack(g);
+            for (int k = 0; k < VEC; ++k) {
+              const float x = fmaf(om[k], dt, ph[k]);
+              if (!sin_reduced_ok(x)) {
+                const double gs = -double(g[k]) * sin_library(double(x));
+                acc_p[k] += gs;
+                acc_w[k] = fma(gs, double(dt), acc_w[k]);
+              }
+            }
+          }
+        }
+        __syncthreads();
+      }
     }
   }
 
