@@ -31,6 +31,8 @@ _SIGS = {
     "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
     "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
+    "oracle_access_count": (None, [_p, _p, _i64, _i64, _p]),
+    "oracle_greedy_hot_set": (None, [_p, _i64, _p, _i64, _f64, _p, _p, _p, _p]),
     "oracle_time_encode_bwd": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p, _p, _p]),
     "oracle_edge_softmax_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _f64, _f64, _p, _p, _p]),
     "oracle_aggregate_fwd": (None, [_p, _i64, _i32, _i32, _p, _p, _p]),
@@ -118,6 +120,31 @@ def gather(uni, table, slot_map=None):
     hit = np.ones(u, dtype=bool)
     hit[miss] = False
     return rows, hit, miss
+
+
+# ------------------------------------------------------------------ greedy cache selection
+def access_count(batches, id_bound, freq=None):
+    """Alg. 1 counting over a list of id arrays (one per pre-sampled batch):
+    freq[x] = number of batches containing x (added to `freq` if given)."""
+    sizes = [len(b) for b in batches]
+    ids = _c(np.concatenate([np.asarray(b, dtype=np.int64) for b in batches])
+             if batches else np.zeros(0), np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    out = np.zeros(id_bound, dtype=np.int32) if freq is None else _c(freq, np.int32).copy()
+    lib().oracle_access_count(_ptr(ids), _ptr(off), len(batches), id_bound, _ptr(out))
+    return out
+
+
+def greedy_hot_set(fv, fe, alpha):
+    """Alg. 1 selection: (hot node ids, hot edge ids), each in selection order."""
+    fv, fe = _c(fv, np.int32), _c(fe, np.int32)
+    nv, ne = fv.shape[0], fe.shape[0]
+    hv = np.empty(max(nv, 1), dtype=np.int64)
+    he = np.empty(max(ne, 1), dtype=np.int64)
+    cv, ce = C.c_int64(0), C.c_int64(0)
+    lib().oracle_greedy_hot_set(_ptr(fv), nv, _ptr(fe), ne, float(alpha), _ptr(hv),
+                                C.byref(cv), _ptr(he), C.byref(ce))
+    return hv[:cv.value].copy(), he[:ce.value].copy()
 
 
 # ------------------------------------------------------------------ time encoding

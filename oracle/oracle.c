@@ -99,6 +99,76 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
   }
 }
 
+/* ---- SlimCache greedy cache selection (Sec. 4.2, Alg. 1) ---- */
+
+/* Counting step: for every batch, each distinct id of the batch adds 1 to its
+ * counter, so freq[x] is the number of batches that touch x.  Ids outside
+ * [0, id_bound) are ignored. */
+void oracle_access_count(const int64_t* ids, const int64_t* batch_off, int64_t num_batches,
+                         int64_t id_bound, int32_t* freq) {
+  for (int64_t k = 0; k < num_batches; ++k) {
+    int64_t n = batch_off[k + 1] - batch_off[k];
+    if (n <= 0) continue;
+    int64_t* b = (int64_t*)malloc((size_t)n * sizeof(int64_t));
+    memcpy(b, ids + batch_off[k], (size_t)n * sizeof(int64_t));
+    qsort(b, (size_t)n, sizeof(int64_t), cmp_i64);
+    for (int64_t i = 0; i < n; ++i) {
+      if (i > 0 && b[i] == b[i - 1]) continue;          /* distinct ids only */
+      if (b[i] >= 0 && b[i] < id_bound) freq[b[i]] += 1;
+    }
+    free(b);
+  }
+}
+
+typedef struct { int32_t f; int64_t id; } freq_id_t;
+
+/* descending frequency, then ascending id */
+static int cmp_freq_desc(const void* a, const void* b) {
+  const freq_id_t* x = (const freq_id_t*)a;
+  const freq_id_t* y = (const freq_id_t*)b;
+  if (x->f != y->f) return x->f > y->f ? -1 : 1;
+  return (x->id > y->id) - (x->id < y->id);
+}
+
+static freq_id_t* ranked(const int32_t* f, int64_t n) {
+  freq_id_t* s = (freq_id_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(freq_id_t));
+  for (int64_t i = 0; i < n; ++i) {
+    s[i].f = f[i];
+    s[i].id = i;
+  }
+  qsort(s, (size_t)n, sizeof(freq_id_t), cmp_freq_desc);
+  return s;
+}
+
+/* Selection step: rank node and edge ids by frequency, then take the more
+ * frequent head of the two lists while i + j < alpha * (|V| + |E|); a node
+ * wins only with a strictly higher count, and an exhausted list never wins.
+ * hot_v / hot_e receive the selected ids in selection order. */
+void oracle_greedy_hot_set(const int32_t* fv, int64_t nv, const int32_t* fe, int64_t ne,
+                           double alpha, int64_t* hot_v, int64_t* n_hot_v, int64_t* hot_e,
+                           int64_t* n_hot_e) {
+  freq_id_t* sv = ranked(fv, nv);
+  freq_id_t* se = ranked(fe, ne);
+  int64_t i = 0, j = 0;
+  while ((double)(i + j) < alpha * (double)(nv + ne) && i + j < nv + ne) {
+    int take_node;
+    if (i >= nv) take_node = 0;
+    else if (j >= ne) take_node = 1;
+    else take_node = sv[i].f > se[j].f;
+    if (take_node) {
+      hot_v[i] = sv[i].id;
+      i += 1;
+    } else {
+      hot_e[j] = se[j].id;
+      j += 1;
+    }
+  }
+  *n_hot_v = i;
+  *n_hot_e = j;
+  free(sv);
+  free(se);
+}
+
 /* ---- time-encoding backward (the Sec. 6.1 time features are trainable):
  * the gradient of cos(omega_j * dt + phi_j) taken at the forward's fp32
  * argument, summed over every edge in fp64 ---- */

@@ -50,6 +50,22 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
                         const float* t_e, const float* omega, const float* phi,
                         int d_t, double* te);
 
+/* SlimCache greedy cache selection (Sec. 4.2, Alg. 1).
+ * Counting: for each batch k (ids[batch_off[k]..batch_off[k+1])), every
+ * distinct id x in [0, id_bound) of the batch does freq[x] += 1 (freq is
+ * accumulated into, not cleared). */
+void oracle_access_count(const int64_t* ids, const int64_t* batch_off, int64_t num_batches,
+                         int64_t id_bound, int32_t* freq);
+
+/* Selection: node and edge ids ranked by descending frequency (ties by
+ * ascending id); while i + j < alpha * (nv + ne), the node head is taken if
+ * its count is strictly greater than the edge head's, otherwise the edge
+ * head (an exhausted list never wins).  hot_v[0..*n_hot_v) and
+ * hot_e[0..*n_hot_e) receive the ids in selection order; capacities nv, ne. */
+void oracle_greedy_hot_set(const int32_t* fv, int64_t nv, const int32_t* fe, int64_t ne,
+                           double alpha, int64_t* hot_v, int64_t* n_hot_v, int64_t* hot_e,
+                           int64_t* n_hot_e);
+
 /* Backward of the time encoding for an upstream gradient dte [E, d_t]:
  *   a = fmaf(omega[j], dt_e, phi[j])  (the forward's fp32 argument)
  *   dphi[j]   = sum_e dte[e,j] * (-sin a)

@@ -24,6 +24,16 @@ MUTATIONS = {
     "te_wrong_segment": ("float dt = t_dst[v] - t_e[e];",
                          "float dt = t_dst[v > 0 ? v - 1 : 0] - t_e[e];"),
     "te_transposed_out": ("te[e * d_t + j] =", "te[(j * 0 + e) * d_t + (d_t - 1 - j)] ="),
+    "count_repeats": ("if (i > 0 && b[i] == b[i - 1]) continue;", "if (0) continue;"),
+    "count_skips_first": ("for (int64_t i = 0; i < n; ++i) {\n      if (i > 0 && b[i] == b[i - 1])",
+                          "for (int64_t i = 1; i < n; ++i) {\n      if (i > 0 && b[i] == b[i - 1])"),
+    "greedy_ties_to_nodes": ("else take_node = sv[i].f > se[j].f;", "else take_node = sv[i].f >= se[j].f;"),
+    "greedy_ascending_rank": ("if (x->f != y->f) return x->f > y->f ? -1 : 1;",
+                              "if (x->f != y->f) return x->f < y->f ? -1 : 1;"),
+    "greedy_ties_desc_id": ("return (x->id > y->id) - (x->id < y->id);\n}\n\nstatic freq_id_t",
+                            "return (x->id < y->id) - (x->id > y->id);\n}\n\nstatic freq_id_t"),
+    "greedy_budget_off_by_one": ("while ((double)(i + j) < alpha * (double)(nv + ne)",
+                                 "while ((double)(i + j) <= alpha * (double)(nv + ne)"),
     "tebwd_cos_for_sin": ("double dcos = -sin((double)arg);", "double dcos = -cos((double)arg);"),
     "tebwd_sign": ("double dcos = -sin((double)arg);", "double dcos = sin((double)arg);"),
     "tebwd_fp64_argument": ("double dcos = -sin((double)arg);",
@@ -62,6 +72,11 @@ PINS = [
     (P.test_time_encode_closed_forms, {}),
     (P.test_time_encode_double_angle_columns, {}),
     (P.test_time_encode_fp32_difference, {}),
+    (P.test_access_count_hand_example, {}),
+    (P.test_access_count_vs_numpy, {}),
+    (P.test_greedy_hot_set_hand_example, {}),
+    (P.test_greedy_hot_set_properties, dict(alpha=0.37)),
+    (P.test_greedy_hot_set_properties, dict(alpha=0.1)),
     (P.test_time_encode_bwd_finite_differences, {}),
     (P.test_time_encode_bwd_pythagorean_with_the_forward, {}),
     (P.test_fwd_vs_torch_sdpa, {}),

@@ -191,6 +191,79 @@ def test_time_encode_fp32_difference():
     assert abs(math.cos(2.0 ** 25 - 1) - math.cos(2.0 ** 25)) > 1e-2
 
 
+# ---------------------------------------------------------------- greedy cache selection (Alg. 1)
+def test_access_count_hand_example():
+    # batch 0 touches 1, 2 (twice), 5; batch 1 touches 2, 9, 1; batch 2 touches 7
+    # and an id outside the universe.  A repeat inside a batch counts once.
+    f = oracle.access_count([[1, 2, 2, 5], [2, 9, 1], [7, 12]], 10)
+    assert f.tolist() == [0, 2, 2, 0, 0, 1, 0, 1, 0, 1]
+    # counters accumulate over calls
+    f2 = oracle.access_count([[0, 0, 9]], 10, freq=f)
+    assert f2.tolist() == [1, 2, 2, 0, 0, 1, 0, 1, 0, 2]
+
+
+def test_access_count_vs_numpy():
+    r = np.random.default_rng(4)
+    bound = 5000
+    batches = [r.zipf(1.3, size=int(r.integers(0, 3000))) % bound for _ in range(40)]
+    want = np.zeros(bound, dtype=np.int64)
+    for b in batches:
+        want += np.bincount(np.unique(b), minlength=bound)
+    assert np.array_equal(oracle.access_count(batches, bound), want)
+
+
+def test_greedy_hot_set_hand_example():
+    # node counts [3, 1, 2], edge counts [2, 2, 0, 5], budget 4 of 7 ids:
+    # e3 (5) beats v0 (3); v0 (3) beats e0 (2); at the tie 2 = 2 the edge
+    # wins, so e0 then e1 (ascending id) fill the budget before v2.
+    hv, he = oracle.greedy_hot_set([3, 1, 2], [2, 2, 0, 5], 4 / 7)
+    assert hv.tolist() == [0] and he.tolist() == [3, 0, 1]
+    # budget 5: the edges with count 2 are used up, so v2 (2) beats e2 (0)
+    hv, he = oracle.greedy_hot_set([3, 1, 2], [2, 2, 0, 5], 5 / 7)
+    assert hv.tolist() == [0, 2] and he.tolist() == [3, 0, 1]
+    # budget 1.0: everything, nodes list exhausted first
+    hv, he = oracle.greedy_hot_set([3, 1, 2], [2, 2, 0, 5], 1.0)
+    assert sorted(hv.tolist()) == [0, 1, 2] and sorted(he.tolist()) == [0, 1, 2, 3]
+    # empty budget and empty lists
+    assert [x.size for x in oracle.greedy_hot_set([3, 1], [2], 0.0)] == [0, 0]
+    hv, he = oracle.greedy_hot_set(np.zeros(0), [4, 1], 1.0)
+    assert hv.size == 0 and he.tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("alpha", [0.0, 0.013, 0.1, 0.37, 0.5, 1.0])
+def test_greedy_hot_set_properties(alpha):
+    # Properties that pin the selection without re-running it: the budget
+    # ceil(alpha * (|V|+|E|)); maximal total frequency (the sum of the
+    # budget's largest counts over both lists); every selected count >= every
+    # unselected count; at the threshold count edges before nodes and, within
+    # a kind, the smallest ids; each list in descending count, ascending id.
+    r = np.random.default_rng(int(alpha * 1000) + 1)
+    fv = r.integers(0, 6, 3000).astype(np.int32)
+    fe = np.minimum(r.zipf(1.6, 7000), 6).astype(np.int32) - 1
+    nv, ne = fv.size, fe.size
+    hv, he = oracle.greedy_hot_set(fv, fe, alpha)
+    B = math.ceil(alpha * (nv + ne))
+    assert hv.size + he.size == B
+    allf = np.sort(np.concatenate([fv, fe]))[::-1]
+    assert fv[hv].sum() + fe[he].sum() == allf[:B].sum()
+    if B == 0:
+        return
+    T = min(fv[hv].min() if hv.size else 99, fe[he].min() if he.size else 99)
+    sel_v = np.zeros(nv, bool); sel_v[hv] = True
+    sel_e = np.zeros(ne, bool); sel_e[he] = True
+    assert np.all(fv[~sel_v] <= T) and np.all(fe[~sel_e] <= T)
+    assert np.all(sel_v[fv > T]) and np.all(sel_e[fe > T])
+    tie_v, tie_e = np.flatnonzero(fv == T), np.flatnonzero(fe == T)
+    if sel_v[tie_v].any():
+        assert sel_e[tie_e].all()
+    for ties, sel in ((tie_v, sel_v), (tie_e, sel_e)):
+        k = int(sel[ties].sum())
+        assert np.array_equal(np.flatnonzero(sel & np.isin(np.arange(sel.size), ties)), ties[:k])
+    for hot, f in ((hv, fv), (he, fe)):
+        order = np.lexsort((hot, -f[hot]))
+        assert np.array_equal(order, np.arange(hot.size))
+
+
 # ---------------------------------------------------------------- time-encoding backward
 def _dyadic_time_block(seed):
     """A block whose fp32 time arguments are exact: dt = k/8 (k <= 32),
