@@ -6,6 +6,8 @@
  *   fast_dedup_gather         uni_ID / inv_Idx + row reconstruction   (Sec. 4.2, Sec. 5)
  *   fast_time_encode          cos(omega * dt + phi) time features     (Sec. 6.1, TGAT)
  *   fast_time_encode_bwd      gradients of omega and phi              (Sec. 6.1)
+ *   fast_access_count         pre-sampling access counts              (Sec. 4.2, Alg. 1)
+ *   fast_greedy_hot_set       hot ids under a cache budget + slot map (Sec. 4.2, Alg. 1)
  *   fast_edge_softmax_fwd/bwd per-edge multi-head logits + ESM        (Sec. 4.3)
  *   fast_temporal_aggregate_fwd/bwd  attention-weighted AGG           (Sec. 4.3, Eq. 1)
  *   fast_edge_attention_fwd/bwd      ESM and AGG fused in one kernel  (Sec. 4.3)
@@ -131,6 +133,53 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
                                 int64_t* uni, int32_t* inv, int64_t* num_unique,
                                 void* rows, int32_t* miss, int64_t* num_miss,
                                 void* ws, size_t ws_bytes, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * SlimCache access counting over pre-sampled batches (Sec. 4.2, Alg. 1: the
+ * counting loop).  For every batch k, each DISTINCT id x of
+ *   ids[batch_offsets[k] .. batch_offsets[k+1])
+ * with 0 <= x < id_bound adds 1 to freq[x]; a repeat inside a batch counts
+ * once, so freq[x] counts the batches that touch x (the transfers a cached
+ * row saves once each batch is compressed).  freq is ACCUMULATED into, so
+ * batches may be counted over several calls; the caller zeroes it first.
+ * ids: device int64; batch_offsets: HOST int64 [num_batches+1],
+ * non-decreasing; freq: device int32 [id_bound].  One launch per batch.
+ * Limits: id_bound < 2^32, num_batches < 2^31 - 1.
+ * Workspace: fast_access_count_workspace(id_bound) bytes (a batch stamp per id).
+ * ------------------------------------------------------------------------ */
+size_t fast_access_count_workspace(int64_t id_bound);
+fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets,
+                                int64_t num_batches, int64_t id_bound, int32_t* freq,
+                                void* ws, size_t ws_bytes, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * SlimCache greedy selection of the cached ids (Sec. 4.2, Alg. 1: node and
+ * edge ids ranked by descending count, ties by ascending id; the two lists
+ * merged under the budget, a node taken only when its count is strictly
+ * greater than the edge's, an exhausted list never taken).  The result is
+ * the first min(budget, num_nodes + num_edges) ids of the combined order
+ * (count descending, edges before nodes at equal count, ascending id).
+ *   hot_v[0..*num_hot_v)  selected node ids in ASCENDING id order
+ *   slot_v[x]             position of node x in hot_v, or -1 (the cache
+ *                         slot map read by fast_dedup_gather); optional
+ *   hot_e, num_hot_e, slot_e  the same for edges
+ * freq_v [num_nodes], freq_e [num_edges]: device int32 counts (from
+ * fast_access_count); counts outside [0, max_freq] are clamped into it, so
+ * pass max_freq >= the largest count (the number of batches counted).
+ * budget: number of ids to cache; Alg. 1's fraction alpha of all ids gives
+ * budget = ceil(alpha * (num_nodes + num_edges)) evaluated in fp64.
+ * hot_v capacity min(budget, num_nodes), hot_e min(budget, num_edges); either
+ * hot list and slot map may be NULL.  num_hot_v, num_hot_e: device int64.
+ * Limits: num_nodes, num_edges < 2^31; 0 <= max_freq <= 2^24.
+ * Workspace: fast_greedy_hot_set_workspace(num_nodes, num_edges, max_freq)
+ * bytes, 256-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t fast_greedy_hot_set_workspace(int64_t num_nodes, int64_t num_edges, int32_t max_freq);
+fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_nodes, const int32_t* freq_e,
+                                  int64_t num_edges, int32_t max_freq, int64_t budget,
+                                  int64_t* hot_v, int64_t* num_hot_v, int32_t* slot_v,
+                                  int64_t* hot_e, int64_t* num_hot_e, int32_t* slot_e,
+                                  void* ws, size_t ws_bytes, fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Time encoding (Sec. 6.1: TGAT's random Fourier time features).

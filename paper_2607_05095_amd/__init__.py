@@ -17,6 +17,8 @@ __all__ = [
     "fast_version", "fast_last_error",
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
     "fast_dedup_gather_workspace", "fast_dedup_gather",
+    "fast_access_count_workspace", "fast_access_count",
+    "fast_greedy_hot_set_workspace", "fast_greedy_hot_set", "hot_set_budget",
     "fast_time_encode", "fast_time_encode_bwd_workspace", "fast_time_encode_bwd",
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
     "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
@@ -61,6 +63,11 @@ _SIGS = {
     "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
                                  _p, _p, _p, _p, _sz, _p]),
+    "fast_access_count_workspace": (_sz, [_i64]),
+    "fast_access_count": (_i32, [_p, _p, _i64, _i64, _p, _p, _sz, _p]),
+    "fast_greedy_hot_set_workspace": (_sz, [_i64, _i64, _i32]),
+    "fast_greedy_hot_set": (_i32, [_p, _i64, _p, _i64, _i32, _i64, _p, _p, _p, _p, _p, _p, _p,
+                                   _sz, _p]),
     "fast_time_encode": (_i32, [_G, _p, _p, _i32, _p, _i32, _p]),
     "fast_time_encode_bwd_workspace": (_sz, [_i64, _i32]),
     "fast_time_encode_bwd": (_i32, [_G, _p, _p, _i32, _p, _i32, _p, _p, _p, _sz, _p]),
@@ -164,6 +171,37 @@ def fast_dedup_gather(ids, n, id_bound, table, table_rows, D, dtype, slot_map, u
                                    _ptr(slot_map), _ptr(uni), _ptr(inv), _ptr(num_unique),
                                    _ptr(rows), _ptr(miss), _ptr(num_miss), _ptr(ws), ws_bytes,
                                    _stream(stream)))
+
+
+def fast_access_count_workspace(id_bound: int) -> int:
+    return lib().fast_access_count_workspace(id_bound)
+
+
+def fast_access_count(ids, batch_offsets, num_batches, id_bound, freq, ws, ws_bytes, stream=None):
+    """batch_offsets: a host sequence of num_batches + 1 int64 offsets into ids."""
+    offs = (C.c_int64 * (num_batches + 1))(*[int(x) for x in batch_offsets])
+    _check(lib().fast_access_count(_ptr(ids), C.cast(offs, C.c_void_p), num_batches, id_bound,
+                                   _ptr(freq), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def fast_greedy_hot_set_workspace(num_nodes: int, num_edges: int, max_freq: int) -> int:
+    return lib().fast_greedy_hot_set_workspace(num_nodes, num_edges, max_freq)
+
+
+def fast_greedy_hot_set(freq_v, num_nodes, freq_e, num_edges, max_freq, budget, hot_v, num_hot_v,
+                        slot_v, hot_e, num_hot_e, slot_e, ws, ws_bytes, stream=None):
+    _check(lib().fast_greedy_hot_set(_ptr(freq_v), num_nodes, _ptr(freq_e), num_edges, max_freq,
+                                     budget, _ptr(hot_v), _ptr(num_hot_v), _ptr(slot_v),
+                                     _ptr(hot_e), _ptr(num_hot_e), _ptr(slot_e), _ptr(ws),
+                                     ws_bytes, _stream(stream)))
+
+
+def hot_set_budget(alpha: float, num_nodes: int, num_edges: int) -> int:
+    """Ids that Alg. 1's loop `while i + j < alpha * (|V| + |E|)` selects:
+    ceil of the fp64 product, at most |V| + |E|."""
+    import math
+    total = int(num_nodes) + int(num_edges)
+    return max(0, min(total, math.ceil(float(alpha) * float(total))))
 
 
 def fast_time_encode(g: TCSR, omega, phi, d_t, te, te_dtype, stream=None):

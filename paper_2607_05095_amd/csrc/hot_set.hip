@@ -1,0 +1,303 @@
+// hot_set.hip -- SlimCache's greedy cache selection (Sec. 4.2, Alg. 1) on the
+// GPU: access counting over pre-sampled batches, then the choice of the hot
+// node and edge ids under a budget of cached rows, and the slot maps that the
+// row reconstruction reads.
+//
+// Counting.  Every batch adds one to the counter of each distinct id it
+// touches.  One launch per batch; each id stamps its slot with the batch tag
+// (atomicExch), and only the access that replaces an older tag increments
+// the counter, so repeats inside a batch count once.  Integer atomics make
+// the counts exact whatever the interleaving.
+//
+// Selection.  Alg. 1 ranks each kind by descending count and merges the two
+// lists, a node winning only with a strictly higher count.  The ids it takes
+// are therefore the first `budget` ids of one combined order: count
+// descending, edges before nodes at equal count, ascending id inside a kind.
+// That set is found without a sort: a histogram of the counts gives the
+// threshold count T with fewer than `budget` ids above it and enough at or
+// above it; all ids above T are taken, and of the ids at exactly T, the
+// first R_e edges and R_v nodes in id order.  One scan per kind over a packed
+// pair (ids above T, ids at T) then gives every id its position among the
+// selected ids (above-T prefix + min(at-T prefix, R)), which is both the slot
+// in the id-ordered hot list and the value of the slot map.
+#include "scan.h"
+
+namespace fast {
+
+constexpr int HS_THREADS = 256;
+constexpr int HS_LDS_BINS = 4096;  // counts below this are binned in LDS first
+
+__global__ void __launch_bounds__(HS_THREADS) k_hs_fill_i32(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * HS_THREADS)
+    p[i] = v;
+}
+
+static uint32_t grid_for(int64_t n, int64_t per_block_items, uint32_t cap = 16384) {
+  int64_t g = (n + per_block_items - 1) / per_block_items;
+  if (g < 1) g = 1;
+  return uint32_t(g < cap ? g : cap);
+}
+
+// ------------------------------------------------------------------ counting
+__global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __restrict__ ids,
+                                                            int64_t n, int64_t id_bound,
+                                                            int32_t tag, int32_t* stamp,
+                                                            int32_t* freq) {
+  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * HS_THREADS) {
+    const int64_t x = ids[i];
+    if (x < 0 || x >= id_bound) continue;
+    if (atomicExch(&stamp[x], tag) != tag) atomicAdd(&freq[x], 1);
+  }
+}
+
+// ------------------------------------------------------------------ selection
+__device__ __forceinline__ int32_t clamp_count(int32_t f, int32_t max_freq) {
+  return f < 0 ? 0 : (f > max_freq ? max_freq : f);
+}
+
+// hist[c] = number of ids whose clamped count is c, c in [0, max_freq].
+// Counts below HS_LDS_BINS go through a per-workgroup LDS histogram (almost
+// every id of a large universe has a small count), the rest straight to HBM.
+__global__ void __launch_bounds__(HS_THREADS) k_hs_hist(const int32_t* __restrict__ f, int64_t n,
+                                                       int32_t max_freq, uint32_t* hist) {
+  __shared__ uint32_t s_h[HS_LDS_BINS];
+  const int nb = max_freq + 1 < HS_LDS_BINS ? max_freq + 1 : HS_LDS_BINS;
+  for (int b = threadIdx.x; b < nb; b += HS_THREADS) s_h[b] = 0;
+  __syncthreads();
+  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * HS_THREADS) {
+    const int32_t c = clamp_count(f[i], max_freq);
+    if (c < nb) atomicAdd(&s_h[c], 1u);
+    else atomicAdd(&hist[c], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < nb; b += HS_THREADS)
+    if (s_h[b]) atomicAdd(&hist[b], s_h[b]);
+}
+
+// Threshold of the selection, written by k_hs_threshold.
+struct HsParams {
+  int32_t T;        // threshold count (max_freq + 1 when nothing is selected)
+  int32_t pad;
+  int64_t R_v;      // nodes taken among those with count T (lowest ids)
+  int64_t R_e;      // edges taken among those with count T (lowest ids)
+};
+
+// One workgroup walks the counts from max_freq down, 256 bins at a time, and
+// stops at the first count T where the ids at or above it reach the budget.
+__global__ void __launch_bounds__(HS_THREADS) k_hs_threshold(
+    const uint32_t* __restrict__ hv, const uint32_t* __restrict__ he, int32_t max_freq,
+    int64_t budget, int64_t nv, int64_t ne, HsParams* prm, int64_t* num_hot_v,
+    int64_t* num_hot_e) {
+  __shared__ uint64_t lds4[4];
+  __shared__ int64_t s_found[4];   // T, ids above T (both kinds), nodes above T, edges above T
+  __shared__ int s_hit;
+  const int64_t B = budget < nv + ne ? budget : nv + ne;
+  if (threadIdx.x == 0) s_hit = 0;
+  __syncthreads();
+  uint64_t carry_all = 0, carry_v = 0;
+  if (B > 0) {
+    for (int64_t top = max_freq; top >= 0; top -= HS_THREADS) {
+      const int64_t c = top - int64_t(threadIdx.x);          // descending counts
+      const uint64_t w_v = c >= 0 ? hv[c] : 0, w_e = c >= 0 ? he[c] : 0;
+      uint64_t tot_all, tot_v;
+      const uint64_t ex_all = block_exclusive_scan<uint64_t>(w_v + w_e, lds4, tot_all);
+      const uint64_t ex_v = block_exclusive_scan<uint64_t>(w_v, lds4, tot_v);
+      const uint64_t above = carry_all + ex_all;   // ids with count > c
+      if (c >= 0 && int64_t(above) < B && int64_t(above + w_v + w_e) >= B) {
+        s_found[0] = c;
+        s_found[1] = int64_t(above);
+        s_found[2] = int64_t(carry_v + ex_v);
+        s_found[3] = int64_t(above) - int64_t(carry_v + ex_v);
+        s_hit = 1;
+      }
+      __syncthreads();
+      if (s_hit) break;
+      carry_all += tot_all;
+      carry_v += tot_v;
+    }
+  }
+  if (threadIdx.x == 0) {
+    HsParams p;
+    p.pad = 0;
+    if (!s_hit) {                       // empty budget
+      p.T = max_freq + 1;
+      p.R_v = p.R_e = 0;
+      *num_hot_v = 0;
+      *num_hot_e = 0;
+    } else {
+      const int32_t T = int32_t(s_found[0]);
+      const int64_t R = B - s_found[1];
+      const int64_t at_e = int64_t(he[T]);
+      p.T = T;
+      p.R_e = R < at_e ? R : at_e;
+      p.R_v = R - p.R_e;
+      *num_hot_v = s_found[2] + p.R_v;
+      *num_hot_e = s_found[3] + p.R_e;
+    }
+    *prm = p;
+  }
+}
+
+// Packed scan item: high word = count above T, low word = count equal to T.
+struct InAboveAt {
+  const int32_t* f;
+  int32_t max_freq;
+  const HsParams* prm;
+  __device__ uint64_t operator()(int64_t i) const {
+    const int32_t c = clamp_count(f[i], max_freq), T = prm->T;
+    return (c > T ? (uint64_t(1) << 32) : 0) | (c == T ? 1u : 0u);
+  }
+};
+struct OutHot {
+  const HsParams* prm;
+  bool edges;
+  int64_t cap;         // capacity of hot
+  int64_t* hot;        // id-ordered hot list, or NULL
+  int32_t* slot;       // slot map, or NULL
+  __device__ void operator()(int64_t i, uint64_t prefix, uint64_t v) const {
+    const int64_t R = edges ? prm->R_e : prm->R_v;
+    const int64_t above = int64_t(prefix >> 32), at = int64_t(prefix & 0xffffffffu);
+    const bool sel = (v >> 32) != 0 || ((v & 1u) != 0 && at < R);
+    const int64_t pos = above + (at < R ? at : R);
+    if (slot) slot[i] = sel ? int32_t(pos) : -1;
+    if (sel && hot && pos < cap) hot[pos] = i;
+  }
+};
+
+struct HsWs {
+  uint32_t* hv;
+  uint32_t* he;
+  HsParams* prm;
+  void* scan_v;
+  void* scan_e;
+};
+
+static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, HsWs* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  char* hv = take(size_t(max_freq + 1) * 4);
+  char* he = take(size_t(max_freq + 1) * 4);
+  char* pr = take(sizeof(HsParams));
+  char* sv = take(scan_workspace<uint64_t>(nv));
+  char* se = take(scan_workspace<uint64_t>(ne));
+  if (ws) {
+    ws->hv = reinterpret_cast<uint32_t*>(hv);
+    ws->he = reinterpret_cast<uint32_t*>(he);
+    ws->prm = reinterpret_cast<HsParams*>(pr);
+    ws->scan_v = sv;
+    ws->scan_e = se;
+  }
+  return off;
+}
+
+}  // namespace fast
+
+using namespace fast;
+
+static const int32_t HS_MAX_FREQ = (1 << 24);
+
+extern "C" size_t fast_access_count_workspace(int64_t id_bound) {
+  if (id_bound < 0 || id_bound >= (int64_t(1) << 32)) return 0;
+  return align_up(size_t(id_bound) * 4, 256) + 256;
+}
+
+extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets,
+                                           int64_t num_batches, int64_t id_bound, int32_t* freq,
+                                           void* ws, size_t ws_bytes, fast_stream_t stream) {
+  const char* fn = "fast_access_count";
+  if (num_batches < 0 || id_bound < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
+  if (num_batches >= (int64_t(1) << 31) - 1)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: too many batches", fn);
+  if (id_bound >= (int64_t(1) << 32)) return fail(FAST_ERR_UNSUPPORTED, "%s: id_bound >= 2^32", fn);
+  if (num_batches == 0 || id_bound == 0) return ok();
+  if (!batch_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: batch_offsets is NULL", fn);
+  if (batch_offsets[0] < 0) return fail(FAST_ERR_INVALID_ARG, "%s: batch_offsets[0] < 0", fn);
+  for (int64_t k = 0; k < num_batches; ++k)
+    if (batch_offsets[k + 1] < batch_offsets[k])
+      return fail(FAST_ERR_INVALID_ARG, "%s: batch_offsets decrease at %lld", fn, (long long)k);
+  if (batch_offsets[num_batches] > batch_offsets[0] && !ids)
+    return fail(FAST_ERR_INVALID_ARG, "%s: ids is NULL", fn);
+  if (!freq) return fail(FAST_ERR_INVALID_ARG, "%s: freq is NULL", fn);
+  const size_t need = fast_access_count_workspace(id_bound);
+  if (!ws || ws_bytes < need)
+    return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
+  if (!aligned(ws, 4) || !aligned(freq, 4))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: freq or workspace not 4-byte aligned", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* stamp = static_cast<int32_t*>(ws);
+  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(id_bound, HS_THREADS * 8)), dim3(HS_THREADS), 0,
+                     st, stamp, id_bound, 0);
+  for (int64_t k = 0; k < num_batches; ++k) {
+    const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
+    if (n == 0) continue;
+    hipLaunchKernelGGL(k_access_count, dim3(grid_for(n, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
+                       ids + batch_offsets[k], n, id_bound, int32_t(k + 1), stamp, freq);
+  }
+  return check_launch(fn);
+}
+
+extern "C" size_t fast_greedy_hot_set_workspace(int64_t num_nodes, int64_t num_edges,
+                                                int32_t max_freq) {
+  if (num_nodes < 0 || num_edges < 0 || max_freq < 0 || max_freq > HS_MAX_FREQ) return 0;
+  if (num_nodes >= (int64_t(1) << 32) || num_edges >= (int64_t(1) << 32)) return 0;
+  return hs_layout(num_nodes, num_edges, max_freq, nullptr, nullptr);
+}
+
+extern "C" fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_nodes,
+                                             const int32_t* freq_e, int64_t num_edges,
+                                             int32_t max_freq, int64_t budget, int64_t* hot_v,
+                                             int64_t* num_hot_v, int32_t* slot_v, int64_t* hot_e,
+                                             int64_t* num_hot_e, int32_t* slot_e, void* ws,
+                                             size_t ws_bytes, fast_stream_t stream) {
+  const char* fn = "fast_greedy_hot_set";
+  if (num_nodes < 0 || num_edges < 0 || budget < 0)
+    return fail(FAST_ERR_INVALID_ARG, "%s: negative size or budget", fn);
+  if (max_freq < 0 || max_freq > HS_MAX_FREQ)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: max_freq outside [0, 2^24]", fn);
+  if (num_nodes >= (int64_t(1) << 31) || num_edges >= (int64_t(1) << 31))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: 2^31 or more ids of one kind", fn);
+  if (!num_hot_v || !num_hot_e) return fail(FAST_ERR_INVALID_ARG, "%s: NULL num_hot_v/num_hot_e", fn);
+  if (num_nodes > 0 && !freq_v) return fail(FAST_ERR_INVALID_ARG, "%s: freq_v is NULL", fn);
+  if (num_edges > 0 && !freq_e) return fail(FAST_ERR_INVALID_ARG, "%s: freq_e is NULL", fn);
+  const size_t need = fast_greedy_hot_set_workspace(num_nodes, num_edges, max_freq);
+  if (!ws || ws_bytes < need)
+    return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  HsWs w;
+  hs_layout(num_nodes, num_edges, max_freq, static_cast<char*>(ws), &w);
+  const int64_t nbins = int64_t(max_freq) + 1;
+  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(nbins, HS_THREADS)), dim3(HS_THREADS), 0, st,
+                     reinterpret_cast<int32_t*>(w.hv), nbins, 0);
+  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(nbins, HS_THREADS)), dim3(HS_THREADS), 0, st,
+                     reinterpret_cast<int32_t*>(w.he), nbins, 0);
+  if (num_nodes > 0)
+    hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_nodes, HS_THREADS * 16, 4096)), dim3(HS_THREADS),
+                       0, st, freq_v, num_nodes, max_freq, w.hv);
+  if (num_edges > 0)
+    hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_edges, HS_THREADS * 16, 4096)), dim3(HS_THREADS),
+                       0, st, freq_e, num_edges, max_freq, w.he);
+  hipLaunchKernelGGL(k_hs_threshold, dim3(1), dim3(HS_THREADS), 0, st, w.hv, w.he, max_freq,
+                     budget, num_nodes, num_edges, w.prm, num_hot_v, num_hot_e);
+  const int64_t B = budget < num_nodes + num_edges ? budget : num_nodes + num_edges;
+  hipError_t e = hipSuccess;
+  if (num_nodes > 0 && (hot_v || slot_v))
+    e = scan_launch<InAboveAt, OutHot, uint64_t>(
+        InAboveAt{freq_v, max_freq, w.prm},
+        OutHot{w.prm, false, B < num_nodes ? B : num_nodes, hot_v, slot_v}, num_nodes, w.scan_v,
+        nullptr, nullptr, st);
+  if (e == hipSuccess && num_edges > 0 && (hot_e || slot_e))
+    e = scan_launch<InAboveAt, OutHot, uint64_t>(
+        InAboveAt{freq_e, max_freq, w.prm},
+        OutHot{w.prm, true, B < num_edges ? B : num_edges, hot_e, slot_e}, num_edges, w.scan_e,
+        nullptr, nullptr, st);
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+  return check_launch(fn);
+}

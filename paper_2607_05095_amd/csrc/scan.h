@@ -1,8 +1,10 @@
-// scan.h -- device-wide exclusive scan over uint32 items (three launches:
-// per-tile reduce, one-block scan of the tile sums, per-tile down-sweep).
-// Item producers and prefix consumers are functors, so callers fuse their
-// own load (counts, bitmap popcounts, miss flags) and store (offsets, word
-// ranks, compaction scatter) into the scan's two passes over the data.
+// scan.h -- device-wide exclusive scan over uint32 (default) or uint64 items
+// (three launches: per-tile reduce, one-block scan of the tile sums, per-tile
+// down-sweep).  Item producers and prefix consumers are functors, so callers
+// fuse their own load (counts, bitmap popcounts, miss flags) and store
+// (offsets, word ranks, compaction scatter) into the scan's two passes over
+// the data.  A uint64 item can carry two 32-bit counters that are scanned
+// together (high and low word), as long as neither total reaches 2^32.
 #pragma once
 
 #include "common.h"
@@ -14,29 +16,30 @@ constexpr int SCAN_ITEMS = 8;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
 
 inline int64_t scan_tiles(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE; }
-// Workspace of one scan over n items: the tile sums plus the total.
+// Workspace of one scan over n items of type T: the tile sums plus the total.
+template <typename T = uint32_t>
 inline size_t scan_workspace(int64_t n) {
-  return align_up(size_t(scan_tiles(n) + 1) * sizeof(uint32_t), 256);
+  return align_up(size_t(scan_tiles(n) + 1) * sizeof(T), 256);
 }
 
 // Exclusive prefix of a 256-thread block; returns the thread's exclusive
-// prefix and writes the block total.  Uses 4 words of LDS.
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* lds4,
-                                                         uint32_t& total) {
+// prefix and writes the block total.  Uses 4 items of LDS.
+template <typename T>
+__device__ __forceinline__ T block_exclusive_scan(T x, T* lds4, T& total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint32_t inc = x;
+  T inc = x;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    uint32_t y = __shfl_up(inc, o, 64);
+    T y = __shfl_up(inc, o, 64);
     if (lane >= o) inc += y;
   }
   if (lane == 63) lds4[wid] = inc;
   __syncthreads();
-  uint32_t before = 0, tot = 0;
+  T before = 0, tot = 0;
 #pragma unroll
   for (int w = 0; w < SCAN_THREADS / 64; ++w) {
-    uint32_t v = lds4[w];
-    before += (w < wid) ? v : 0u;
+    T v = lds4[w];
+    before += (w < wid) ? v : T(0);
     tot += v;
   }
   __syncthreads();
@@ -44,34 +47,34 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* l
   return before + inc - x;
 }
 
-template <class In>
-__global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(In in, int64_t n, uint32_t* tsum) {
-  __shared__ uint32_t lds4[4];
+template <class In, typename T = uint32_t>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(In in, int64_t n, T* tsum) {
+  __shared__ T lds4[4];
   const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
-  uint32_t s = 0;
+  T s = 0;
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int64_t i = base + k * SCAN_THREADS + threadIdx.x;
     if (i < n) s += in(i);
   }
-  uint32_t total;
+  T total;
   block_exclusive_scan(s, lds4, total);
   if (threadIdx.x == 0) tsum[blockIdx.x] = total;
 }
 
 // One 256-thread block scans the nt tile sums in place (exclusive) and
 // stores the grand total at tsum[nt] and into the optional outputs.
-template <int UNUSED = 0>
-__global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(uint32_t* tsum, int64_t nt,
+template <typename T = uint32_t>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* tsum, int64_t nt,
                                                            int64_t* total_i64,
                                                            int32_t* total_i32) {
-  __shared__ uint32_t lds4[4];
-  uint32_t carry = 0;
+  __shared__ T lds4[4];
+  T carry = 0;
   for (int64_t b0 = 0; b0 < nt; b0 += SCAN_THREADS) {
     const int64_t i = b0 + threadIdx.x;
-    const uint32_t x = (i < nt) ? tsum[i] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan(x, lds4, total);
+    const T x = (i < nt) ? tsum[i] : T(0);
+    T total;
+    const T ex = block_exclusive_scan(x, lds4, total);
     if (i < nt) tsum[i] = carry + ex;
     carry += total;
   }
@@ -82,29 +85,29 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(uint32_t* tsum, int64
   }
 }
 
-template <class In, class Out>
+template <class In, class Out, typename T = uint32_t>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
-                                                            const uint32_t* tsum, Out out) {
-  __shared__ uint32_t tile[SCAN_TILE + SCAN_TILE / 32];
-  __shared__ uint32_t lds4[4];
+                                                            const T* tsum, Out out) {
+  __shared__ T tile[SCAN_TILE + SCAN_TILE / 32];
+  __shared__ T lds4[4];
   const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
   // striped, coalesced load into LDS (padded every 32 words against bank conflicts)
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int j = k * SCAN_THREADS + threadIdx.x;
     const int64_t i = base + j;
-    tile[j + (j >> 5)] = (i < n) ? in(i) : 0u;
+    tile[j + (j >> 5)] = (i < n) ? in(i) : T(0);
   }
   __syncthreads();
-  uint32_t v[SCAN_ITEMS], s = 0;
+  T v[SCAN_ITEMS], s = 0;
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int j = threadIdx.x * SCAN_ITEMS + k;
     v[k] = tile[j + (j >> 5)];
     s += v[k];
   }
-  uint32_t total;
-  uint32_t run = block_exclusive_scan(s, lds4, total) + tsum[blockIdx.x];
+  T total;
+  T run = block_exclusive_scan(s, lds4, total) + tsum[blockIdx.x];
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int64_t i = base + threadIdx.x * SCAN_ITEMS + k;
@@ -113,19 +116,22 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
   }
 }
 
-// Enqueues the three launches.  ws must hold scan_workspace(n) bytes.
-// total_i64 / total_i32 (device, optional) receive the sum of all items.
-template <class In, class Out>
+// Enqueues the three launches.  ws must hold scan_workspace<T>(n) bytes; the
+// grand total is left at ((T*)ws)[scan_tiles(n)].  total_i64 / total_i32
+// (device, optional) receive the sum of all items.
+template <class In, class Out, typename T = uint32_t>
 hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
                        int32_t* total_i32, hipStream_t st) {
-  uint32_t* tsum = static_cast<uint32_t*>(ws);
+  T* tsum = static_cast<T*>(ws);
   const int64_t nt = scan_tiles(n);
   if (nt > 0) {
-    hipLaunchKernelGGL(k_scan_reduce<In>, dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n, tsum);
+    hipLaunchKernelGGL((k_scan_reduce<In, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n,
+                       tsum);
   }
-  hipLaunchKernelGGL(k_scan_top<0>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, nt, total_i64, total_i32);
+  hipLaunchKernelGGL(k_scan_top<T>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, nt, total_i64,
+                     total_i32);
   if (nt > 0) {
-    hipLaunchKernelGGL((k_scan_down<In, Out>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
+    hipLaunchKernelGGL((k_scan_down<In, Out, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
                        in, n, tsum, out);
   }
   return hipGetLastError();

@@ -107,6 +107,7 @@ class Batch:
     edge_cache_rows: Optional[int]  # None: edge table is indexed by id
     edge_map: Optional[tuple] = None  # (a, b): rank r -> id (a*(r-1)+b) % bound
     seed: int = 0
+    node_map: Optional[tuple] = None  # the same for node ids (Zipf laws only)
     extra: dict = field(default_factory=dict)
 
     @property
@@ -254,7 +255,28 @@ def make_batch(cfg: int, seed: Optional[int] = None) -> Batch:
                  dtype=c["dtype"], blocks=blocks, node_ids=node_ids,
                  edge_ids=all_eids, node_bound=node_bound, edge_bound=edge_bound,
                  node_D=c["node_D"], edge_D=c["edge_D"],
-                 edge_cache_rows=c["edge_cache_rows"], edge_map=edge_map, seed=seed)
+                 edge_cache_rows=c["edge_cache_rows"], edge_map=edge_map, seed=seed,
+                 node_map=node_map)
+
+
+def presampled_ids(cfg: int, num_batches: int, seed: Optional[int] = None):
+    """Node and edge ids of `num_batches` pre-sampled batches of one graph:
+    the id laws, sizes and rank -> id maps of make_batch(cfg, seed), with a
+    fresh draw per batch (stream 100 + k), so that the hot ids agree with
+    the batch that make_batch returns.  An edge law that is a per-batch
+    permutation becomes uniform over its bound.  Returns (node_batches,
+    edge_batches, node_bound, edge_bound)."""
+    c = CONFIGS[cfg]
+    b = make_batch(cfg, seed)
+    nodes, edges = [], []
+    node_law, edge_law = c["node_law"], c["edge_law"]
+    if edge_law[0] == "perm":
+        edge_law = ("uniform", b.edge_bound)
+    for k in range(num_batches):
+        r = _rng(b.seed, 100 + k)
+        nodes.append(_draw_ids(node_law, b.node_ids.size, r, b.node_map))
+        edges.append(_draw_ids(edge_law, b.edge_ids.size, r, b.edge_map))
+    return nodes, edges, b.node_bound, b.edge_bound
 
 
 def tiny_graph(counts, H=2, dh=4, seed=7):

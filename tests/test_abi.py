@@ -195,3 +195,48 @@ def test_time_encode_bwd_validation_and_workspace_query():
     assert call(g=ctypes.byref(_g(N=-1))) == INVALID
     assert call(g=ctypes.byref(_g(E=1 << 31))) == UNSUPPORTED
     assert fast.fast_last_error() != ""
+
+
+def test_hot_set_validation_and_workspace_queries():
+    L = fast.lib()
+    assert L.fast_access_count_workspace(1000) >= 4000
+    assert L.fast_access_count_workspace(-1) == 0
+    assert L.fast_access_count_workspace(1 << 32) == 0
+    offs = (ctypes.c_int64 * 3)(0, 10, 25)
+    bad = (ctypes.c_int64 * 3)(0, 10, 5)
+    p = lambda a: ctypes.cast(a, ctypes.c_void_p)
+    wsb = L.fast_access_count_workspace(1000)
+    # host-side checks (no launch happens for any of these)
+    assert L.fast_access_count(FAKE, p(offs), -1, 1000, FAKE, FAKE, wsb, None) == INVALID
+    assert L.fast_access_count(FAKE, p(bad), 2, 1000, FAKE, FAKE, wsb, None) == INVALID
+    assert L.fast_access_count(FAKE, None, 2, 1000, FAKE, FAKE, wsb, None) == INVALID
+    assert L.fast_access_count(None, p(offs), 2, 1000, FAKE, FAKE, wsb, None) == INVALID
+    assert L.fast_access_count(FAKE, p(offs), 2, 1000, None, FAKE, wsb, None) == INVALID
+    assert L.fast_access_count(FAKE, p(offs), 2, 1000, FAKE, FAKE, wsb - 1, None) == WORKSPACE
+    assert L.fast_access_count(FAKE, p(offs), 2, 1 << 32, FAKE, FAKE, wsb, None) == UNSUPPORTED
+    assert L.fast_access_count(None, None, 0, 1000, None, None, 0, None) == OK     # nothing to count
+
+    ws = L.fast_greedy_hot_set_workspace(1000, 5000, 64)
+    assert ws > 2 * 65 * 4
+    assert L.fast_greedy_hot_set_workspace(1000, 5000, -1) == 0
+    assert L.fast_greedy_hot_set_workspace(1000, 5000, (1 << 24) + 1) == 0
+
+    def sel(**k):
+        return L.fast_greedy_hot_set(
+            k.get("fv", FAKE), k.get("nv", 1000), k.get("fe", FAKE), k.get("ne", 5000),
+            k.get("mf", 64), k.get("budget", 100), FAKE, k.get("nhv", FAKE), None, FAKE,
+            k.get("nhe", FAKE), None, k.get("ws", FAKE), k.get("wsb", ws), None)
+
+    assert sel(nv=-1) == INVALID
+    assert sel(budget=-1) == INVALID
+    assert sel(mf=-1) == UNSUPPORTED
+    assert sel(nv=1 << 31) == UNSUPPORTED
+    assert sel(nhv=None) == INVALID
+    assert sel(fv=None) == INVALID
+    assert sel(fe=None) == INVALID
+    assert sel(wsb=ws - 1) == WORKSPACE
+    assert sel(ws=FAKE + 8) == UNSUPPORTED                      # workspace alignment
+    assert fast.hot_set_budget(0.1, 5, 5) == 1                  # fp64 0.1 * 10 == 1.0
+    assert fast.hot_set_budget(0.15, 5, 5) == 2
+    assert fast.hot_set_budget(2.0, 5, 5) == 10
+    assert fast.hot_set_budget(0.0, 5, 5) == 0

@@ -1,0 +1,163 @@
+"""GPU parity of SlimCache's greedy cache selection (Alg. 1) through the C
+ABI: access counts bit-exact against the oracle, and the hot node / edge
+sets and slot maps bit-exact against the oracle's selection (the oracle
+returns ids in selection order, the library in ascending id order, so sets
+are compared sorted and the slot map is checked against that order).
+
+At the big-dedup universe (1e7 nodes, 2e8 edges) the oracle's sort of 2.1e8
+ids is out of reach; there the counts are still compared bit-exactly, and
+the selection is checked by properties that fix it at any size: the budget,
+the count threshold (everything above taken, nothing below), edges before
+nodes and lowest ids first at the threshold, the slot map as the rank in
+the hot list, and maximal total count.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05095_amd as fast
+from synth import presampled_ids
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+def _count_gpu(batches, bound, freq=None):
+    sizes = [b.size for b in batches]
+    ids = torch.from_numpy(np.concatenate(batches).astype(np.int64)).cuda()
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    f = torch.zeros(bound, dtype=torch.int32, device="cuda") if freq is None else freq
+    wsb = fast.fast_access_count_workspace(bound)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_access_count(ids, offs, len(batches), bound, f, ws, wsb)
+    torch.cuda.synchronize()
+    return f
+
+
+def _select_gpu(fv, fe, max_freq, budget, want_slots=True):
+    nv, ne = fv.numel(), fe.numel()
+    hv = torch.full((max(min(budget, nv), 1),), -7, dtype=torch.int64, device="cuda")
+    he = torch.full((max(min(budget, ne), 1),), -7, dtype=torch.int64, device="cuda")
+    nhv = torch.empty(1, dtype=torch.int64, device="cuda")
+    nhe = torch.empty(1, dtype=torch.int64, device="cuda")
+    sv = torch.empty(nv, dtype=torch.int32, device="cuda") if want_slots else None
+    se = torch.empty(ne, dtype=torch.int32, device="cuda") if want_slots else None
+    wsb = fast.fast_greedy_hot_set_workspace(nv, ne, max_freq)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_greedy_hot_set(fv, nv, fe, ne, max_freq, budget, hv, nhv, sv, he, nhe, se, ws, wsb)
+    torch.cuda.synchronize()
+    a, b = int(nhv.item()), int(nhe.item())
+    return hv[:a].cpu().numpy(), he[:b].cpu().numpy(), sv, se
+
+
+def _check_slots(slot, hot, n):
+    want = np.full(n, -1, dtype=np.int32)
+    want[hot] = np.arange(hot.size, dtype=np.int32)
+    assert np.array_equal(slot.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("cfg,k", [(2, 12), (3, 4), (1, 6)])
+def test_access_count_and_selection_vs_oracle(cfg, k):
+    nodes, edges, nb, eb = presampled_ids(cfg, k)
+    _announce(f"hot set cfg={cfg} batches={k} |V|={nb} |E|={eb}")
+    fv = _count_gpu(nodes, nb)
+    fe = _count_gpu(edges, eb)
+    rv, re_ = oracle.access_count(nodes, nb), oracle.access_count(edges, eb)
+    assert np.array_equal(fv.cpu().numpy(), rv)
+    assert np.array_equal(fe.cpu().numpy(), re_)
+    for alpha in (0.0, 0.003, 0.01, 0.1, 0.35, 1.0, 1.5):
+        B = fast.hot_set_budget(alpha, nb, eb)
+        hv, he, sv, se = _select_gpu(fv, fe, k, B)
+        ov, oe = oracle.greedy_hot_set(rv, re_, alpha)
+        assert hv.size + he.size == B == ov.size + oe.size, alpha
+        assert np.array_equal(hv, np.sort(ov)), f"node set alpha={alpha}"
+        assert np.array_equal(he, np.sort(oe)), f"edge set alpha={alpha}"
+        _check_slots(sv, hv, nb)
+        _check_slots(se, he, eb)
+
+
+def test_access_count_repeats_invalid_ids_and_accumulation():
+    _announce("access count edge cases")
+    bound = 1000
+    batches = [np.array([5, 5, 5, 999, 0, -1, 1000, 7 << 40], np.int64),
+               np.zeros(0, np.int64), np.array([5, 3, 3], np.int64)]
+    f = _count_gpu(batches, bound)
+    f = _count_gpu([np.array([3, 998], np.int64)], bound, freq=f)      # accumulates
+    want = oracle.access_count([np.array([3, 998])], bound,
+                               freq=oracle.access_count(batches, bound))
+    assert np.array_equal(f.cpu().numpy(), want)
+    assert f[5].item() == 2 and f[3].item() == 2 and f[999].item() == 1
+
+
+def test_selection_edge_cases():
+    _announce("hot set edge cases")
+    dev = lambda a: torch.tensor(a, dtype=torch.int32, device="cuda")
+    # the hand example of the oracle pins: budget 4 of 7 ids
+    hv, he, sv, se = _select_gpu(dev([3, 1, 2]), dev([2, 2, 0, 5]), 5, 4)
+    assert hv.tolist() == [0] and he.tolist() == [0, 1, 3]
+    assert sv.cpu().tolist() == [0, -1, -1] and se.cpu().tolist() == [0, 1, -1, 2]
+    # all counts equal: edges first, lowest ids
+    hv, he, _, _ = _select_gpu(dev([1] * 5), dev([1] * 4), 1, 6)
+    assert he.tolist() == [0, 1, 2, 3] and hv.tolist() == [0, 1]
+    # no nodes; no edges; zero budget; counts above max_freq are clamped
+    hv, he, _, _ = _select_gpu(dev([]), dev([0, 9, 2]), 9, 2)
+    assert hv.size == 0 and he.tolist() == [1, 2]
+    hv, he, _, _ = _select_gpu(dev([4, 0, 4]), dev([]), 4, 2)
+    assert hv.tolist() == [0, 2] and he.size == 0
+    hv, he, sv, se = _select_gpu(dev([4, 0]), dev([1]), 4, 0)
+    assert hv.size == 0 and he.size == 0 and sv.cpu().tolist() == [-1, -1]
+    # a budget beyond every id takes everything
+    hv, he, _, _ = _select_gpu(dev([0, 0]), dev([0]), 3, 10)
+    assert hv.tolist() == [0, 1] and he.tolist() == [0]
+    # a wide count range (several 256-count chunks of the threshold search,
+    # counts above the LDS-binned range)
+    r = np.random.default_rng(1)
+    fv_np = r.integers(0, 9000, 20000).astype(np.int32)
+    fe_np = r.integers(0, 9000, 30000).astype(np.int32)
+    for alpha in (0.001, 0.2, 0.77):
+        B = fast.hot_set_budget(alpha, fv_np.size, fe_np.size)
+        hv, he, _, _ = _select_gpu(dev(fv_np), dev(fe_np), 9000, B, want_slots=False)
+        ov, oe = oracle.greedy_hot_set(fv_np, fe_np, alpha)
+        assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe))
+
+
+def test_bigdedup_universe_properties():
+    k = 4
+    nodes, edges, nb, eb = presampled_ids(4, k)
+    _announce(f"hot set bigdedup |V|={nb} |E|={eb} batches={k}")
+    fv = _count_gpu(nodes, nb)
+    fe = _count_gpu(edges, eb)
+    rv = oracle.access_count(nodes, nb)
+    assert np.array_equal(fv.cpu().numpy(), rv)
+    re_ = oracle.access_count(edges, eb)
+    assert np.array_equal(fe.cpu().numpy(), re_)
+    del nodes, edges
+    B = fast.hot_set_budget(0.01, nb, eb)           # ~2.1e6 cached rows
+    hv, he, sv, se = _select_gpu(fv, fe, k, B)
+    assert hv.size + he.size == B
+    # threshold T: every selected count >= T >= every unselected count
+    T = min(rv[hv].min() if hv.size else k + 1, re_[he].min() if he.size else k + 1)
+    sel_v = np.zeros(nb, bool); sel_v[hv] = True
+    sel_e = np.zeros(eb, bool); sel_e[he] = True
+    assert np.all(sel_v[rv > T]) and np.all(sel_e[re_ > T])
+    assert not np.any(sel_v[rv < T]) and not np.any(sel_e[re_ < T])
+    tie_v, tie_e = np.flatnonzero(rv == T), np.flatnonzero(re_ == T)
+    nt_v, nt_e = int(sel_v[tie_v].sum()), int(sel_e[tie_e].sum())
+    if nt_v:
+        assert nt_e == tie_e.size                       # edges before nodes at T
+    assert sel_v[tie_v[:nt_v]].all() and sel_e[tie_e[:nt_e]].all()   # lowest ids first
+    # maximal total count: the budget's largest counts over both kinds
+    hist = np.bincount(rv, minlength=k + 1) + np.bincount(re_, minlength=k + 1)
+    best, left = 0, B
+    for c in range(k, -1, -1):
+        t = min(left, int(hist[c]))
+        best += t * c
+        left -= t
+    assert int(rv[hv].sum()) + int(re_[he].sum()) == best
+    assert np.all(np.diff(hv) > 0) and np.all(np.diff(he) > 0)
+    _check_slots(sv, hv, nb)
+    _check_slots(se, he, eb)
