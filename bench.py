@@ -241,7 +241,8 @@ def time_encode_bwd_bytes(N, E, d_t, esz):
 def widened_ops(b, step, torch, fast, reps=10):
     """Operators beyond the timed step, each timed alone with HIP events on
     its launch stream (mean of `reps` launches after one warm-up): the
-    time-encoding backward of each layer block, on a seeded upstream gradient."""
+    time-encoding backward of each layer block, on a seeded upstream
+    gradient, and the cache selection of Alg. 1."""
     from synth import _randn
     esz = 4 if b.dtype == "f32" else 2
     res = {}
@@ -273,7 +274,80 @@ def widened_ops(b, step, torch, fast, reps=10):
             "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
         del dte, ws
+    res.update(hot_set_ops(b, torch, fast))
     return res
+
+
+def _events_ms(torch, fn, reps):
+    st = torch.cuda.current_stream()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record(st)
+    for _ in range(reps):
+        fn()
+    e.record(st)
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / reps
+
+
+def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3):
+    """SlimCache's pre-training cache selection (Alg. 1) over `num_batches`
+    pre-sampled batches of this workload's graph: access counting of node and
+    edge ids, then the greedy selection of alpha * (|V| + |E|) ids with both
+    slot maps."""
+    from synth import presampled_ids
+    nodes, edges, nb, eb = presampled_ids(b.cfg, num_batches)
+    res = {}
+    freqs = []
+    for kind, batches, bound in (("nodes", nodes, nb), ("edges", edges, eb)):
+        ids = torch.from_numpy(np.concatenate(batches)).cuda()
+        offs = np.concatenate([[0], np.cumsum([x.size for x in batches])]).astype(np.int64)
+        f = torch.zeros(bound, dtype=torch.int32, device="cuda")
+        wsb = fast.fast_access_count_workspace(bound)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+
+        def count():
+            fast.fast_access_count(ids, offs, num_batches, bound, f, ws, wsb)
+        count()
+        ms = _events_ms(torch, count, reps)
+        f.zero_()
+        count()
+        freqs.append(f)
+        n = int(ids.numel())
+        res[f"access_count_{kind}"] = {
+            "ms": round(ms, 4), "ids": n, "id_bound": bound, "batches": num_batches,
+            "bound": "random 4-byte atomics (one exchange per id, one add per distinct id)",
+            "ids_per_s": round(n / (ms * 1e-3), 1),
+        }
+        del ids, ws
+    fv, fe = freqs
+    B = fast.hot_set_budget(alpha, nb, eb)
+    hv = torch.empty(max(min(B, nb), 1), dtype=torch.int64, device="cuda")
+    he = torch.empty(max(min(B, eb), 1), dtype=torch.int64, device="cuda")
+    nhv = torch.empty(1, dtype=torch.int64, device="cuda")
+    nhe = torch.empty(1, dtype=torch.int64, device="cuda")
+    sv = torch.empty(nb, dtype=torch.int32, device="cuda")
+    se = torch.empty(eb, dtype=torch.int32, device="cuda")
+    wsb = fast.fast_greedy_hot_set_workspace(nb, eb, num_batches)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+
+    def select():
+        fast.fast_greedy_hot_set(fv, nb, fe, eb, num_batches, B, hv, nhv, sv, he, nhe, se, ws, wsb)
+    select()
+    ms = _events_ms(torch, select, reps)
+    nbytes = greedy_hot_set_bytes(nb, eb, B)
+    res["greedy_hot_set"] = {
+        "ms": round(ms, 4), "budget": B, "hot_nodes": int(nhv.item()), "hot_edges": int(nhe.item()),
+        "algorithmic_bytes": nbytes, "bound": "hbm",
+        "achieved_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+        "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+    }
+    return res
+
+
+def greedy_hot_set_bytes(nv, ne, B):
+    """Read every count once, write every slot-map entry, write the hot ids."""
+    return 4 * (nv + ne) + 4 * (nv + ne) + 8 * B
 
 
 def cpu_baseline(b, step, torch, frac, min_seconds=10.0):

@@ -7,7 +7,8 @@
 // touches.  One launch per batch; each id stamps its slot with the batch tag
 // (atomicExch), and only the access that replaces an older tag increments
 // the counter, so repeats inside a batch count once.  Integer atomics make
-// the counts exact whatever the interleaving.
+// the counts exact whatever the interleaving; an LDS hash per workgroup
+// drops most repeats before they reach HBM.
 //
 // Selection.  Alg. 1 ranks each kind by descending count and merges the two
 // lists, a node winning only with a strictly higher count.  The ids it takes
@@ -26,6 +27,7 @@ namespace fast {
 
 constexpr int HS_THREADS = 256;
 constexpr int HS_LDS_BINS = 4096;  // counts below this are binned in LDS first
+constexpr int HS_REG_BINS = 4;     // counts below this are binned in registers
 
 __global__ void __launch_bounds__(HS_THREADS) k_hs_fill_i32(int32_t* p, int64_t n, int32_t v) {
   for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
@@ -40,15 +42,54 @@ static uint32_t grid_for(int64_t n, int64_t per_block_items, uint32_t cap = 1638
 }
 
 // ------------------------------------------------------------------ counting
+constexpr int HS_CHUNK = 4096;              // ids per workgroup step
+constexpr int HS_HASH = 2 * HS_CHUNK;       // LDS hash slots (load <= 1/2)
+constexpr int HS_PROBES = 32;
+constexpr uint32_t HS_EMPTY = 0xffffffffu;  // never an id: id_bound < 2^32
+
+// Marks id x for batch `tag`; counts it if the batch had not marked it yet.
+__device__ __forceinline__ void stamp_and_count(int64_t x, int32_t tag, int32_t* stamp,
+                                                int32_t* freq) {
+  // read the stamp in L2 first; a stale read falls through to the exchange,
+  // which decides exactly
+  if (__hip_atomic_load(&stamp[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == tag) return;
+  if (atomicExch(&stamp[x], tag) != tag) atomicAdd(&freq[x], 1);
+}
+
+// A hot id repeats thousands of times in a batch.  Each workgroup takes
+// HS_CHUNK ids at a time and drops repeats inside the chunk through an LDS
+// hash of 32-bit keys (a plain read first, a compare-and-swap only into an
+// empty slot), so only an id's first occurrence in the chunk touches HBM.
+// A probe sequence that finds no room also goes to HBM: the stamp there
+// decides exactly, the hash is only a filter.
 __global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __restrict__ ids,
                                                             int64_t n, int64_t id_bound,
                                                             int32_t tag, int32_t* stamp,
                                                             int32_t* freq) {
-  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
-       i += int64_t(gridDim.x) * HS_THREADS) {
-    const int64_t x = ids[i];
-    if (x < 0 || x >= id_bound) continue;
-    if (atomicExch(&stamp[x], tag) != tag) atomicAdd(&freq[x], 1);
+  __shared__ uint32_t s_key[HS_HASH];
+  for (int64_t c0 = int64_t(blockIdx.x) * HS_CHUNK; c0 < n; c0 += int64_t(gridDim.x) * HS_CHUNK) {
+    for (int j = threadIdx.x; j < HS_HASH; j += HS_THREADS) s_key[j] = HS_EMPTY;
+    __syncthreads();
+    const int m = int(n - c0 < HS_CHUNK ? n - c0 : HS_CHUNK);
+    for (int j = threadIdx.x; j < m; j += HS_THREADS) {
+      const int64_t x = ids[c0 + j];
+      if (x < 0 || x >= id_bound) continue;
+      const uint32_t key = uint32_t(x);
+      uint32_t h = (key * 0x9E3779B1u) >> 19;          // 13 bits: HS_HASH slots
+      bool first = true;
+      for (int p = 0; p < HS_PROBES; ++p) {
+        const uint32_t k = s_key[h];
+        if (k == key) { first = false; break; }
+        if (k == HS_EMPTY) {
+          const uint32_t old = atomicCAS(&s_key[h], HS_EMPTY, key);
+          if (old == HS_EMPTY) break;                   // inserted: first in the chunk
+          if (old == key) { first = false; break; }
+        }
+        h = (h + 1) & (HS_HASH - 1);
+      }
+      if (first) stamp_and_count(x, tag, stamp, freq);
+    }
+    __syncthreads();
   }
 }
 
@@ -66,12 +107,24 @@ __global__ void __launch_bounds__(HS_THREADS) k_hs_hist(const int32_t* __restric
   const int nb = max_freq + 1 < HS_LDS_BINS ? max_freq + 1 : HS_LDS_BINS;
   for (int b = threadIdx.x; b < nb; b += HS_THREADS) s_h[b] = 0;
   __syncthreads();
+  // Most ids of a large universe share the few smallest counts: those are
+  // counted in registers, so the LDS atomics see only the rare larger ones.
+  uint32_t r[HS_REG_BINS] = {};
   for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * HS_THREADS) {
     const int32_t c = clamp_count(f[i], max_freq);
-    if (c < nb) atomicAdd(&s_h[c], 1u);
-    else atomicAdd(&hist[c], 1u);
+    if (c < HS_REG_BINS) {
+#pragma unroll
+      for (int b = 0; b < HS_REG_BINS; ++b) r[b] += (c == b);
+    } else if (c < nb) {
+      atomicAdd(&s_h[c], 1u);
+    } else {
+      atomicAdd(&hist[c], 1u);
+    }
   }
+#pragma unroll
+  for (int b = 0; b < HS_REG_BINS; ++b)
+    if (b < nb && r[b]) atomicAdd(&s_h[b], r[b]);
   __syncthreads();
   for (int b = threadIdx.x; b < nb; b += HS_THREADS)
     if (s_h[b]) atomicAdd(&hist[b], s_h[b]);
@@ -237,7 +290,7 @@ extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* ba
   for (int64_t k = 0; k < num_batches; ++k) {
     const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
     if (n == 0) continue;
-    hipLaunchKernelGGL(k_access_count, dim3(grid_for(n, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
+    hipLaunchKernelGGL(k_access_count, dim3(grid_for(n, HS_CHUNK)), dim3(HS_THREADS), 0, st,
                        ids + batch_offsets[k], n, id_bound, int32_t(k + 1), stamp, freq);
   }
   return check_launch(fn);

@@ -63,20 +63,49 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(In in, int64_t n, 
 }
 
 // One 256-thread block scans the nt tile sums in place (exclusive) and
-// stores the grand total at tsum[nt] and into the optional outputs.
+// stores the grand total at tsum[nt] and into the optional outputs.  The
+// sums are walked SCAN_TILE at a time (coalesced loads through LDS, then
+// SCAN_ITEMS consecutive sums per thread), so a scan of 10^8 items needs
+// about 50 block-wide steps here.
 template <typename T = uint32_t>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* tsum, int64_t nt,
                                                            int64_t* total_i64,
                                                            int32_t* total_i32) {
+  __shared__ T tile[SCAN_TILE + SCAN_TILE / 32];
   __shared__ T lds4[4];
   T carry = 0;
-  for (int64_t b0 = 0; b0 < nt; b0 += SCAN_THREADS) {
-    const int64_t i = b0 + threadIdx.x;
-    const T x = (i < nt) ? tsum[i] : T(0);
+  for (int64_t b0 = 0; b0 < nt; b0 += SCAN_TILE) {
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+      const int j = k * SCAN_THREADS + threadIdx.x;
+      const int64_t i = b0 + j;
+      tile[j + (j >> 5)] = (i < nt) ? tsum[i] : T(0);
+    }
+    __syncthreads();
+    T v[SCAN_ITEMS], s = 0;
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+      const int j = threadIdx.x * SCAN_ITEMS + k;
+      v[k] = tile[j + (j >> 5)];
+      s += v[k];
+    }
     T total;
-    const T ex = block_exclusive_scan(x, lds4, total);
-    if (i < nt) tsum[i] = carry + ex;
+    T run = carry + block_exclusive_scan(s, lds4, total);
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+      const int j = threadIdx.x * SCAN_ITEMS + k;
+      tile[j + (j >> 5)] = run;
+      run += v[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+      const int j = k * SCAN_THREADS + threadIdx.x;
+      const int64_t i = b0 + j;
+      if (i < nt) tsum[i] = tile[j + (j >> 5)];
+    }
     carry += total;
+    __syncthreads();
   }
   if (threadIdx.x == 0) {
     tsum[nt] = carry;
