@@ -31,6 +31,7 @@ _SIGS = {
     "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
     "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
+    "oracle_sample_recent": (None, [_p, _i64, _p, _p, _p, _p, _p, _i64, _i32, _p, _p, _p, _p]),
     "oracle_access_count": (None, [_p, _p, _i64, _i64, _p]),
     "oracle_greedy_hot_set": (None, [_p, _i64, _p, _i64, _f64, _p, _p, _p, _p]),
     "oracle_time_encode_bwd": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p, _p, _p]),
@@ -120,6 +121,26 @@ def gather(uni, table, slot_map=None):
     hit = np.ones(u, dtype=bool)
     hit[miss] = False
     return rows, hit, miss
+
+
+# ------------------------------------------------------------------ temporal sampling
+def sample_recent(indptr, nbr, ts, eid, roots, root_t, k):
+    """Most-recent-k sampling: (off int32 [R+1], src int64, edge_t float32, edge_id int64)."""
+    indptr, nbr, eid = _c(indptr, np.int64), _c(nbr, np.int64), _c(eid, np.int64)
+    ts, roots, root_t = _c(ts, np.float32), _c(roots, np.int64), _c(root_t, np.float32)
+    R = roots.shape[0]
+    valid = roots[(roots >= 0) & (roots < indptr.shape[0] - 1)]
+    # room for every entry of every root, more than R * k when degrees are large
+    cap = max(R * k, int((indptr[valid + 1] - indptr[valid]).sum()), 1)
+    off = np.empty(R + 1, dtype=np.int32)
+    src = np.empty(cap, dtype=np.int64)
+    et = np.empty(cap, dtype=np.float32)
+    ei = np.empty(cap, dtype=np.int64)
+    lib().oracle_sample_recent(_ptr(indptr), indptr.shape[0] - 1, _ptr(nbr), _ptr(ts), _ptr(eid),
+                               _ptr(roots), _ptr(root_t), R, k, _ptr(off), _ptr(src), _ptr(et),
+                               _ptr(ei))
+    E = int(off[-1])
+    return off, src[:E].copy(), et[:E].copy(), ei[:E].copy()
 
 
 # ------------------------------------------------------------------ greedy cache selection

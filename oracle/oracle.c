@@ -99,6 +99,39 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
   }
 }
 
+/* ---- most-recent-k temporal neighbour sampling (Sec. 6.1: top-k recent
+ * sampling over the T-CSR temporal graph) ---- */
+void oracle_sample_recent(const int64_t* indptr, int64_t num_nodes, const int64_t* nbr,
+                          const float* ts, const int64_t* eid, const int64_t* roots,
+                          const float* root_t, int64_t R, int k, int32_t* off, int64_t* src,
+                          float* et, int64_t* ei) {
+  int64_t e = 0;
+  off[0] = 0;
+  for (int64_t i = 0; i < R; ++i) {
+    int64_t v = roots[i];
+    if (v >= 0 && v < num_nodes) {
+      /* candidates: the node's entries strictly earlier than the query time */
+      int64_t c = 0;
+      for (int64_t p = indptr[v]; p < indptr[v + 1]; ++p)
+        if (ts[p] < root_t[i]) c += 1;
+      /* keep the last k of them in entry order, i.e. drop the c - k first */
+      int64_t skip = c > k ? c - k : 0;
+      for (int64_t p = indptr[v]; p < indptr[v + 1]; ++p) {
+        if (!(ts[p] < root_t[i])) continue;
+        if (skip > 0) {
+          skip -= 1;
+          continue;
+        }
+        src[e] = nbr[p];
+        et[e] = ts[p];
+        ei[e] = eid[p];
+        e += 1;
+      }
+    }
+    off[i + 1] = (int32_t)e;
+  }
+}
+
 /* ---- SlimCache greedy cache selection (Sec. 4.2, Alg. 1) ---- */
 
 /* Counting step: for every batch, each distinct id of the batch adds 1 to its

@@ -50,6 +50,19 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
                         const float* t_e, const float* omega, const float* phi,
                         int d_t, double* te);
 
+/* Most-recent-k temporal neighbour sampling (Sec. 6.1) over a T-CSR graph:
+ * node v's entries are p in [indptr[v], indptr[v+1]) with neighbour nbr[p],
+ * time ts[p] and edge id eid[p], in time order.  For root i (node roots[i],
+ * query time root_t[i]) the candidates are the entries with ts < root_t[i];
+ * the root's segment holds the last min(k, #candidates) of them in entry
+ * order.  Roots outside [0, num_nodes) get empty segments.  Output: off[R+1]
+ * and per sampled edge src (neighbour), et (time), ei (edge id); capacity
+ * R * k. */
+void oracle_sample_recent(const int64_t* indptr, int64_t num_nodes, const int64_t* nbr,
+                          const float* ts, const int64_t* eid, const int64_t* roots,
+                          const float* root_t, int64_t R, int k, int32_t* off, int64_t* src,
+                          float* et, int64_t* ei);
+
 /* SlimCache greedy cache selection (Sec. 4.2, Alg. 1).
  * Counting: for each batch k (ids[batch_off[k]..batch_off[k+1])), every
  * distinct id x in [0, id_bound) of the batch does freq[x] += 1 (freq is

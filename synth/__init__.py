@@ -279,6 +279,64 @@ def presampled_ids(cfg: int, num_batches: int, seed: Optional[int] = None):
     return nodes, edges, b.node_bound, b.edge_bound
 
 
+@dataclass
+class TemporalGraph:
+    """A T-CSR temporal graph: node v's entries are p in [indptr[v],
+    indptr[v+1]), each an event of v with neighbour nbr[p] at time ts[p]
+    (event id eid[p]), in time order (ties in event order).  `events` holds
+    the chronological stream (src, dst, t) the graph was built from."""
+    indptr: np.ndarray   # int64 [V+1]
+    nbr: np.ndarray      # int64 [M]
+    ts: np.ndarray       # float32 [M]
+    eid: np.ndarray      # int64 [M]
+    ev_src: np.ndarray   # int64 [num_events]
+    ev_dst: np.ndarray   # int64 [num_events]
+    ev_t: np.ndarray     # float32 [num_events], non-decreasing
+
+    @property
+    def num_nodes(self) -> int:
+        return self.indptr.shape[0] - 1
+
+
+def make_temporal_graph(num_nodes: int, num_events: int, seed: int = 0, zipf_s: float = 1.1):
+    """Event stream over `num_nodes` nodes: endpoints Zipf(zipf_s) ranks mapped
+    by a seeded affine bijection (a few hub nodes hold most events, as in the
+    paper's interaction graphs), times sorted U(0, T_MAX).  Every event is
+    stored under both endpoints (an undirected temporal graph)."""
+    r = _rng(seed, 20)
+    amap = _affine(num_nodes, r)
+    law = ("zipf", num_nodes, zipf_s)
+    src = _draw_ids(law, num_events, r, amap)
+    dst = _draw_ids(law, num_events, r, amap)
+    t = np.sort(r.random(num_events) * T_MAX).astype(np.float32)
+    node = np.concatenate([src, dst])
+    nbr = np.concatenate([dst, src])
+    ts = np.concatenate([t, t])
+    eid = np.concatenate([np.arange(num_events), np.arange(num_events)]).astype(np.int64)
+    # order by node, then time, then event id: a stable sort by time first
+    # (the stream is already in time order), then a stable sort by node
+    by_t = np.argsort(ts, kind="stable")
+    order = by_t[np.argsort(node[by_t], kind="stable")]
+    indptr = np.concatenate([[0], np.cumsum(np.bincount(node, minlength=num_nodes))]).astype(np.int64)
+    return TemporalGraph(indptr, nbr[order].astype(np.int64), ts[order].astype(np.float32),
+                         eid[order], src, dst, t)
+
+
+def sampler_roots(g: TemporalGraph, num_events: int, seed: int = 0):
+    """Roots of one training batch: `num_events` consecutive events from the
+    last fifth of the stream, each giving (src, t), (dst, t) and a uniform
+    negative destination at t.  Returns (roots int64 [3B], root_t float32 [3B])."""
+    r = _rng(seed, 21)
+    n = g.ev_t.shape[0]
+    lo = int(0.8 * n)
+    e0 = int(r.integers(lo, max(lo + 1, n - num_events)))
+    sl = slice(e0, e0 + num_events)
+    neg = r.integers(0, g.num_nodes, num_events, dtype=np.int64)
+    roots = np.concatenate([g.ev_src[sl], g.ev_dst[sl], neg]).astype(np.int64)
+    t = g.ev_t[sl]
+    return roots, np.concatenate([t, t, t]).astype(np.float32)
+
+
 def tiny_graph(counts, H=2, dh=4, seed=7):
     """A hand-sized block with the given per-destination edge counts (zeros
     allowed); timestamps and ids drawn like the named workloads."""

@@ -24,6 +24,10 @@ MUTATIONS = {
     "te_wrong_segment": ("float dt = t_dst[v] - t_e[e];",
                          "float dt = t_dst[v > 0 ? v - 1 : 0] - t_e[e];"),
     "te_transposed_out": ("te[e * d_t + j] =", "te[(j * 0 + e) * d_t + (d_t - 1 - j)] ="),
+    "sample_not_strict": ("if (ts[p] < root_t[i]) c += 1;", "if (ts[p] <= root_t[i]) c += 1;"),
+    "sample_oldest_k": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = 0;"),
+    "sample_k_minus_one": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = c > k - 1 ? c - k + 1 : 0;"),
+    "sample_eid_for_nbr": ("src[e] = nbr[p];", "src[e] = eid[p];"),
     "count_repeats": ("if (i > 0 && b[i] == b[i - 1]) continue;", "if (0) continue;"),
     "count_skips_first": ("for (int64_t i = 0; i < n; ++i) {\n      if (i > 0 && b[i] == b[i - 1])",
                           "for (int64_t i = 1; i < n; ++i) {\n      if (i > 0 && b[i] == b[i - 1])"),
@@ -72,6 +76,8 @@ PINS = [
     (P.test_time_encode_closed_forms, {}),
     (P.test_time_encode_double_angle_columns, {}),
     (P.test_time_encode_fp32_difference, {}),
+    (P.test_sample_recent_hand_example, {}),
+    (P.test_sample_recent_vs_numpy, dict(k=3)),
     (P.test_access_count_hand_example, {}),
     (P.test_access_count_vs_numpy, {}),
     (P.test_greedy_hot_set_hand_example, {}),

@@ -191,6 +191,45 @@ def test_time_encode_fp32_difference():
     assert abs(math.cos(2.0 ** 25 - 1) - math.cos(2.0 ** 25)) > 1e-2
 
 
+# ---------------------------------------------------------------- most-recent-k sampling
+def test_sample_recent_hand_example():
+    # node 0 has events at t = 1, 2, 2, 5, 7; node 1 none; node 2 one at t = 3
+    indptr = np.array([0, 5, 5, 6], np.int64)
+    nbr = np.array([10, 11, 12, 13, 14, 20], np.int64)
+    ts = np.array([1, 2, 2, 5, 7, 3], np.float32)
+    eid = np.array([100, 101, 102, 103, 104, 200], np.int64)
+    roots = np.array([0, 0, 0, 1, 2, 7, -1], np.int64)
+    rt = np.array([5, 100, 1, 9, 3.5, 1, 1], np.float32)
+    off, src, et, ei = oracle.sample_recent(indptr, nbr, ts, eid, roots, rt, 2)
+    # t = 5: earlier events at 1, 2, 2 -> the last two (the two at t = 2);
+    # t = 100: the two latest; t = 1: none (strictly earlier only)
+    assert off.tolist() == [0, 2, 4, 4, 4, 5, 5, 5]
+    assert src.tolist() == [11, 12, 13, 14, 20]
+    assert et.tolist() == [2, 2, 5, 7, 3]
+    assert ei.tolist() == [101, 102, 103, 104, 200]
+
+
+@pytest.mark.parametrize("k", [1, 3, 10])
+def test_sample_recent_vs_numpy(k):
+    from synth import make_temporal_graph, sampler_roots
+    g = make_temporal_graph(3000, 20000, seed=k)
+    roots, rt = sampler_roots(g, 300, seed=k)
+    rt[::7] = g.ev_t[::97][:rt[::7].size]          # some query times equal to event times
+    off, src, et, ei = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots, rt, k)
+    for i, (v, t) in enumerate(zip(roots, rt)):
+        lo, hi = g.indptr[v], g.indptr[v + 1]
+        pos = lo + np.flatnonzero(g.ts[lo:hi] < t)[-k:] if k else []
+        sl = slice(off[i], off[i + 1])
+        assert np.array_equal(src[sl], g.nbr[pos]) and np.array_equal(ei[sl], g.eid[pos])
+        assert np.array_equal(et[sl], g.ts[pos])
+        # the most recent: every earlier entry left out is no later than those taken
+        earlier = g.ts[lo:hi][g.ts[lo:hi] < t]
+        assert off[i + 1] - off[i] == min(k, earlier.size)
+        if earlier.size > k:
+            assert np.sort(earlier)[-k - 1] <= et[sl].min()
+        assert np.all(et[sl] < t)
+
+
 # ---------------------------------------------------------------- greedy cache selection (Alg. 1)
 def test_access_count_hand_example():
     # batch 0 touches 1, 2 (twice), 5; batch 1 touches 2, 9, 1; batch 2 touches 7
