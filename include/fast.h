@@ -6,6 +6,7 @@
  *   fast_dedup_gather         uni_ID / inv_Idx + row reconstruction   (Sec. 4.2, Sec. 5)
  *   fast_time_encode          cos(omega * dt + phi) time features     (Sec. 6.1, TGAT)
  *   fast_time_encode_bwd      gradients of omega and phi              (Sec. 6.1)
+ *   fast_sample_recent        most-recent-k temporal neighbours       (Sec. 6.1, T-CSR)
  *   fast_access_count         pre-sampling access counts              (Sec. 4.2, Alg. 1)
  *   fast_greedy_hot_set       hot ids under a cache budget + slot map (Sec. 4.2, Alg. 1)
  *   fast_edge_softmax_fwd/bwd per-edge multi-head logits + ESM        (Sec. 4.3)
@@ -74,6 +75,20 @@ typedef struct fast_tcsr {
   const float* dst_t;         /* [N] destination (query) timestamps            */
 } fast_tcsr_t;
 
+/* A temporal graph in T-CSR form (the time-sorted CSR of TGL, on which FAST
+ * samples, Sec. 6.1 / Sec. 7): node v's entries are p in
+ * [indptr[v], indptr[v+1]), each an event of v with neighbour nbr[p] at
+ * time ts[p] and edge id eid[p], in non-decreasing time within each node.
+ * All pointers are DEVICE pointers. */
+typedef struct fast_temporal_graph {
+  int64_t num_nodes;          /* V >= 0                                          */
+  int64_t num_entries;        /* M >= 0                                          */
+  const int64_t* indptr;      /* [V+1] int64, non-decreasing, indptr[V] = M      */
+  const int64_t* nbr;         /* [M] neighbour node id                           */
+  const float* ts;            /* [M] event time, sorted within each node         */
+  const int64_t* eid;         /* [M] edge (event) id                             */
+} fast_temporal_graph_t;
+
 /* Message for the last non-OK status returned on the calling thread ("" if
  * none).  The string stays valid until the next failing call on that thread. */
 const char* fast_last_error(void);
@@ -133,6 +148,33 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
                                 int64_t* uni, int32_t* inv, int64_t* num_unique,
                                 void* rows, int32_t* miss, int64_t* num_miss,
                                 void* ws, size_t ws_bytes, fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Most-recent-k temporal neighbour sampling (Sec. 6.1: top-k recent
+ * sampling, k = 10 in the paper's experiments).  Root i is node roots[i]
+ * queried at time root_t[i]; its candidates are the entries of that node
+ * with ts < root_t[i] (strictly earlier), and its segment of the sampled
+ * block holds the LAST min(k, #candidates) of them in entry order (the most
+ * recent, oldest first):
+ *   dst_offsets[i+1] - dst_offsets[i] = min(k, #candidates),  dst_offsets[0] = 0
+ *   src_ids / edge_t / edge_ids of each sampled edge = nbr / ts / eid
+ * A root outside [0, V) gets an empty segment.  The result is the sampled
+ * block of one layer in the form fast_tcsr_t describes (with dst_t =
+ * root_t); a second hop samples (src_ids, edge_t) of the first.
+ * roots [R] int64, root_t [R] fp32: device.  Outputs: dst_offsets [R+1]
+ * int32 (its last entry is the number of sampled edges E), src_ids and
+ * edge_ids int64, edge_t fp32, capacity R * k each.  Offsets that are out of
+ * range are clamped, so a malformed graph never causes an out-of-bounds
+ * read; entries that are not time-sorted give unspecified neighbours.
+ * Limits: 0 <= k, R * k < 2^31.
+ * Workspace: fast_sample_recent_workspace(R) bytes, 256-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t fast_sample_recent_workspace(int64_t num_roots);
+fast_status_t fast_sample_recent(const fast_temporal_graph_t* g, const int64_t* roots,
+                                 const float* root_t, int64_t num_roots, int k,
+                                 int32_t* dst_offsets, int64_t* src_ids, float* edge_t,
+                                 int64_t* edge_ids, void* ws, size_t ws_bytes,
+                                 fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * SlimCache access counting over pre-sampled batches (Sec. 4.2, Alg. 1: the

@@ -13,7 +13,8 @@ import ctypes as C
 import os
 
 __all__ = [
-    "FastError", "lib", "TCSR", "tcsr", "F32", "BF16", "dtype_of",
+    "FastError", "lib", "TCSR", "tcsr", "TemporalGraphDesc", "temporal_graph", "F32", "BF16",
+    "dtype_of", "fast_sample_recent_workspace", "fast_sample_recent",
     "fast_version", "fast_last_error",
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
     "fast_dedup_gather_workspace", "fast_dedup_gather",
@@ -52,8 +53,21 @@ class TCSR(C.Structure):
     ]
 
 
+class TemporalGraphDesc(C.Structure):
+    """fast_temporal_graph_t: a T-CSR temporal graph (device pointers)."""
+    _fields_ = [
+        ("num_nodes", C.c_int64),
+        ("num_entries", C.c_int64),
+        ("indptr", C.c_void_p),
+        ("nbr", C.c_void_p),
+        ("ts", C.c_void_p),
+        ("eid", C.c_void_p),
+    ]
+
+
 _p, _i64, _i32, _f32, _sz = C.c_void_p, C.c_int64, C.c_int, C.c_float, C.c_size_t
 _G = C.POINTER(TCSR)
+_TG = C.POINTER(TemporalGraphDesc)
 _SIGS = {
     "fast_last_error": (C.c_char_p, []),
     "fast_version": (C.c_char_p, []),
@@ -63,6 +77,8 @@ _SIGS = {
     "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
                                  _p, _p, _p, _p, _sz, _p]),
+    "fast_sample_recent_workspace": (_sz, [_i64]),
+    "fast_sample_recent": (_i32, [_TG, _p, _p, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]),
     "fast_access_count_workspace": (_sz, [_i64]),
     "fast_access_count": (_i32, [_p, _p, _i64, _i64, _p, _p, _sz, _p]),
     "fast_greedy_hot_set_workspace": (_sz, [_i64, _i64, _i32]),
@@ -138,6 +154,15 @@ def tcsr(dst_offsets, num_edges: int, src_ids=None, edge_t=None, edge_ids=None, 
     return g
 
 
+def temporal_graph(indptr, nbr, ts, eid) -> TemporalGraphDesc:
+    """Builds a fast_temporal_graph_t over device tensors; the struct keeps a
+    reference to each tensor while it is alive."""
+    g = TemporalGraphDesc(indptr.shape[0] - 1, int(nbr.shape[0]), _ptr(indptr), _ptr(nbr),
+                          _ptr(ts), _ptr(eid))
+    g._keep = (indptr, nbr, ts, eid)
+    return g
+
+
 # ------------------------------------------------------------------ entry points
 def fast_last_error() -> str:
     return lib().fast_last_error().decode()
@@ -171,6 +196,17 @@ def fast_dedup_gather(ids, n, id_bound, table, table_rows, D, dtype, slot_map, u
                                    _ptr(slot_map), _ptr(uni), _ptr(inv), _ptr(num_unique),
                                    _ptr(rows), _ptr(miss), _ptr(num_miss), _ptr(ws), ws_bytes,
                                    _stream(stream)))
+
+
+def fast_sample_recent_workspace(num_roots: int) -> int:
+    return lib().fast_sample_recent_workspace(num_roots)
+
+
+def fast_sample_recent(g: TemporalGraphDesc, roots, root_t, num_roots, k, dst_offsets, src_ids,
+                       edge_t, edge_ids, ws, ws_bytes, stream=None):
+    _check(lib().fast_sample_recent(C.byref(g), _ptr(roots), _ptr(root_t), num_roots, k,
+                                    _ptr(dst_offsets), _ptr(src_ids), _ptr(edge_t),
+                                    _ptr(edge_ids), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def fast_access_count_workspace(id_bound: int) -> int:

@@ -240,3 +240,31 @@ def test_hot_set_validation_and_workspace_queries():
     assert fast.hot_set_budget(0.15, 5, 5) == 2
     assert fast.hot_set_budget(2.0, 5, 5) == 10
     assert fast.hot_set_budget(0.0, 5, 5) == 0
+
+
+def test_sample_recent_validation():
+    L = fast.lib()
+    tg = fast.TemporalGraphDesc(100, 1000, FAKE, FAKE, FAKE, FAKE)
+    gp = ctypes.byref(tg)
+    ws = L.fast_sample_recent_workspace(50)
+    assert ws > 50 * 12
+    assert L.fast_sample_recent_workspace(-1) == 0
+
+    def call(**k):
+        return L.fast_sample_recent(k.get("g", gp), k.get("roots", FAKE), k.get("rt", FAKE),
+                                    k.get("R", 50), k.get("k", 10), k.get("off", FAKE),
+                                    k.get("src", FAKE), FAKE, FAKE, k.get("ws", FAKE),
+                                    k.get("wsb", ws), None)
+    assert call(g=None) == INVALID
+    assert call(k=-1) == INVALID
+    assert call(R=-1) == INVALID
+    assert call(R=1 << 28, k=16) == UNSUPPORTED
+    assert call(off=None) == INVALID
+    assert call(roots=None) == INVALID
+    assert call(src=None) == INVALID
+    assert call(wsb=ws - 1) == WORKSPACE
+    assert call(ws=FAKE + 64) == UNSUPPORTED
+    bad = fast.TemporalGraphDesc(100, 1000, None, FAKE, FAKE, FAKE)
+    assert call(g=ctypes.byref(bad)) == INVALID
+    bad = fast.TemporalGraphDesc(100, 1000, FAKE, FAKE, None, FAKE)
+    assert call(g=ctypes.byref(bad)) == INVALID

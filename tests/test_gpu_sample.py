@@ -1,0 +1,158 @@
+"""GPU parity of the most-recent-k temporal sampler through the C ABI,
+bit-exact against the oracle (offsets, neighbour ids, times, edge ids).
+
+Small and medium graphs are compared root for root in full; on the large
+graph (hub nodes with millions of entries) the oracle's linear scans are
+run on a sample of roots, each root's segment checked one by one.  Two hops
+are chained as in training (hop-2 roots are the hop-1 neighbours at their
+edge times) and the result is fed to the contract check and the time
+encoding.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05095_amd as fast
+from synth import make_temporal_graph, omega_phi, sampler_roots
+from tests.parity import assert_close, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+class DevGraph:
+    def __init__(self, g):
+        self.h = g
+        self.d = fast.temporal_graph(to_dev(g.indptr), to_dev(g.nbr), to_dev(g.ts), to_dev(g.eid))
+
+
+def _sample_gpu(dg, roots, rt, k):
+    R = roots.shape[0]
+    cap = max(R * k, 1)
+    off = torch.full((R + 1,), -5, dtype=torch.int32, device="cuda")
+    src = torch.empty(cap, dtype=torch.int64, device="cuda")
+    et = torch.empty(cap, dtype=torch.float32, device="cuda")
+    ei = torch.empty(cap, dtype=torch.int64, device="cuda")
+    wsb = fast.fast_sample_recent_workspace(R)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    d_roots = roots if isinstance(roots, torch.Tensor) else to_dev(np.asarray(roots, np.int64))
+    d_rt = rt if isinstance(rt, torch.Tensor) else to_dev(np.asarray(rt, np.float32))
+    fast.fast_sample_recent(dg.d, d_roots, d_rt, R, k, off, src, et, ei, ws, wsb)
+    torch.cuda.synchronize()
+    E = int(off[-1].item())
+    return off, src[:E], et[:E], ei[:E]
+
+
+def _host(*ts):
+    return [t.cpu().numpy() for t in ts]
+
+
+def _assert_equal_sample(got, want, what):
+    names = ("offsets", "src_ids", "edge_t", "edge_ids")
+    for n, g, w in zip(names, _host(*got), want):
+        assert g.shape == w.shape and np.array_equal(g, w), f"{what}: {n} differ"
+
+
+@pytest.mark.parametrize("nodes,events,k", [(3000, 20000, 1), (3000, 20000, 10),
+                                            (100000, 1000000, 10), (100000, 1000000, 20)])
+def test_sample_recent_vs_oracle(nodes, events, k):
+    _announce(f"sample recent V={nodes} events={events} k={k}")
+    g = make_temporal_graph(nodes, events, seed=k + nodes)
+    dg = DevGraph(g)
+    roots, rt = sampler_roots(g, 2000, seed=k)
+    roots[::53] = -1                                  # invalid roots
+    roots[1::97] = nodes + 5
+    n_eq = rt[2::11].size                             # query times equal to event times
+    rt[2::11] = g.ev_t[(np.arange(n_eq) * 101) % g.ev_t.size]
+    got = _sample_gpu(dg, roots, rt, k)
+    want = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots, rt, k)
+    _assert_equal_sample(got, want, f"V={nodes} k={k}")
+
+
+def test_two_hops_feed_the_block_operators():
+    _announce("sample two hops -> contract check -> time encoding")
+    g = make_temporal_graph(50000, 500000, seed=4)
+    dg = DevGraph(g)
+    roots, rt = sampler_roots(g, 600, seed=4)
+    k = 10
+    off1, src1, et1, ei1 = _sample_gpu(dg, roots, rt, k)
+    w1 = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots, rt, k)
+    _assert_equal_sample((off1, src1, et1, ei1), w1, "hop 1")
+    off2, src2, et2, ei2 = _sample_gpu(dg, src1, et1, k)
+    w2 = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, w1[1], w1[2], k)
+    _assert_equal_sample((off2, src2, et2, ei2), w2, "hop 2")
+    # the hop-2 block satisfies the operators' contract: dt > 0 everywhere
+    E2 = int(off2[-1].item())
+    blk = fast.tcsr(off2, E2, src_ids=src2, edge_t=et2, edge_ids=ei2, dst_t=et1)
+    v = torch.empty(5, dtype=torch.int64, device="cuda")
+    fast.fast_check_tcsr(blk, g.num_nodes, events_bound(g), v)
+    assert v.cpu().tolist() == [0, 0, 0, 0, 0]
+    assert torch.all(et2 < torch.repeat_interleave(et1, (off2[1:] - off2[:-1]).long()))
+    om, ph = omega_phi(100)
+    te = torch.empty((max(E2, 1), 100), device="cuda")
+    fast.fast_time_encode(blk, to_dev(om), to_dev(ph), 100, te, fast.F32)
+    torch.cuda.synchronize()
+    ref = oracle.time_encode(w2[0], w1[2], w2[2], om, ph)
+    assert_close(te[:E2], ref, "f32", "time encoding of the sampled hop-2 block")
+
+
+def events_bound(g):
+    return int(g.ev_t.shape[0])
+
+
+def test_sample_recent_edge_cases():
+    _announce("sample recent edge cases")
+    g = make_temporal_graph(2000, 10000, seed=1)
+    dg = DevGraph(g)
+    roots, rt = sampler_roots(g, 100, seed=1)
+    # k = 0: every segment empty
+    off, src, _, _ = _sample_gpu(dg, roots, rt, 0)
+    assert off.cpu().tolist() == [0] * 301 and src.numel() == 0
+    # no roots
+    off, _, _, _ = _sample_gpu(dg, np.zeros(0, np.int64), np.zeros(0, np.float32), 10)
+    assert off.cpu().tolist() == [0]
+    # query before every event and after every event
+    r = np.arange(50, dtype=np.int64)
+    off, _, _, _ = _sample_gpu(dg, r, np.full(50, -1.0, np.float32), 10)
+    assert off.cpu().tolist() == [0] * 51
+    got = _sample_gpu(dg, r, np.full(50, 1e9, np.float32), 10)
+    want = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, r, np.full(50, 1e9, np.float32), 10)
+    _assert_equal_sample(got, want, "query after every event")
+    # a graph with nodes but no entries
+    empty = fast.temporal_graph(to_dev(np.zeros(11, np.int64)), torch.empty(0, dtype=torch.int64,
+                                device="cuda"), torch.empty(0, device="cuda"),
+                                torch.empty(0, dtype=torch.int64, device="cuda"))
+    off = torch.empty(4, dtype=torch.int32, device="cuda")
+    wsb = fast.fast_sample_recent_workspace(3)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    buf = torch.empty(30, dtype=torch.int64, device="cuda")
+    fast.fast_sample_recent(empty, to_dev(np.array([0, 1, 2], np.int64)),
+                            to_dev(np.ones(3, np.float32)), 3, 10, off, buf,
+                            torch.empty(30, device="cuda"), buf.clone(), ws, wsb)
+    torch.cuda.synchronize()
+    assert off.cpu().tolist() == [0, 0, 0, 0]
+
+
+def test_sample_recent_large_graph_sampled_roots():
+    # 2e7 events (4e7 entries, hubs with millions of entries); the batch of
+    # 8000 events the benchmark samples, checked on 400 roots
+    g = make_temporal_graph(10_000_000, 20_000_000, seed=9)
+    _announce(f"sample recent large graph: V={g.num_nodes} M={g.indptr[-1]}")
+    dg = DevGraph(g)
+    roots, rt = sampler_roots(g, 8000, seed=9)
+    k = 10
+    off, src, et, ei = _sample_gpu(dg, roots, rt, k)
+    off, src, et, ei = _host(off, src, et, ei)
+    pick = np.unique(np.concatenate([np.random.default_rng(0).choice(roots.size, 400, replace=False),
+                                     [0, roots.size - 1]]))
+    w = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots[pick], rt[pick], k)
+    for j, i in enumerate(pick):
+        sl, ws = slice(off[i], off[i + 1]), slice(w[0][j], w[0][j + 1])
+        assert np.array_equal(src[sl], w[1][ws]) and np.array_equal(et[sl], w[2][ws])
+        assert np.array_equal(ei[sl], w[3][ws])
+    counts = np.diff(off)
+    assert counts.min() >= 0 and counts.max() <= k and off[-1] == counts.sum()
