@@ -242,7 +242,8 @@ def widened_ops(b, step, torch, fast, reps=10):
     """Operators beyond the timed step, each timed alone with HIP events on
     its launch stream (mean of `reps` launches after one warm-up): the
     time-encoding backward of each layer block, on a seeded upstream
-    gradient, and the cache selection of Alg. 1."""
+    gradient, the cache selection of Alg. 1, and two hops of most-recent-k
+    temporal sampling."""
     from synth import _randn
     esz = 4 if b.dtype == "f32" else 2
     res = {}
@@ -275,6 +276,41 @@ def widened_ops(b, step, torch, fast, reps=10):
         }
         del dte, ws
     res.update(hot_set_ops(b, torch, fast))
+    res.update(sampler_ops(b, torch, fast))
+    return res
+
+
+def sampler_ops(b, torch, fast, num_events=20_000_000, reps=5):
+    """Two hops of most-recent-k sampling for one batch of this workload's
+    shape (roots / 3 events, fan-out k) on an event-stream temporal graph
+    over the workload's node universe (each event stored under both ends)."""
+    from synth import make_temporal_graph, sampler_roots
+    k = int(b.blocks[-1].counts.max())
+    g = make_temporal_graph(b.node_bound, num_events, seed=b.seed)
+    roots, rt = sampler_roots(g, b.blocks[-1].num_dst // 3, seed=b.seed)
+    dg = fast.temporal_graph(*(torch.from_numpy(x).cuda() for x in (g.indptr, g.nbr, g.ts, g.eid)))
+    res, q_roots, q_t = {}, torch.from_numpy(roots).cuda(), torch.from_numpy(rt).cuda()
+    for hop in (1, 2):
+        R = int(q_roots.numel())
+        off = torch.empty(R + 1, dtype=torch.int32, device="cuda")
+        src = torch.empty(max(R * k, 1), dtype=torch.int64, device="cuda")
+        et = torch.empty(max(R * k, 1), dtype=torch.float32, device="cuda")
+        ei = torch.empty(max(R * k, 1), dtype=torch.int64, device="cuda")
+        wsb = fast.fast_sample_recent_workspace(R)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+
+        def call():
+            fast.fast_sample_recent(dg, q_roots, q_t, R, k, off, src, et, ei, ws, wsb)
+        call()
+        ms = _events_ms(torch, call, reps)
+        E = int(off[-1].item())
+        res[f"sample_recent_hop{hop}"] = {
+            "ms": round(ms, 4), "roots": R, "k": k, "sampled_edges": E,
+            "graph": f"{g.num_nodes} nodes, {num_events} events ({int(g.indptr[-1])} entries)",
+            "bound": "latency (binary search per root over its time-sorted entries)",
+            "sampled_edges_per_s": round(E / (ms * 1e-3), 1),
+        }
+        q_roots, q_t = src[:E].clone(), et[:E].clone()
     return res
 
 
