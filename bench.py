@@ -12,11 +12,11 @@ value = sampled edges per step / step time.  The roofline entry covers the
 dominant kernel, the fused backward of the layer-1 block, timed with HIP
 events on the stream it runs on.
 
-    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large] [--pipelined]
+    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large] [--no-pipelined]
 
-The timed steps run serially on one stream (prep, then attention).  With
---pipelined the line also reports the same steps software-pipelined: prep of
-batch i+1 on a second stream overlaps attention of batch i.
+`value` times the steps serially on one stream (prep, then attention).  The
+line also reports the same steps software-pipelined (unless --no-pipelined):
+prep of batch i+1 on a second stream overlaps attention of batch i.
 """
 from __future__ import annotations
 
@@ -465,8 +465,8 @@ def main():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="bigdedup")
     ap.add_argument("--cpu-frac", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--pipelined", action="store_true",
-                    help="also time the steps software-pipelined over two streams")
+    ap.add_argument("--no-pipelined", dest="pipelined", action="store_false",
+                    help="skip the second timing of the steps software-pipelined over two streams")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
