@@ -31,6 +31,8 @@ _SIGS = {
     "oracle_dedup": (_i64, [_p, _i64, _p, _p]),
     "oracle_gather": (_i64, [_p, _i64, _p, _i64, _i64, _p, _p, _p]),
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
+    "oracle_occurrence_csr": (None, [_p, _i64, _i64, _p, _p]),
+    "oracle_index_add_rows": (None, [_p, _i64, _i64, _i64, _p, _p]),
     "oracle_sample_recent": (None, [_p, _i64, _p, _p, _p, _p, _p, _i64, _i32, _p, _p, _p, _p]),
     "oracle_access_count": (None, [_p, _p, _i64, _i64, _p]),
     "oracle_greedy_hot_set": (None, [_p, _i64, _p, _i64, _f64, _p, _p, _p, _p]),
@@ -121,6 +123,50 @@ def gather(uni, table, slot_map=None):
     hit = np.ones(u, dtype=bool)
     hit[miss] = False
     return rows, hit, miss
+
+
+# ------------------------------------------------------------------ indexed operands
+def occurrence_csr(index, num_rows):
+    """(occ_off int32 [num_rows+1], occ int32 [valid positions]) of an index."""
+    index = _c(index, np.int32)
+    n = index.shape[0]
+    off = np.empty(num_rows + 1, dtype=np.int32)
+    occ = np.empty(2 * n + 1, dtype=np.int32)     # slack: a planted mistake may overrun n
+    lib().oracle_occurrence_csr(_ptr(index), n, num_rows, _ptr(off), _ptr(occ))
+    return off, occ[:int(off[-1])].copy()
+
+
+def index_add_rows(index, num_rows, src):
+    """dst [num_rows, ...] float64 = sum of the rows of src at the positions of each index value."""
+    index = _c(index, np.int32)
+    src = _f64(src)
+    row_shape = src.shape[1:]
+    D = int(np.prod(row_shape, dtype=np.int64))
+    dst = np.zeros((num_rows,) + row_shape, dtype=np.float64)
+    lib().oracle_index_add_rows(_ptr(index), index.shape[0], num_rows, D,
+                                _ptr(np.ascontiguousarray(src.reshape(index.shape[0], D))), _ptr(dst))
+    return dst
+
+
+def edge_attention_fwd_indexed(off, Q, K, k_index, V, v_index, scale, slope):
+    """Fused forward whose edge e reads row k_index[e] of K and v_index[e] of V
+    (None = row e): the plain operator on the gathered rows."""
+    K, V = _f64(K), _f64(V)
+    Ke = K if k_index is None else K[np.asarray(k_index, np.int64)]
+    Ve = V if v_index is None else V[np.asarray(v_index, np.int64)]
+    return edge_attention_fwd(off, Q, Ke, Ve, scale, slope)
+
+
+def edge_attention_bwd_indexed(off, Q, K, k_index, V, v_index, dO, scale, slope):
+    """(dQ, dK_edge, dV_edge, dK_rows, dV_rows): the per-edge gradients of the
+    gathered operator, and their sums over the edges that read each row."""
+    K, V = _f64(K), _f64(V)
+    Ke = K if k_index is None else K[np.asarray(k_index, np.int64)]
+    Ve = V if v_index is None else V[np.asarray(v_index, np.int64)]
+    dQ, dKe, dVe = edge_attention_bwd(off, Q, Ke, Ve, dO, scale, slope)
+    dKr = dKe if k_index is None else index_add_rows(k_index, K.shape[0], dKe)
+    dVr = dVe if v_index is None else index_add_rows(v_index, V.shape[0], dVe)
+    return dQ, dKe, dVe, dKr, dVr
 
 
 # ------------------------------------------------------------------ temporal sampling

@@ -99,6 +99,36 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
   }
 }
 
+/* ---- indexed operands (Sec. 4.2: rows reconstructed through the inverse
+ * index of the compressed ids): occurrence lists and the transposed gather ---- */
+
+/* Occurrence lists of an index: row u lists, in ascending order, every
+ * position p with index[p] == u (a stable counting sort by index value).
+ * Positions whose index lies outside [0, num_rows) are left out. */
+void oracle_occurrence_csr(const int32_t* index, int64_t n, int64_t num_rows, int32_t* occ_off,
+                           int32_t* occ) {
+  for (int64_t u = 0; u <= num_rows; ++u) occ_off[u] = 0;
+  for (int64_t p = 0; p < n; ++p)
+    if (index[p] >= 0 && index[p] < num_rows) occ_off[index[p] + 1] += 1;
+  for (int64_t u = 0; u < num_rows; ++u) occ_off[u + 1] += occ_off[u];
+  int32_t* cursor = (int32_t*)malloc((size_t)(num_rows > 0 ? num_rows : 1) * sizeof(int32_t));
+  for (int64_t u = 0; u < num_rows; ++u) cursor[u] = occ_off[u];
+  for (int64_t p = 0; p < n; ++p)
+    if (index[p] >= 0 && index[p] < num_rows) occ[cursor[index[p]]++] = (int32_t)p;
+  free(cursor);
+}
+
+/* dst[u] = sum of src[p] over the positions p with index[p] == u (the
+ * gradient of a row that several positions read), fp64; 0 if none. */
+void oracle_index_add_rows(const int32_t* index, int64_t n, int64_t num_rows, int64_t D,
+                           const double* src, double* dst) {
+  for (int64_t i = 0; i < num_rows * D; ++i) dst[i] = 0.0;
+  for (int64_t p = 0; p < n; ++p) {
+    if (index[p] < 0 || index[p] >= num_rows) continue;
+    for (int64_t j = 0; j < D; ++j) dst[(int64_t)index[p] * D + j] += src[p * D + j];
+  }
+}
+
 /* ---- most-recent-k temporal neighbour sampling (Sec. 6.1: top-k recent
  * sampling over the T-CSR temporal graph) ---- */
 void oracle_sample_recent(const int64_t* indptr, int64_t num_nodes, const int64_t* nbr,

@@ -50,6 +50,17 @@ void oracle_time_encode(const int32_t* off, int64_t N, const float* t_dst,
                         const float* t_e, const float* omega, const float* phi,
                         int d_t, double* te);
 
+/* Occurrence lists (indexed operands, Sec. 4.2): occ_off[num_rows+1] and, for
+ * row u, occ[occ_off[u] .. occ_off[u+1]) = the positions p with index[p] == u
+ * in ascending order.  Index values outside [0, num_rows) are left out. */
+void oracle_occurrence_csr(const int32_t* index, int64_t n, int64_t num_rows, int32_t* occ_off,
+                           int32_t* occ);
+
+/* Transposed gather: dst[u, :] = sum over p with index[p] == u of src[p, :]
+ * (fp64; rows of D values; 0 for a row no position reads). */
+void oracle_index_add_rows(const int32_t* index, int64_t n, int64_t num_rows, int64_t D,
+                           const double* src, double* dst);
+
 /* Most-recent-k temporal neighbour sampling (Sec. 6.1) over a T-CSR graph:
  * node v's entries are p in [indptr[v], indptr[v+1]) with neighbour nbr[p],
  * time ts[p] and edge id eid[p], in time order.  For root i (node roots[i],

@@ -24,6 +24,11 @@ MUTATIONS = {
     "te_wrong_segment": ("float dt = t_dst[v] - t_e[e];",
                          "float dt = t_dst[v > 0 ? v - 1 : 0] - t_e[e];"),
     "te_transposed_out": ("te[e * d_t + j] =", "te[(j * 0 + e) * d_t + (d_t - 1 - j)] ="),
+    "occ_unstable": ("for (int64_t p = 0; p < n; ++p)\n    if (index[p] >= 0 && index[p] < num_rows) occ[cursor[",
+                     "for (int64_t p = n - 1; p >= 0; --p)\n    if (index[p] >= 0 && index[p] < num_rows) occ[cursor["),
+    "occ_offsets_shifted": ("occ_off[index[p] + 1] += 1;", "occ_off[index[p]] += 1;"),
+    "index_add_drops_last": ("for (int64_t p = 0; p < n; ++p) {\n    if (index[p] < 0 || index[p] >= num_rows) continue;",
+                             "for (int64_t p = 0; p < n - 1; ++p) {\n    if (index[p] < 0 || index[p] >= num_rows) continue;"),
     "sample_not_strict": ("if (ts[p] < root_t[i]) c += 1;", "if (ts[p] <= root_t[i]) c += 1;"),
     "sample_oldest_k": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = 0;"),
     "sample_k_minus_one": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = c > k - 1 ? c - k + 1 : 0;"),
@@ -76,6 +81,9 @@ PINS = [
     (P.test_time_encode_closed_forms, {}),
     (P.test_time_encode_double_angle_columns, {}),
     (P.test_time_encode_fp32_difference, {}),
+    (P.test_occurrence_csr_vs_numpy, {}),
+    (P.test_index_add_rows_vs_numpy, {}),
+    (P.test_indexed_attention_gradients_by_finite_differences, {}),
     (P.test_sample_recent_hand_example, {}),
     (P.test_sample_recent_vs_numpy, dict(k=3)),
     (P.test_access_count_hand_example, {}),

@@ -191,6 +191,72 @@ def test_time_encode_fp32_difference():
     assert abs(math.cos(2.0 ** 25 - 1) - math.cos(2.0 ** 25)) > 1e-2
 
 
+# ---------------------------------------------------------------- indexed operands
+def test_occurrence_csr_vs_numpy():
+    r = np.random.default_rng(2)
+    U = 700
+    idx = (r.zipf(1.4, 20000) - 1).astype(np.int32)
+    idx[::37] = -3                                   # left out
+    idx[5::41] = U + 9
+    off, occ = oracle.occurrence_csr(idx, U)
+    valid = (idx >= 0) & (idx < U)
+    assert np.array_equal(np.diff(off), np.bincount(idx[valid], minlength=U))
+    pos = np.flatnonzero(valid)
+    assert np.array_equal(occ, pos[np.argsort(idx[valid], kind="stable")])
+
+
+def test_index_add_rows_vs_numpy():
+    r = np.random.default_rng(3)
+    idx = r.integers(-1, 50, 3000).astype(np.int32)
+    src = r.standard_normal((3000, 4, 5))
+    got = oracle.index_add_rows(idx, 48, src)
+    want = np.zeros((48, 4, 5))
+    ok = (idx >= 0) & (idx < 48)
+    np.add.at(want, idx[ok], src[ok])
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
+def test_indexed_attention_gradients_by_finite_differences():
+    # compact K and V rows read by several edges each: the gradient of
+    # L = sum(dOut * out) with respect to a compact row is the derivative of
+    # the forward taken through every edge that reads it
+    r = np.random.default_rng(8)
+    counts = [3, 1, 4, 2, 5]
+    off = _csr(counts)
+    N, E, H, dh, Uk, Uv = len(counts), int(off[-1]), 2, 3, 6, 4
+    Q = r.standard_normal((N, H, dh))
+    K = r.standard_normal((Uk, H, dh))
+    V = r.standard_normal((Uv, H, dh))
+    dO = r.standard_normal((N, H, dh))
+    kidx = r.integers(0, Uk, E).astype(np.int32)
+    vidx = r.integers(0, Uv, E).astype(np.int32)
+    kidx[:3] = 2                                     # row 2 read three times
+    scale = 1 / math.sqrt(dh)
+    _, _, _, dKr, dVr = oracle.edge_attention_bwd_indexed(off, Q, K, kidx, V, vidx, dO, scale, SLOPE)
+
+    def loss(Kx, Vx):
+        out = oracle.edge_attention_fwd_indexed(off, Q, Kx, kidx, Vx, vidx, scale, SLOPE)[0]
+        return float(np.sum(dO * out))
+
+    hstep = 1e-6
+    for (arr, grad, which) in ((K, dKr, 0), (V, dVr, 1)):
+        for u in range(arr.shape[0]):
+            for h in range(H):
+                for i in range(dh):
+                    lo, hi = arr.copy(), arr.copy()
+                    lo[u, h, i] -= hstep
+                    hi[u, h, i] += hstep
+                    fd = ((loss(hi, V) - loss(lo, V)) if which == 0 else
+                          (loss(K, hi) - loss(K, lo))) / (2 * hstep)
+                    assert abs(grad[u, h, i] - fd) <= 1e-6 * (1 + abs(fd)), (which, u, h, i)
+    # identity index: the plain operator
+    ident = np.arange(E, dtype=np.int32)
+    Ke, Ve = K[kidx], V[vidx]
+    a = oracle.edge_attention_fwd_indexed(off, Q, Ke, ident, Ve, None, scale, SLOPE)[0]
+    b = oracle.edge_attention_fwd(off, Q, Ke, Ve, scale, SLOPE)[0]
+    assert np.array_equal(a, b)
+
+
 # ---------------------------------------------------------------- most-recent-k sampling
 def test_sample_recent_hand_example():
     # node 0 has events at t = 1, 2, 2, 5, 7; node 1 none; node 2 one at t = 3
