@@ -12,6 +12,10 @@
  *   fast_edge_softmax_fwd/bwd per-edge multi-head logits + ESM        (Sec. 4.3)
  *   fast_temporal_aggregate_fwd/bwd  attention-weighted AGG           (Sec. 4.3, Eq. 1)
  *   fast_edge_attention_fwd/bwd      ESM and AGG fused in one kernel  (Sec. 4.3)
+ *   fast_edge_attention_fwd/bwd_indexed  the same with K/V read through an
+ *                             index into de-duplicated rows           (Sec. 4.2)
+ *   fast_occurrence_csr, fast_index_add_rows  the gradient of a shared row
+ *                             as the ordered sum over its readers     (Sec. 4.2)
  *
  * Conventions shared by every entry point
  *   - Memory: every array argument is a DEVICE pointer into HBM owned by the
@@ -325,6 +329,62 @@ fast_status_t fast_edge_attention_bwd(const fast_tcsr_t* g, int H, int dh, fast_
                                       float scale, float neg_slope, const float* lse,
                                       const void* dout, void* dQ, void* dK, void* dV,
                                       fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Indexed operands (Sec. 4.2: the compressed batch carries each distinct id
+ * once plus an inverse index; here the fused operator reads its K and V rows
+ * through such an index instead of from a rebuilt per-edge copy).
+ *   edge e reads K[k_index[e]] and V[v_index[e]]   (a NULL index: row e)
+ * Otherwise identical to fast_edge_attention_fwd / _bwd.  K: [k_rows, H, dh],
+ * V: [v_rows, H, dh] of dtype; k_index, v_index: [E] int32 device; an index
+ * value outside [0, rows) reads the nearest valid row.  An index requires
+ * rows >= 1.  The backward writes the PER-EDGE gradients dK_edge, dV_edge
+ * [E, H, dh] (the gradient of each edge's read); the gradient of a shared
+ * row is their sum over the edges that read it: build the occurrence lists
+ * of the index with fast_occurrence_csr, then fast_index_add_rows.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_edge_attention_fwd_indexed(const fast_tcsr_t* g, int H, int dh,
+                                              fast_dtype_t dtype, const void* Q, const void* K,
+                                              const int32_t* k_index, int64_t k_rows,
+                                              const void* V, const int32_t* v_index,
+                                              int64_t v_rows, float scale, float neg_slope,
+                                              void* out, float* lse, fast_stream_t stream);
+fast_status_t fast_edge_attention_bwd_indexed(const fast_tcsr_t* g, int H, int dh,
+                                              fast_dtype_t dtype, const void* Q, const void* K,
+                                              const int32_t* k_index, int64_t k_rows,
+                                              const void* V, const int32_t* v_index,
+                                              int64_t v_rows, float scale, float neg_slope,
+                                              const float* lse, const void* dout, void* dQ,
+                                              void* dK_edge, void* dV_edge, fast_stream_t stream);
+
+/* Occurrence lists of an index (a stable counting sort by index value):
+ *   occ_off[u+1] - occ_off[u] = number of p with index[p] == u,  occ_off[0] = 0
+ *   occ[occ_off[u] .. occ_off[u+1]) = those positions p, ascending
+ * for u in [0, num_rows).  Positions whose index is outside [0, num_rows) are
+ * left out: they fill occ from occ_off[num_rows] on.  index: [n] int32
+ * device; occ_off: [num_rows+1] int32; occ: [n] int32.  Bit-exact and
+ * deterministic.  Limits: n, num_rows < 2^31 - 1.
+ * Workspace: fast_occurrence_csr_workspace(n, num_rows) bytes, 256-byte aligned. */
+size_t fast_occurrence_csr_workspace(int64_t n, int64_t num_rows);
+fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, int64_t num_rows,
+                                  int32_t* occ_off, int32_t* occ, void* ws, size_t ws_bytes,
+                                  fast_stream_t stream);
+
+/* Transposed gather: for every row u in [0, num_rows)
+ *   dst[u, :] = sum over j in [occ_off[u], occ_off[u+1]) of src[occ[j], :]
+ * in that order, accumulated in fp64 and rounded once to fp32 (0 for a row
+ * with no occurrence).  Deterministic: rows with many occurrences are split
+ * into fixed pieces whose sums are added in piece order.  src: [n, D] of
+ * src_dtype (e.g. the per-edge gradients of the indexed backward); dst:
+ * [num_rows, D] fp32, overwritten.  occ_off, occ: from fast_occurrence_csr
+ * (values are clamped into range, so malformed lists never read out of
+ * bounds).  Limits: n, num_rows < 2^31 - 1, D >= 1.
+ * Workspace: fast_index_add_rows_workspace(n, num_rows, D) bytes, 256-byte aligned. */
+size_t fast_index_add_rows_workspace(int64_t n, int64_t num_rows, int D);
+fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32_t* occ, int64_t n,
+                                  int64_t num_rows, int D, fast_dtype_t src_dtype,
+                                  const void* src, float* dst, void* ws, size_t ws_bytes,
+                                  fast_stream_t stream);
 
 #ifdef __cplusplus
 }

@@ -24,6 +24,9 @@ __all__ = [
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
     "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
     "fast_edge_attention_fwd", "fast_edge_attention_bwd",
+    "fast_edge_attention_fwd_indexed", "fast_edge_attention_bwd_indexed",
+    "fast_occurrence_csr_workspace", "fast_occurrence_csr",
+    "fast_index_add_rows_workspace", "fast_index_add_rows",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -94,6 +97,14 @@ _SIGS = {
     "fast_edge_attention_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p, _p]),
     "fast_edge_attention_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p,
                                        _p, _p, _p, _p]),
+    "fast_edge_attention_fwd_indexed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _p,
+                                               _i64, _f32, _f32, _p, _p, _p]),
+    "fast_edge_attention_bwd_indexed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _p,
+                                               _i64, _f32, _f32, _p, _p, _p, _p, _p, _p]),
+    "fast_occurrence_csr_workspace": (_sz, [_i64, _i64]),
+    "fast_occurrence_csr": (_i32, [_p, _i64, _i64, _p, _p, _p, _sz, _p]),
+    "fast_index_add_rows_workspace": (_sz, [_i64, _i64, _i32]),
+    "fast_index_add_rows": (_i32, [_p, _p, _i64, _i64, _i32, _i32, _p, _p, _p, _sz, _p]),
 }
 
 _lib = None
@@ -289,3 +300,40 @@ def fast_edge_attention_bwd(g: TCSR, H, dh, dtype, Q, K, V, scale, neg_slope, ls
     _check(lib().fast_edge_attention_bwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), _ptr(V),
                                          scale, neg_slope, _ptr(lse), _ptr(dout), _ptr(dQ),
                                          _ptr(dK), _ptr(dV), _stream(stream)))
+
+
+def fast_edge_attention_fwd_indexed(g: TCSR, H, dh, dtype, Q, K, k_index, k_rows, V, v_index,
+                                    v_rows, scale, neg_slope, out, lse, stream=None):
+    _check(lib().fast_edge_attention_fwd_indexed(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K),
+                                                 _ptr(k_index), k_rows, _ptr(V), _ptr(v_index),
+                                                 v_rows, scale, neg_slope, _ptr(out), _ptr(lse),
+                                                 _stream(stream)))
+
+
+def fast_edge_attention_bwd_indexed(g: TCSR, H, dh, dtype, Q, K, k_index, k_rows, V, v_index,
+                                    v_rows, scale, neg_slope, lse, dout, dQ, dK_edge, dV_edge,
+                                    stream=None):
+    _check(lib().fast_edge_attention_bwd_indexed(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K),
+                                                 _ptr(k_index), k_rows, _ptr(V), _ptr(v_index),
+                                                 v_rows, scale, neg_slope, _ptr(lse), _ptr(dout),
+                                                 _ptr(dQ), _ptr(dK_edge), _ptr(dV_edge),
+                                                 _stream(stream)))
+
+
+def fast_occurrence_csr_workspace(n: int, num_rows: int) -> int:
+    return lib().fast_occurrence_csr_workspace(n, num_rows)
+
+
+def fast_occurrence_csr(index, n, num_rows, occ_off, occ, ws, ws_bytes, stream=None):
+    _check(lib().fast_occurrence_csr(_ptr(index), n, num_rows, _ptr(occ_off), _ptr(occ), _ptr(ws),
+                                     ws_bytes, _stream(stream)))
+
+
+def fast_index_add_rows_workspace(n: int, num_rows: int, D: int) -> int:
+    return lib().fast_index_add_rows_workspace(n, num_rows, D)
+
+
+def fast_index_add_rows(occ_off, occ, n, num_rows, D, src_dtype, src, dst, ws, ws_bytes,
+                        stream=None):
+    _check(lib().fast_index_add_rows(_ptr(occ_off), _ptr(occ), n, num_rows, D, src_dtype, _ptr(src),
+                                     _ptr(dst), _ptr(ws), ws_bytes, _stream(stream)))

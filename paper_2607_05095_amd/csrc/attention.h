@@ -103,7 +103,21 @@ struct AttnArgs {
   void* dV;
   float* alpha_out;
   float* dalpha_out;
+  // indexed operands: edge e reads row kidx[e] of K and vidx[e] of V (NULL:
+  // row e); an index outside [0, rows) reads the nearest row
+  const int32_t* kidx;
+  const int32_t* vidx;
+  int64_t k_rows, v_rows;
 };
+
+// Row of K or V read by edge e.
+template <bool IDX>
+__device__ __forceinline__ int64_t operand_row(const int32_t* idx, int64_t rows, int64_t e) {
+  if constexpr (IDX) {
+    if (idx) return clamp64(idx[e], 0, rows - 1);
+  }
+  return e;
+}
 
 // ------------------------------------------------------------------ lane map
 template <int P>
@@ -226,7 +240,7 @@ __device__ __forceinline__ int64_t slot_row(int64_t base, int i, int64_t e1) {
       _Pragma("unroll") for (int j_ = 0; j_ < VE; ++j_) arr[p_][j_] = 0.f
 
 // ============================================================ fused forward
-template <typename T, int VE, int P, int LPH_CT, bool NT>
+template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX = false>
 __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
@@ -246,8 +260,9 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd(AttnArg
 #pragma unroll
     for (int i = 0; i < ATT_CH_FWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      load_raw<T, VE, P, NT>(K, e, F, m, kr[i]);
-      load_raw<T, VE, P, NT>(V, e, F, m, vr[i]);
+      // indexed rows are shared across segments: keep them cacheable
+      load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kr[i]);
+      load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vr[i]);
     }
     float t[ATT_CH_FWD];
     float cm = -INFINITY;
@@ -299,7 +314,7 @@ struct BwdState {
 
 // Edges [base, min(base+CH, e1)): loads K and V, forms t (log2-unit logit)
 // and dalpha = <dOut, V>, and folds them into the running sums.
-template <typename T, int VE, int P, int LPH_CT, bool NT>
+template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX>
 __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m, int64_t base,
                                           int64_t e1, bool has_lse, float sl2,
                                           BwdState<VE, P>& S, float (&t)[ATT_CH_BWD],
@@ -311,8 +326,8 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
 #pragma unroll
   for (int i = 0; i < ATT_CH_BWD; ++i) {
     const int64_t e = slot_row(base, i, e1);
-    load_raw<T, VE, P, NT>(K, e, F, m, kr[i]);
-    load_raw<T, VE, P, NT>(V, e, F, m, vr[i]);
+    load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kr[i]);
+    load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vr[i]);
   }
   float cm = -INFINITY;
 #pragma unroll
@@ -375,7 +390,7 @@ __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m,
   store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dV), e, a.L.F, m, dv);
 }
 
-template <typename T, int VE, int P, int LPH_CT, bool NT>
+template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX = false>
 __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
@@ -399,11 +414,12 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
 #pragma unroll
   for (int c = 0; c < ATT_NSAVE; ++c) {
     const int64_t base = e0 + c * ATT_CH_BWD;
-    if (base < e1) bwd_chunk<T, VE, P, LPH_CT, NT>(a, m, base, e1, has_lse, sl2, S, st[c], sda[c]);
+    if (base < e1)
+      bwd_chunk<T, VE, P, LPH_CT, NT, IDX>(a, m, base, e1, has_lse, sl2, S, st[c], sda[c]);
   }
   for (int64_t base = e0 + ATT_NSAVE * ATT_CH_BWD; base < e1; base += ATT_CH_BWD) {
     float tt[ATT_CH_BWD], td[ATT_CH_BWD];
-    bwd_chunk<T, VE, P, LPH_CT, NT>(a, m, base, e1, has_lse, sl2, S, tt, td);
+    bwd_chunk<T, VE, P, LPH_CT, NT, IDX>(a, m, base, e1, has_lse, sl2, S, tt, td);
   }
 
   // dQ = scale/Z * (A - D B)
@@ -431,8 +447,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      load_row<T, VE, P>(static_cast<const T*>(a.K), e, F, m, kx[i]);
-      load_row<T, VE, P>(static_cast<const T*>(a.V), e, F, m, vx[i]);
+      load_row<T, VE, P>(static_cast<const T*>(a.K), operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
+      load_row<T, VE, P>(static_cast<const T*>(a.V), operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
     }
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i) {
@@ -594,7 +610,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) k_agg_bwd(AttnArgs a) {
 #undef FAST_ZERO
 
 // ============================================================ host side
-enum class Op { kAttnFwd, kAttnBwd, kSoftmaxFwd, kSoftmaxBwd, kAggFwd, kAggBwd };
+enum class Op { kAttnFwd, kAttnBwd, kSoftmaxFwd, kSoftmaxBwd, kAggFwd, kAggBwd,
+                kAttnFwdIdx, kAttnBwdIdx };
 
 // Picks the vector width and lane mapping for (H, dh, dtype) given every row
 // pointer the op touches (all must be aligned to the vector access), for
@@ -611,6 +628,8 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
 bool attn_launch_fused(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
                        hipStream_t st);
 bool attn_launch_unfused(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
+                         hipStream_t st);
+bool attn_launch_indexed(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
                          hipStream_t st);
 
 // Dispatch over the instantiated layouts: a fast set with compile-time lanes

@@ -112,7 +112,7 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
     return fail(FAST_ERR_INVALID_ARG, "%s: NaN scale/slope", fn);
   if (g->num_dst == 0 && g->num_edges > 0)
     return fail(FAST_ERR_INVALID_ARG, "%s: E > 0 edges but no destination", fn);
-  const int wg = op == Op::kAttnBwd ? ATT_BLOCK_BWD : ATT_BLOCK;
+  const int wg = (op == Op::kAttnBwd || op == Op::kAttnBwdIdx) ? ATT_BLOCK_BWD : ATT_BLOCK;
   fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, wg, a.L);
   if (s != FAST_OK) return s;
   // Non-temporal streaming only when every per-edge row starts and ends on a
@@ -129,8 +129,10 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
   const dim3 grid{uint32_t(nb)}, block{uint32_t(a.L.block)};
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool fused = op == Op::kAttnFwd || op == Op::kAttnBwd;
-  const bool done = fused ? attn_launch_fused(op, dt, a, grid, block, st)
-                          : attn_launch_unfused(op, dt, a, grid, block, st);
+  const bool indexed = op == Op::kAttnFwdIdx || op == Op::kAttnBwdIdx;
+  const bool done = indexed ? attn_launch_indexed(op, dt, a, grid, block, st)
+                    : fused ? attn_launch_fused(op, dt, a, grid, block, st)
+                            : attn_launch_unfused(op, dt, a, grid, block, st);
   if (!done)
     return fail(FAST_ERR_UNSUPPORTED, "%s: no kernel for VE=%d P=%d LPH=%d", fn, a.L.VE, a.L.P, a.L.LPH);
   return check_launch(fn);

@@ -1,0 +1,495 @@
+// indexed_rows.hip -- the two reductions that indexed operands need (Sec. 4.2:
+// many positions of a batch read one de-duplicated row through the inverse
+// index; the gradient of that row is the sum over those positions).
+//
+// fast_occurrence_csr: for every row, its positions in ascending order -- a
+// stable counting sort of the index, done as an LSD radix sort of (key,
+// position) pairs over 8-bit digits.  Each pass: per-tile digit histograms,
+// one scan of the (digit, tile) counts, and a scatter in which every item
+// finds its rank among the tile's items with the same digit from 8 wave
+// ballots, in position order -- stable, so after the last pass each row's
+// positions are ascending.  Positions whose index is outside the row range
+// get the key num_rows and sort behind every valid one.
+//
+// fast_index_add_rows: dst[u] = sum of src rows over the occurrences of u,
+// in occurrence order, accumulated in fp64 and rounded once to fp32.  A row read by many positions (a
+// hub id of a skewed batch) is cut into pieces of IA_PIECE occurrences:
+// every piece is summed by one group of lanes, and a row with several pieces
+// adds its piece sums in piece order.  The cut depends only on the counts,
+// so the result is the same on every run.
+#include "scan.h"
+
+namespace fast {
+
+// ------------------------------------------------------------------ radix sort
+constexpr int RS_THREADS = 256;
+constexpr int RS_WAVES = RS_THREADS / 64;
+constexpr int RS_ROUNDS = 8;                        // 64-item rounds per wave
+constexpr int RS_TILE = RS_THREADS * RS_ROUNDS;     // 2048 items per tile
+constexpr int RS_DIGITS = 256;
+
+inline int64_t rs_tiles(int64_t n) { return (n + RS_TILE - 1) / RS_TILE; }
+
+// Key and value of item i: in the first pass the key comes from the index
+// (num_rows for a position outside the row range) and the value is i.
+struct RsSrc {
+  const int32_t* index;   // first pass
+  const int32_t* keys;    // later passes
+  const int32_t* vals;
+  int32_t num_rows;
+  __device__ void get(int64_t i, uint32_t& k, int32_t& v) const {
+    if (index) {
+      const int32_t x = index[i];
+      k = (x >= 0 && x < num_rows) ? uint32_t(x) : uint32_t(num_rows);
+      v = int32_t(i);
+    } else {
+      k = uint32_t(keys[i]);
+      v = vals[i];
+    }
+  }
+};
+
+// Items of a tile: wave w takes items [w*512, (w+1)*512) in rounds of 64
+// consecutive items, so (wave, round, lane) order is position order.
+__device__ __forceinline__ int64_t rs_item(int64_t tile, int w, int r, int lane) {
+  return tile * RS_TILE + int64_t(w) * (RS_ROUNDS * 64) + r * 64 + lane;
+}
+
+// Lanes of the wave holding the same digit as this lane (inactive lanes excluded).
+__device__ __forceinline__ uint64_t digit_match(uint32_t d, bool valid) {
+  uint64_t m = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (d >> b) & 1u;
+    const uint64_t bal = __ballot(bit);
+    m &= bit ? bal : ~bal;
+  }
+  return m;
+}
+
+// hist[d * T + tile] = items of the tile whose digit is d.
+__global__ void __launch_bounds__(RS_THREADS) k_rs_hist(RsSrc src, int64_t n, int shift,
+                                                       uint32_t* hist, int64_t T) {
+  __shared__ uint32_t s_h[RS_DIGITS];
+  s_h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t tile = blockIdx.x;
+#pragma unroll
+  for (int k = 0; k < RS_ROUNDS; ++k) {
+    const int64_t i = tile * RS_TILE + int64_t(k) * RS_THREADS + threadIdx.x;
+    if (i < n) {
+      uint32_t key;
+      int32_t v;
+      src.get(i, key, v);
+      atomicAdd(&s_h[(key >> shift) & 255u], 1u);
+    }
+  }
+  __syncthreads();
+  hist[int64_t(threadIdx.x) * T + tile] = s_h[threadIdx.x];
+}
+
+// base[d * T + tile] (after the scan) = first output slot of the tile's
+// items with digit d.  Writes keys (unless NULL) and values.
+__global__ void __launch_bounds__(RS_THREADS) k_rs_scatter(RsSrc src, int64_t n, int shift,
+                                                          const uint32_t* base, int64_t T,
+                                                          int32_t* keys_out, int32_t* vals_out) {
+  __shared__ uint32_t s_cnt[RS_WAVES][RS_DIGITS];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t tile = blockIdx.x;
+  const uint64_t lt = (uint64_t(1) << lane) - 1;
+#pragma unroll
+  for (int j = 0; j < RS_WAVES; ++j) s_cnt[j][threadIdx.x] = 0;
+  __syncthreads();
+  // A: counts per (wave, digit)
+  for (int r = 0; r < RS_ROUNDS; ++r) {
+    const int64_t i = rs_item(tile, w, r, lane);
+    const bool valid = i < n;
+    uint32_t key = 0;
+    int32_t v = 0;
+    if (valid) src.get(i, key, v);
+    const uint32_t d = (key >> shift) & 255u;
+    const uint64_t m = digit_match(d, valid);
+    if (valid && (m & lt) == 0) s_cnt[w][d] += uint32_t(__popcll(m));   // lowest lane of its digit
+  }
+  __syncthreads();
+  // exclusive prefix over the waves, per digit
+  {
+    uint32_t run = 0;
+#pragma unroll
+    for (int j = 0; j < RS_WAVES; ++j) {
+      const uint32_t c = s_cnt[j][threadIdx.x];
+      s_cnt[j][threadIdx.x] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  // B: rank inside the tile and scatter
+  for (int r = 0; r < RS_ROUNDS; ++r) {
+    const int64_t i = rs_item(tile, w, r, lane);
+    const bool valid = i < n;
+    uint32_t key = 0;
+    int32_t v = 0;
+    if (valid) src.get(i, key, v);
+    const uint32_t d = (key >> shift) & 255u;
+    const uint64_t m = digit_match(d, valid);
+    const uint32_t before = s_cnt[w][d];
+    if (valid) {
+      const int64_t pos = int64_t(base[int64_t(d) * T + tile]) + before + uint32_t(__popcll(m & lt));
+      if (keys_out) keys_out[pos] = int32_t(key);
+      vals_out[pos] = v;
+    }
+    if (valid && (m & lt) == 0) s_cnt[w][d] = before + uint32_t(__popcll(m));
+  }
+}
+
+struct InU32 {
+  const uint32_t* p;
+  __device__ uint32_t operator()(int64_t i) const { return p[i]; }
+};
+struct OutU32InPlace {
+  uint32_t* p;
+  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { p[i] = prefix; }
+};
+
+// counts of the valid index values
+__global__ void __launch_bounds__(RS_THREADS) k_occ_count(const int32_t* __restrict__ index,
+                                                         int64_t n, int32_t num_rows,
+                                                         int32_t* count) {
+  for (int64_t i = int64_t(blockIdx.x) * RS_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * RS_THREADS) {
+    const int32_t x = index[i];
+    if (x >= 0 && x < num_rows) atomicAdd(&count[x], 1);
+  }
+}
+
+__global__ void __launch_bounds__(RS_THREADS) k_ir_fill(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = int64_t(blockIdx.x) * RS_THREADS + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * RS_THREADS)
+    p[i] = v;
+}
+
+struct InCount {
+  const int32_t* c;
+  __device__ uint32_t operator()(int64_t i) const { return uint32_t(c[i]); }
+};
+struct OutOff {
+  int32_t* off;
+  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { off[i] = int32_t(prefix); }
+};
+
+struct OccWs {
+  int32_t* count;
+  void* scan_c;
+  int32_t* keys[2];
+  int32_t* vals[2];
+  uint32_t* hist;
+  void* scan_h;
+};
+
+static size_t occ_layout(int64_t n, int64_t num_rows, char* base, OccWs* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  const int64_t T = rs_tiles(n);
+  char* c = take(size_t(num_rows) * 4);
+  char* sc = take(scan_workspace(num_rows));
+  char* k0 = take(size_t(n) * 4);
+  char* k1 = take(size_t(n) * 4);
+  char* v0 = take(size_t(n) * 4);
+  char* v1 = take(size_t(n) * 4);
+  char* h = take(size_t(T) * RS_DIGITS * 4);
+  char* sh = take(scan_workspace(T * RS_DIGITS));
+  if (ws) {
+    ws->count = reinterpret_cast<int32_t*>(c);
+    ws->scan_c = sc;
+    ws->keys[0] = reinterpret_cast<int32_t*>(k0);
+    ws->keys[1] = reinterpret_cast<int32_t*>(k1);
+    ws->vals[0] = reinterpret_cast<int32_t*>(v0);
+    ws->vals[1] = reinterpret_cast<int32_t*>(v1);
+    ws->hist = reinterpret_cast<uint32_t*>(h);
+    ws->scan_h = sh;
+  }
+  return off;
+}
+
+static uint32_t grid_cap(int64_t n, int64_t per, uint32_t cap = 8192) {
+  int64_t g = (n + per - 1) / per;
+  if (g < 1) g = 1;
+  return uint32_t(g < cap ? g : cap);
+}
+
+// ------------------------------------------------------------------ index add
+constexpr int IA_THREADS = 256;
+constexpr int IA_PIECE = 64;   // occurrences summed by one group
+
+// Packed per-row item: high word = pieces of the row, low word = pieces of
+// the row if it has more than one (slots of piece sums), else 0.
+struct InPieces {
+  const int32_t* occ_off;
+  int64_t n;
+  __device__ uint64_t operator()(int64_t u) const {
+    const int64_t c = clamp64(int64_t(occ_off[u + 1]) - occ_off[u], 0, n);
+    const uint64_t np = c > 0 ? uint64_t((c + IA_PIECE - 1) / IA_PIECE) : 0;
+    return (np << 32) | (np > 1 ? np : 0);
+  }
+};
+struct OutPieces {
+  int32_t* piece_off;   // [num_rows + 1]
+  int32_t* multi_off;   // [num_rows + 1]
+  int64_t num_rows;
+  __device__ void operator()(int64_t u, uint64_t prefix, uint64_t v) const {
+    piece_off[u] = int32_t(prefix >> 32);
+    multi_off[u] = int32_t(prefix & 0xffffffffu);
+    if (u == num_rows - 1) {
+      piece_off[u + 1] = int32_t((prefix + v) >> 32);
+      multi_off[u + 1] = int32_t((prefix + v) & 0xffffffffu);
+    }
+  }
+};
+
+// One group of `lanes` lanes per piece; lane l owns the VE-chunks l, l+lanes, ...
+// Sums are fp64 (a hub row adds hundreds of thousands of rows, whose fp32 sum
+// could lose the digits a cancelling total keeps); dst is rounded once.
+template <typename T, int VE>
+__global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
+    const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
+    const int32_t* __restrict__ piece_off, const int32_t* __restrict__ multi_off,
+    int64_t num_rows, int64_t piece_bound, int64_t multi_bound, int64_t n, int lanes, int D,
+    const T* __restrict__ src, float* __restrict__ dst, double* __restrict__ partial) {
+  const int64_t q = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
+  const int l = int(threadIdx.x) % lanes;
+  if (q >= piece_bound || q >= piece_off[num_rows]) return;
+  // row u with piece_off[u] <= q < piece_off[u + 1]
+  int64_t lo = 0, hi = num_rows - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (piece_off[mid] <= q) lo = mid; else hi = mid - 1;
+  }
+  const int64_t u = lo;
+  const int64_t k = q - piece_off[u];                       // piece of row u
+  // offsets and positions are clamped into range, so malformed occurrence
+  // lists give wrong sums but never an out-of-bounds access
+  const int64_t r0 = clamp64(occ_off[u], 0, n);
+  const int64_t j0 = clamp64(r0 + k * IA_PIECE, 0, n);
+  const int64_t j1 = clamp64(j0 + IA_PIECE < occ_off[u + 1] ? j0 + IA_PIECE : occ_off[u + 1], j0, n);
+  const int64_t npieces = int64_t(piece_off[u + 1]) - piece_off[u];
+  const int64_t slot = int64_t(multi_off[u]) + k;
+  if (npieces != 1 && slot >= multi_bound) return;
+  const int chunks = D / VE;
+  for (int c = l; c < chunks; c += lanes) {
+    double acc[VE];
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] = 0.0;
+    for (int64_t j = j0; j < j1; ++j) {
+      float x[VE];
+      VecIO<T, VE>::load(src + clamp64(occ[j], 0, n - 1) * D + c * VE, x);
+#pragma unroll
+      for (int t = 0; t < VE; ++t) acc[t] += double(x[t]);
+    }
+    if (npieces == 1) {
+      float o[VE];
+#pragma unroll
+      for (int t = 0; t < VE; ++t) o[t] = float(acc[t]);
+      VecIO<float, VE>::store(dst + u * D + c * VE, o);
+    } else {
+#pragma unroll
+      for (int t = 0; t < VE; ++t) partial[slot * D + c * VE + t] = acc[t];
+    }
+  }
+}
+
+// One group per row: zeros for a row no position reads, the ordered sum of
+// its piece sums for a row of several pieces.
+template <int VE>
+__global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
+    const int32_t* __restrict__ piece_off, const int32_t* __restrict__ multi_off,
+    int64_t num_rows, int64_t multi_bound, int lanes, int D, const double* __restrict__ partial,
+    float* __restrict__ dst) {
+  const int64_t u = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
+  const int l = int(threadIdx.x) % lanes;
+  if (u >= num_rows) return;
+  const int64_t np = int64_t(piece_off[u + 1]) - piece_off[u];
+  if (np == 1) return;
+  const int64_t m0 = multi_off[u];
+  const int64_t m1 = m0 + np < multi_bound ? m0 + np : multi_bound;
+  const int chunks = D / VE;
+  for (int c = l; c < chunks; c += lanes) {
+    double acc[VE];
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] = 0.0;
+    for (int64_t m = m0; m < m1 && np > 1; ++m) {
+#pragma unroll
+      for (int t = 0; t < VE; ++t) acc[t] += partial[m * D + c * VE + t];
+    }
+    float o[VE];
+#pragma unroll
+    for (int t = 0; t < VE; ++t) o[t] = float(acc[t]);
+    VecIO<float, VE>::store(dst + u * D + c * VE, o);
+  }
+}
+
+struct IaWs {
+  int32_t* piece_off;
+  int32_t* multi_off;
+  void* scan;
+  double* partial;
+};
+
+static int64_t ia_multi_bound(int64_t n) { return (2 * n) / IA_PIECE + 1; }
+
+static size_t ia_layout(int64_t n, int64_t num_rows, int D, char* base, IaWs* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  char* po = take(size_t(num_rows + 1) * 4);
+  char* mo = take(size_t(num_rows + 1) * 4);
+  char* sc = take(scan_workspace<uint64_t>(num_rows));
+  char* pa = take(size_t(ia_multi_bound(n)) * size_t(D) * 8);
+  if (ws) {
+    ws->piece_off = reinterpret_cast<int32_t*>(po);
+    ws->multi_off = reinterpret_cast<int32_t*>(mo);
+    ws->scan = sc;
+    ws->partial = reinterpret_cast<double*>(pa);
+  }
+  return off;
+}
+
+static int pow2_at_least(int x, int cap) {
+  int p = 1;
+  while (p < x && p < cap) p <<= 1;
+  return p;
+}
+
+}  // namespace fast
+
+using namespace fast;
+
+extern "C" size_t fast_occurrence_csr_workspace(int64_t n, int64_t num_rows) {
+  if (n < 0 || num_rows < 0 || n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return 0;
+  return occ_layout(n, num_rows, nullptr, nullptr);
+}
+
+extern "C" fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, int64_t num_rows,
+                                             int32_t* occ_off, int32_t* occ, void* ws,
+                                             size_t ws_bytes, fast_stream_t stream) {
+  const char* fn = "fast_occurrence_csr";
+  if (n < 0 || num_rows < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
+  if (n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: n or num_rows beyond 2^31", fn);
+  if (!occ_off) return fail(FAST_ERR_INVALID_ARG, "%s: occ_off is NULL", fn);
+  if (n > 0 && (!index || !occ)) return fail(FAST_ERR_INVALID_ARG, "%s: index/occ is NULL", fn);
+  const size_t need = fast_occurrence_csr_workspace(n, num_rows);
+  if (!ws || ws_bytes < need)
+    return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  OccWs w;
+  occ_layout(n, num_rows, static_cast<char*>(ws), &w);
+  // row offsets: counts of the valid index values, scanned
+  if (num_rows > 0) {
+    hipLaunchKernelGGL(k_ir_fill, dim3(grid_cap(num_rows, RS_THREADS * 4)), dim3(RS_THREADS), 0, st,
+                       w.count, num_rows, 0);
+    if (n > 0)
+      hipLaunchKernelGGL(k_occ_count, dim3(grid_cap(n, RS_THREADS * 8)), dim3(RS_THREADS), 0, st,
+                         index, n, int32_t(num_rows), w.count);
+  }
+  hipError_t e = scan_launch(InCount{w.count}, OutOff{occ_off}, num_rows, w.scan_c, nullptr,
+                             occ_off + num_rows, st);
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+  if (n == 0) return check_launch(fn);
+  // positions sorted stably by key, 8 bits per pass (keys <= num_rows)
+  int bits = 1;
+  while ((int64_t(1) << bits) <= num_rows) ++bits;
+  const int passes = (bits + 7) / 8;
+  const int64_t T = rs_tiles(n);
+  for (int p = 0; p < passes; ++p) {
+    RsSrc src{p == 0 ? index : nullptr, w.keys[(p + 1) & 1], w.vals[(p + 1) & 1], int32_t(num_rows)};
+    const bool last = p == passes - 1;
+    int32_t* kout = last ? nullptr : w.keys[p & 1];
+    int32_t* vout = last ? occ : w.vals[p & 1];
+    hipLaunchKernelGGL(k_rs_hist, dim3(uint32_t(T)), dim3(RS_THREADS), 0, st, src, n, 8 * p, w.hist, T);
+    e = scan_launch(InU32{w.hist}, OutU32InPlace{w.hist}, T * RS_DIGITS, w.scan_h, nullptr, nullptr, st);
+    if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+    hipLaunchKernelGGL(k_rs_scatter, dim3(uint32_t(T)), dim3(RS_THREADS), 0, st, src, n, 8 * p,
+                       w.hist, T, kout, vout);
+  }
+  return check_launch(fn);
+}
+
+extern "C" size_t fast_index_add_rows_workspace(int64_t n, int64_t num_rows, int D) {
+  if (n < 0 || num_rows < 0 || D < 1 || n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return 0;
+  return ia_layout(n, num_rows, D, nullptr, nullptr);
+}
+
+extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32_t* occ,
+                                             int64_t n, int64_t num_rows, int D,
+                                             fast_dtype_t src_dtype, const void* src, float* dst,
+                                             void* ws, size_t ws_bytes, fast_stream_t stream) {
+  const char* fn = "fast_index_add_rows";
+  if (n < 0 || num_rows < 0 || D < 1) return fail(FAST_ERR_INVALID_ARG, "%s: bad size", fn);
+  if (n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: n or num_rows beyond 2^31", fn);
+  if (src_dtype != FAST_F32 && src_dtype != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
+  if (num_rows == 0) return ok();
+  if (!occ_off || !dst) return fail(FAST_ERR_INVALID_ARG, "%s: occ_off/dst is NULL", fn);
+  if (n > 0 && (!occ || !src)) return fail(FAST_ERR_INVALID_ARG, "%s: occ/src is NULL", fn);
+  const size_t need = fast_index_add_rows_workspace(n, num_rows, D);
+  if (!ws || ws_bytes < need)
+    return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
+  const int esz = elem_size(src_dtype);
+  // vector width: divides D and matches both row pointers
+  int VE = 1;
+  for (int v : {4, 2}) {
+    if (D % v == 0 && aligned(src, size_t(v) * esz) && aligned(dst, size_t(v) * 4)) {
+      VE = v;
+      break;
+    }
+  }
+  if (!aligned(src, size_t(esz)) || !aligned(dst, 4))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: src/dst misaligned", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  IaWs w;
+  ia_layout(n, num_rows, D, static_cast<char*>(ws), &w);
+  hipError_t e = scan_launch<InPieces, OutPieces, uint64_t>(
+      InPieces{occ_off, n}, OutPieces{w.piece_off, w.multi_off, num_rows}, num_rows, w.scan, nullptr,
+      nullptr, st);
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+  const int lanes = pow2_at_least(D / VE, 64);
+  // pieces: at most n / IA_PIECE + (rows read at all) <= n / IA_PIECE + min(n, num_rows) + 1
+  const int64_t piece_bound = n / IA_PIECE + (n < num_rows ? n : num_rows) + 1;
+  const int64_t groups_per_block = IA_THREADS / lanes;
+  if (n > 0) {
+    const int64_t nb = (piece_bound + groups_per_block - 1) / groups_per_block;
+#define FAST_IA(T_, VE_)                                                                          \
+  hipLaunchKernelGGL((k_ia_pieces<T_, VE_>), dim3(uint32_t(nb)), dim3(IA_THREADS), 0, st, occ_off, \
+                     occ, w.piece_off, w.multi_off, num_rows, piece_bound, ia_multi_bound(n), n,   \
+                     lanes, D,                                                                      \
+                     static_cast<const T_*>(src), dst, w.partial)
+    if (src_dtype == FAST_F32) {
+      if (VE == 4) FAST_IA(float, 4); else if (VE == 2) FAST_IA(float, 2); else FAST_IA(float, 1);
+    } else {
+      if (VE == 4) FAST_IA(uint16_t, 4); else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
+    }
+#undef FAST_IA
+  }
+  const int64_t nr = (num_rows + groups_per_block - 1) / groups_per_block;
+  if (VE == 4)
+    hipLaunchKernelGGL(k_ia_rows<4>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
+                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
+  else if (VE == 2)
+    hipLaunchKernelGGL(k_ia_rows<2>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
+                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
+  else
+    hipLaunchKernelGGL(k_ia_rows<1>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
+                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
+  return check_launch(fn);
+}

@@ -268,3 +268,32 @@ def test_sample_recent_validation():
     assert call(g=ctypes.byref(bad)) == INVALID
     bad = fast.TemporalGraphDesc(100, 1000, FAKE, FAKE, None, FAKE)
     assert call(g=ctypes.byref(bad)) == INVALID
+
+
+def test_indexed_operands_validation():
+    L = fast.lib()
+    gp = ctypes.byref(_g())
+    # an index with no rows behind it; NULL operands; dtype
+    assert L.fast_edge_attention_fwd_indexed(gp, 2, 50, 0, FAKE, FAKE, FAKE, 0, FAKE, None, 0,
+                                             1.0, 0.2, FAKE, None, None) == INVALID
+    assert L.fast_edge_attention_fwd_indexed(gp, 2, 50, 0, FAKE, None, FAKE, 5, FAKE, None, 0,
+                                             1.0, 0.2, FAKE, None, None) == INVALID
+    assert L.fast_edge_attention_bwd_indexed(gp, 2, 50, 0, FAKE, FAKE, FAKE, 5, FAKE, FAKE, 5,
+                                             1.0, 0.2, None, FAKE, FAKE, None, FAKE, None) == INVALID
+    assert L.fast_edge_attention_bwd_indexed(gp, 2, 50, 9, FAKE, FAKE, FAKE, 5, FAKE, FAKE, 5,
+                                             1.0, 0.2, None, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    ws = L.fast_occurrence_csr_workspace(1000, 50)
+    assert ws >= 4 * 1000 * 4 and L.fast_occurrence_csr_workspace(-1, 5) == 0
+    assert L.fast_occurrence_csr(FAKE, 1000, 50, FAKE, FAKE, FAKE, ws - 1, None) == WORKSPACE
+    assert L.fast_occurrence_csr(None, 1000, 50, FAKE, FAKE, FAKE, ws, None) == INVALID
+    assert L.fast_occurrence_csr(FAKE, 1000, 50, None, FAKE, FAKE, ws, None) == INVALID
+    assert L.fast_occurrence_csr(FAKE, -1, 50, FAKE, FAKE, FAKE, ws, None) == INVALID
+    assert L.fast_occurrence_csr(FAKE, 1000, 50, FAKE, FAKE, FAKE + 8, ws, None) == UNSUPPORTED
+    wa = L.fast_index_add_rows_workspace(1000, 50, 100)
+    assert wa > 0 and L.fast_index_add_rows_workspace(1000, 50, 0) == 0
+    assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 0, FAKE, FAKE, FAKE, wa - 1, None) == WORKSPACE
+    assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 3, FAKE, FAKE, FAKE, wa, None) == INVALID
+    assert L.fast_index_add_rows(None, FAKE, 1000, 50, 100, 0, FAKE, FAKE, FAKE, wa, None) == INVALID
+    assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 0, None, FAKE, FAKE, wa, None) == INVALID
+    assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 0, FAKE + 2, FAKE, FAKE, wa, None) == UNSUPPORTED
+    assert L.fast_index_add_rows(FAKE, FAKE, 1000, 0, 100, 0, FAKE, None, None, 0, None) == OK

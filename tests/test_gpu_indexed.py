@@ -1,0 +1,192 @@
+"""GPU parity of indexed operands through the C ABI: the fused attention
+reading K and V through an index into de-duplicated rows (forward and
+per-edge backward), the occurrence lists of an index (bit-exact), and the
+transposed gather that turns per-edge gradients into row gradients.
+
+Each GPU op is compared with the oracle on the same inputs: the attention
+against the oracle on the gathered rows (sampled segments at the full-size
+workloads), the occurrence lists bit-exactly, and the row sums against the
+oracle's fp64 sums of the same per-edge rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05095_amd as fast
+from synth import _randn, make_batch
+from tests.parity import (SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks,
+                          sample_segments, sub_csr, tdtype, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+DT = {"f32": fast.F32, "bf16": fast.BF16}
+
+
+def _announce(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+def _host(t):
+    return t.detach().float().cpu().double().numpy()
+
+
+def _occ_gpu(index_np, num_rows):
+    n = index_np.shape[0]
+    idx = to_dev(np.ascontiguousarray(index_np, np.int32)) if n else \
+        torch.empty(0, dtype=torch.int32, device="cuda")
+    off = torch.full((num_rows + 1,), -9, dtype=torch.int32, device="cuda")
+    occ = torch.full((max(n, 1),), -9, dtype=torch.int32, device="cuda")
+    wsb = fast.fast_occurrence_csr_workspace(n, num_rows)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_occurrence_csr(idx, n, num_rows, off, occ, ws, wsb)
+    torch.cuda.synchronize()
+    return off, occ
+
+
+def _index_add_gpu(off, occ, n, num_rows, src):
+    D = int(np.prod(src.shape[1:])) if src.dim() > 1 else 1
+    dst = torch.full((num_rows, D), float("nan"), device="cuda")
+    wsb = fast.fast_index_add_rows_workspace(n, num_rows, D)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    dt = fast.BF16 if src.dtype == torch.bfloat16 else fast.F32
+    fast.fast_index_add_rows(off, occ, n, num_rows, D, dt, src, dst, ws, wsb)
+    torch.cuda.synchronize()
+    return dst
+
+
+@pytest.mark.parametrize("n,rows", [(0, 5), (10, 0), (1, 1), (5000, 37), (300_000, 200),
+                                    (300_000, 60_000), (2_000_000, 541_000), (5_052_000, 1_000_000)])
+def test_occurrence_csr_bit_exact(n, rows):
+    _announce(f"occurrence csr n={n} rows={rows}")
+    r = np.random.default_rng(n + rows)
+    idx = ((r.zipf(1.2, n) - 1) % max(rows, 1)).astype(np.int32) if rows else r.integers(-3, 3, n).astype(np.int32)
+    if n > 20:
+        idx[::29] = -1                                   # positions outside the row range
+        idx[3::31] = rows + 7
+    off, occ = _occ_gpu(idx, rows)
+    want_off, want_occ = oracle.occurrence_csr(idx, rows)
+    assert np.array_equal(off.cpu().numpy(), want_off)
+    assert np.array_equal(occ.cpu().numpy()[:want_off[-1]], want_occ)
+
+
+@pytest.mark.parametrize("D,dt,rows", [(100, "f32", 300), (128, "bf16", 5000), (172, "f32", 40),
+                                       (7, "f32", 1000), (50, "bf16", 3), (1, "f32", 100)])
+def test_index_add_rows_vs_oracle(D, dt, rows):
+    _announce(f"index add D={D} {dt} rows={rows}")
+    r = np.random.default_rng(D * 7 + rows)
+    n = 200_000
+    idx = ((r.zipf(1.3, n) - 1) % rows).astype(np.int32)   # hub rows with tens of thousands of reads
+    idx[::97] = -1
+    src = _randn((n, D), dt, "cuda", D + rows)
+    off, occ = _occ_gpu(idx, rows + 2)                      # two rows nobody reads
+    got = _index_add_gpu(off, occ, n, rows + 2, src)
+    want = oracle.index_add_rows(idx, rows + 2, _host(src))
+    assert_close(got, want, "f32", f"index add D={D}")
+    again = _index_add_gpu(off, occ, n, rows + 2, src)
+    assert torch.equal(got, again), "index add must be bitwise reproducible"
+    assert torch.all(got[rows:] == 0)
+
+
+def _indexed_block(b, i, seed):
+    """Operands of block i with K read through the de-duplication inverse of
+    the block's source node ids and V through that of its edge ids."""
+    blk = b.blocks[i]
+    _, kidx = np.unique(blk.src_ids, return_inverse=True)
+    _, vidx = np.unique(blk.edge_ids, return_inverse=True)
+    Uk, Uv = int(kidx.max()) + 1, int(vidx.max()) + 1
+    base = 7000 + 16 * seed
+    ops = dict(Q=_randn((blk.num_dst, b.H, b.dh), b.dtype, "cuda", base),
+               K=_randn((Uk, b.H, b.dh), b.dtype, "cuda", base + 1),
+               V=_randn((Uv, b.H, b.dh), b.dtype, "cuda", base + 2),
+               dO=_randn((blk.num_dst, b.H, b.dh), b.dtype, "cuda", base + 3))
+    return blk, kidx.astype(np.int32), vidx.astype(np.int32), Uk, Uv, ops
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_indexed_attention_workloads(cfg):
+    b = make_batch(cfg)
+    for i, blk in enumerate(b.blocks):
+        _announce(f"indexed attention cfg={cfg} block={i}")
+        blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
+        off = oracle.csr_offsets(blk.counts)
+        N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
+        scale = float(np.float32(1 / np.sqrt(dh)))
+        d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
+        g = fast.tcsr(d_off, E)
+        tt = tdtype(dt)
+        out = torch.empty((N, H, dh), dtype=tt, device="cuda")
+        lse = torch.empty((N, H), device="cuda")
+        fast.fast_edge_attention_fwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v, Uv,
+                                             scale, SLOPE, out, lse)
+        dQ = torch.empty((N, H, dh), dtype=tt, device="cuda")
+        dKe = torch.empty((E, H, dh), dtype=tt, device="cuda")
+        dVe = torch.empty((E, H, dh), dtype=tt, device="cuda")
+        fast.fast_edge_attention_bwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v,
+                                             Uv, scale, SLOPE, lse, o["dO"], dQ, dKe, dVe)
+        torch.cuda.synchronize()
+        segs = np.arange(N) if E <= 200_000 else \
+            sample_segments(N, 1500, seed=cfg * 10 + i, include=[0, N - 1])
+        sub_off, eidx = sub_csr(off, segs)
+        sg, ei = torch.as_tensor(segs, device="cuda"), torch.as_tensor(eidx, device="cuda")
+        Q64, dO64 = _host(o["Q"][sg]), _host(o["dO"][sg])
+        K64 = _host(o["K"][torch.as_tensor(kidx[eidx].astype(np.int64), device="cuda")])
+        V64 = _host(o["V"][torch.as_tensor(vidx[eidx].astype(np.int64), device="cuda")])
+        r_out, r_lse, _, _ = oracle.edge_attention_fwd(sub_off, Q64, K64, V64, scale, SLOPE)
+        r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(sub_off, Q64, K64, V64, dO64, scale, SLOPE)
+        what = f"cfg{cfg}/L{i + 1} indexed"
+        assert_close(out[sg], r_out, dt, what + " out")
+        nz = np.diff(sub_off) > 0
+        assert_close(_host(lse[sg])[nz], r_lse[nz], "f32", what + " lse")
+        assert_close(dVe[ei], r_dV, dt, what + " dV_edge")
+        assert_bwd_close(dQ[sg], dKe[ei], sub_off, r_dQ, r_dK, alts, dt, what)
+        # row gradients: occurrence lists bit-exact, then the ordered fp64 sums
+        # of the per-edge gradients (compared on a sample of rows, hubs included)
+        for name, idx, U, per_edge in (("K", kidx, Uk, dKe), ("V", vidx, Uv, dVe)):
+            occ_off, occ = _occ_gpu(idx, U)
+            w_off, w_occ = oracle.occurrence_csr(idx, U)
+            assert np.array_equal(occ_off.cpu().numpy(), w_off), f"{what} occ_off {name}"
+            assert np.array_equal(occ.cpu().numpy()[:E], w_occ), f"{what} occ {name}"
+            rows_grad = _index_add_gpu(occ_off, occ, E, U, per_edge.reshape(E, H * dh))
+            counts = np.diff(w_off)
+            pick = np.unique(np.concatenate([np.argsort(counts)[-20:],
+                                             np.random.default_rng(i).choice(U, min(U, 300), replace=False)]))
+            sub = np.full(U, -1, np.int32)
+            sub[pick] = np.arange(pick.size, dtype=np.int32)
+            sel = np.flatnonzero(sub[idx] >= 0)
+            src = _host(per_edge.reshape(E, H * dh)[torch.as_tensor(sel, device="cuda")])
+            want = oracle.index_add_rows(sub[idx[sel]], pick.size, src)
+            assert_close(rows_grad[torch.as_tensor(pick, device="cuda")], want, "f32",
+                         f"{what} d{name} rows")
+        del o, out, dQ, dKe, dVe
+        torch.cuda.empty_cache()
+
+
+def test_identity_index_equals_plain_operator():
+    _announce("indexed attention with identity index vs plain")
+    b = make_batch(1)
+    blk = b.blocks[0]
+    N, E, H, dh = blk.num_dst, blk.num_edges, b.H, b.dh
+    off = to_dev(oracle.csr_offsets(blk.counts))
+    g = fast.tcsr(off, E)
+    Q, K, V, dO = (_randn(s, "f32", "cuda", 50 + j) for j, s in
+                   enumerate([(N, H, dh), (E, H, dh), (E, H, dh), (N, H, dh)]))
+    ident = torch.arange(E, dtype=torch.int32, device="cuda")
+    scale = float(np.float32(1 / np.sqrt(dh)))
+    outs = []
+    for indexed in (False, True):
+        out = torch.empty((N, H, dh), device="cuda")
+        lse = torch.empty((N, H), device="cuda")
+        dQ, dK, dV = (torch.empty_like(x) for x in (Q, K, V))
+        if indexed:
+            fast.fast_edge_attention_fwd_indexed(g, H, dh, fast.F32, Q, K, ident, E, V, None, E, scale,
+                                                 SLOPE, out, lse)
+            fast.fast_edge_attention_bwd_indexed(g, H, dh, fast.F32, Q, K, ident, E, V, None, E, scale,
+                                                 SLOPE, lse, dO, dQ, dK, dV)
+        else:
+            fast.fast_edge_attention_fwd(g, H, dh, fast.F32, Q, K, V, scale, SLOPE, out, lse)
+            fast.fast_edge_attention_bwd(g, H, dh, fast.F32, Q, K, V, scale, SLOPE, lse, dO, dQ, dK, dV)
+        torch.cuda.synchronize()
+        outs.append((out, lse, dQ, dK, dV))
+    for a, c in zip(*outs):
+        assert torch.equal(a, c)
