@@ -242,8 +242,8 @@ def widened_ops(b, step, torch, fast, reps=10):
     """Operators beyond the timed step, each timed alone with HIP events on
     its launch stream (mean of `reps` launches after one warm-up): the
     time-encoding backward of each layer block, on a seeded upstream
-    gradient, the cache selection of Alg. 1, and two hops of most-recent-k
-    temporal sampling."""
+    gradient, the cache selection of Alg. 1, two hops of most-recent-k
+    temporal sampling, and the layer-1 attention with indexed operands."""
     from synth import _randn
     esz = 4 if b.dtype == "f32" else 2
     res = {}
@@ -277,7 +277,74 @@ def widened_ops(b, step, torch, fast, reps=10):
         del dte, ws
     res.update(hot_set_ops(b, torch, fast))
     res.update(sampler_ops(b, torch, fast))
+    res.update(indexed_ops(b, step, torch, fast))
     return res
+
+
+def indexed_ops(b, step, torch, fast, reps=5):
+    """The layer-1 fused attention with indexed operands: K read through the
+    de-duplication inverse of the block's source node ids, V through that of
+    its edge ids (compact rows), then the row gradients of both (occurrence
+    lists + ordered row sums)."""
+    from synth import _randn
+    blk, d = b.blocks[0], step.blocks[0]
+    N, E, H, dh = blk.num_dst, blk.num_edges, b.H, b.dh
+    F, esz = H * dh, (4 if b.dtype == "f32" else 2)
+    _, kidx = np.unique(blk.src_ids, return_inverse=True)
+    _, vidx = np.unique(blk.edge_ids, return_inverse=True)
+    Uk, Uv = int(kidx.max()) + 1, int(vidx.max()) + 1
+    tdt = torch.float32 if b.dtype == "f32" else torch.bfloat16
+    K = _randn((Uk, H, dh), b.dtype, "cuda", 9001)
+    V = _randn((Uv, H, dh), b.dtype, "cuda", 9002)
+    ki = torch.from_numpy(kidx.astype(np.int32)).cuda()
+    vi = torch.from_numpy(vidx.astype(np.int32)).cuda()
+    g = d["g"][0]
+    out = torch.empty((N, H, dh), dtype=tdt, device="cuda")
+    lse = torch.empty((N, H), device="cuda")
+    dQ = torch.empty((N, H, dh), dtype=tdt, device="cuda")
+    dKe = torch.empty((E, H, dh), dtype=tdt, device="cuda")
+    dVe = torch.empty((E, H, dh), dtype=tdt, device="cuda")
+    bufs = {}
+    for name, idx, U in (("K", ki, Uk), ("V", vi, Uv)):
+        wo = fast.fast_occurrence_csr_workspace(E, U)
+        wa = fast.fast_index_add_rows_workspace(E, U, F)
+        bufs[name] = dict(idx=idx, U=U, off=torch.empty(U + 1, dtype=torch.int32, device="cuda"),
+                          occ=torch.empty(E, dtype=torch.int32, device="cuda"),
+                          wso=torch.empty(wo, dtype=torch.uint8, device="cuda"), wo=wo,
+                          wsa=torch.empty(wa, dtype=torch.uint8, device="cuda"), wa=wa,
+                          dst=torch.empty((U, F), device="cuda"))
+
+    def fwd():
+        fast.fast_edge_attention_fwd_indexed(g, H, dh, step.DT, d["Q"], K, ki, Uk, V, vi, Uv, step.scale,
+                                             SLOPE, out, lse)
+
+    def bwd():
+        fast.fast_edge_attention_bwd_indexed(g, H, dh, step.DT, d["Q"], K, ki, Uk, V, vi, Uv, step.scale,
+                                             SLOPE, lse, d["dO"], dQ, dKe, dVe)
+
+    def occ():
+        for x in bufs.values():
+            fast.fast_occurrence_csr(x["idx"], E, x["U"], x["off"], x["occ"], x["wso"], x["wo"])
+
+    def add():
+        for x, src in ((bufs["K"], dKe), (bufs["V"], dVe)):
+            fast.fast_index_add_rows(x["off"], x["occ"], E, x["U"], F, step.DT, src, x["dst"],
+                                     x["wsa"], x["wa"])
+    for f in (fwd, bwd, occ, add):
+        f()
+    t = {k: _events_ms(torch, f, reps) for k, f in (("fwd", fwd), ("bwd", bwd), ("occurrence_lists", occ),
+                                                   ("row_sums", add))}
+    # compulsory bytes: each compact row once; per-edge bytes: as the plain operator
+    fwd_rows = (2 * N) * F * esz + (Uk + Uv) * F * esz + 8 * E + 4 * N * H + 4 * (N + 1)
+    return {"attention_indexed_L1": {
+        "ms": {k: round(v, 4) for k, v in t.items()},
+        "compact_rows": {"K": Uk, "V": Uv, "edges": E},
+        "fwd_compulsory_bytes": fwd_rows,
+        "fwd_gbs_compulsory": round(fwd_rows / (t["fwd"] * 1e-3) / 1e9, 1),
+        "fwd_gbs_per_edge_rows": round(attn_fwd_bytes(N, E, F, esz, H) / (t["fwd"] * 1e-3) / 1e9, 1),
+        "note": "K and V read through indices into de-duplicated rows; backward writes per-edge "
+                "gradients, then occurrence lists and ordered row sums give the row gradients",
+    }}
 
 
 def sampler_ops(b, torch, fast, num_events=20_000_000, reps=5):

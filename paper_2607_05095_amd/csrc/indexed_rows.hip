@@ -12,11 +12,12 @@
 // get the key num_rows and sort behind every valid one.
 //
 // fast_index_add_rows: dst[u] = sum of src rows over the occurrences of u,
-// in occurrence order, accumulated in fp64 and rounded once to fp32.  A row read by many positions (a
-// hub id of a skewed batch) is cut into pieces of IA_PIECE occurrences:
-// every piece is summed by one group of lanes, and a row with several pieces
-// adds its piece sums in piece order.  The cut depends only on the counts,
-// so the result is the same on every run.
+// in occurrence order, accumulated in fp64 and rounded once to fp32.  A row
+// with at most IA_PIECE occurrences is summed by one group of lanes; a row
+// read by more positions (a hub id of a skewed batch) is cut into pieces of
+// about sqrt(count) occurrences, each summed by its own group, and the row
+// adds its piece sums in piece order.  The cut depends only on the counts, so the
+// result is the same on every run.
 #include "scan.h"
 
 namespace fast {
@@ -151,16 +152,22 @@ struct OutU32InPlace {
   __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { p[i] = prefix; }
 };
 
-// counts of the valid index values
-__global__ void __launch_bounds__(RS_THREADS) k_occ_count(const int32_t* __restrict__ index,
-                                                         int64_t n, int32_t num_rows,
-                                                         int32_t* count) {
-  for (int64_t i = int64_t(blockIdx.x) * RS_THREADS + threadIdx.x; i < n;
-       i += int64_t(gridDim.x) * RS_THREADS) {
-    const int32_t x = index[i];
-    if (x >= 0 && x < num_rows) atomicAdd(&count[x], 1);
+// occ_off[u] = number of sorted keys below u (a lower bound in the sorted
+// keys; positions outside the row range carry the key num_rows), u in
+// [0, num_rows].  No atomics: a hub row's count costs nothing extra.
+__global__ void __launch_bounds__(RS_THREADS) k_occ_offsets(const int32_t* __restrict__ keys,
+                                                           int64_t n, int64_t num_rows,
+                                                           int32_t* __restrict__ occ_off) {
+  const int64_t u = int64_t(blockIdx.x) * RS_THREADS + threadIdx.x;
+  if (u > num_rows) return;
+  int64_t lo = 0, hi = n;
+  while (lo < hi) {
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if (int64_t(keys[mid]) < u) lo = mid + 1; else hi = mid;
   }
+  occ_off[u] = int32_t(lo);
 }
+
 
 __global__ void __launch_bounds__(RS_THREADS) k_ir_fill(int32_t* p, int64_t n, int32_t v) {
   for (int64_t i = int64_t(blockIdx.x) * RS_THREADS + threadIdx.x; i < n;
@@ -168,18 +175,7 @@ __global__ void __launch_bounds__(RS_THREADS) k_ir_fill(int32_t* p, int64_t n, i
     p[i] = v;
 }
 
-struct InCount {
-  const int32_t* c;
-  __device__ uint32_t operator()(int64_t i) const { return uint32_t(c[i]); }
-};
-struct OutOff {
-  int32_t* off;
-  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { off[i] = int32_t(prefix); }
-};
-
 struct OccWs {
-  int32_t* count;
-  void* scan_c;
   int32_t* keys[2];
   int32_t* vals[2];
   uint32_t* hist;
@@ -194,8 +190,6 @@ static size_t occ_layout(int64_t n, int64_t num_rows, char* base, OccWs* ws) {
     return base ? base + o : nullptr;
   };
   const int64_t T = rs_tiles(n);
-  char* c = take(size_t(num_rows) * 4);
-  char* sc = take(scan_workspace(num_rows));
   char* k0 = take(size_t(n) * 4);
   char* k1 = take(size_t(n) * 4);
   char* v0 = take(size_t(n) * 4);
@@ -203,8 +197,6 @@ static size_t occ_layout(int64_t n, int64_t num_rows, char* base, OccWs* ws) {
   char* h = take(size_t(T) * RS_DIGITS * 4);
   char* sh = take(scan_workspace(T * RS_DIGITS));
   if (ws) {
-    ws->count = reinterpret_cast<int32_t*>(c);
-    ws->scan_c = sc;
     ws->keys[0] = reinterpret_cast<int32_t*>(k0);
     ws->keys[1] = reinterpret_cast<int32_t*>(k1);
     ws->vals[0] = reinterpret_cast<int32_t*>(v0);
@@ -224,105 +216,140 @@ static uint32_t grid_cap(int64_t n, int64_t per, uint32_t cap = 8192) {
 // ------------------------------------------------------------------ index add
 constexpr int IA_THREADS = 256;
 constexpr int IA_PIECE = 64;   // occurrences summed by one group
+constexpr int IA_UNROLL = 4;   // rows in flight per lane
 
-// Packed per-row item: high word = pieces of the row, low word = pieces of
-// the row if it has more than one (slots of piece sums), else 0.
-struct InPieces {
+// Piece length of a row with c > IA_PIECE occurrences: the smallest power of
+// two >= max(IA_PIECE, sqrt(c)), so the piece sums and the final sum of the
+// pieces take about the same time (a 240k-occurrence hub row: 469 pieces of
+// 512).  A function of c alone, so the cut is the same on every run.
+__device__ __forceinline__ int64_t ia_piece_len(int64_t c) {
+  int64_t p = IA_PIECE;
+  while (p * p < c) p <<= 1;
+  return p;
+}
+
+// Pieces of a row with more than IA_PIECE occurrences (0 for shorter rows,
+// which one group sums directly); at most 2 c / IA_PIECE.
+__device__ __forceinline__ int64_t ia_multi_pieces(int64_t c) {
+  if (c <= IA_PIECE) return 0;
+  const int64_t p = ia_piece_len(c);
+  return (c + p - 1) / p;
+}
+
+struct InMulti {
   const int32_t* occ_off;
   int64_t n;
-  __device__ uint64_t operator()(int64_t u) const {
-    const int64_t c = clamp64(int64_t(occ_off[u + 1]) - occ_off[u], 0, n);
-    const uint64_t np = c > 0 ? uint64_t((c + IA_PIECE - 1) / IA_PIECE) : 0;
-    return (np << 32) | (np > 1 ? np : 0);
+  __device__ uint32_t operator()(int64_t u) const {
+    return uint32_t(ia_multi_pieces(clamp64(int64_t(occ_off[u + 1]) - occ_off[u], 0, n)));
   }
 };
-struct OutPieces {
-  int32_t* piece_off;   // [num_rows + 1]
-  int32_t* multi_off;   // [num_rows + 1]
-  int64_t num_rows;
-  __device__ void operator()(int64_t u, uint64_t prefix, uint64_t v) const {
-    piece_off[u] = int32_t(prefix >> 32);
-    multi_off[u] = int32_t(prefix & 0xffffffffu);
-    if (u == num_rows - 1) {
-      piece_off[u + 1] = int32_t((prefix + v) >> 32);
-      multi_off[u + 1] = int32_t((prefix + v) & 0xffffffffu);
-    }
+struct OutMulti {
+  int32_t* multi_off;
+  __device__ void operator()(int64_t u, uint32_t prefix, uint32_t) const {
+    multi_off[u] = int32_t(prefix);
   }
 };
 
-// One group of `lanes` lanes per piece; lane l owns the VE-chunks l, l+lanes, ...
-// Sums are fp64 (a hub row adds hundreds of thousands of rows, whose fp32 sum
-// could lose the digits a cancelling total keeps); dst is rounded once.
+// acc += src rows occ[j0 .. j1) in order, chunk c of VE values; IA_UNROLL
+// row loads are issued before they are added (in the same order).
+template <typename T, int VE>
+__device__ __forceinline__ void ia_sum(const int32_t* __restrict__ occ, int64_t j0, int64_t j1,
+                                       int64_t n, int D, int c, const T* __restrict__ src,
+                                       double (&acc)[VE]) {
+  int64_t j = j0;
+  for (; j + IA_UNROLL <= j1; j += IA_UNROLL) {
+    float x[IA_UNROLL][VE];
+#pragma unroll
+    for (int r = 0; r < IA_UNROLL; ++r)
+      VecIO<T, VE>::load(src + clamp64(occ[j + r], 0, n - 1) * D + c * VE, x[r]);
+#pragma unroll
+    for (int r = 0; r < IA_UNROLL; ++r)
+#pragma unroll
+      for (int t = 0; t < VE; ++t) acc[t] += double(x[r][t]);
+  }
+  for (; j < j1; ++j) {
+    float x[VE];
+    VecIO<T, VE>::load(src + clamp64(occ[j], 0, n - 1) * D + c * VE, x);
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] += double(x[t]);
+  }
+}
+
+// Pieces of the long rows: one group of `lanes` lanes per piece q in
+// [0, multi_off[num_rows]); its sum goes to partial[q].
 template <typename T, int VE>
 __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
     const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
-    const int32_t* __restrict__ piece_off, const int32_t* __restrict__ multi_off,
-    int64_t num_rows, int64_t piece_bound, int64_t multi_bound, int64_t n, int lanes, int D,
-    const T* __restrict__ src, float* __restrict__ dst, double* __restrict__ partial) {
+    const int32_t* __restrict__ multi_off, int64_t num_rows, int64_t multi_bound, int64_t n,
+    int lanes, int D, const T* __restrict__ src, double* __restrict__ partial) {
   const int64_t q = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
   const int l = int(threadIdx.x) % lanes;
-  if (q >= piece_bound || q >= piece_off[num_rows]) return;
-  // row u with piece_off[u] <= q < piece_off[u + 1]
+  if (q >= multi_bound || q >= multi_off[num_rows]) return;
+  // the long row u with multi_off[u] <= q < multi_off[u + 1]
   int64_t lo = 0, hi = num_rows - 1;
   while (lo < hi) {
     const int64_t mid = (lo + hi + 1) >> 1;
-    if (piece_off[mid] <= q) lo = mid; else hi = mid - 1;
+    if (multi_off[mid] <= q) lo = mid; else hi = mid - 1;
   }
-  const int64_t u = lo;
-  const int64_t k = q - piece_off[u];                       // piece of row u
+  const int64_t u = lo, k = q - multi_off[u];
   // offsets and positions are clamped into range, so malformed occurrence
   // lists give wrong sums but never an out-of-bounds access
   const int64_t r0 = clamp64(occ_off[u], 0, n);
-  const int64_t j0 = clamp64(r0 + k * IA_PIECE, 0, n);
-  const int64_t j1 = clamp64(j0 + IA_PIECE < occ_off[u + 1] ? j0 + IA_PIECE : occ_off[u + 1], j0, n);
-  const int64_t npieces = int64_t(piece_off[u + 1]) - piece_off[u];
-  const int64_t slot = int64_t(multi_off[u]) + k;
-  if (npieces != 1 && slot >= multi_bound) return;
+  const int64_t r1 = clamp64(occ_off[u + 1], r0, n);
+  const int64_t len = ia_piece_len(r1 - r0);
+  const int64_t j0 = clamp64(r0 + k * len, r0, r1);
+  const int64_t j1 = j0 + len < r1 ? j0 + len : r1;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
-    for (int64_t j = j0; j < j1; ++j) {
-      float x[VE];
-      VecIO<T, VE>::load(src + clamp64(occ[j], 0, n - 1) * D + c * VE, x);
+    ia_sum<T, VE>(occ, j0, j1, n, D, c, src, acc);
 #pragma unroll
-      for (int t = 0; t < VE; ++t) acc[t] += double(x[t]);
-    }
-    if (npieces == 1) {
-      float o[VE];
-#pragma unroll
-      for (int t = 0; t < VE; ++t) o[t] = float(acc[t]);
-      VecIO<float, VE>::store(dst + u * D + c * VE, o);
-    } else {
-#pragma unroll
-      for (int t = 0; t < VE; ++t) partial[slot * D + c * VE + t] = acc[t];
-    }
+    for (int t = 0; t < VE; ++t) partial[q * D + c * VE + t] = acc[t];
   }
 }
 
-// One group per row: zeros for a row no position reads, the ordered sum of
-// its piece sums for a row of several pieces.
-template <int VE>
+// One group per row: a short row sums its occurrences directly (zeros for
+// none), a long row adds its piece sums in piece order.  fp64 sums, rounded
+// once to fp32.
+template <typename T, int VE>
 __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
-    const int32_t* __restrict__ piece_off, const int32_t* __restrict__ multi_off,
-    int64_t num_rows, int64_t multi_bound, int lanes, int D, const double* __restrict__ partial,
+    const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
+    const int32_t* __restrict__ multi_off, int64_t num_rows, int64_t multi_bound, int64_t n,
+    int lanes, int D, const T* __restrict__ src, const double* __restrict__ partial,
     float* __restrict__ dst) {
   const int64_t u = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
   const int l = int(threadIdx.x) % lanes;
   if (u >= num_rows) return;
-  const int64_t np = int64_t(piece_off[u + 1]) - piece_off[u];
-  if (np == 1) return;
+  const int64_t j0 = clamp64(occ_off[u], 0, n);
+  const int64_t j1 = clamp64(occ_off[u + 1], j0, n);
   const int64_t m0 = multi_off[u];
-  const int64_t m1 = m0 + np < multi_bound ? m0 + np : multi_bound;
+  const int64_t m1 = multi_off[u + 1] < multi_bound ? multi_off[u + 1] : multi_bound;
+  const bool longrow = ia_multi_pieces(j1 - j0) > 0;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
-    for (int64_t m = m0; m < m1 && np > 1; ++m) {
+    if (!longrow) {
+      ia_sum<T, VE>(occ, j0, j1, n, D, c, src, acc);
+    } else {
+      int64_t m = m0;
+      for (; m + IA_UNROLL <= m1; m += IA_UNROLL) {     // loads ahead, adds in order
+        double x[IA_UNROLL][VE];
 #pragma unroll
-      for (int t = 0; t < VE; ++t) acc[t] += partial[m * D + c * VE + t];
+        for (int r = 0; r < IA_UNROLL; ++r)
+#pragma unroll
+          for (int t = 0; t < VE; ++t) x[r][t] = partial[(m + r) * D + c * VE + t];
+#pragma unroll
+        for (int r = 0; r < IA_UNROLL; ++r)
+#pragma unroll
+          for (int t = 0; t < VE; ++t) acc[t] += x[r][t];
+      }
+      for (; m < m1; ++m)
+#pragma unroll
+        for (int t = 0; t < VE; ++t) acc[t] += partial[m * D + c * VE + t];
     }
     float o[VE];
 #pragma unroll
@@ -332,7 +359,6 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
 }
 
 struct IaWs {
-  int32_t* piece_off;
   int32_t* multi_off;
   void* scan;
   double* partial;
@@ -347,12 +373,10 @@ static size_t ia_layout(int64_t n, int64_t num_rows, int D, char* base, IaWs* ws
     off += align_up(bytes, 256);
     return base ? base + o : nullptr;
   };
-  char* po = take(size_t(num_rows + 1) * 4);
   char* mo = take(size_t(num_rows + 1) * 4);
-  char* sc = take(scan_workspace<uint64_t>(num_rows));
+  char* sc = take(scan_workspace(num_rows));
   char* pa = take(size_t(ia_multi_bound(n)) * size_t(D) * 8);
   if (ws) {
-    ws->piece_off = reinterpret_cast<int32_t*>(po);
     ws->multi_off = reinterpret_cast<int32_t*>(mo);
     ws->scan = sc;
     ws->partial = reinterpret_cast<double*>(pa);
@@ -392,27 +416,21 @@ extern "C" fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, in
   hipStream_t st = static_cast<hipStream_t>(stream);
   OccWs w;
   occ_layout(n, num_rows, static_cast<char*>(ws), &w);
-  // row offsets: counts of the valid index values, scanned
-  if (num_rows > 0) {
-    hipLaunchKernelGGL(k_ir_fill, dim3(grid_cap(num_rows, RS_THREADS * 4)), dim3(RS_THREADS), 0, st,
-                       w.count, num_rows, 0);
-    if (n > 0)
-      hipLaunchKernelGGL(k_occ_count, dim3(grid_cap(n, RS_THREADS * 8)), dim3(RS_THREADS), 0, st,
-                         index, n, int32_t(num_rows), w.count);
+  if (n == 0) {
+    hipLaunchKernelGGL(k_ir_fill, dim3(grid_cap(num_rows + 1, RS_THREADS * 4)), dim3(RS_THREADS), 0,
+                       st, occ_off, num_rows + 1, 0);
+    return check_launch(fn);
   }
-  hipError_t e = scan_launch(InCount{w.count}, OutOff{occ_off}, num_rows, w.scan_c, nullptr,
-                             occ_off + num_rows, st);
-  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-  if (n == 0) return check_launch(fn);
   // positions sorted stably by key, 8 bits per pass (keys <= num_rows)
   int bits = 1;
   while ((int64_t(1) << bits) <= num_rows) ++bits;
   const int passes = (bits + 7) / 8;
   const int64_t T = rs_tiles(n);
+  hipError_t e = hipSuccess;
   for (int p = 0; p < passes; ++p) {
     RsSrc src{p == 0 ? index : nullptr, w.keys[(p + 1) & 1], w.vals[(p + 1) & 1], int32_t(num_rows)};
     const bool last = p == passes - 1;
-    int32_t* kout = last ? nullptr : w.keys[p & 1];
+    int32_t* kout = w.keys[p & 1];
     int32_t* vout = last ? occ : w.vals[p & 1];
     hipLaunchKernelGGL(k_rs_hist, dim3(uint32_t(T)), dim3(RS_THREADS), 0, st, src, n, 8 * p, w.hist, T);
     e = scan_launch(InU32{w.hist}, OutU32InPlace{w.hist}, T * RS_DIGITS, w.scan_h, nullptr, nullptr, st);
@@ -420,6 +438,9 @@ extern "C" fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, in
     hipLaunchKernelGGL(k_rs_scatter, dim3(uint32_t(T)), dim3(RS_THREADS), 0, st, src, n, 8 * p,
                        w.hist, T, kout, vout);
   }
+  // row offsets from the sorted keys
+  hipLaunchKernelGGL(k_occ_offsets, dim3(uint32_t((num_rows + RS_THREADS) / RS_THREADS)),
+                     dim3(RS_THREADS), 0, st, w.keys[(passes - 1) & 1], n, num_rows, occ_off);
   return check_launch(fn);
 }
 
@@ -459,37 +480,28 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
   hipStream_t st = static_cast<hipStream_t>(stream);
   IaWs w;
   ia_layout(n, num_rows, D, static_cast<char*>(ws), &w);
-  hipError_t e = scan_launch<InPieces, OutPieces, uint64_t>(
-      InPieces{occ_off, n}, OutPieces{w.piece_off, w.multi_off, num_rows}, num_rows, w.scan, nullptr,
-      nullptr, st);
+  hipError_t e = scan_launch(InMulti{occ_off, n}, OutMulti{w.multi_off}, num_rows, w.scan, nullptr,
+                             w.multi_off + num_rows, st);
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   const int lanes = pow2_at_least(D / VE, 64);
-  // pieces: at most n / IA_PIECE + (rows read at all) <= n / IA_PIECE + min(n, num_rows) + 1
-  const int64_t piece_bound = n / IA_PIECE + (n < num_rows ? n : num_rows) + 1;
   const int64_t groups_per_block = IA_THREADS / lanes;
-  if (n > 0) {
-    const int64_t nb = (piece_bound + groups_per_block - 1) / groups_per_block;
-#define FAST_IA(T_, VE_)                                                                          \
-  hipLaunchKernelGGL((k_ia_pieces<T_, VE_>), dim3(uint32_t(nb)), dim3(IA_THREADS), 0, st, occ_off, \
-                     occ, w.piece_off, w.multi_off, num_rows, piece_bound, ia_multi_bound(n), n,   \
-                     lanes, D,                                                                      \
-                     static_cast<const T_*>(src), dst, w.partial)
-    if (src_dtype == FAST_F32) {
-      if (VE == 4) FAST_IA(float, 4); else if (VE == 2) FAST_IA(float, 2); else FAST_IA(float, 1);
-    } else {
-      if (VE == 4) FAST_IA(uint16_t, 4); else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
-    }
-#undef FAST_IA
+  const int64_t mb = ia_multi_bound(n);
+  const int64_t np_blocks = (mb + groups_per_block - 1) / groups_per_block;
+  const int64_t nr_blocks = (num_rows + groups_per_block - 1) / groups_per_block;
+#define FAST_IA(T_, VE_)                                                                           \
+  do {                                                                                             \
+    const T_* s_ = static_cast<const T_*>(src);                                                    \
+    if (n > 0)                                                                                     \
+      hipLaunchKernelGGL((k_ia_pieces<T_, VE_>), dim3(uint32_t(np_blocks)), dim3(IA_THREADS), 0,   \
+                         st, occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, s_, w.partial);  \
+    hipLaunchKernelGGL((k_ia_rows<T_, VE_>), dim3(uint32_t(nr_blocks)), dim3(IA_THREADS), 0, st,    \
+                       occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, s_, w.partial, dst);   \
+  } while (0)
+  if (src_dtype == FAST_F32) {
+    if (VE == 4) FAST_IA(float, 4); else if (VE == 2) FAST_IA(float, 2); else FAST_IA(float, 1);
+  } else {
+    if (VE == 4) FAST_IA(uint16_t, 4); else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
   }
-  const int64_t nr = (num_rows + groups_per_block - 1) / groups_per_block;
-  if (VE == 4)
-    hipLaunchKernelGGL(k_ia_rows<4>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
-                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
-  else if (VE == 2)
-    hipLaunchKernelGGL(k_ia_rows<2>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
-                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
-  else
-    hipLaunchKernelGGL(k_ia_rows<1>, dim3(uint32_t(nr)), dim3(IA_THREADS), 0, st, w.piece_off,
-                       w.multi_off, num_rows, ia_multi_bound(n), lanes, D, w.partial, dst);
+#undef FAST_IA
   return check_launch(fn);
 }
