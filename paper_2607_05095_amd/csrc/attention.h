@@ -82,6 +82,7 @@ struct AttnLayout {
   int SPB;        // segments per workgroup
   int block;      // workgroup size
   bool nt;        // streamed rows cover whole cache lines: non-temporal policy
+  bool rm;        // row-major lanes (attention_rowmajor.h): lane c owns elements 4c..4c+3
 };
 
 struct AttnArgs {

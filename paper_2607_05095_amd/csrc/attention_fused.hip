@@ -5,6 +5,7 @@
 #include <type_traits>
 
 #include "attention.h"
+#include "attention_rowmajor.h"
 
 namespace fast {
 
@@ -21,6 +22,14 @@ static int lanes_override() {
     const char* e = std::getenv("FAST_ATTN_LANES_PER_HEAD");
     const int x = e ? std::atoi(e) : 0;
     return (x > 0 && x <= 64 && (x & (x - 1)) == 0) ? x : 0;
+  }();
+  return v;
+}
+
+static bool rowmajor_enabled() {
+  static const bool v = [] {
+    const char* e = std::getenv("FAST_ATTN_ROWMAJOR");
+    return !(e && e[0] == '0');
   }();
   return v;
 }
@@ -115,11 +124,36 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
   const int wg = (op == Op::kAttnBwd || op == Op::kAttnBwdIdx) ? ATT_BLOCK_BWD : ATT_BLOCK;
   fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, wg, a.L);
   if (s != FAST_OK) return s;
+  // fp32 rows whose heads break the 16-byte alignment (dh % 4 != 0) but whose
+  // width does not (F % 4 == 0): the fused operators use row-major lanes so
+  // every row moves as 16-byte accesses (FAST_ATTN_ROWMAJOR=0 turns it off).
+  const bool fused_op = op == Op::kAttnFwd || op == Op::kAttnBwd || op == Op::kAttnFwdIdx ||
+                        op == Op::kAttnBwdIdx;
+  a.L.rm = false;
+  if (fused_op && rowmajor_enabled() && dt == FAST_F32 && H == 2 && dh % 4 != 0 &&
+      (H * dh) % 4 == 0 && (H * dh) / 4 <= 64) {
+    bool al = true;
+    for (int k = 0; k < nrows; ++k)
+      if (rows[k] && !aligned(rows[k], 16)) al = false;
+    if (al) {
+      a.L.rm = true;
+      a.L.VE = 4;
+      a.L.P = 1;
+      a.L.CPH = 0;
+      a.L.LPH = 0;
+      a.L.G = next_pow2((H * dh) / 4 < 16 ? 16 : (H * dh) / 4);
+      a.L.block = wg;
+      a.L.SPB = wg / a.L.G;
+    }
+  }
   // Non-temporal streaming only when every per-edge row starts and ends on a
   // cache line, so no two rows share a line.
   a.L.nt = (size_t(a.L.F) * elem_size(dt)) % CACHE_LINE == 0;
   for (const void* p : {a.K, a.V, static_cast<const void*>(a.dK), static_cast<const void*>(a.dV)})
     if (p && !aligned(p, CACHE_LINE)) a.L.nt = false;
+#ifdef FAST_ATTN_FORCE_NT
+  a.L.nt = true;   // tuning build: streaming policy whatever the row alignment
+#endif
   if (g->num_dst == 0) return ok();
   if (!g->dst_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: dst_offsets is NULL", fn);
   a.N = g->num_dst;
@@ -152,6 +186,7 @@ static void launch_fused(Op op, const AttnArgs& a, dim3 grid, dim3 block, hipStr
 
 bool attn_launch_fused(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
                        hipStream_t st) {
+  if (a.L.rm) return attn_launch_rm<false>(op, a, grid, block, st);
   const bool bf = dt == FAST_BF16;
   const int VE = a.L.VE, P = a.L.P, LPH = a.L.LPH;
 #define FAST_TRY(T_, VE_, P_, L_)                                                     \

@@ -8,11 +8,13 @@
 #include <type_traits>
 
 #include "attention.h"
+#include "attention_rowmajor.h"
 
 namespace fast {
 
 bool attn_launch_indexed(Op op, fast_dtype_t dt, const AttnArgs& a, dim3 grid, dim3 block,
                          hipStream_t st) {
+  if (a.L.rm) return attn_launch_rm<true>(op, a, grid, block, st);
   const bool bf = dt == FAST_BF16;
   const int VE = a.L.VE, P = a.L.P, LPH = a.L.LPH;
 #define FAST_TRY(T_, VE_, P_, L_)                                                          \
