@@ -309,14 +309,15 @@ def make_temporal_graph(num_nodes: int, num_events: int, seed: int = 0, zipf_s: 
     src = _draw_ids(law, num_events, r, amap)
     dst = _draw_ids(law, num_events, r, amap)
     t = np.sort(r.random(num_events) * T_MAX).astype(np.float32)
-    node = np.concatenate([src, dst])
-    nbr = np.concatenate([dst, src])
-    ts = np.concatenate([t, t])
-    eid = np.concatenate([np.arange(num_events), np.arange(num_events)]).astype(np.int64)
-    # order by node, then time, then event id: a stable sort by time first
-    # (the stream is already in time order), then a stable sort by node
-    by_t = np.argsort(ts, kind="stable")
-    order = by_t[np.argsort(node[by_t], kind="stable")]
+    # each event's two entries side by side in stream order, which is (time,
+    # event id) order already; one stable sort by node keeps it within a node
+    node = np.empty(2 * num_events, np.int64)
+    nbr = np.empty(2 * num_events, np.int64)
+    node[0::2], node[1::2] = src, dst
+    nbr[0::2], nbr[1::2] = dst, src
+    ts = np.repeat(t, 2)
+    eid = np.repeat(np.arange(num_events, dtype=np.int64), 2)
+    order = np.argsort(node, kind="stable")
     indptr = np.concatenate([[0], np.cumsum(np.bincount(node, minlength=num_nodes))]).astype(np.int64)
     return TemporalGraph(indptr, nbr[order].astype(np.int64), ts[order].astype(np.float32),
                          eid[order], src, dst, t)
