@@ -232,13 +232,28 @@ def attn_fwd_bytes(N, E, F, esz, H):
     return (2 * E + 2 * N) * F * esz + 4 * N * H + 4 * (N + 1)
 
 
+def _oracle_time(fn, min_seconds=0.5, max_runs=5):
+    """Mean wall time (s) of fn() on the host over up to max_runs calls."""
+    times = []
+    while len(times) < max_runs and sum(times) < min_seconds:
+        t0 = time.perf_counter()
+        fn()
+        times.append(time.perf_counter() - t0)
+    return float(np.mean(times))
+
+
+def _oracle_entry(seconds, units, unit, sample):
+    return {"ms": round(seconds * 1e3, 3), "rate": round(units / seconds, 1), "unit": unit,
+            "sample": sample, "cores": 1, "kind": "oracle"}
+
+
 def time_encode_bwd_bytes(N, E, d_t, esz):
     """Read dte [E, d_t], edge times, destination times and offsets, omega and
     phi; write domega and dphi."""
     return E * (4 + d_t * esz) + 8 * N + 4 + 16 * d_t
 
 
-def widened_ops(b, step, torch, fast, reps=10):
+def widened_ops(b, step, torch, fast, reps=10, with_oracle=False):
     """Operators beyond the timed step, each timed alone with HIP events on
     its launch stream (mean of `reps` launches after one warm-up): the
     time-encoding backward of each layer block, on a seeded upstream
@@ -273,15 +288,29 @@ def widened_ops(b, step, torch, fast, reps=10):
             "ms": round(ms, 4), "algorithmic_bytes": nbytes, "bound": "alu (fp64 sine per element)",
             "achieved_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "edges_per_s": round(E / (ms * 1e-3), 1),
         }
+        if with_oracle and i == 0:
+            import oracle
+            from synth import omega_phi
+            blk = b.blocks[0]
+            ns = max(1, blk.num_dst // 10)
+            off = oracle.csr_offsets(blk.counts[:ns])
+            es = int(off[-1])
+            g64 = dte[:es].double().cpu().numpy()
+            om, ph = omega_phi(b.d_t)
+            sec = _oracle_time(lambda: oracle.time_encode_bwd(off, blk.dst_t[:ns], blk.edge_t[:es],
+                                                              om, ph, g64))
+            res["time_encode_bwd_L1"]["oracle"] = _oracle_entry(
+                sec, es, "edges/s", f"first 10% of the layer-1 segments ({es} edges)")
         del dte, ws
-    res.update(hot_set_ops(b, torch, fast))
-    res.update(sampler_ops(b, torch, fast))
-    res.update(indexed_ops(b, step, torch, fast))
+    res.update(hot_set_ops(b, torch, fast, with_oracle=with_oracle))
+    res.update(sampler_ops(b, torch, fast, with_oracle=with_oracle))
+    res.update(indexed_ops(b, step, torch, fast, with_oracle=with_oracle))
     return res
 
 
-def indexed_ops(b, step, torch, fast, reps=5):
+def indexed_ops(b, step, torch, fast, reps=5, with_oracle=False):
     """The layer-1 fused attention with indexed operands: K read through the
     de-duplication inverse of the block's source node ids, V through that of
     its edge ids (compact rows), then the row gradients of both (occurrence
@@ -336,7 +365,23 @@ def indexed_ops(b, step, torch, fast, reps=5):
                                                    ("row_sums", add))}
     # compulsory bytes: each compact row once; per-edge bytes: as the plain operator
     fwd_rows = (2 * N) * F * esz + (Uk + Uv) * F * esz + 8 * E + 4 * N * H + 4 * (N + 1)
-    return {"attention_indexed_L1": {
+    orc = None
+    if with_oracle:
+        import oracle
+        ns = max(1, N // 50)
+        off = oracle.csr_offsets(blk.counts[:ns])
+        es = int(off[-1])
+        Qh, dOh = d["Q"][:ns].cpu(), d["dO"][:ns].cpu()
+        Kh, Vh = K.cpu(), V.cpu()
+        kh, vh = kidx[:es].astype(np.int32), vidx[:es].astype(np.int32)
+
+        def run():
+            oracle.edge_attention_fwd_indexed(off, Qh, Kh, kh, Vh, vh, step.scale, SLOPE)
+            oracle.edge_attention_bwd_indexed(off, Qh, Kh, kh, Vh, vh, dOh, step.scale, SLOPE)
+        sec = _oracle_time(run)
+        orc = _oracle_entry(sec, es, "edges/s",
+                            f"first 2% of the layer-1 segments ({es} edges): forward, backward and row sums")
+    out_entry = {
         "ms": {k: round(v, 4) for k, v in t.items()},
         "compact_rows": {"K": Uk, "V": Uv, "edges": E},
         "fwd_compulsory_bytes": fwd_rows,
@@ -344,10 +389,14 @@ def indexed_ops(b, step, torch, fast, reps=5):
         "fwd_gbs_per_edge_rows": round(attn_fwd_bytes(N, E, F, esz, H) / (t["fwd"] * 1e-3) / 1e9, 1),
         "note": "K and V read through indices into de-duplicated rows; backward writes per-edge "
                 "gradients, then occurrence lists and ordered row sums give the row gradients",
-    }}
+        "edges_per_s": round(E / (sum(t.values()) * 1e-3), 1),
+    }
+    if orc is not None:
+        out_entry["oracle"] = orc
+    return {"attention_indexed_L1": out_entry}
 
 
-def sampler_ops(b, torch, fast, num_events=20_000_000, reps=5):
+def sampler_ops(b, torch, fast, num_events=20_000_000, reps=5, with_oracle=False):
     """Two hops of most-recent-k sampling for one batch of this workload's
     shape (roots / 3 events, fan-out k) on an event-stream temporal graph
     over the workload's node universe (each event stored under both ends)."""
@@ -378,6 +427,15 @@ def sampler_ops(b, torch, fast, num_events=20_000_000, reps=5):
             "sampled_edges_per_s": round(E / (ms * 1e-3), 1),
         }
         q_roots, q_t = src[:E].clone(), et[:E].clone()
+        if with_oracle and hop == 1:
+            import oracle
+            nr = max(1, roots.size // 10)
+            holder = {}
+            sec = _oracle_time(lambda: holder.update(
+                r=oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots[:nr], rt[:nr], k)))
+            ne = int(holder["r"][0][-1])
+            res["sample_recent_hop1"]["oracle"] = _oracle_entry(
+                sec, ne, "sampled edges/s", f"first 10% of the hop-1 roots ({nr} roots, {ne} edges)")
     return res
 
 
@@ -393,7 +451,7 @@ def _events_ms(torch, fn, reps):
     return s.elapsed_time(e) / reps
 
 
-def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3):
+def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3, with_oracle=False):
     """SlimCache's pre-training cache selection (Alg. 1) over `num_batches`
     pre-sampled batches of this workload's graph: access counting of node and
     edge ids, then the greedy selection of alpha * (|V| + |E|) ids with both
@@ -422,6 +480,11 @@ def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3):
             "bound": "random 4-byte atomics (one exchange per id, one add per distinct id)",
             "ids_per_s": round(n / (ms * 1e-3), 1),
         }
+        if with_oracle:
+            import oracle
+            sec = _oracle_time(lambda: oracle.access_count(batches[:1], bound))
+            res[f"access_count_{kind}"]["oracle"] = _oracle_entry(
+                sec, batches[0].size, "ids/s", f"one pre-sampled batch ({batches[0].size} ids)")
         del ids, ws
     fv, fe = freqs
     B = fast.hot_set_budget(alpha, nb, eb)
@@ -444,7 +507,15 @@ def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3):
         "algorithmic_bytes": nbytes, "bound": "hbm",
         "achieved_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
         "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "ids_per_s": round((nb + eb) / (ms * 1e-3), 1),
     }
+    if with_oracle:
+        import oracle
+        sv_n, se_n = max(1, nb // 100), max(1, eb // 100)
+        fv_h, fe_h = fv[:sv_n].cpu().numpy(), fe[:se_n].cpu().numpy()
+        sec = _oracle_time(lambda: oracle.greedy_hot_set(fv_h, fe_h, alpha))
+        res["greedy_hot_set"]["oracle"] = _oracle_entry(
+            sec, sv_n + se_n, "ids/s", f"first 1% of each universe ({sv_n} nodes, {se_n} edges)")
     return res
 
 
@@ -601,7 +672,7 @@ def main():
     torch.cuda.synchronize()
     breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec_all.items()}
 
-    widened = widened_ops(b, step, torch, fast)
+    widened = widened_ops(b, step, torch, fast, with_oracle=not args.no_cpu_baseline)
     log(f"widened ops: {widened}")
 
     esz = 4 if b.dtype == "f32" else 2
@@ -638,7 +709,8 @@ def main():
 
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
         "widened_ops": widened,
-        "widened_note": "operators beyond the timed step, timed alone outside the timed region",
+        "widened_note": "operators beyond the timed step, timed alone outside the timed region; "
+                        "with the CPU baseline, each also gives the oracle's rate on a bounded sample",
         "breakdown_note": "operators timed one by one in 3 extra serial steps outside the timed region",
         "kernel_source_sha": kernel_source_hash(),
     }
