@@ -114,10 +114,17 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* tsum, int64_t nt,
   }
 }
 
+// Down-sweep: the tile's items are loaded striped (coalesced) into LDS, each
+// thread scans SCAN_ITEMS consecutive items, and the exclusive prefixes
+// replace the items in LDS (plus the running total after the last item), so
+// that `out` is called in striped order too -- neighbouring lanes write
+// neighbouring outputs (offsets, ranks, slot maps) -- with each item's value
+// recovered as the difference of consecutive prefixes.
 template <class In, class Out, typename T = uint32_t>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
                                                             const T* tsum, Out out) {
-  __shared__ T tile[SCAN_TILE + SCAN_TILE / 32];
+  constexpr int PAD_END = SCAN_TILE + SCAN_TILE / 32;
+  __shared__ T tile[PAD_END + 1];
   __shared__ T lds4[4];
   const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
   // striped, coalesced load into LDS (padded every 32 words against bank conflicts)
@@ -136,12 +143,25 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
     s += v[k];
   }
   T total;
+  // (the block scan's barriers also order every read of tile above before
+  // the writes below)
   T run = block_exclusive_scan(s, lds4, total) + tsum[blockIdx.x];
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
-    const int64_t i = base + threadIdx.x * SCAN_ITEMS + k;
-    if (i < n) out(i, run, v[k]);
+    const int j = threadIdx.x * SCAN_ITEMS + k;
+    tile[j + (j >> 5)] = run;
     run += v[k];
+  }
+  if (threadIdx.x == SCAN_THREADS - 1) tile[PAD_END] = run;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int j = k * SCAN_THREADS + threadIdx.x;
+    const int64_t i = base + j;
+    const int j1 = j + 1;
+    const T p0 = tile[j + (j >> 5)];
+    const T p1 = j1 < SCAN_TILE ? tile[j1 + (j1 >> 5)] : tile[PAD_END];
+    if (i < n) out(i, p0, T(p1 - p0));
   }
 }
 
