@@ -37,8 +37,8 @@ SLOPE = 0.2
 WORKLOADS = {"bigdedup": 4, "large": 3}
 METRIC = "sampled edges/sec, fused edge-softmax+aggregation fwd+bwd; % HBM roofline"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_bwd_{workload}.json")
-KERNEL_SOURCES = ["paper_2607_05095_amd/csrc/attention.h", "paper_2607_05095_amd/csrc/attention_fused.hip",
-                  "paper_2607_05095_amd/csrc/common.h"]
+KERNEL_SOURCES = ["paper_2607_05095_amd/csrc/attention.h", "paper_2607_05095_amd/csrc/attention_rowmajor.h",
+                  "paper_2607_05095_amd/csrc/attention_fused.hip", "paper_2607_05095_amd/csrc/common.h"]
 
 
 def log(msg):
