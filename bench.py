@@ -581,18 +581,24 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     }
 
 
-def read_traffic(workload):
-    """HBM traffic of the dominant kernel on this workload, from the committed
-    rocprofv3 counter summary, or None when there is none for this workload or
-    the kernel source changed since the counters were taken."""
+def read_counters(workload):
+    """rocprofv3 counter record of the dominant kernel on this workload (HBM
+    bytes per launch, L2 hit rate, occupancy), from the committed summary, or
+    an empty dict when there is none for this workload or the kernel source
+    changed since the counters were taken."""
     try:
         with open(TRAFFIC_FILE.format(workload=workload)) as f:
             t = json.load(f)
     except (OSError, ValueError):
-        return None
+        return {}
     if t.get("kernel_source_sha") != kernel_source_hash() or t.get("workload") != workload:
-        return None
-    return t.get("bytes_per_launch")
+        return {}
+    return t
+
+
+def read_traffic(workload):
+    """HBM bytes per launch of the dominant kernel, or None (see read_counters)."""
+    return read_counters(workload).get("bytes_per_launch")
 
 
 def main():
@@ -688,6 +694,8 @@ def main():
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(args.workload),
         "algorithmic_bytes_per_launch": bwd_bytes, "avg_launch_ms": round(bwd_ms, 4),
+        "l2_hit_rate": read_counters(args.workload).get("l2_hit_rate"),
+        "occupancy_pct": read_counters(args.workload).get("occupancy_pct"),
     }
     result = {
         "metric": METRIC,

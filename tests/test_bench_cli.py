@@ -24,3 +24,19 @@ def test_byte_models_match_the_design_figures():
     fb = sum(bench.attn_fwd_bytes(n, e, 100, 4, 2) + bench.attn_bwd_bytes(n, e, 100, 4, 2)
              for n, e in ((264_000, 2_640_000), (24_000, 240_000)))
     assert abs(fb - 7_488_000_000) / 7_488_000_000 < 0.001
+
+
+def test_counter_records_are_whole_and_checked_against_the_source(tmp_path, monkeypatch):
+    sys.path.insert(0, ROOT)
+    import bench
+    for w in ("bigdedup", "large"):
+        with open(bench.TRAFFIC_FILE.format(workload=w)) as f:
+            rec = json.load(f)
+        assert rec["workload"] == w
+        assert 0 < rec["l2_hit_rate"] < 1 and 0 < rec["occupancy_pct"] <= 100
+        assert rec["bytes_per_launch"] > 0 and os.path.exists(os.path.join(ROOT, rec["source"]))
+        # a record taken on other kernel sources is not reported
+        stale = dict(rec, kernel_source_sha="0" * 16)
+        (tmp_path / f"t_{w}.json").write_text(json.dumps(stale))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "t_{workload}.json"))
+    assert bench.read_counters("bigdedup") == {} and bench.read_traffic("large") is None
