@@ -524,6 +524,47 @@ def greedy_hot_set_bytes(nv, ne, B):
     return 4 * (nv + ne) + 4 * (nv + ne) + 8 * B
 
 
+def time_encode_summary(b, breakdown):
+    """Time encoding of both layer blocks in the serial step: algorithmic bytes
+    E (4 + d_t b) + 8 N per block against the measured times."""
+    b_out = 4 if b.dtype == "f32" else 2
+    ms = sum(breakdown.get(f"time_encode_L{i + 1}", 0.0) for i in range(len(b.blocks)))
+    nbytes = sum(x.num_edges * (4 + b.d_t * b_out) + 8 * x.num_dst for x in b.blocks)
+    return {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
+            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ms > 0 else None,
+            "cosines_per_s": sum(x.num_edges for x in b.blocks) * b.d_t / (ms * 1e-3) if ms > 0 else None}
+
+
+def host_cpu_model():
+    """Model name of the host CPU (first entry of /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def attention_sequence_ms(step, torch, reps=50, warm=5):
+    """Median over `reps` runs of the fused attention of one step as a unit:
+    HIP events on the launch stream around the four launches (layer-1 and
+    layer-2 forward, layer-2 and layer-1 backward), after `warm` warm-ups."""
+    st = torch.cuda.current_stream()
+    for _ in range(warm):
+        step.attn(0)
+    times = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(st)
+        step.attn(0)
+        e.record(st)
+        e.synchronize()
+        times.append(s.elapsed_time(e))
+    return float(np.median(times))
+
+
 def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     """The fp64 oracle, single-threaded, on a bounded sample of the same batch:
     the first `frac` of the segments of each layer block and the matching
@@ -573,6 +614,7 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     dt = float(np.mean(times))
     return {
         "value": sample_edges / dt, "unit": "sampled edges/s", "cores": 1, "kind": "oracle",
+        "host_threads": os.cpu_count(), "cpu_model": host_cpu_model(),
         "sample": f"{frac:.0%} of the segments of each layer block ({sample_edges} sampled edges) "
                   f"and of the node/edge ids, through offsets, dedup+gather, time encoding and "
                   f"fused attention fwd+bwd in fp64, single-threaded; mean of {len(times)} "
@@ -686,9 +728,10 @@ def main():
     L1 = b.blocks[0]
     bwd_bytes = attn_bwd_bytes(L1.num_dst, L1.num_edges, F, esz, b.H)
     achieved = bwd_bytes / (bwd_ms * 1e-3) / 1e9
-    fused_ms = sum(v for k, v in breakdown.items() if k.startswith("attn_"))   # serial pass
+    fused_ms = attention_sequence_ms(step, torch)
     fused_bytes = sum(attn_fwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) +
                       attn_bwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) for x in b.blocks)
+    fused_bytes_no_lse = sum((6 * x.num_edges + 5 * x.num_dst) * F * esz for x in b.blocks)
     roofline = {
         "kernel": "k_attn_bwd (fused ESM+AGG backward, layer-1 block)",
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -709,9 +752,14 @@ def main():
         "roofline": roofline,
         "fused_attention": {
             "edges_per_s": b.sampled_edges / (fused_ms * 1e-3), "ms": round(fused_ms, 4),
+            "timing": "HIP events around the four launches (L1 fwd, L2 fwd, L2 bwd, L1 bwd), "
+                      "5 warm-ups, median of 50",
             "algorithmic_bytes": fused_bytes,
             "hbm_frac": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_without_lse": fused_bytes_no_lse,
+            "hbm_frac_without_lse": round(fused_bytes_no_lse / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
+        "time_encode": time_encode_summary(b, breakdown),
         "schedule": "serial: prep (offsets, dedup+gather, time encoding) then attention of each "
                     "batch on one stream",
 
@@ -732,6 +780,7 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(b, step, torch, args.cpu_frac)
+        result["cpu_baseline"]["gpu_over_cpu"] = round(result["value"] / result["cpu_baseline"]["value"], 1)
     print(json.dumps(result), flush=True)
 
 

@@ -405,6 +405,33 @@ def test_dedup_edge_cases(case):
         assert nm == u and np.array_equal(miss[:nm].cpu().numpy(), np.arange(u))
 
 
+@pytest.mark.parametrize("D,dt", [(4, "bf16"), (12, "bf16"), (44, "bf16"), (172, "bf16"), (252, "bf16"),
+                                  (260, "bf16"), (508, "bf16"), (6, "f32"), (86, "f32"), (126, "f32")])
+def test_gather_rows_of_odd_eight_byte_width(D, dt):
+    """Rows of 16h + 8 bytes (every other row off the 16-byte grid) are
+    copied bit-exactly, directly and through a slot map whose slots mix both
+    parities and misses; D = 4 bf16 (8-byte rows) is the narrow case."""
+    _announce(f"gather rows D={D} {dt}")
+    r = np.random.default_rng(D)
+    bound, n = 20_000, 30_000
+    ids = r.integers(0, bound, n).astype(np.int64)
+    table = make_table(bound, D, dt, device="cuda", seed=D, stream=5)
+    uni, inv, u, rows, miss, nm = _dedup(ids, bound, table)
+    ref_uni, ref_inv = oracle.dedup(ids)
+    assert np.array_equal(uni, ref_uni) and np.array_equal(inv, ref_inv) and nm == 0
+    ref_rows, _, _ = oracle.gather(ref_uni, _bits(table))
+    assert np.array_equal(_bits(rows), ref_rows)
+    cache_rows = 5_001
+    sm_np = r.integers(0, cache_rows, bound).astype(np.int32)
+    sm_np[r.random(bound) < 0.3] = -1
+    cache = make_table(cache_rows, D, dt, device="cuda", seed=D + 1, stream=6)
+    uni, inv, u, rows, miss, nm = _dedup(ids, bound, cache, slot_map=to_dev(sm_np))
+    ref_rows, hit, ref_miss = oracle.gather(ref_uni, _bits(cache), sm_np)
+    assert nm == ref_miss.size and np.array_equal(miss[:nm].cpu().numpy(), ref_miss)
+    assert np.array_equal(_bits(rows)[hit], ref_rows[hit])
+    assert np.all(_bits(rows)[~hit] == 0), "a miss row must be left untouched"
+
+
 # ------------------------------------------------------------------ time encoding (a4)
 def _te_gpu(blk_off, dst_t, edge_t, omega, phi, dt="f32"):
     E = edge_t.shape[0]
