@@ -170,7 +170,7 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
  * edge_ids int64, edge_t fp32, capacity R * k each.  Offsets that are out of
  * range are clamped, so a malformed graph never causes an out-of-bounds
  * read; entries that are not time-sorted give unspecified neighbours.
- * Limits: 0 <= k, R * k < 2^31.
+ * Limits: 0 <= k, R < 2^31, R * k < 2^31.
  * Workspace: fast_sample_recent_workspace(R) bytes, 256-byte aligned.
  * ------------------------------------------------------------------------ */
 size_t fast_sample_recent_workspace(int64_t num_roots);

@@ -113,6 +113,8 @@ extern "C" fast_status_t fast_sample_recent(const fast_temporal_graph_t* g, cons
   if (!g) return fail(FAST_ERR_INVALID_ARG, "%s: graph is NULL", fn);
   if (g->num_nodes < 0 || g->num_entries < 0 || num_roots < 0 || k < 0)
     return fail(FAST_ERR_INVALID_ARG, "%s: negative size or k", fn);
+  if (num_roots >= (int64_t(1) << 31))   // also with k = 0: the workspace is sized per root
+    return fail(FAST_ERR_UNSUPPORTED, "%s: num_roots >= 2^31", fn);
   if (num_roots * int64_t(k) >= (int64_t(1) << 31))
     return fail(FAST_ERR_UNSUPPORTED, "%s: num_roots * k >= 2^31", fn);
   if (!dst_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: dst_offsets is NULL", fn);

@@ -259,6 +259,8 @@ def test_sample_recent_validation():
     assert call(k=-1) == INVALID
     assert call(R=-1) == INVALID
     assert call(R=1 << 28, k=16) == UNSUPPORTED
+    # k = 0 keeps the product small, but the per-root workspace would not fit
+    assert call(R=1 << 31, k=0, wsb=1 << 20) == UNSUPPORTED
     assert call(off=None) == INVALID
     assert call(roots=None) == INVALID
     assert call(src=None) == INVALID
