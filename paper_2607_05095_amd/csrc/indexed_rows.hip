@@ -324,8 +324,9 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
   if (u >= num_rows) return;
   const int64_t j0 = clamp64(occ_off[u], 0, n);
   const int64_t j1 = clamp64(occ_off[u + 1], j0, n);
-  const int64_t m0 = multi_off[u];
-  const int64_t m1 = multi_off[u + 1] < multi_bound ? multi_off[u + 1] : multi_bound;
+  // piece range clamped too: the piece counts of malformed lists may wrap
+  const int64_t m0 = clamp64(multi_off[u], 0, multi_bound);
+  const int64_t m1 = clamp64(multi_off[u + 1], m0, multi_bound);
   const bool longrow = ia_multi_pieces(j1 - j0) > 0;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {

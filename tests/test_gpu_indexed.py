@@ -190,3 +190,19 @@ def test_identity_index_equals_plain_operator():
         outs.append((out, lse, dQ, dK, dV))
     for a, c in zip(*outs):
         assert torch.equal(a, c)
+
+
+def test_index_add_rows_malformed_lists_stay_in_bounds():
+    """Occurrence offsets that decrease or leave [0, n] and positions outside
+    [0, n) give unspecified sums, but every access stays in range: the call
+    succeeds, the sums of the (finite) source rows are finite, and a second
+    call gives bitwise the same rows."""
+    _announce("index add with malformed occurrence lists")
+    r = np.random.default_rng(11)
+    n, rows, D = 10_000, 500, 8
+    off = torch.as_tensor(r.integers(-5, n + 6, rows + 1).astype(np.int32), device="cuda")
+    occ = torch.as_tensor(r.integers(-3, n + 4, n).astype(np.int32), device="cuda")
+    src = _randn((n, D), "f32", "cuda", 12)
+    got = _index_add_gpu(off, occ, n, rows, src)
+    assert torch.isfinite(got).all()
+    assert torch.equal(got, _index_add_gpu(off, occ, n, rows, src))
