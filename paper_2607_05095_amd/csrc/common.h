@@ -36,15 +36,18 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t nb) {
 // ------------------------------------------------------------------ bf16
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
-}
+// fp32 -> bf16 with round-to-nearest-even, two values packed (lo in the low
+// half): one v_cvt_pk_bf16_f32 on gfx950.  Its result equals the rounding
+// written out -- add 0x7fff plus the lowest kept bit and keep the high half,
+// a NaN keeping its sign and payload with the quiet bit set -- for every one
+// of the 2^32 fp32 bit patterns (checked exhaustively on MI355X), so the
+// instruction replaces a per-element branch on NaN.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
-  return bf16_rne(lo) | (bf16_rne(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
+__device__ __forceinline__ uint32_t bf16_rne(float f) { return bf16_pack(f, 0.f) & 0xffffu; }
 
 // ------------------------------------------------------------------ vectors
 // VecIO<T,VE>: VE consecutive elements of storage type T (float, or uint16_t

@@ -17,10 +17,10 @@
 // C1 + C2 + C3 (each the fp32 rounding of what remained of pi/2, derived
 // exactly from Machin's formula for pi), every step one fused multiply-add,
 // so |r| <= pi/4 carries about 1e-7 absolute error for |x| <= 2^16.  The
-// reduced angle r + q*pi/2 (q = k mod 4) is then handed to v_cos_f32 in
-// revolutions, r/(2 pi) + q/4, a value below one revolution, where the
-// hardware cosine measured 3e-7 worst-case absolute error against fp64 on
-// MI355X.  Larger arguments take the library cosf.
+// reduced angle r + q*pi/2 (q = k mod 4, taken as the fraction of k/4) is
+// then handed to v_cos_f32 in revolutions, r/(2 pi) + q/4, a value below one
+// revolution, where the hardware cosine measured 3e-7 worst-case absolute
+// error against fp64 on MI355X.  Larger arguments take the library cosf.
 #include "common.h"
 
 namespace fast {
@@ -44,8 +44,8 @@ __device__ __forceinline__ float cos_rr(float x) {
   float r = fmaf(-k, C1, x);
   r = fmaf(-k, C2, r);
   r = fmaf(-k, C3, r);
-  const float q = float(int32_t(k) & 3);        // quadrant, exact
-  return __builtin_amdgcn_cosf(fmaf(r, INV_TWO_PI, 0.25f * q));
+  const float q = __builtin_amdgcn_fractf(0.25f * k);   // (k mod 4) / 4, exact
+  return __builtin_amdgcn_cosf(fmaf(r, INV_TWO_PI, q));
 }
 
 // Large arguments (|x| > 2^16, or not finite) take the library cosf.
