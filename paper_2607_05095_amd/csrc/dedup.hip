@@ -72,6 +72,10 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
   return off;
 }
 
+__global__ void __launch_bounds__(64) k_set_i64(int64_t* p, int64_t v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
 __global__ void __launch_bounds__(DD_THREADS) k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
   for (int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * DD_THREADS)
@@ -350,8 +354,13 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
     hipLaunchKernelGGL(k_dedup_inv, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
                        dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words, inv);
 
-  // 6. rows through the slot map, miss flags, 7. ordered miss list
-  const bool want_miss = miss || num_miss;
+  // 6. rows through the slot map, miss flags, 7. ordered miss list.  Without
+  // a slot map and with a row for every id (id_bound <= table_rows) nothing
+  // can miss: no flags, no scan, and the miss count is 0.
+  const bool all_hit = !slot_map && id_bound <= table_rows;
+  const bool want_miss = (miss || num_miss) && !all_hit;
+  if (all_hit && num_miss)
+    hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(64), 0, st, num_miss, int64_t(0));
   if (rows || want_miss) {
     const int64_t row_bytes = int64_t(D > 0 ? D : 0) * elem_size(dtype);
     uint8_t* flags = want_miss ? w.flags : nullptr;
