@@ -33,6 +33,7 @@ _SIGS = {
     "oracle_time_encode": (None, [_p, _i64, _p, _p, _p, _p, _i32, _p]),
     "oracle_occurrence_csr": (None, [_p, _i64, _i64, _p, _p]),
     "oracle_index_add_rows": (None, [_p, _i64, _i64, _i64, _p, _p]),
+    "oracle_index_add_scaled_rows": (None, [_p, _p, _i64, _i64, _i64, _i64, _p, _p, _p]),
     "oracle_sample_recent": (None, [_p, _i64, _p, _p, _p, _p, _p, _i64, _i32, _p, _p, _p, _p]),
     "oracle_access_count": (None, [_p, _p, _i64, _i64, _p]),
     "oracle_greedy_hot_set": (None, [_p, _i64, _p, _i64, _f64, _p, _p, _p, _p]),
@@ -146,6 +147,36 @@ def index_add_rows(index, num_rows, src):
     lib().oracle_index_add_rows(_ptr(index), index.shape[0], num_rows, D,
                                 _ptr(np.ascontiguousarray(src.reshape(index.shape[0], D))), _ptr(dst))
     return dst
+
+
+def index_add_scaled_rows(index, off, num_rows, scal, src):
+    """dst [num_rows, H, dh] float64: for every edge e (segment v by off) with
+    index[e] == u, add scal[e, h] * src[v, h, :] to row u."""
+    index, off = _c(index, np.int32), _c(off, np.int32)
+    scal, src = _f64(scal), _f64(src)
+    N, H, dh = src.shape
+    assert scal.shape == (index.shape[0], H) and off.shape[0] == N + 1
+    dst = np.zeros((num_rows, H, dh), dtype=np.float64)
+    lib().oracle_index_add_scaled_rows(_ptr(index), _ptr(off), N, num_rows, H, dh, _ptr(scal),
+                                       _ptr(src), _ptr(dst))
+    return dst
+
+
+def edge_attention_bwd_scalars(off, Q, K, V, dO, scale, slope):
+    """(dQ, g [E,H], alpha [E,H]): the backward written with its per-edge
+    coefficients, dK[e,h,:] = g[e,h] * Q[v,h,:] and dV[e,h,:] = alpha[e,h] *
+    dO[v,h,:] for edge e of segment v.  From the softmax and aggregation
+    definitions (Sec. 4.3): dalpha = <dO[v,h], V[e,h]>, D = sum over the
+    segment of alpha * dalpha, g = alpha (dalpha - D) LReLU'(pre) scale."""
+    off = _c(off, np.int32)
+    alpha, _, pre = edge_softmax_fwd(off, Q, K, scale, slope)
+    dalpha, _ = aggregate_bwd(off, alpha, V, dO)
+    seg = np.repeat(np.arange(off.shape[0] - 1), np.diff(off))
+    D = np.zeros((off.shape[0] - 1, alpha.shape[1]))
+    np.add.at(D, seg, alpha * dalpha)
+    g = alpha * (dalpha - D[seg]) * np.where(pre > 0, 1.0, slope) * scale
+    dQ, _ = edge_softmax_bwd(off, Q, K, scale, slope, alpha, dalpha)
+    return dQ, g, alpha
 
 
 def edge_attention_fwd_indexed(off, Q, K, k_index, V, v_index, scale, slope):

@@ -129,6 +129,25 @@ void oracle_index_add_rows(const int32_t* index, int64_t n, int64_t num_rows, in
   }
 }
 
+/* dst[u, h, :] = sum over the edges e with index[e] == u of
+ * scal[e, h] * src[v, h, :], v the destination segment of e (off): the
+ * gradient of a shared K or V row written as the per-edge coefficient times
+ * the row of the segment that edge belongs to (chain rule through the
+ * gather; Sec. 4.3 backward), fp64; 0 for a row no edge reads. */
+void oracle_index_add_scaled_rows(const int32_t* index, const int32_t* off, int64_t N,
+                                  int64_t num_rows, int64_t H, int64_t dh, const double* scal,
+                                  const double* src, double* dst) {
+  const int64_t D = H * dh;
+  for (int64_t i = 0; i < num_rows * D; ++i) dst[i] = 0.0;
+  for (int64_t v = 0; v < N; ++v)
+    for (int64_t e = off[v]; e < off[v + 1]; ++e) {
+      if (index[e] < 0 || index[e] >= num_rows) continue;
+      for (int64_t h = 0; h < H; ++h)
+        for (int64_t j = 0; j < dh; ++j)
+          dst[(int64_t)index[e] * D + h * dh + j] += scal[e * H + h] * src[v * D + h * dh + j];
+    }
+}
+
 /* ---- most-recent-k temporal neighbour sampling (Sec. 6.1: top-k recent
  * sampling over the T-CSR temporal graph) ---- */
 void oracle_sample_recent(const int64_t* indptr, int64_t num_nodes, const int64_t* nbr,

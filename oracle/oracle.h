@@ -61,6 +61,13 @@ void oracle_occurrence_csr(const int32_t* index, int64_t n, int64_t num_rows, in
 void oracle_index_add_rows(const int32_t* index, int64_t n, int64_t num_rows, int64_t D,
                            const double* src, double* dst);
 
+/* Row gradients from per-edge coefficients: dst[u, h, :] = sum over edges e
+ * (segments v by off[N+1], edges in order) with index[e] == u of
+ * scal[e, h] * src[v, h, :] (fp64; 0 for a row no edge reads). */
+void oracle_index_add_scaled_rows(const int32_t* index, const int32_t* off, int64_t N,
+                                  int64_t num_rows, int64_t H, int64_t dh, const double* scal,
+                                  const double* src, double* dst);
+
 /* Most-recent-k temporal neighbour sampling (Sec. 6.1) over a T-CSR graph:
  * node v's entries are p in [indptr[v], indptr[v+1]) with neighbour nbr[p],
  * time ts[p] and edge id eid[p], in time order.  For root i (node roots[i],

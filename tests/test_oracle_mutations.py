@@ -29,6 +29,10 @@ MUTATIONS = {
     "occ_offsets_shifted": ("occ_off[index[p] + 1] += 1;", "occ_off[index[p]] += 1;"),
     "index_add_drops_last": ("for (int64_t p = 0; p < n; ++p) {\n    if (index[p] < 0 || index[p] >= num_rows) continue;",
                              "for (int64_t p = 0; p < n - 1; ++p) {\n    if (index[p] < 0 || index[p] >= num_rows) continue;"),
+    "scaled_rows_edge_row": ("scal[e * H + h] * src[v * D + h * dh + j];",
+                             "scal[e * H + h] * src[(v > 0 ? v - 1 : 0) * D + h * dh + j];"),
+    "scaled_rows_head_swap": ("dst[(int64_t)index[e] * D + h * dh + j] += scal[e * H + h]",
+                              "dst[(int64_t)index[e] * D + h * dh + j] += scal[e * H + (H - 1 - h)]"),
     "sample_not_strict": ("if (ts[p] < root_t[i]) c += 1;", "if (ts[p] <= root_t[i]) c += 1;"),
     "sample_oldest_k": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = 0;"),
     "sample_k_minus_one": ("int64_t skip = c > k ? c - k : 0;", "int64_t skip = c > k - 1 ? c - k + 1 : 0;"),
@@ -83,6 +87,8 @@ PINS = [
     (P.test_time_encode_fp32_difference, {}),
     (P.test_occurrence_csr_vs_numpy, {}),
     (P.test_index_add_rows_vs_numpy, {}),
+    (P.test_index_add_scaled_rows_vs_numpy, {}),
+    (P.test_bwd_scalars_are_the_per_edge_gradient_coefficients, {}),
     (P.test_indexed_attention_gradients_by_finite_differences, {}),
     (P.test_sample_recent_hand_example, {}),
     (P.test_sample_recent_vs_numpy, dict(k=3)),

@@ -216,6 +216,45 @@ def test_index_add_rows_vs_numpy():
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
+def test_bwd_scalars_are_the_per_edge_gradient_coefficients():
+    # per-edge coefficients against the pinned backward: g[e,h] Q[v,h,:] is
+    # dK[e,h,:] and alpha[e,h] dO[v,h,:] is dV[e,h,:] (v the segment of e);
+    # alpha sums to 1 over a non-empty segment; an empty segment has no edges
+    r = np.random.default_rng(12)
+    counts = [4, 0, 1, 6, 3, 0, 2]
+    off = _csr(counts)
+    N, E, H, dh = len(counts), int(off[-1]), 3, 5
+    Q, dO = r.standard_normal((N, H, dh)), r.standard_normal((N, H, dh))
+    K, V = r.standard_normal((E, H, dh)), r.standard_normal((E, H, dh))
+    for slope in (SLOPE, 1.0, 0.0):
+        dQ, g, al = oracle.edge_attention_bwd_scalars(off, Q, K, V, dO, 0.7, slope)
+        rdQ, rdK, rdV = oracle.edge_attention_bwd(off, Q, K, V, dO, 0.7, slope)
+        seg = np.repeat(np.arange(N), counts)
+        np.testing.assert_allclose(g[:, :, None] * Q[seg], rdK, rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(al[:, :, None] * dO[seg], rdV, rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(dQ, rdQ, rtol=1e-12, atol=1e-14)
+        sums = np.zeros((N, H))
+        np.add.at(sums, seg, al)
+        np.testing.assert_allclose(sums[np.array(counts) > 0], 1.0, rtol=1e-12)
+
+
+def test_index_add_scaled_rows_vs_numpy():
+    # the scaled transposed gather is the plain one applied to the per-edge
+    # rows scal[e,h] * src[seg e, h, :]; indices outside the rows are left out
+    r = np.random.default_rng(13)
+    counts = r.integers(0, 6, 300)
+    off = _csr(counts)
+    N, E, H, dh, U = counts.size, int(off[-1]), 2, 3, 40
+    idx = r.integers(-2, U + 2, E).astype(np.int32)
+    scal, src = r.standard_normal((E, H)), r.standard_normal((N, H, dh))
+    seg = np.repeat(np.arange(N), counts)
+    want = np.zeros((U, H, dh))
+    ok = (idx >= 0) & (idx < U)
+    np.add.at(want, idx[ok], scal[ok][:, :, None] * src[seg[ok]])
+    np.testing.assert_allclose(oracle.index_add_scaled_rows(idx, off, U, scal, src), want,
+                               rtol=1e-12, atol=1e-12)
+
+
 def test_indexed_attention_gradients_by_finite_differences():
     # compact K and V rows read by several edges each: the gradient of
     # L = sum(dOut * out) with respect to a compact row is the derivative of
@@ -249,6 +288,15 @@ def test_indexed_attention_gradients_by_finite_differences():
                     fd = ((loss(hi, V) - loss(lo, V)) if which == 0 else
                           (loss(K, hi) - loss(K, lo))) / (2 * hstep)
                     assert abs(grad[u, h, i] - fd) <= 1e-6 * (1 + abs(fd)), (which, u, h, i)
+    # the same row gradients from the per-edge coefficients: dK row u is the
+    # sum of g[e] Q[seg e] over the edges reading u, dV row u that of
+    # alpha[e] dO[seg e]; compared with the finite differences above through
+    # the gradients they already matched
+    _, g, al = oracle.edge_attention_bwd_scalars(off, Q, K[kidx], V[vidx], dO, scale, SLOPE)
+    np.testing.assert_allclose(oracle.index_add_scaled_rows(kidx, off, Uk, g, Q), dKr,
+                               rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.index_add_scaled_rows(vidx, off, Uv, al, dO), dVr,
+                               rtol=1e-12, atol=1e-12)
     # identity index: the plain operator
     ident = np.arange(E, dtype=np.int32)
     Ke, Ve = K[kidx], V[vidx]
