@@ -16,6 +16,8 @@
  *                             index into de-duplicated rows           (Sec. 4.2)
  *   fast_occurrence_csr, fast_index_add_rows  the gradient of a shared row
  *                             as the ordered sum over its readers     (Sec. 4.2)
+ *   fast_edge_attention_bwd_indexed_coef, fast_index_add_scaled_rows  the
+ *                             same from per-edge coefficients         (Sec. 4.2, 4.3)
  *
  * Conventions shared by every entry point
  *   - Memory: every array argument is a DEVICE pointer into HBM owned by the
@@ -385,6 +387,44 @@ fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32_t* occ, in
                                   int64_t num_rows, int D, fast_dtype_t src_dtype,
                                   const void* src, float* dst, void* ws, size_t ws_bytes,
                                   fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Row gradients of indexed operands in coefficient form.  The backward of
+ * edge e of segment v is dK_e[h,:] = g[e,h] * Q[v,h,:] and dV_e[h,:] =
+ * alpha[e,h] * dout[v,h,:] (Sec. 4.3: the softmax and aggregation backward,
+ * g = alpha (dalpha - D) LReLU'(pre) scale), so a shared row's gradient
+ * needs only the two coefficients per edge and head, not the per-edge rows:
+ *
+ * fast_edge_attention_bwd_indexed_coef: as fast_edge_attention_bwd_indexed
+ *   (same arguments and dQ), but writes g_edge [E,H] and alpha_edge [E,H]
+ *   (fp32, device) in place of dK_edge and dV_edge.
+ *
+ * fast_index_add_scaled_rows: for every row u,
+ *   dst[u,h,:] = sum over the occurrences e of u (occ_off/occ of the index,
+ *                from fast_occurrence_csr) of scal[e,h] * src[v,h,:],
+ *   v the segment of edge e in dst_offsets [num_dst+1].  dK rows: scal =
+ *   g_edge, src = Q, the occurrence lists of k_index; dV rows: scal =
+ *   alpha_edge, src = dout, those of v_index.  Products and sums in fp64,
+ *   in occurrence order (long rows cut into pieces as fast_index_add_rows
+ *   does), rounded once to fp32; dst [num_rows, H, dh] fp32, overwritten.
+ *   src [num_dst, H, dh] of src_dtype, scal [n, H] fp32 (n = edges).
+ *   Malformed lists or offsets give wrong sums, never out-of-bounds accesses.
+ * Limits: n, num_dst < 2^31, num_rows < 2^31 - 1.
+ * Workspace: fast_index_add_scaled_rows_workspace(n, num_rows, H, dh) bytes,
+ *   256-byte aligned.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_edge_attention_bwd_indexed_coef(
+    const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype, const void* Q, const void* K,
+    const int32_t* k_index, int64_t k_rows, const void* V, const int32_t* v_index,
+    int64_t v_rows, float scale, float neg_slope, const float* lse, const void* dout, void* dQ,
+    float* g_edge, float* alpha_edge, fast_stream_t stream);
+size_t fast_index_add_scaled_rows_workspace(int64_t n, int64_t num_rows, int H, int dh);
+fast_status_t fast_index_add_scaled_rows(const int32_t* occ_off, const int32_t* occ, int64_t n,
+                                         int64_t num_rows, const int32_t* dst_offsets,
+                                         int64_t num_dst, int H, int dh,
+                                         fast_dtype_t src_dtype, const float* scal,
+                                         const void* src, float* dst, void* ws,
+                                         size_t ws_bytes, fast_stream_t stream);
 
 #ifdef __cplusplus
 }

@@ -27,6 +27,8 @@ __all__ = [
     "fast_edge_attention_fwd_indexed", "fast_edge_attention_bwd_indexed",
     "fast_occurrence_csr_workspace", "fast_occurrence_csr",
     "fast_index_add_rows_workspace", "fast_index_add_rows",
+    "fast_edge_attention_bwd_indexed_coef",
+    "fast_index_add_scaled_rows_workspace", "fast_index_add_scaled_rows",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -105,6 +107,11 @@ _SIGS = {
     "fast_occurrence_csr": (_i32, [_p, _i64, _i64, _p, _p, _p, _sz, _p]),
     "fast_index_add_rows_workspace": (_sz, [_i64, _i64, _i32]),
     "fast_index_add_rows": (_i32, [_p, _p, _i64, _i64, _i32, _i32, _p, _p, _p, _sz, _p]),
+    "fast_edge_attention_bwd_indexed_coef": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _p,
+                                                    _i64, _f32, _f32, _p, _p, _p, _p, _p, _p]),
+    "fast_index_add_scaled_rows_workspace": (_sz, [_i64, _i64, _i32, _i32]),
+    "fast_index_add_scaled_rows": (_i32, [_p, _p, _i64, _i64, _p, _i64, _i32, _i32, _i32, _p, _p,
+                                          _p, _p, _sz, _p]),
 }
 
 _lib = None
@@ -337,3 +344,26 @@ def fast_index_add_rows(occ_off, occ, n, num_rows, D, src_dtype, src, dst, ws, w
                         stream=None):
     _check(lib().fast_index_add_rows(_ptr(occ_off), _ptr(occ), n, num_rows, D, src_dtype, _ptr(src),
                                      _ptr(dst), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def fast_edge_attention_bwd_indexed_coef(g: TCSR, H, dh, dtype, Q, K, k_index, k_rows, V, v_index,
+                                         v_rows, scale, neg_slope, lse, dout, dQ, g_edge,
+                                         alpha_edge, stream=None):
+    _check(lib().fast_edge_attention_bwd_indexed_coef(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K),
+                                                      _ptr(k_index), k_rows, _ptr(V),
+                                                      _ptr(v_index), v_rows, scale, neg_slope,
+                                                      _ptr(lse), _ptr(dout), _ptr(dQ),
+                                                      _ptr(g_edge), _ptr(alpha_edge),
+                                                      _stream(stream)))
+
+
+def fast_index_add_scaled_rows_workspace(n: int, num_rows: int, H: int, dh: int) -> int:
+    return lib().fast_index_add_scaled_rows_workspace(n, num_rows, H, dh)
+
+
+def fast_index_add_scaled_rows(occ_off, occ, n, num_rows, dst_offsets, num_dst, H, dh, src_dtype,
+                               scal, src, dst, ws, ws_bytes, stream=None):
+    _check(lib().fast_index_add_scaled_rows(_ptr(occ_off), _ptr(occ), n, num_rows,
+                                            _ptr(dst_offsets), num_dst, H, dh, src_dtype,
+                                            _ptr(scal), _ptr(src), _ptr(dst), _ptr(ws), ws_bytes,
+                                            _stream(stream)))

@@ -109,6 +109,10 @@ struct AttnArgs {
   const int32_t* kidx;
   const int32_t* vidx;
   int64_t k_rows, v_rows;
+  // indexed backward, coefficient form: per edge and head g (dK = g Q[seg])
+  // and alpha (dV = alpha dOut[seg]) instead of the dK, dV rows
+  float* g_out;
+  float* al_out;
 };
 
 // Row of K or V read by edge e.
@@ -374,11 +378,20 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
   }
 }
 
-template <typename T, int VE, int P, bool NT>
+template <typename T, int VE, int P, bool NT, bool IDX>
 __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m, int64_t e, float t,
                                          float da, float invZ, float D, const BwdState<VE, P>& S) {
   const float al = exp2_hw(t - S.mx) * invZ;
   const float g = al * (da - D) * lrelu_grad(t, a.slope) * a.scale;
+  if constexpr (IDX) {
+    if (a.g_out) {                       // the head's first lane writes its coefficients
+      if (m.l == 0) {
+        a.g_out[e * a.L.H + m.h] = g;
+        a.al_out[e * a.L.H + m.h] = al;
+      }
+      return;
+    }
+  }
   float dk[P][VE], dv[P][VE];
 #pragma unroll
   for (int p = 0; p < P; ++p)
@@ -440,7 +453,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
     const int64_t base = e0 + c * ATT_CH_BWD;
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i)
-      if (base + i < e1) bwd_emit<T, VE, P, NT>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
+      if (base + i < e1) bwd_emit<T, VE, P, NT, IDX>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
   }
   // long segments: re-read K and V for the edges past the register window
   for (int64_t base = e0 + ATT_NSAVE * ATT_CH_BWD; base < e1; base += ATT_CH_BWD) {
@@ -455,7 +468,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
     for (int i = 0; i < ATT_CH_BWD; ++i) {
       const float t = lrelu(head_dot<VE, P, LPH_CT>(S.q, kx[i], m.lph) * sl2, a.slope);
       const float da = head_dot<VE, P, LPH_CT>(S.go, vx[i], m.lph);
-      if (base + i < e1) bwd_emit<T, VE, P, NT>(a, m, base + i, t, da, invZ, D, S);
+      if (base + i < e1) bwd_emit<T, VE, P, NT, IDX>(a, m, base + i, t, da, invZ, D, S);
     }
   }
 }

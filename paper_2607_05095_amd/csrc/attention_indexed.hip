@@ -96,3 +96,28 @@ extern "C" fast_status_t fast_edge_attention_bwd_indexed(
   const void* rows[] = {Q, K, V, dout, dQ, dK_edge, dV_edge};
   return attn_run(fn, Op::kAttnBwdIdx, g, H, dh, dtype, a, rows, 7, stream);
 }
+
+extern "C" fast_status_t fast_edge_attention_bwd_indexed_coef(
+    const fast_tcsr_t* g, int H, int dh, fast_dtype_t dtype, const void* Q, const void* K,
+    const int32_t* k_index, int64_t k_rows, const void* V, const int32_t* v_index, int64_t v_rows,
+    float scale, float neg_slope, const float* lse, const void* dout, void* dQ, float* g_edge,
+    float* alpha_edge, fast_stream_t stream) {
+  const char* fn = "fast_edge_attention_bwd_indexed_coef";
+  if (g && g->num_dst > 0) {
+    FAST_NEED(Q, fn); FAST_NEED(dout, fn); FAST_NEED(dQ, fn);
+    if (g->num_edges > 0) {
+      FAST_NEED(K, fn); FAST_NEED(V, fn); FAST_NEED(g_edge, fn); FAST_NEED(alpha_edge, fn);
+    }
+  }
+  if ((g_edge && !aligned(g_edge, 4)) || (alpha_edge && !aligned(alpha_edge, 4)))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: g_edge/alpha_edge not 4-byte aligned", fn);
+  if (check_rows(fn, k_index, k_rows) || check_rows(fn, v_index, v_rows))
+    return FAST_ERR_INVALID_ARG;
+  AttnArgs a = {};
+  a.scale = scale; a.slope = neg_slope;
+  a.Q = Q; a.K = K; a.V = V; a.dO = dout; a.lse_in = lse; a.dQ = dQ;
+  a.kidx = k_index; a.vidx = v_index; a.k_rows = k_rows; a.v_rows = v_rows;
+  a.g_out = g_edge; a.al_out = alpha_edge;
+  const void* rows[] = {Q, K, V, dout, dQ};
+  return attn_run(fn, Op::kAttnBwdIdx, g, H, dh, dtype, a, rows, 5, stream);
+}

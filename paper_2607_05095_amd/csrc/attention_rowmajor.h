@@ -248,7 +248,7 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
   }
 }
 
-template <int H, bool NT>
+template <int H, bool NT, bool IDX>
 __device__ __forceinline__ void rm_bwd_emit(const AttnArgs& a, const RmMap<H>& m, int64_t e,
                                             const float (&t)[H], const float (&da)[H],
                                             const float (&invZ)[H], const float (&D)[H],
@@ -258,6 +258,18 @@ __device__ __forceinline__ void rm_bwd_emit(const AttnArgs& a, const RmMap<H>& m
   for (int h = 0; h < H; ++h) {
     al[h] = exp2_hw(t[h] - S.mx[h]) * invZ[h];
     g[h] = al[h] * (da[h] - D[h]) * lrelu_grad(t[h], a.slope) * a.scale;
+  }
+  if constexpr (IDX) {
+    if (a.g_out) {                       // every lane holds all heads' values
+      if (m.c == 0) {
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+          a.g_out[e * H + h] = g[h];
+          a.al_out[e * H + h] = al[h];
+        }
+      }
+      return;
+    }
   }
   float dk[4], dv[4];
 #pragma unroll
@@ -323,7 +335,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
     const int64_t base = e0 + c * RM_CH_BWD;
 #pragma unroll
     for (int i = 0; i < RM_CH_BWD; ++i)
-      if (base + i < e1) rm_bwd_emit<H, NT>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
+      if (base + i < e1) rm_bwd_emit<H, NT, IDX>(a, m, base + i, st[c][i], sda[c][i], invZ, D, S);
   }
   // long segments: re-read K and V for the edges past the register window
   for (int64_t base = e0 + ATT_RM_NSAVE * RM_CH_BWD; base < e1; base += RM_CH_BWD) {
@@ -341,7 +353,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
       rm_dots<H, G>(S.go, vx[i], m, da);
 #pragma unroll
       for (int h = 0; h < H; ++h) t[h] = lrelu(d[h] * sl2, a.slope);
-      if (base + i < e1) rm_bwd_emit<H, NT>(a, m, base + i, t, da, invZ, D, S);
+      if (base + i < e1) rm_bwd_emit<H, NT, IDX>(a, m, base + i, t, da, invZ, D, S);
     }
   }
 }

@@ -250,38 +250,90 @@ struct OutMulti {
   }
 };
 
-// acc += src rows occ[j0 .. j1) in order, chunk c of VE values; IA_UNROLL
-// row loads are issued before they are added (in the same order).
+// Row sources of the index-add kernels.  Position p of an occurrence list
+// contributes, to chunk c (VE values) of its row's sum:
+//   PlainRows:  src row p;
+//   ScaledRows: scal[p, head] * src row seg[p] -- edge p's coefficient times
+//               the row of the destination segment it belongs to, one head
+//               coefficient per element (a chunk spans at most two heads,
+//               since VE <= dh).
+// Products are formed in fp64 (exact for fp32 factors), sums in fp64.
 template <typename T, int VE>
+struct PlainRows {
+  const T* __restrict__ src;
+  int D;
+  int64_t n;
+  struct Item {
+    float x[VE];
+  };
+  __device__ void chunk(int) {}
+  __device__ Item fetch(int32_t p, int c) const {
+    Item it;
+    VecIO<T, VE>::load(src + clamp64(p, 0, n - 1) * D + c * VE, it.x);
+    return it;
+  }
+  __device__ void add(double (&acc)[VE], const Item& it) const {
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] += double(it.x[t]);
+  }
+};
+
+template <typename T, int VE>
+struct ScaledRows {
+  const T* __restrict__ src;        // [N, H, dh]
+  const float* __restrict__ scal;   // [n, H]
+  const int32_t* __restrict__ seg;  // [n]: destination segment of edge p
+  int D, H, dh;
+  int64_t n, N;
+  int h0, h1, split;                // heads of the chunk; elements t < split use h0
+  struct Item {
+    float x[VE];
+    float s0, s1;
+  };
+  __device__ void chunk(int c) {
+    const int c0 = c * VE;
+    h0 = c0 / dh;
+    h1 = (c0 + VE - 1) / dh;
+    split = (h0 + 1) * dh - c0;
+  }
+  __device__ Item fetch(int32_t p, int c) const {
+    const int64_t e = clamp64(p, 0, n - 1);
+    const int64_t v = clamp64(seg[e], 0, N - 1);
+    Item it;
+    VecIO<T, VE>::load(src + v * D + c * VE, it.x);
+    it.s0 = scal[e * H + h0];
+    it.s1 = scal[e * H + h1];
+    return it;
+  }
+  __device__ void add(double (&acc)[VE], const Item& it) const {
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] = fma(double(t < split ? it.s0 : it.s1), double(it.x[t]), acc[t]);
+  }
+};
+
+// acc += the contributions of positions occ[j0 .. j1) in order, chunk c;
+// IA_UNROLL positions are fetched before they are added (in the same order).
+template <int VE, class Src>
 __device__ __forceinline__ void ia_sum(const int32_t* __restrict__ occ, int64_t j0, int64_t j1,
-                                       int64_t n, int D, int c, const T* __restrict__ src,
-                                       double (&acc)[VE]) {
+                                       int c, const Src& src, double (&acc)[VE]) {
   int64_t j = j0;
   for (; j + IA_UNROLL <= j1; j += IA_UNROLL) {
-    float x[IA_UNROLL][VE];
+    typename Src::Item x[IA_UNROLL];
 #pragma unroll
-    for (int r = 0; r < IA_UNROLL; ++r)
-      VecIO<T, VE>::load(src + clamp64(occ[j + r], 0, n - 1) * D + c * VE, x[r]);
+    for (int r = 0; r < IA_UNROLL; ++r) x[r] = src.fetch(occ[j + r], c);
 #pragma unroll
-    for (int r = 0; r < IA_UNROLL; ++r)
-#pragma unroll
-      for (int t = 0; t < VE; ++t) acc[t] += double(x[r][t]);
+    for (int r = 0; r < IA_UNROLL; ++r) src.add(acc, x[r]);
   }
-  for (; j < j1; ++j) {
-    float x[VE];
-    VecIO<T, VE>::load(src + clamp64(occ[j], 0, n - 1) * D + c * VE, x);
-#pragma unroll
-    for (int t = 0; t < VE; ++t) acc[t] += double(x[t]);
-  }
+  for (; j < j1; ++j) src.add(acc, src.fetch(occ[j], c));
 }
 
 // Pieces of the long rows: one group of `lanes` lanes per piece q in
 // [0, multi_off[num_rows]); its sum goes to partial[q].
-template <typename T, int VE>
+template <int VE, class Src>
 __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
     const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
     const int32_t* __restrict__ multi_off, int64_t num_rows, int64_t multi_bound, int64_t n,
-    int lanes, int D, const T* __restrict__ src, double* __restrict__ partial) {
+    int lanes, int D, Src src, double* __restrict__ partial) {
   const int64_t q = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
   const int l = int(threadIdx.x) % lanes;
   if (q >= multi_bound || q >= multi_off[num_rows]) return;
@@ -301,10 +353,11 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
   const int64_t j1 = j0 + len < r1 ? j0 + len : r1;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {
+    src.chunk(c);
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
-    ia_sum<T, VE>(occ, j0, j1, n, D, c, src, acc);
+    ia_sum<VE>(occ, j0, j1, c, src, acc);
 #pragma unroll
     for (int t = 0; t < VE; ++t) partial[q * D + c * VE + t] = acc[t];
   }
@@ -313,12 +366,11 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
 // One group per row: a short row sums its occurrences directly (zeros for
 // none), a long row adds its piece sums in piece order.  fp64 sums, rounded
 // once to fp32.
-template <typename T, int VE>
+template <int VE, class Src>
 __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
     const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
     const int32_t* __restrict__ multi_off, int64_t num_rows, int64_t multi_bound, int64_t n,
-    int lanes, int D, const T* __restrict__ src, const double* __restrict__ partial,
-    float* __restrict__ dst) {
+    int lanes, int D, Src src, const double* __restrict__ partial, float* __restrict__ dst) {
   const int64_t u = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
   const int l = int(threadIdx.x) % lanes;
   if (u >= num_rows) return;
@@ -330,11 +382,12 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
   const bool longrow = ia_multi_pieces(j1 - j0) > 0;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {
+    src.chunk(c);
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
     if (!longrow) {
-      ia_sum<T, VE>(occ, j0, j1, n, D, c, src, acc);
+      ia_sum<VE>(occ, j0, j1, c, src, acc);
     } else {
       int64_t m = m0;
       for (; m + IA_UNROLL <= m1; m += IA_UNROLL) {     // loads ahead, adds in order
@@ -357,6 +410,21 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
     for (int t = 0; t < VE; ++t) o[t] = float(acc[t]);
     VecIO<float, VE>::store(dst + u * D + c * VE, o);
   }
+}
+
+// seg[e] = the segment v with off[v] <= e < off[v + 1] (a binary search in
+// the offsets; clamped into [0, N) whatever the offsets hold).
+__global__ void __launch_bounds__(IA_THREADS) k_edge_seg(const int32_t* __restrict__ off,
+                                                        int64_t N, int64_t n,
+                                                        int32_t* __restrict__ seg) {
+  const int64_t e = int64_t(blockIdx.x) * IA_THREADS + threadIdx.x;
+  if (e >= n) return;
+  int64_t lo = 0, hi = N - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (int64_t(off[mid]) <= e) lo = mid; else hi = mid - 1;
+  }
+  seg[e] = int32_t(lo);
 }
 
 struct IaWs {
@@ -445,6 +513,46 @@ extern "C" fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, in
   return check_launch(fn);
 }
 
+// Launches the row sums over occurrence lists for a row source: the piece
+// count scan, the long rows' pieces, then one group per row.
+template <int VE, class Src>
+static hipError_t ia_launch(const int32_t* occ_off, const int32_t* occ, int64_t n,
+                            int64_t num_rows, int D, const Src& src, const IaWs& w, float* dst,
+                            hipStream_t st) {
+  hipError_t e = scan_launch(InMulti{occ_off, n}, OutMulti{w.multi_off}, num_rows, w.scan, nullptr,
+                             w.multi_off + num_rows, st);
+  if (e != hipSuccess) return e;
+  const int lanes = pow2_at_least(D / VE, 64);
+  const int64_t groups_per_block = IA_THREADS / lanes;
+  const int64_t mb = ia_multi_bound(n);
+  const int64_t np_blocks = (mb + groups_per_block - 1) / groups_per_block;
+  const int64_t nr_blocks = (num_rows + groups_per_block - 1) / groups_per_block;
+  if (n > 0)
+    hipLaunchKernelGGL((k_ia_pieces<VE, Src>), dim3(uint32_t(np_blocks)), dim3(IA_THREADS), 0, st,
+                       occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, src, w.partial);
+  hipLaunchKernelGGL((k_ia_rows<VE, Src>), dim3(uint32_t(nr_blocks)), dim3(IA_THREADS), 0, st,
+                     occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, src, w.partial, dst);
+  return hipGetLastError();
+}
+
+// Widest vector (4, 2 or 1 values) that divides D, is at most `cap` and fits
+// the alignment of both row pointers.
+static int ia_vector(int D, int cap, const void* src, int esz, const float* dst) {
+  for (int v : {4, 2})
+    if (v <= cap && D % v == 0 && aligned(src, size_t(v) * esz) && aligned(dst, size_t(v) * 4))
+      return v;
+  return 1;
+}
+
+static fast_status_t ia_common_checks(const char* fn, int64_t n, int64_t num_rows, int D,
+                                      fast_dtype_t src_dtype) {
+  if (n < 0 || num_rows < 0 || D < 1) return fail(FAST_ERR_INVALID_ARG, "%s: bad size", fn);
+  if (n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: n or num_rows beyond 2^31", fn);
+  if (src_dtype != FAST_F32 && src_dtype != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
+  return FAST_OK;
+}
+
 extern "C" size_t fast_index_add_rows_workspace(int64_t n, int64_t num_rows, int D) {
   if (n < 0 || num_rows < 0 || D < 1 || n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
     return 0;
@@ -456,10 +564,7 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
                                              fast_dtype_t src_dtype, const void* src, float* dst,
                                              void* ws, size_t ws_bytes, fast_stream_t stream) {
   const char* fn = "fast_index_add_rows";
-  if (n < 0 || num_rows < 0 || D < 1) return fail(FAST_ERR_INVALID_ARG, "%s: bad size", fn);
-  if (n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
-    return fail(FAST_ERR_UNSUPPORTED, "%s: n or num_rows beyond 2^31", fn);
-  if (src_dtype != FAST_F32 && src_dtype != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
+  if (fast_status_t c = ia_common_checks(fn, n, num_rows, D, src_dtype)) return c;
   if (num_rows == 0) return ok();
   if (!occ_off || !dst) return fail(FAST_ERR_INVALID_ARG, "%s: occ_off/dst is NULL", fn);
   if (n > 0 && (!occ || !src)) return fail(FAST_ERR_INVALID_ARG, "%s: occ/src is NULL", fn);
@@ -468,41 +573,83 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
     return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
   if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
   const int esz = elem_size(src_dtype);
-  // vector width: divides D and matches both row pointers
-  int VE = 1;
-  for (int v : {4, 2}) {
-    if (D % v == 0 && aligned(src, size_t(v) * esz) && aligned(dst, size_t(v) * 4)) {
-      VE = v;
-      break;
-    }
-  }
   if (!aligned(src, size_t(esz)) || !aligned(dst, 4))
     return fail(FAST_ERR_UNSUPPORTED, "%s: src/dst misaligned", fn);
+  const int VE = ia_vector(D, 4, src, esz, dst);
   hipStream_t st = static_cast<hipStream_t>(stream);
   IaWs w;
   ia_layout(n, num_rows, D, static_cast<char*>(ws), &w);
-  hipError_t e = scan_launch(InMulti{occ_off, n}, OutMulti{w.multi_off}, num_rows, w.scan, nullptr,
-                             w.multi_off + num_rows, st);
-  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-  const int lanes = pow2_at_least(D / VE, 64);
-  const int64_t groups_per_block = IA_THREADS / lanes;
-  const int64_t mb = ia_multi_bound(n);
-  const int64_t np_blocks = (mb + groups_per_block - 1) / groups_per_block;
-  const int64_t nr_blocks = (num_rows + groups_per_block - 1) / groups_per_block;
-#define FAST_IA(T_, VE_)                                                                           \
-  do {                                                                                             \
-    const T_* s_ = static_cast<const T_*>(src);                                                    \
-    if (n > 0)                                                                                     \
-      hipLaunchKernelGGL((k_ia_pieces<T_, VE_>), dim3(uint32_t(np_blocks)), dim3(IA_THREADS), 0,   \
-                         st, occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, s_, w.partial);  \
-    hipLaunchKernelGGL((k_ia_rows<T_, VE_>), dim3(uint32_t(nr_blocks)), dim3(IA_THREADS), 0, st,    \
-                       occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, s_, w.partial, dst);   \
-  } while (0)
+  hipError_t e = hipSuccess;
+#define FAST_IA(T_, VE_) \
+  e = ia_launch<VE_>(occ_off, occ, n, num_rows, D, PlainRows<T_, VE_>{static_cast<const T_*>(src), D, n}, w, dst, st)
   if (src_dtype == FAST_F32) {
     if (VE == 4) FAST_IA(float, 4); else if (VE == 2) FAST_IA(float, 2); else FAST_IA(float, 1);
   } else {
     if (VE == 4) FAST_IA(uint16_t, 4); else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
   }
 #undef FAST_IA
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+  return check_launch(fn);
+}
+
+static size_t ias_layout(int64_t n, int64_t num_rows, int D, char* base, int32_t** seg, IaWs* ws) {
+  const size_t seg_bytes = align_up(size_t(n) * 4, 256);
+  if (seg) *seg = reinterpret_cast<int32_t*>(base);
+  return seg_bytes + ia_layout(n, num_rows, D, base ? base + seg_bytes : nullptr, ws);
+}
+
+extern "C" size_t fast_index_add_scaled_rows_workspace(int64_t n, int64_t num_rows, int H, int dh) {
+  if (H < 1 || dh < 1 || int64_t(H) * dh >= (int64_t(1) << 31)) return 0;
+  const int D = H * dh;
+  if (n < 0 || num_rows < 0 || n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
+    return 0;
+  return ias_layout(n, num_rows, D, nullptr, nullptr, nullptr);
+}
+
+extern "C" fast_status_t fast_index_add_scaled_rows(
+    const int32_t* occ_off, const int32_t* occ, int64_t n, int64_t num_rows,
+    const int32_t* dst_offsets, int64_t num_dst, int H, int dh, fast_dtype_t src_dtype,
+    const float* scal, const void* src, float* dst, void* ws, size_t ws_bytes,
+    fast_stream_t stream) {
+  const char* fn = "fast_index_add_scaled_rows";
+  if (H < 1 || dh < 1 || int64_t(H) * dh >= (int64_t(1) << 31))
+    return fail(FAST_ERR_INVALID_ARG, "%s: bad H = %d or dh = %d", fn, H, dh);
+  const int D = H * dh;
+  if (fast_status_t c = ia_common_checks(fn, n, num_rows, D, src_dtype)) return c;
+  if (num_dst < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative num_dst", fn);
+  if (num_dst >= (int64_t(1) << 31)) return fail(FAST_ERR_UNSUPPORTED, "%s: num_dst >= 2^31", fn);
+  if (n > 0 && num_dst == 0) return fail(FAST_ERR_INVALID_ARG, "%s: edges but no destination", fn);
+  if (num_rows == 0) return ok();
+  if (!occ_off || !dst) return fail(FAST_ERR_INVALID_ARG, "%s: occ_off/dst is NULL", fn);
+  if (n > 0 && (!occ || !src || !scal || !dst_offsets))
+    return fail(FAST_ERR_INVALID_ARG, "%s: occ/dst_offsets/scal/src is NULL", fn);
+  const size_t need = fast_index_add_scaled_rows_workspace(n, num_rows, H, dh);
+  if (!ws || ws_bytes < need)
+    return fail(FAST_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu", fn, ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
+  const int esz = elem_size(src_dtype);
+  if (!aligned(src, size_t(esz)) || !aligned(dst, 4) || !aligned(scal, 4))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: src/dst/scal misaligned", fn);
+  const int VE = ia_vector(D, dh, src, esz, dst);   // a chunk spans at most two heads
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* seg = nullptr;
+  IaWs w;
+  ias_layout(n, num_rows, D, static_cast<char*>(ws), &seg, &w);
+  if (n > 0)
+    hipLaunchKernelGGL(k_edge_seg, dim3(uint32_t((n + IA_THREADS - 1) / IA_THREADS)), dim3(IA_THREADS),
+                       0, st, dst_offsets, num_dst, n, seg);
+  hipError_t e = hipSuccess;
+#define FAST_IAS(T_, VE_)                                                                          \
+  e = ia_launch<VE_>(occ_off, occ, n, num_rows, D,                                                 \
+                     ScaledRows<T_, VE_>{static_cast<const T_*>(src), scal, seg, D, H, dh, n,      \
+                                         num_dst, 0, 0, 0},                                        \
+                     w, dst, st)
+  if (src_dtype == FAST_F32) {
+    if (VE == 4) FAST_IAS(float, 4); else if (VE == 2) FAST_IAS(float, 2); else FAST_IAS(float, 1);
+  } else {
+    if (VE == 4) FAST_IAS(uint16_t, 4); else if (VE == 2) FAST_IAS(uint16_t, 2); else FAST_IAS(uint16_t, 1);
+  }
+#undef FAST_IAS
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   return check_launch(fn);
 }

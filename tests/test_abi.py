@@ -299,3 +299,37 @@ def test_indexed_operands_validation():
     assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 0, None, FAKE, FAKE, wa, None) == INVALID
     assert L.fast_index_add_rows(FAKE, FAKE, 1000, 50, 100, 0, FAKE + 2, FAKE, FAKE, wa, None) == UNSUPPORTED
     assert L.fast_index_add_rows(FAKE, FAKE, 1000, 0, 100, 0, FAKE, None, None, 0, None) == OK
+
+
+def test_coefficient_form_validation():
+    L = fast.lib()
+    gp = ctypes.byref(_g())
+    coef = lambda **k: L.fast_edge_attention_bwd_indexed_coef(
+        gp, 2, 50, 0, FAKE, FAKE, FAKE, 5, FAKE, FAKE, 5, 1.0, 0.2, None, FAKE, FAKE,
+        k.get("g", FAKE), k.get("al", FAKE), None)
+    assert coef(g=None) == INVALID
+    assert coef(al=None) == INVALID
+    assert coef(g=FAKE + 2) == UNSUPPORTED
+    assert L.fast_edge_attention_bwd_indexed_coef(gp, 2, 50, 0, FAKE, FAKE, FAKE, 0, FAKE, None, 0,
+                                                  1.0, 0.2, None, FAKE, FAKE, FAKE, FAKE,
+                                                  None) == INVALID      # index without rows
+    ws = L.fast_index_add_scaled_rows_workspace(1000, 50, 2, 50)
+    assert ws >= 1000 * 4 + L.fast_index_add_rows_workspace(1000, 50, 100)
+    assert L.fast_index_add_scaled_rows_workspace(1000, 50, 0, 50) == 0
+    assert L.fast_index_add_scaled_rows_workspace(-1, 50, 2, 50) == 0
+    call = lambda **k: L.fast_index_add_scaled_rows(
+        k.get("off", FAKE), FAKE, k.get("n", 1000), k.get("rows", 50), k.get("doff", FAKE),
+        k.get("N", 100), k.get("H", 2), 50, k.get("dt", 0), k.get("scal", FAKE), k.get("src", FAKE),
+        k.get("dst", FAKE), FAKE, k.get("ws", ws), None)
+    assert call(ws=ws - 1) == WORKSPACE
+    assert call(H=0) == INVALID
+    assert call(dt=3) == INVALID
+    assert call(N=-1) == INVALID
+    assert call(N=0) == INVALID                  # edges but no destination
+    assert call(N=1 << 31) == UNSUPPORTED
+    assert call(off=None) == INVALID
+    assert call(doff=None) == INVALID
+    assert call(scal=None) == INVALID
+    assert call(src=FAKE + 2) == UNSUPPORTED
+    assert call(scal=FAKE + 2) == UNSUPPORTED
+    assert call(rows=0, dst=None, ws=0) == OK    # nothing to write

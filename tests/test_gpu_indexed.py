@@ -206,3 +206,86 @@ def test_index_add_rows_malformed_lists_stay_in_bounds():
     got = _index_add_gpu(off, occ, n, rows, src)
     assert torch.isfinite(got).all()
     assert torch.equal(got, _index_add_gpu(off, occ, n, rows, src))
+
+
+# ------------------------------------------------------------------ coefficient form
+def _scaled_rows_gpu(off_occ, occ, n, num_rows, dst_off, N, H, dh, scal, src):
+    dst = torch.full((num_rows, H, dh), float("nan"), device="cuda")
+    wsb = fast.fast_index_add_scaled_rows_workspace(n, num_rows, H, dh)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    dt = fast.BF16 if src.dtype == torch.bfloat16 else fast.F32
+    fast.fast_index_add_scaled_rows(off_occ, occ, n, num_rows, dst_off, N, H, dh, dt, scal, src,
+                                    dst, ws, wsb)
+    torch.cuda.synchronize()
+    return dst
+
+
+@pytest.mark.parametrize("H,dh,dt,rows", [(2, 50, "f32", 300), (4, 32, "bf16", 5000), (1, 7, "f32", 40),
+                                          (3, 4, "bf16", 1000), (2, 1, "f32", 100)])
+def test_index_add_scaled_rows_vs_oracle(H, dh, dt, rows):
+    _announce(f"scaled row sums H={H} dh={dh} {dt} rows={rows}")
+    r = np.random.default_rng(H * 100 + dh + rows)
+    counts = r.integers(0, 12, 20_000).astype(np.int32)
+    counts[::53] = 0                                        # empty segments
+    off = oracle.csr_offsets(counts)
+    N, E = counts.size, int(off[-1])
+    idx = ((r.zipf(1.3, E) - 1) % rows).astype(np.int32)   # hub rows read by thousands of edges
+    idx[::97] = -1
+    scal = torch.as_tensor(r.standard_normal((E, H)).astype(np.float32), device="cuda")
+    src = _randn((N, H, dh), dt, "cuda", H + dh)
+    occ_off, occ = _occ_gpu(idx, rows + 2)                  # two rows nobody reads
+    got = _scaled_rows_gpu(occ_off, occ, E, rows + 2, to_dev(off), N, H, dh, scal, src)
+    want = oracle.index_add_scaled_rows(idx, off, rows + 2, scal.cpu().numpy(), _host(src))
+    assert_close(got, want, "f32", f"scaled rows H={H} dh={dh}")
+    again = _scaled_rows_gpu(occ_off, occ, E, rows + 2, to_dev(off), N, H, dh, scal, src)
+    assert torch.equal(got, again), "scaled row sums must be bitwise reproducible"
+    assert torch.all(got[rows:] == 0)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_indexed_coefficients_and_row_gradients(cfg):
+    b = make_batch(cfg)
+    for i, blk in enumerate(b.blocks):
+        _announce(f"coefficient-form backward cfg={cfg} block={i}")
+        blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
+        off = oracle.csr_offsets(blk.counts)
+        N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
+        scale = float(np.float32(1 / np.sqrt(dh)))
+        d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
+        g = fast.tcsr(d_off, E)
+        dQ = torch.empty((N, H, dh), dtype=tdtype(dt), device="cuda")
+        ge = torch.empty((E, H), device="cuda")
+        ae = torch.empty((E, H), device="cuda")
+        fast.fast_edge_attention_bwd_indexed_coef(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"],
+                                                  d_v, Uv, scale, SLOPE, None, o["dO"], dQ, ge, ae)
+        torch.cuda.synchronize()
+        segs = np.arange(N) if E <= 200_000 else \
+            sample_segments(N, 1500, seed=cfg * 10 + i + 5, include=[0, N - 1])
+        sub_off, eidx = sub_csr(off, segs)
+        sg, ei = torch.as_tensor(segs, device="cuda"), torch.as_tensor(eidx, device="cuda")
+        Q64, dO64 = _host(o["Q"][sg]), _host(o["dO"][sg])
+        K64 = _host(o["K"][torch.as_tensor(kidx[eidx].astype(np.int64), device="cuda")])
+        V64 = _host(o["V"][torch.as_tensor(vidx[eidx].astype(np.int64), device="cuda")])
+        r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(sub_off, Q64, K64, V64, dO64, scale, SLOPE)
+        lseg = np.repeat(np.arange(segs.size), np.diff(sub_off))
+        g64, a64 = ge[ei].double().cpu().numpy(), ae[ei].double().cpu().numpy()
+        dK_formed = torch.from_numpy(g64[:, :, None] * Q64[lseg])
+        dV_formed = torch.from_numpy(a64[:, :, None] * dO64[lseg])
+        what = f"cfg{cfg}/L{i + 1} coefficients"
+        assert_close(dV_formed, r_dV, dt, what + " alpha dO")
+        assert_bwd_close(dQ[sg], dK_formed, sub_off, r_dQ, r_dK, alts, dt, what)
+        # row gradients from the GPU's coefficients against the oracle's fp64
+        # sums of the same coefficients, on a sample of rows (hubs included)
+        for name, idx, U, scal, src in (("K", kidx, Uk, ge, o["Q"]), ("V", vidx, Uv, ae, o["dO"])):
+            occ_off, occ = _occ_gpu(idx, U)
+            rows_grad = _scaled_rows_gpu(occ_off, occ, E, U, d_off, N, H, dh, scal, src)
+            counts_u = np.bincount(idx, minlength=U)
+            pick = np.unique(np.concatenate([np.argsort(counts_u)[-20:],
+                                             np.random.default_rng(i).choice(U, min(U, 300), replace=False)]))
+            sub = np.full(U, -1, np.int32)
+            sub[pick] = np.arange(pick.size, dtype=np.int32)
+            want = oracle.index_add_scaled_rows(sub[idx], off, pick.size, scal.cpu().numpy(), _host(src))
+            assert_close(rows_grad[torch.as_tensor(pick, device="cuda")], want, "f32",
+                         f"{what} d{name} rows")
+        del o, dQ, ge, ae
+        torch.cuda.empty_cache()
