@@ -359,10 +359,30 @@ def indexed_ops(b, step, torch, fast, reps=5, with_oracle=False):
         for x, src in ((bufs["K"], dKe), (bufs["V"], dVe)):
             fast.fast_index_add_rows(x["off"], x["occ"], E, x["U"], F, step.DT, src, x["dst"],
                                      x["wsa"], x["wa"])
-    for f in (fwd, bwd, occ, add):
+
+    # coefficient form: per-edge g and alpha, then row gradients from the
+    # segment rows of Q and dOut
+    ge = torch.empty((E, H), device="cuda")
+    ae = torch.empty((E, H), device="cuda")
+    for name, x in bufs.items():
+        x["ws_s"] = fast.fast_index_add_scaled_rows_workspace(E, x["U"], H, dh)
+        x["wss"] = torch.empty(x["ws_s"], dtype=torch.uint8, device="cuda")
+        x["dst_s"] = torch.empty((x["U"], H, dh), device="cuda")
+
+    def bwd_coef():
+        fast.fast_edge_attention_bwd_indexed_coef(g, H, dh, step.DT, d["Q"], K, ki, Uk, V, vi, Uv,
+                                                  step.scale, SLOPE, lse, d["dO"], dQ, ge, ae)
+
+    def add_scaled():
+        for x, scal, src in ((bufs["K"], ge, d["Q"]), (bufs["V"], ae, d["dO"])):
+            fast.fast_index_add_scaled_rows(x["off"], x["occ"], E, x["U"], d["off"][0], N, H, dh,
+                                            step.DT, scal, src, x["dst_s"], x["wss"], x["ws_s"])
+    for f in (fwd, bwd, occ, add, bwd_coef, add_scaled):
         f()
     t = {k: _events_ms(torch, f, reps) for k, f in (("fwd", fwd), ("bwd", bwd), ("occurrence_lists", occ),
                                                    ("row_sums", add))}
+    t_coef = {k: _events_ms(torch, f, reps) for k, f in (("bwd_coef", bwd_coef),
+                                                         ("scaled_row_sums", add_scaled))}
     # compulsory bytes: each compact row once; per-edge bytes: as the plain operator
     fwd_rows = (2 * N) * F * esz + (Uk + Uv) * F * esz + 8 * E + 4 * N * H + 4 * (N + 1)
     orc = None
@@ -390,6 +410,12 @@ def indexed_ops(b, step, torch, fast, reps=5, with_oracle=False):
         "note": "K and V read through indices into de-duplicated rows; backward writes per-edge "
                 "gradients, then occurrence lists and ordered row sums give the row gradients",
         "edges_per_s": round(E / (sum(t.values()) * 1e-3), 1),
+        "coefficient_form_ms": {k: round(v, 4) for k, v in t_coef.items()},
+        "coefficient_form_note": "backward writes per-edge g and alpha (8H bytes per edge) instead of "
+                                 "dK/dV rows; row gradients sum g*Q[seg] and alpha*dOut[seg] over the "
+                                 "same occurrence lists",
+        "coefficient_form_edges_per_s": round(
+            E / ((t["fwd"] + t["occurrence_lists"] + sum(t_coef.values())) * 1e-3), 1),
     }
     if orc is not None:
         out_entry["oracle"] = orc

@@ -250,13 +250,14 @@ struct OutMulti {
   }
 };
 
-// Row sources of the index-add kernels.  Position p of an occurrence list
+// Row sources of the index-add kernels.  Occurrence j (position p = occ[j])
 // contributes, to chunk c (VE values) of its row's sum:
 //   PlainRows:  src row p;
-//   ScaledRows: scal[p, head] * src row seg[p] -- edge p's coefficient times
-//               the row of the destination segment it belongs to, one head
-//               coefficient per element (a chunk spans at most two heads,
-//               since VE <= dh).
+//   ScaledRows: coefficient seg_scal[j, head] times src row occ_seg[j] --
+//               the coefficient of edge p and the destination segment it
+//               belongs to, laid out in occurrence order by k_coef_permute,
+//               one head coefficient per element (a chunk spans at most two
+//               heads, since VE <= dh).
 // Products are formed in fp64 (exact for fp32 factors), sums in fp64.
 template <typename T, int VE>
 struct PlainRows {
@@ -267,9 +268,9 @@ struct PlainRows {
     float x[VE];
   };
   __device__ void chunk(int) {}
-  __device__ Item fetch(int32_t p, int c) const {
+  __device__ Item fetch(const int32_t* __restrict__ occ, int64_t j, int c) const {
     Item it;
-    VecIO<T, VE>::load(src + clamp64(p, 0, n - 1) * D + c * VE, it.x);
+    VecIO<T, VE>::load(src + clamp64(occ[j], 0, n - 1) * D + c * VE, it.x);
     return it;
   }
   __device__ void add(double (&acc)[VE], const Item& it) const {
@@ -280,12 +281,12 @@ struct PlainRows {
 
 template <typename T, int VE>
 struct ScaledRows {
-  const T* __restrict__ src;        // [N, H, dh]
-  const float* __restrict__ scal;   // [n, H]
-  const int32_t* __restrict__ seg;  // [n]: destination segment of edge p
+  const T* __restrict__ src;          // [N, H, dh]
+  const float* __restrict__ occ_scal; // [n, H], occurrence order
+  const int32_t* __restrict__ occ_seg;// [n], occurrence order
   int D, H, dh;
-  int64_t n, N;
-  int h0, h1, split;                // heads of the chunk; elements t < split use h0
+  int64_t N;
+  int h0, h1, split;                  // heads of the chunk; elements t < split use h0
   struct Item {
     float x[VE];
     float s0, s1;
@@ -296,13 +297,12 @@ struct ScaledRows {
     h1 = (c0 + VE - 1) / dh;
     split = (h0 + 1) * dh - c0;
   }
-  __device__ Item fetch(int32_t p, int c) const {
-    const int64_t e = clamp64(p, 0, n - 1);
-    const int64_t v = clamp64(seg[e], 0, N - 1);
+  __device__ Item fetch(const int32_t* __restrict__, int64_t j, int c) const {
+    const int64_t v = clamp64(occ_seg[j], 0, N - 1);
     Item it;
     VecIO<T, VE>::load(src + v * D + c * VE, it.x);
-    it.s0 = scal[e * H + h0];
-    it.s1 = scal[e * H + h1];
+    it.s0 = occ_scal[j * H + h0];
+    it.s1 = occ_scal[j * H + h1];
     return it;
   }
   __device__ void add(double (&acc)[VE], const Item& it) const {
@@ -320,11 +320,11 @@ __device__ __forceinline__ void ia_sum(const int32_t* __restrict__ occ, int64_t 
   for (; j + IA_UNROLL <= j1; j += IA_UNROLL) {
     typename Src::Item x[IA_UNROLL];
 #pragma unroll
-    for (int r = 0; r < IA_UNROLL; ++r) x[r] = src.fetch(occ[j + r], c);
+    for (int r = 0; r < IA_UNROLL; ++r) x[r] = src.fetch(occ, j + r, c);
 #pragma unroll
     for (int r = 0; r < IA_UNROLL; ++r) src.add(acc, x[r]);
   }
-  for (; j < j1; ++j) src.add(acc, src.fetch(occ[j], c));
+  for (; j < j1; ++j) src.add(acc, src.fetch(occ, j, c));
 }
 
 // Pieces of the long rows: one group of `lanes` lanes per piece q in
@@ -412,8 +412,9 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
   }
 }
 
-// seg[e] = the segment v with off[v] <= e < off[v + 1] (a binary search in
-// the offsets; clamped into [0, N) whatever the offsets hold).
+// seg[e] = the segment v with off[v] <= e < off[v + 1]: a binary search in
+// the offsets per edge, in edge order (neighbouring threads walk the same
+// path); clamped into [0, N) whatever the offsets hold.
 __global__ void __launch_bounds__(IA_THREADS) k_edge_seg(const int32_t* __restrict__ off,
                                                         int64_t N, int64_t n,
                                                         int32_t* __restrict__ seg) {
@@ -425,6 +426,20 @@ __global__ void __launch_bounds__(IA_THREADS) k_edge_seg(const int32_t* __restri
     if (int64_t(off[mid]) <= e) lo = mid; else hi = mid - 1;
   }
   seg[e] = int32_t(lo);
+}
+
+// Occurrence order for the scaled sums: for every valid occurrence j (below
+// occ_off[num_rows]) of edge e = occ[j], occ_seg[j] = seg[e] and
+// occ_scal[j, :] = scal[e, :] (positions clamped into range).
+__global__ void __launch_bounds__(IA_THREADS) k_coef_permute(
+    const int32_t* __restrict__ occ, const int32_t* __restrict__ occ_off, int64_t num_rows,
+    int64_t n, const int32_t* __restrict__ seg, const float* __restrict__ scal, int H,
+    int32_t* __restrict__ occ_seg, float* __restrict__ occ_scal) {
+  const int64_t j = int64_t(blockIdx.x) * IA_THREADS + threadIdx.x;
+  if (j >= clamp64(occ_off[num_rows], 0, n)) return;
+  const int64_t e = clamp64(occ[j], 0, n - 1);
+  occ_seg[j] = seg[e];
+  for (int h = 0; h < H; ++h) occ_scal[j * H + h] = scal[e * H + h];
 }
 
 struct IaWs {
@@ -592,10 +607,15 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
   return check_launch(fn);
 }
 
-static size_t ias_layout(int64_t n, int64_t num_rows, int D, char* base, int32_t** seg, IaWs* ws) {
+static size_t ias_layout(int64_t n, int64_t num_rows, int H, int D, char* base, int32_t** seg,
+                         int32_t** occ_seg, float** occ_scal, IaWs* ws) {
   const size_t seg_bytes = align_up(size_t(n) * 4, 256);
+  const size_t scal_bytes = align_up(size_t(n) * size_t(H) * 4, 256);
   if (seg) *seg = reinterpret_cast<int32_t*>(base);
-  return seg_bytes + ia_layout(n, num_rows, D, base ? base + seg_bytes : nullptr, ws);
+  if (occ_seg) *occ_seg = reinterpret_cast<int32_t*>(base + seg_bytes);
+  if (occ_scal) *occ_scal = reinterpret_cast<float*>(base + 2 * seg_bytes);
+  const size_t head = 2 * seg_bytes + scal_bytes;
+  return head + ia_layout(n, num_rows, D, base ? base + head : nullptr, ws);
 }
 
 extern "C" size_t fast_index_add_scaled_rows_workspace(int64_t n, int64_t num_rows, int H, int dh) {
@@ -603,7 +623,7 @@ extern "C" size_t fast_index_add_scaled_rows_workspace(int64_t n, int64_t num_ro
   const int D = H * dh;
   if (n < 0 || num_rows < 0 || n >= (int64_t(1) << 31) || num_rows >= (int64_t(1) << 31) - 1)
     return 0;
-  return ias_layout(n, num_rows, D, nullptr, nullptr, nullptr);
+  return ias_layout(n, num_rows, H, D, nullptr, nullptr, nullptr, nullptr, nullptr);
 }
 
 extern "C" fast_status_t fast_index_add_scaled_rows(
@@ -632,16 +652,20 @@ extern "C" fast_status_t fast_index_add_scaled_rows(
     return fail(FAST_ERR_UNSUPPORTED, "%s: src/dst/scal misaligned", fn);
   const int VE = ia_vector(D, dh, src, esz, dst);   // a chunk spans at most two heads
   hipStream_t st = static_cast<hipStream_t>(stream);
-  int32_t* seg = nullptr;
+  int32_t *seg = nullptr, *occ_seg = nullptr;
+  float* occ_scal = nullptr;
   IaWs w;
-  ias_layout(n, num_rows, D, static_cast<char*>(ws), &seg, &w);
-  if (n > 0)
-    hipLaunchKernelGGL(k_edge_seg, dim3(uint32_t((n + IA_THREADS - 1) / IA_THREADS)), dim3(IA_THREADS),
-                       0, st, dst_offsets, num_dst, n, seg);
+  ias_layout(n, num_rows, H, D, static_cast<char*>(ws), &seg, &occ_seg, &occ_scal, &w);
+  if (n > 0) {
+    const dim3 grid{uint32_t((n + IA_THREADS - 1) / IA_THREADS)};
+    hipLaunchKernelGGL(k_edge_seg, grid, dim3(IA_THREADS), 0, st, dst_offsets, num_dst, n, seg);
+    hipLaunchKernelGGL(k_coef_permute, grid, dim3(IA_THREADS), 0, st, occ, occ_off, num_rows, n, seg,
+                       scal, H, occ_seg, occ_scal);
+  }
   hipError_t e = hipSuccess;
 #define FAST_IAS(T_, VE_)                                                                          \
   e = ia_launch<VE_>(occ_off, occ, n, num_rows, D,                                                 \
-                     ScaledRows<T_, VE_>{static_cast<const T_*>(src), scal, seg, D, H, dh, n,      \
+                     ScaledRows<T_, VE_>{static_cast<const T_*>(src), occ_scal, occ_seg, D, H, dh, \
                                          num_dst, 0, 0, 0},                                        \
                      w, dst, st)
   if (src_dtype == FAST_F32) {
