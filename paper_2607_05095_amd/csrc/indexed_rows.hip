@@ -250,6 +250,14 @@ struct OutMulti {
   }
 };
 
+// Eight fp32 values of a row sum (the bf16 sources' widest vector).
+template <> struct VecIO<float, 8> {
+  __device__ static void store(float* p, const float* x) {
+    VecIO<float, 4>::store(p, x);
+    VecIO<float, 4>::store(p + 4, x + 4);
+  }
+};
+
 // Row sources of the index-add kernels.  Occurrence j (position p = occ[j])
 // contributes, to chunk c (VE values) of its row's sum:
 //   PlainRows:  src row p;
@@ -550,9 +558,10 @@ static hipError_t ia_launch(const int32_t* occ_off, const int32_t* occ, int64_t 
   return hipGetLastError();
 }
 
-// Widest vector (4, 2 or 1 values) that divides D, is at most `cap` and fits
-// the alignment of both row pointers.
+// Widest vector (8 values for bf16 sources, else 4, 2 or 1) that divides D,
+// is at most `cap` and fits the alignment of both row pointers.
 static int ia_vector(int D, int cap, const void* src, int esz, const float* dst) {
+  if (esz == 2 && 8 <= cap && D % 8 == 0 && aligned(src, 16) && aligned(dst, 16)) return 8;
   for (int v : {4, 2})
     if (v <= cap && D % v == 0 && aligned(src, size_t(v) * esz) && aligned(dst, size_t(v) * 4))
       return v;
@@ -590,7 +599,7 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
   const int esz = elem_size(src_dtype);
   if (!aligned(src, size_t(esz)) || !aligned(dst, 4))
     return fail(FAST_ERR_UNSUPPORTED, "%s: src/dst misaligned", fn);
-  const int VE = ia_vector(D, 4, src, esz, dst);
+  const int VE = ia_vector(D, 8, src, esz, dst);
   hipStream_t st = static_cast<hipStream_t>(stream);
   IaWs w;
   ia_layout(n, num_rows, D, static_cast<char*>(ws), &w);
@@ -600,7 +609,8 @@ extern "C" fast_status_t fast_index_add_rows(const int32_t* occ_off, const int32
   if (src_dtype == FAST_F32) {
     if (VE == 4) FAST_IA(float, 4); else if (VE == 2) FAST_IA(float, 2); else FAST_IA(float, 1);
   } else {
-    if (VE == 4) FAST_IA(uint16_t, 4); else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
+    if (VE == 8) FAST_IA(uint16_t, 8); else if (VE == 4) FAST_IA(uint16_t, 4);
+    else if (VE == 2) FAST_IA(uint16_t, 2); else FAST_IA(uint16_t, 1);
   }
 #undef FAST_IA
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
@@ -671,7 +681,8 @@ extern "C" fast_status_t fast_index_add_scaled_rows(
   if (src_dtype == FAST_F32) {
     if (VE == 4) FAST_IAS(float, 4); else if (VE == 2) FAST_IAS(float, 2); else FAST_IAS(float, 1);
   } else {
-    if (VE == 4) FAST_IAS(uint16_t, 4); else if (VE == 2) FAST_IAS(uint16_t, 2); else FAST_IAS(uint16_t, 1);
+    if (VE == 8) FAST_IAS(uint16_t, 8); else if (VE == 4) FAST_IAS(uint16_t, 4);
+    else if (VE == 2) FAST_IAS(uint16_t, 2); else FAST_IAS(uint16_t, 1);
   }
 #undef FAST_IAS
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
