@@ -679,6 +679,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-pipelined", dest="pipelined", action="store_false",
                     help="skip the second timing of the steps software-pipelined over two streams")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the serial step captured once as a HIP graph and replayed")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -738,6 +740,17 @@ def main():
     if args.pipelined:
         ms_pipe = timed(lambda: step.run_pipelined(args.steps, side))
         log(f"{ms_pipe:.3f} ms/step (pipelined)")
+
+    # optionally, the serial step captured once as a HIP graph, replayed K times
+    ms_graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step.run_serial()
+        graph.replay()
+        torch.cuda.synchronize()
+        ms_graph = timed(lambda: [graph.replay() for _ in range(args.steps)])
+        log(f"{ms_graph:.3f} ms/step (graph replay)")
 
     # per-operator breakdown: separate serial steps, every operator timed
     rec_all = {}
@@ -802,6 +815,12 @@ def main():
             "value": b.sampled_edges / (ms_pipe * 1e-3),
             "schedule": "prep of batch i+1 on a second stream overlaps attention of batch i; "
                         "attention(i) waits for prep(i); double-buffered prep outputs",
+        }
+    if ms_graph is not None:
+        result["graph"] = {
+            "ms_per_step": round(ms_graph, 4),
+            "value": b.sampled_edges / (ms_graph * 1e-3),
+            "schedule": "the serial step captured once as a HIP graph, replayed K times",
         }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

@@ -91,3 +91,39 @@ def test_pipelined_schedule_leaves_the_serial_results():
     piped1 = _snapshot(step, 1)
     for a, c in zip(serial, piped1):
         assert torch.equal(a, c)
+
+
+@pytest.mark.parametrize("cfg", [0, 2])
+def test_graph_replays_match_the_eager_step(cfg):
+    """One step captured as a HIP graph (every call takes caller buffers and
+    enqueues only kernels: no allocation, synchronisation or memset) gives
+    bitwise the eager step's results on every replay, with eager work and
+    synchronisations between the replays."""
+    print(f"[parity] bench step as a graph cfg={cfg}", flush=True)
+    b = make_batch(cfg)
+    step = bench.Step(b, torch, fast)
+    step.run_serial()
+    torch.cuda.synchronize()
+    eager = _snapshot(step, 0)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step.run_serial()                       # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step.run_serial()
+    for rep in range(3):
+        for x in step.blocks:                   # poison, eagerly, between replays
+            for k in ("out", "dQ", "dK", "dV"):
+                x[k].fill_(float("nan"))
+            x["te"][0].fill_(float("nan"))
+        for x in (step.node[0], step.edge[0]):
+            x["rows"].fill_(float("nan"))
+            x["uni"].fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, c in zip(eager, _snapshot(step, 0)):
+            assert torch.equal(a, c), f"replay {rep}"
