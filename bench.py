@@ -686,7 +686,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding "
+        print(json.dumps({"error": "bench.py runs on one GPU only; the multi-GPU sharding "
                                    "design is described but not built", "n_gpus": args.gpus}))
         sys.exit(2)
 

@@ -57,7 +57,7 @@ extern "C" {
 typedef enum {
   FAST_OK = 0,
   FAST_ERR_INVALID_ARG = 1,  /* NULL required pointer, negative size, bad enum */
-  FAST_ERR_UNSUPPORTED = 2,  /* shape/dtype/alignment this build does not handle */
+  FAST_ERR_UNSUPPORTED = 2,  /* shape/dtype/alignment the library does not handle */
   FAST_ERR_WORKSPACE = 3,    /* ws NULL or ws_bytes smaller than the query */
   FAST_ERR_HIP = 4           /* a HIP launch or runtime call failed */
 } fast_status_t;
