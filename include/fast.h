@@ -191,9 +191,11 @@ fast_status_t fast_sample_recent(const fast_temporal_graph_t* g, const int64_t* 
  * row saves once each batch is compressed).  freq is ACCUMULATED into, so
  * batches may be counted over several calls; the caller zeroes it first.
  * ids: device int64; batch_offsets: HOST int64 [num_batches+1],
- * non-decreasing; freq: device int32 [id_bound].  One launch per batch.
+ * non-decreasing; freq: device int32 [id_bound].  A few launches per batch.
  * Limits: id_bound < 2^32, num_batches < 2^31 - 1.
- * Workspace: fast_access_count_workspace(id_bound) bytes (a batch stamp per id).
+ * Workspace: fast_access_count_workspace(id_bound) bytes, 16-byte aligned
+ *   (a batch stamp per id; for dense universes, id_bound at most 32 times the
+ *   mean batch size, the same space holds a byte map per batch instead).
  * ------------------------------------------------------------------------ */
 size_t fast_access_count_workspace(int64_t id_bound);
 fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets,

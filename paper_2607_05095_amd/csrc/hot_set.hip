@@ -21,6 +21,9 @@
 // pair (ids above T, ids at T) then gives every id its position among the
 // selected ids (above-T prefix + min(at-T prefix, R)), which is both the slot
 // in the id-ordered hot list and the value of the slot map.
+#include <cstdlib>
+#include <cstring>
+
 #include "scan.h"
 
 namespace fast {
@@ -91,6 +94,51 @@ __global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __re
     }
     __syncthreads();
   }
+}
+
+// Dense universes (id_bound at most AC_BYTEMAP_RATIO times the mean batch
+// size): each batch marks its ids in a byte map with plain stores (repeats
+// store the same 1), then one streaming pass adds the map into freq -- no
+// atomics at all.  The map lives in the stamp workspace (1 byte per id of the
+// 4 there) and is cleared before every batch.
+constexpr int64_t AC_BYTEMAP_RATIO = 32;
+
+__global__ void __launch_bounds__(HS_THREADS) k_ac_clear(uint4* p, int64_t n16) {
+  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n16;
+       i += int64_t(gridDim.x) * HS_THREADS)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+__global__ void __launch_bounds__(HS_THREADS) k_ac_mark(const int64_t* __restrict__ ids, int64_t n,
+                                                       int64_t id_bound, uint8_t* map) {
+  const int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x;
+  if (i >= n) return;
+  const int64_t x = ids[i];
+  if (x >= 0 && x < id_bound) map[x] = 1;
+}
+
+// freq[x] += map[x], four ids per thread; bytes past id_bound are never set.
+__global__ void __launch_bounds__(HS_THREADS) k_ac_accumulate(const uint32_t* __restrict__ map4,
+                                                             int64_t n4, int32_t* freq) {
+  for (int64_t t = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; t < n4;
+       t += int64_t(gridDim.x) * HS_THREADS) {
+    const uint32_t m = map4[t];
+    if (m == 0u) continue;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if ((m >> (8 * k)) & 0xffu) freq[4 * t + k] += 1;
+  }
+}
+
+static bool use_count_bytemap(int64_t total_ids, int64_t num_batches, int64_t id_bound) {
+  static const int mode = [] {
+    const char* e = std::getenv("FAST_COUNT_MARK");   // tuning override: bytemap | stamp
+    if (!e) return 0;
+    return std::strcmp(e, "bytemap") == 0 ? 1 : std::strcmp(e, "stamp") == 0 ? 2 : 0;
+  }();
+  if (mode) return mode == 1;
+  const int64_t mean = num_batches > 0 ? total_ids / num_batches : 0;
+  return id_bound <= AC_BYTEMAP_RATIO * (mean > 0 ? mean : 1);
 }
 
 // ------------------------------------------------------------------ selection
@@ -295,6 +343,22 @@ extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* ba
   if (!aligned(ws, 4) || !aligned(freq, 4))
     return fail(FAST_ERR_UNSUPPORTED, "%s: freq or workspace not 4-byte aligned", fn);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (use_count_bytemap(batch_offsets[num_batches] - batch_offsets[0], num_batches, id_bound)) {
+    if (!aligned(ws, 16)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 16-byte aligned", fn);
+    uint8_t* map = static_cast<uint8_t*>(ws);
+    const int64_t n16 = (id_bound + 15) / 16;          // within the id_bound * 4 + 256 bytes
+    for (int64_t k = 0; k < num_batches; ++k) {
+      const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
+      if (n == 0) continue;
+      hipLaunchKernelGGL(k_ac_clear, dim3(grid_for(n16, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
+                         reinterpret_cast<uint4*>(map), n16);
+      hipLaunchKernelGGL(k_ac_mark, dim3(uint32_t((n + HS_THREADS - 1) / HS_THREADS)), dim3(HS_THREADS),
+                         0, st, ids + batch_offsets[k], n, id_bound, map);
+      hipLaunchKernelGGL(k_ac_accumulate, dim3(grid_for(n16 * 4, HS_THREADS * 4)), dim3(HS_THREADS), 0,
+                         st, reinterpret_cast<const uint32_t*>(map), n16 * 4, freq);
+    }
+    return check_launch(fn);
+  }
   int32_t* stamp = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(id_bound, HS_THREADS * 8)), dim3(HS_THREADS), 0,
                      st, stamp, id_bound, 0);

@@ -80,17 +80,19 @@ def test_access_count_and_selection_vs_oracle(cfg, k):
         _check_slots(se, he, eb)
 
 
-def test_access_count_repeats_invalid_ids_and_accumulation():
-    _announce("access count edge cases")
-    bound = 1000
-    batches = [np.array([5, 5, 5, 999, 0, -1, 1000, 7 << 40], np.int64),
+@pytest.mark.parametrize("bound", [1000, 40])
+def test_access_count_repeats_invalid_ids_and_accumulation(bound):
+    # bound 1000 over ~4 ids a batch takes the stamp path, bound 40 the byte map
+    _announce(f"access count edge cases bound={bound}")
+    top = bound - 1
+    batches = [np.array([5, 5, 5, top, 0, -1, bound, 7 << 40], np.int64),
                np.zeros(0, np.int64), np.array([5, 3, 3], np.int64)]
     f = _count_gpu(batches, bound)
-    f = _count_gpu([np.array([3, 998], np.int64)], bound, freq=f)      # accumulates
-    want = oracle.access_count([np.array([3, 998])], bound,
+    f = _count_gpu([np.array([3, top - 1], np.int64)], bound, freq=f)      # accumulates
+    want = oracle.access_count([np.array([3, top - 1])], bound,
                                freq=oracle.access_count(batches, bound))
     assert np.array_equal(f.cpu().numpy(), want)
-    assert f[5].item() == 2 and f[3].item() == 2 and f[999].item() == 1
+    assert f[5].item() == 2 and f[3].item() == 2 and f[top].item() == 1
 
 
 def test_selection_edge_cases():
