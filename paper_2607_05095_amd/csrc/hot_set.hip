@@ -253,39 +253,118 @@ __global__ void __launch_bounds__(HS_THREADS) k_hs_threshold(
   }
 }
 
-// Packed scan item: high word = count above T, low word = count equal to T.
-struct InAboveAt {
-  const int32_t* f;
-  int32_t max_freq;
-  const HsParams* prm;
-  __device__ uint64_t operator()(int64_t i) const {
-    const int32_t c = clamp_count(f[i], max_freq), T = prm->T;
-    return (c > T ? (uint64_t(1) << 32) : 0) | (c == T ? 1u : 0u);
+// Positions of the selected ids, in two passes over the counts with 16-byte
+// accesses.  Each id carries a packed pair (high word: its count is above T,
+// low word: its count equals T).  Pass A adds the pairs up per tile of
+// HS_SEL_TILE ids; the tile sums are scanned (exclusive); pass B recomputes
+// the pairs and scans each tile in id order -- four rounds of 1024 ids, four
+// consecutive ids per thread -- from the tile's prefix.  An id is selected if
+// it is above T, or at T among the first R (of its kind) in id order; its
+// position, (ids above T before it) + min(ids at T before it, R), is both its
+// slot in the id-ordered hot list and its slot-map value.
+constexpr int HS_SEL_ROUNDS = 4;
+constexpr int HS_SEL_TILE = HS_THREADS * 4 * HS_SEL_ROUNDS;   // 4096 ids
+
+__device__ __forceinline__ uint64_t sel_pair(int32_t raw, int32_t max_freq, int32_t T) {
+  const int32_t c = clamp_count(raw, max_freq);
+  return (c > T ? (uint64_t(1) << 32) : 0) | (c == T ? 1u : 0u);
+}
+
+// The pairs of ids i0 .. i0+3 (0 for positions at or past n).
+__device__ __forceinline__ void sel_pairs4(const int32_t* __restrict__ f, int64_t n, int64_t i0,
+                                           bool vec, int32_t max_freq, int32_t T, uint64_t (&p)[4]) {
+  if (vec && i0 + 3 < n) {
+    const int4 v = *reinterpret_cast<const int4*>(f + i0);
+    p[0] = sel_pair(v.x, max_freq, T);
+    p[1] = sel_pair(v.y, max_freq, T);
+    p[2] = sel_pair(v.z, max_freq, T);
+    p[3] = sel_pair(v.w, max_freq, T);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) p[k] = i0 + k < n ? sel_pair(f[i0 + k], max_freq, T) : 0;
   }
+}
+
+__global__ void __launch_bounds__(HS_THREADS) k_sel_tiles(const int32_t* __restrict__ f, int64_t n,
+                                                         int32_t max_freq,
+                                                         const HsParams* __restrict__ prm,
+                                                         uint64_t* __restrict__ tsum) {
+  __shared__ uint64_t lds4[4];
+  const int32_t T = prm->T;
+  const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
+  const int64_t base = int64_t(blockIdx.x) * HS_SEL_TILE;
+  uint64_t s = 0;
+#pragma unroll
+  for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
+    uint64_t p[4];
+    sel_pairs4(f, n, base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4, vec, max_freq, T, p);
+    s += p[0] + p[1] + p[2] + p[3];
+  }
+  uint64_t total;
+  block_exclusive_scan<uint64_t>(s, lds4, total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(HS_THREADS) k_sel_write(
+    const int32_t* __restrict__ f, int64_t n, int32_t max_freq, const HsParams* __restrict__ prm,
+    bool edges, const uint64_t* __restrict__ tprefix, int64_t cap, int64_t* __restrict__ hot,
+    int32_t* __restrict__ slot) {
+  __shared__ uint64_t lds4[4];
+  const int32_t T = prm->T;
+  const int64_t R = edges ? prm->R_e : prm->R_v;
+  const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
+  const bool svec = slot && (reinterpret_cast<uintptr_t>(slot) & 15u) == 0;
+  const int64_t base = int64_t(blockIdx.x) * HS_SEL_TILE;
+  uint64_t run = tprefix[blockIdx.x];
+  for (int r = 0; r < HS_SEL_ROUNDS; ++r) {     // every thread reaches every block scan
+    const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
+    uint64_t p[4];
+    sel_pairs4(f, n, i0, vec, max_freq, T, p);
+    uint64_t total;
+    uint64_t pre = run + block_exclusive_scan<uint64_t>(p[0] + p[1] + p[2] + p[3], lds4, total);
+    int32_t out[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t above = int64_t(pre >> 32), at = int64_t(pre & 0xffffffffu);
+      const bool sel = (p[k] >> 32) != 0 || ((p[k] & 1u) != 0 && at < R);
+      const int64_t pos = above + (at < R ? at : R);
+      out[k] = sel ? int32_t(pos) : -1;
+      if (sel && hot && pos < cap) hot[pos] = i0 + k;
+      pre += p[k];
+    }
+    if (slot) {
+      if (svec && i0 + 3 < n) {
+        *reinterpret_cast<int4*>(slot + i0) = make_int4(out[0], out[1], out[2], out[3]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (i0 + k < n) slot[i0 + k] = out[k];
+      }
+    }
+    run += total;
+  }
+}
+
+struct InU64 {
+  const uint64_t* p;
+  __device__ uint64_t operator()(int64_t i) const { return p[i]; }
 };
-struct OutHot {
-  const HsParams* prm;
-  bool edges;
-  int64_t cap;         // capacity of hot
-  int64_t* hot;        // id-ordered hot list, or NULL
-  int32_t* slot;       // slot map, or NULL
-  __device__ void operator()(int64_t i, uint64_t prefix, uint64_t v) const {
-    const int64_t R = edges ? prm->R_e : prm->R_v;
-    const int64_t above = int64_t(prefix >> 32), at = int64_t(prefix & 0xffffffffu);
-    const bool sel = (v >> 32) != 0 || ((v & 1u) != 0 && at < R);
-    const int64_t pos = above + (at < R ? at : R);
-    if (slot) slot[i] = sel ? int32_t(pos) : -1;
-    if (sel && hot && pos < cap) hot[pos] = i;
-  }
+struct OutU64InPlace {
+  uint64_t* p;
+  __device__ void operator()(int64_t i, uint64_t prefix, uint64_t) const { p[i] = prefix; }
 };
 
 struct HsWs {
   uint32_t* hv;
   uint32_t* he;
   HsParams* prm;
+  uint64_t* tsum_v;   // per-tile pair sums, then their exclusive prefixes
+  uint64_t* tsum_e;
   void* scan_v;
   void* scan_e;
 };
+
+static int64_t sel_tiles(int64_t n) { return (n + HS_SEL_TILE - 1) / HS_SEL_TILE; }
 
 static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, HsWs* ws) {
   size_t off = 0;
@@ -297,12 +376,16 @@ static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, Hs
   char* hv = take(size_t(max_freq + 1) * 4);
   char* he = take(size_t(max_freq + 1) * 4);
   char* pr = take(sizeof(HsParams));
-  char* sv = take(scan_workspace<uint64_t>(nv));
-  char* se = take(scan_workspace<uint64_t>(ne));
+  char* tv = take(size_t(sel_tiles(nv)) * 8);
+  char* te = take(size_t(sel_tiles(ne)) * 8);
+  char* sv = take(scan_workspace<uint64_t>(sel_tiles(nv)));
+  char* se = take(scan_workspace<uint64_t>(sel_tiles(ne)));
   if (ws) {
     ws->hv = reinterpret_cast<uint32_t*>(hv);
     ws->he = reinterpret_cast<uint32_t*>(he);
     ws->prm = reinterpret_cast<HsParams*>(pr);
+    ws->tsum_v = reinterpret_cast<uint64_t*>(tv);
+    ws->tsum_e = reinterpret_cast<uint64_t*>(te);
     ws->scan_v = sv;
     ws->scan_e = se;
   }
@@ -416,16 +499,20 @@ extern "C" fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_
                      budget, num_nodes, num_edges, w.prm, num_hot_v, num_hot_e);
   const int64_t B = budget < num_nodes + num_edges ? budget : num_nodes + num_edges;
   hipError_t e = hipSuccess;
-  if (num_nodes > 0 && (hot_v || slot_v))
-    e = scan_launch<InAboveAt, OutHot, uint64_t>(
-        InAboveAt{freq_v, max_freq, w.prm},
-        OutHot{w.prm, false, B < num_nodes ? B : num_nodes, hot_v, slot_v}, num_nodes, w.scan_v,
-        nullptr, nullptr, st);
-  if (e == hipSuccess && num_edges > 0 && (hot_e || slot_e))
-    e = scan_launch<InAboveAt, OutHot, uint64_t>(
-        InAboveAt{freq_e, max_freq, w.prm},
-        OutHot{w.prm, true, B < num_edges ? B : num_edges, hot_e, slot_e}, num_edges, w.scan_e,
-        nullptr, nullptr, st);
+  auto select = [&](const int32_t* f, int64_t n, bool edges, uint64_t* tsum, void* scan_ws,
+                    int64_t* hot, int32_t* slot) {
+    if (n == 0 || (!hot && !slot) || e != hipSuccess) return;
+    const int64_t tiles = sel_tiles(n);
+    hipLaunchKernelGGL(k_sel_tiles, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
+                       w.prm, tsum);
+    e = scan_launch<InU64, OutU64InPlace, uint64_t>(InU64{tsum}, OutU64InPlace{tsum}, tiles, scan_ws,
+                                                   nullptr, nullptr, st);
+    if (e != hipSuccess) return;
+    hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
+                       w.prm, edges, tsum, B < n ? B : n, hot, slot);
+  };
+  select(freq_v, num_nodes, false, w.tsum_v, w.scan_v, hot_v, slot_v);
+  select(freq_e, num_edges, true, w.tsum_e, w.scan_e, hot_e, slot_e);
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   return check_launch(fn);
 }
