@@ -405,6 +405,25 @@ def test_dedup_edge_cases(case):
         assert nm == u and np.array_equal(miss[:nm].cpu().numpy(), np.arange(u))
 
 
+@pytest.mark.parametrize("bound,n", [(2**29, 3000), (2**33 + 5, 50_000), (3 * 10**7 + 13, 300_000),
+                                     (40_000, 1200)])
+def test_dedup_sparse_universes(bound, n):
+    """Universes far larger than the batch (marking through the per-workgroup
+    LDS hash and one global OR per touched word), up to 2^33 ids, with
+    Zipf-like hot ids (a few ids repeated in every workgroup's share), ids at
+    both ends of the universe, and many workgroups."""
+    _announce(f"dedup sparse universe bound={bound} n={n}")
+    r = np.random.default_rng(bound % 1000 + n)
+    hot = r.integers(0, bound, 16)
+    ids = np.where(r.random(n) < 0.4, hot[r.integers(0, 16, n)], r.integers(0, bound, n)).astype(np.int64)
+    ids[:4] = [0, bound - 1, bound - 1, 0]
+    uni, inv, u, _, _, nm = _dedup(ids, bound, None)
+    ref_uni, ref_inv = oracle.dedup(ids)
+    assert u == ref_uni.size and np.array_equal(uni, ref_uni)
+    assert np.array_equal(inv, ref_inv)
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("D,dt", [(4, "bf16"), (12, "bf16"), (44, "bf16"), (172, "bf16"), (252, "bf16"),
                                   (260, "bf16"), (508, "bf16"), (6, "f32"), (86, "f32"), (126, "f32")])
 def test_gather_rows_of_odd_eight_byte_width(D, dt):
