@@ -6,16 +6,24 @@
 // distinct set is a bitmap over that universe; the rank of an id is the
 // exclusive popcount prefix of the bitmap words below it plus a popcount
 // inside its word.  This is exact and deterministic whatever the id order or
-// thread interleaving, and needs no sort.  The bitmap is built one of two
+// thread interleaving, and needs no sort.  The bitmap is built one of three
 // ways, chosen from (n, id_bound) alone:
 //   * byte map (id_bound <= 32 n): every id stores 1 into its own byte with a
 //     plain store (racing stores of the same value are benign), then one
 //     pass packs 32 bytes into each bitmap word -- O(n + id_bound) bytes,
 //     no atomics at all;
-//   * hashed atomics (sparse universes): ids are merged per workgroup in an
-//     LDS hash table and each touched word gets one global atomicOr.  Rows are then copied with
-// 16/8/4-byte vector moves, one thread per vector of a row, from the table
-// slot that the optional cache slot map names.
+//   * buckets (sparse universes): each workgroup merges its 2048 ids per
+//     bitmap word in an LDS hash table, counts its merged words per universe
+//     bucket (at most 4096 buckets of at most 2^19 ids), and after a scan of
+//     those counts lists them grouped by bucket; one workgroup per bucket
+//     then ORs its list into an LDS bitmap and writes the bucket's word
+//     records, ranked inside the bucket, and a scan over the bucket totals
+//     gives each bucket's base rank.  Only LDS atomics; every word record is
+//     written once, with no clearing pass;
+//   * hashed atomics (universes too large for buckets): the same LDS merge,
+//     then one global atomicOr per merged word into a cleared bitmap.
+// Rows are then copied with 16/8/4-byte vector moves, one thread per vector
+// of a row, from the table slot that the optional cache slot map names.
 #include <cstdlib>
 #include <cstring>
 
@@ -28,14 +36,60 @@ constexpr int DD_THREADS = 256;
 // Byte-map marking when the universe is at most this many times the batch.
 constexpr int64_t BYTEMAP_RATIO = 32;
 
-static bool use_bytemap(int64_t n, int64_t id_bound) {
+// Bucketed marking: a bucket spans 2^bits ids, bits in [10, 19] chosen so
+// that there are about 512 buckets (its bitmap of 32 .. 16384 words fits in
+// 64 KB of LDS); at most 4096 buckets, and at most 2^24 (bucket, workgroup)
+// counts.
+constexpr int BK_MIN_BITS = 10;
+constexpr int BK_MAX_BITS = 19;
+constexpr int64_t BK_TARGET_BUCKETS = 512;
+constexpr int64_t BK_MAX_BUCKETS = 4096;
+constexpr int64_t BK_MAX_COUNTS = int64_t(1) << 24;
+constexpr int BK_MAX_WORDS = 1 << (BK_MAX_BITS - 5);
+
+// Ids merged per workgroup in the LDS word hash (bucketed and hashed marking).
+constexpr int MARK_ITEMS = 8;
+constexpr int MARK_IDS = DD_THREADS * MARK_ITEMS;
+constexpr int MARK_SLOTS = 2 * MARK_IDS;        // load factor <= 1/2: probing always ends
+static_assert(MARK_SLOTS == 4096, "the hash below yields 12 bits");
+constexpr uint32_t MARK_EMPTY = 0xffffffffu;     // never a word index (W <= 2^30)
+
+enum MarkPath { MARK_BYTES, MARK_BUCKETS, MARK_HASH };
+
+struct BkPlan {
+  int bits = 0;       // 0: no bucketed plan for this universe and batch
+  int64_t B = 0;      // buckets
+  int64_t nblk = 0;   // merging workgroups (MARK_IDS ids each)
+};
+
+static BkPlan bucket_plan(int64_t n, int64_t id_bound) {
+  BkPlan p;
+  int bits = BK_MIN_BITS;
+  while (bits < BK_MAX_BITS && ((id_bound + (int64_t(1) << bits) - 1) >> bits) > BK_TARGET_BUCKETS)
+    ++bits;
+  const int64_t B = (id_bound + (int64_t(1) << bits) - 1) >> bits;
+  const int64_t nblk = (n + MARK_IDS - 1) / MARK_IDS;
+  if (B > BK_MAX_BUCKETS || B * nblk > BK_MAX_COUNTS) return p;
+  p.bits = bits;
+  p.B = B;
+  p.nblk = nblk;
+  return p;
+}
+
+static MarkPath mark_path(int64_t n, int64_t id_bound, BkPlan* plan) {
   static const int mode = [] {
-    const char* e = std::getenv("FAST_DEDUP_MARK");   // tuning override: bytemap | hash
+    const char* e = std::getenv("FAST_DEDUP_MARK");   // tuning override: bytemap | bucket | hash
     if (!e) return 0;
-    return std::strcmp(e, "bytemap") == 0 ? 1 : std::strcmp(e, "hash") == 0 ? 2 : 0;
+    return std::strcmp(e, "bytemap") == 0 ? 1 : std::strcmp(e, "hash") == 0 ? 2
+         : std::strcmp(e, "bucket") == 0 ? 3 : 0;
   }();
-  if (mode) return mode == 1;
-  return id_bound <= BYTEMAP_RATIO * (n > 0 ? n : 1);
+  const BkPlan p = bucket_plan(n, id_bound);
+  if (plan) *plan = p;
+  if (mode == 1) return MARK_BYTES;
+  if (mode == 2) return MARK_HASH;
+  if (mode == 3) return p.bits ? MARK_BUCKETS : MARK_HASH;
+  if (id_bound <= BYTEMAP_RATIO * (n > 0 ? n : 1)) return MARK_BYTES;
+  return p.bits ? MARK_BUCKETS : MARK_HASH;
 }
 
 // Word record w: .x = bits of ids 32w .. 32w+31, .y = number of set bits in
@@ -44,30 +98,51 @@ static bool use_bytemap(int64_t n, int64_t id_bound) {
 struct DedupWs {
   uint8_t* bytemap;   // [32 W] (byte-map marking only)
   uint2* words;       // [W] word records
-  void* scan_w;       // scan workspace over W words
+  void* scan_w;       // scan workspace over W words (byte map, hash)
   uint8_t* flags;     // [n] miss flags
   void* scan_n;       // scan workspace over n flags
+  uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup), then list offsets
+  void* bk_scan_c;    // scan workspace over the counts
+  uint2* bk_list;     // [<= n] (word inside the bucket, bits), grouped by bucket
+  uint32_t* bk_base;  // [B] distinct ids per bucket, then the bucket's base rank
+  void* bk_scan_b;    // scan workspace over the buckets
+  int32_t* bk_listed; // number of list entries
 };
 
 static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws) {
   const int64_t W = (id_bound + 31) / 32;
+  BkPlan p;
+  const MarkPath path = mark_path(n, id_bound, &p);
+  const bool bk = path == MARK_BUCKETS;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
     off += align_up(bytes, 256);
     return base ? base + o : nullptr;
   };
-  char* by = take(use_bytemap(n, id_bound) ? size_t(W) * 32 : 0);
+  char* by = take(path == MARK_BYTES ? size_t(W) * 32 : 0);
   char* wr = take(size_t(W) * 8);
-  char* sw = take(scan_workspace(W));
+  char* sw = take(bk ? 0 : scan_workspace(W));
   char* fl = take(size_t(n));
   char* sn = take(scan_workspace(n));
+  char* bc = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
+  char* bs = take(bk ? scan_workspace(p.B * p.nblk) : 0);
+  char* bl = take(bk ? size_t(n) * 8 : 0);
+  char* bb = take(bk ? size_t(p.B) * 4 : 0);
+  char* bt = take(bk ? scan_workspace(p.B) : 0);
+  char* bn = take(bk ? 4 : 0);
   if (ws) {
     ws->bytemap = reinterpret_cast<uint8_t*>(by);
     ws->words = reinterpret_cast<uint2*>(wr);
     ws->scan_w = sw;
     ws->flags = reinterpret_cast<uint8_t*>(fl);
     ws->scan_n = sn;
+    ws->bk_count = reinterpret_cast<uint32_t*>(bc);
+    ws->bk_scan_c = bs;
+    ws->bk_list = reinterpret_cast<uint2*>(bl);
+    ws->bk_base = reinterpret_cast<uint32_t*>(bb);
+    ws->bk_scan_b = bt;
+    ws->bk_listed = reinterpret_cast<int32_t*>(bn);
   }
   return off;
 }
@@ -119,12 +194,6 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_pack(const uint4* __restri
 // atomics), so a word receives at most one global atomicOr per workgroup.
 // Zipf-hot ids (the hottest is ~12% of a batch) would otherwise serialise
 // hundreds of thousands of atomics on one L2 address.
-constexpr int MARK_ITEMS = 8;
-constexpr int MARK_IDS = DD_THREADS * MARK_ITEMS;
-constexpr int MARK_SLOTS = 2 * MARK_IDS;        // load factor <= 1/2: probing always ends
-static_assert(MARK_SLOTS == 4096, "the hash below yields 12 bits");
-constexpr uint32_t MARK_EMPTY = 0xffffffffu;     // never a word index (W <= 2^30)
-
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __restrict__ ids,
                                                            int64_t n, int64_t id_bound,
                                                            uint2* words) {
@@ -161,6 +230,140 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark(const int64_t* __rest
   }
 }
 
+// LDS merge of one workgroup's MARK_IDS ids by bitmap word (the hash table
+// of the hashed marking): on return keys[s] holds a word index or
+// MARK_EMPTY and bits[s] the OR of that word's bits among the ids.  All ids
+// are loaded before the first insertion.
+__device__ __forceinline__ void merge_words(const int64_t* __restrict__ ids, int64_t n,
+                                            int64_t id_bound, uint32_t* keys, uint32_t* bits) {
+  for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
+    keys[s] = MARK_EMPTY;
+    bits[s] = 0u;
+  }
+  const int64_t base = int64_t(blockIdx.x) * MARK_IDS;
+  int64_t v[MARK_ITEMS];
+#pragma unroll
+  for (int k = 0; k < MARK_ITEMS; ++k) {
+    const int64_t i = base + k * DD_THREADS + threadIdx.x;
+    v[k] = i < n ? ids[i] : int64_t(-1);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < MARK_ITEMS; ++k) {
+    const int64_t id = v[k];
+    if (id < 0 || id >= id_bound) continue;
+    const uint32_t w = uint32_t(id >> 5);
+    const uint32_t bit = 1u << (id & 31);
+    uint32_t h = (w * 2654435761u) >> (32 - 12);     // Fibonacci hashing into 4096 slots
+    for (;;) {
+      const uint32_t prev = atomicCAS(&keys[h], MARK_EMPTY, w);
+      if (prev == MARK_EMPTY || prev == w) {
+        atomicOr(&bits[h], bit);
+        break;
+      }
+      h = (h + 1) & (MARK_SLOTS - 1);
+    }
+  }
+  __syncthreads();
+}
+
+// Bucketed marking, counting pass: workgroup g merges its ids by word and
+// counts its merged words per bucket (bucket = word >> wshift) into
+// count[b * nblk + g], so that an exclusive scan of `count` in index order
+// gives every (bucket, workgroup) pair the start of its run in the list.
+__global__ void __launch_bounds__(DD_THREADS) k_bk_count(const int64_t* __restrict__ ids, int64_t n,
+                                                         int64_t id_bound, int wshift, int B,
+                                                         int nblk, uint32_t* __restrict__ count) {
+  __shared__ uint32_t keys[MARK_SLOTS];
+  __shared__ uint32_t bits[MARK_SLOTS];
+  __shared__ uint32_t h[BK_MAX_BUCKETS];
+  for (int b = threadIdx.x; b < B; b += DD_THREADS) h[b] = 0u;
+  merge_words(ids, n, id_bound, keys, bits);
+  for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
+    const uint32_t w = keys[s];
+    if (w != MARK_EMPTY) atomicAdd(&h[w >> wshift], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < B; b += DD_THREADS) count[int64_t(b) * nblk + blockIdx.x] = h[b];
+}
+
+// Bucketed marking, listing pass: the same merge, and each merged word goes
+// to its (bucket, workgroup) run as (word inside the bucket, bits); the order
+// inside a run is whatever the LDS atomics give (marking does not use it).
+__global__ void __launch_bounds__(DD_THREADS) k_bk_list(const int64_t* __restrict__ ids, int64_t n,
+                                                        int64_t id_bound, int wshift, int B,
+                                                        int nblk, const uint32_t* __restrict__ start,
+                                                        uint2* __restrict__ list) {
+  __shared__ uint32_t keys[MARK_SLOTS];
+  __shared__ uint32_t bits[MARK_SLOTS];
+  __shared__ uint32_t cur[BK_MAX_BUCKETS];
+  for (int b = threadIdx.x; b < B; b += DD_THREADS) cur[b] = start[int64_t(b) * nblk + blockIdx.x];
+  merge_words(ids, n, id_bound, keys, bits);
+  const uint32_t low = (1u << wshift) - 1u;
+  for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
+    const uint32_t w = keys[s];
+    if (w != MARK_EMPTY) {
+      const uint32_t pos = atomicAdd(&cur[w >> wshift], 1u);
+      list[pos] = make_uint2(w & low, bits[s]);
+    }
+  }
+}
+
+// Bucketed marking, one workgroup per bucket of 2^wshift words: OR the
+// bucket's list into an LDS bitmap, then write every record of the bucket
+// below W in striped (coalesced) order with its rank inside the bucket (one
+// block-wide scan per 256 words), and leave the bucket's distinct-id count
+// in total[b].
+__global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict__ list,
+                                                        const uint32_t* __restrict__ start, int nblk,
+                                                        int B, const int32_t* __restrict__ listed,
+                                                        int wshift, int64_t W,
+                                                        uint2* __restrict__ words,
+                                                        uint32_t* __restrict__ total) {
+  __shared__ uint32_t bm[BK_MAX_WORDS];
+  __shared__ uint32_t lds4[4];
+  const int WB = 1 << wshift;
+  const int b = blockIdx.x;
+  for (int j = threadIdx.x; j < WB; j += DD_THREADS) bm[j] = 0u;
+  __syncthreads();
+  const uint32_t s = nblk ? start[int64_t(b) * nblk] : 0u;
+  const uint32_t e = b + 1 < B ? (nblk ? start[int64_t(b + 1) * nblk] : 0u) : uint32_t(*listed);
+  constexpr int U = 8;   // list entries per thread in flight before the ORs
+  for (uint32_t i0 = s; i0 < e; i0 += U * DD_THREADS) {
+    uint2 x[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t i = i0 + k * DD_THREADS + threadIdx.x;
+      x[k] = i < e ? list[i] : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      if (x[k].y) atomicOr(&bm[x[k].x], x[k].y);
+    }
+  }
+  __syncthreads();
+  const int64_t w0 = int64_t(b) * WB;
+  uint32_t carry = 0;
+  for (int j0 = 0; j0 < WB; j0 += DD_THREADS) {
+    const int j = j0 + threadIdx.x;
+    const uint32_t x = j < WB ? bm[j] : 0u;
+    uint32_t tot;
+    const uint32_t pre = carry + block_exclusive_scan(uint32_t(__popc(x)), lds4, tot);
+    if (j < WB && w0 + j < W) words[w0 + j] = make_uint2(x, pre);
+    carry += tot;
+  }
+  if (threadIdx.x == 0) total[b] = carry;
+}
+
+struct BkIn {
+  const uint32_t* p;
+  __device__ uint32_t operator()(int64_t i) const { return p[i]; }
+};
+struct BkOutInPlace {
+  uint32_t* p;
+  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { p[i] = prefix; }
+};
+
 struct InPopc {
   const uint2* wr;
   __device__ uint32_t operator()(int64_t i) const { return __popc(wr[i].x); }
@@ -172,14 +375,17 @@ struct OutPrefix {   // rewrites the whole record: contiguous 8-byte stores
   }
 };
 
-// uni: every set bit of word w is written at its rank.
+// uni: every set bit of word w is written at its rank.  With bucketed
+// marking the record holds the rank inside the bucket of 2^wshift words and
+// base[] the bucket's base rank; otherwise base is NULL.
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint2* __restrict__ words,
-                                                          int64_t W, int64_t* __restrict__ uni) {
+                                                          int64_t W, const uint32_t* __restrict__ base,
+                                                          int wshift, int64_t* __restrict__ uni) {
   const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (w >= W) return;
   const uint2 rec = words[w];
   uint32_t bits = rec.x;
-  uint32_t r = rec.y;
+  uint32_t r = rec.y + (base ? base[w >> wshift] : 0u);
   while (bits) {
     const int b = __ffs(bits) - 1;
     uni[r++] = (w << 5) + b;
@@ -190,7 +396,8 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint2* __restric
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restrict__ ids, int64_t n,
                                                           int64_t id_bound,
                                                           const uint2* __restrict__ words,
-                                                          int32_t* __restrict__ inv) {
+                                                          const uint32_t* __restrict__ base,
+                                                          int wshift, int32_t* __restrict__ inv) {
   const int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
   if (i >= n) return;
   const int64_t id = ids[i];
@@ -198,9 +405,10 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restr
     inv[i] = -1;
     return;
   }
-  const uint2 rec = words[id >> 5];
+  const int64_t w = id >> 5;
+  const uint2 rec = words[w];
   const uint32_t below = rec.x & ((1u << (id & 31)) - 1u);
-  inv[i] = int32_t(rec.y + __popc(below));
+  inv[i] = int32_t(rec.y + (base ? base[w >> wshift] : 0u) + __popc(below));
 }
 
 // Row copy: thread t of a block moves vector c of row k; a block covers
@@ -352,44 +560,69 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
   dedup_layout(n, id_bound, static_cast<char*>(ws), &w);
   const int64_t W = (id_bound + 31) / 32;
 
-  // 1. clear, 2. mark ids
-  if (use_bytemap(n, id_bound)) {
-    if (W > 0) {
-      const int64_t n16 = W * 2;        // 32 W bytes as 16-byte vectors
-      const int64_t nb = (n16 + DD_THREADS - 1) / DD_THREADS;
-      hipLaunchKernelGGL(k_fill_u128, dim3(uint32_t(nb < 8192 ? nb : 8192)), dim3(DD_THREADS), 0,
-                         st, reinterpret_cast<uint4*>(w.bytemap), n16);
+  BkPlan p;
+  const MarkPath path = mark_path(n, id_bound, &p);
+  const uint32_t* base = nullptr;   // bucket base ranks (bucketed marking only)
+  const int wshift = path == MARK_BUCKETS ? p.bits - 5 : 0;
+  hipError_t e = hipSuccess;
+  // 1. mark ids, 2. word ranks (exclusive popcount prefix) and u
+  if (path == MARK_BUCKETS) {
+    const int B = int(p.B), nblk = int(p.nblk);
+    if (nblk > 0) {
+      hipLaunchKernelGGL(k_bk_count, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
+                         wshift, B, nblk, w.bk_count);
     }
-    if (n > 0)
-      hipLaunchKernelGGL(k_dedup_mark_bytes, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
-                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bytemap);
-    if (W > 0)
-      hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
-                         dim3(DD_THREADS), 0, st, reinterpret_cast<const uint4*>(w.bytemap), W,
-                         w.words);
+    e = scan_launch(BkIn{w.bk_count}, BkOutInPlace{w.bk_count}, p.B * p.nblk, w.bk_scan_c, nullptr,
+                    w.bk_listed, st);
+    if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
+    if (nblk > 0) {
+      hipLaunchKernelGGL(k_bk_list, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
+                         wshift, B, nblk, w.bk_count, w.bk_list);
+    }
+    if (B > 0) {
+      hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_list, w.bk_count,
+                         nblk, B, w.bk_listed, wshift, W, w.words, w.bk_base);
+    }
+    e = scan_launch(BkIn{w.bk_base}, BkOutInPlace{w.bk_base}, p.B, w.bk_scan_b, num_unique, nullptr,
+                    st);
+    base = w.bk_base;
   } else {
-    if (W > 0) {
-      const int64_t nb = (2 * W + DD_THREADS - 1) / DD_THREADS;
-      hipLaunchKernelGGL(k_fill_u32, dim3(uint32_t(nb < 4096 ? nb : 4096)), dim3(DD_THREADS), 0,
-                         st, reinterpret_cast<uint32_t*>(w.words), 2 * W, 0u);
+    if (path == MARK_BYTES) {
+      if (W > 0) {
+        const int64_t n16 = W * 2;        // 32 W bytes as 16-byte vectors
+        const int64_t nb = (n16 + DD_THREADS - 1) / DD_THREADS;
+        hipLaunchKernelGGL(k_fill_u128, dim3(uint32_t(nb < 8192 ? nb : 8192)), dim3(DD_THREADS), 0,
+                           st, reinterpret_cast<uint4*>(w.bytemap), n16);
+      }
+      if (n > 0)
+        hipLaunchKernelGGL(k_dedup_mark_bytes, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
+                           dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bytemap);
+      if (W > 0)
+        hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
+                           dim3(DD_THREADS), 0, st, reinterpret_cast<const uint4*>(w.bytemap), W,
+                           w.words);
+    } else {
+      if (W > 0) {
+        const int64_t nb = (2 * W + DD_THREADS - 1) / DD_THREADS;
+        hipLaunchKernelGGL(k_fill_u32, dim3(uint32_t(nb < 4096 ? nb : 4096)), dim3(DD_THREADS), 0,
+                           st, reinterpret_cast<uint32_t*>(w.words), 2 * W, 0u);
+      }
+      if (n > 0)
+        hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + MARK_IDS - 1) / MARK_IDS)),
+                           dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words);
     }
-    if (n > 0)
-      hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + MARK_IDS - 1) / MARK_IDS)),
-                         dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words);
+    e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique, nullptr, st);
   }
-  // 3. word ranks (exclusive popcount prefix) and u
-  hipError_t e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique,
-                             nullptr, st);
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-  // 4. uni, 5. inv
+  // 3. uni, 4. inv
   if (W > 0)
     hipLaunchKernelGGL(k_dedup_uni, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, w.words, W, uni);
+                       dim3(DD_THREADS), 0, st, w.words, W, base, wshift, uni);
   if (n > 0)
     hipLaunchKernelGGL(k_dedup_inv, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words, inv);
+                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words, base, wshift, inv);
 
-  // 6. rows through the slot map, miss flags, 7. ordered miss list.  Without
+  // 5. rows through the slot map, miss flags, 6. ordered miss list.  Without
   // a slot map and with a row for every id (id_bound <= table_rows) nothing
   // can miss: no flags, no scan, and the miss count is 0.
   const bool all_hit = !slot_map && id_bound <= table_rows;
