@@ -145,7 +145,7 @@ fast_status_t fast_check_tcsr(const fast_tcsr_t* g, int64_t src_bound, int64_t e
  *   table may be NULL), miss cap n (or NULL; *num_miss is still written
  *   when num_miss != NULL).
  * Limits: n < 2^31, id_bound <= 2^35.
- * Workspace: fast_dedup_gather_workspace(n, id_bound) bytes.
+ * Workspace: fast_dedup_gather_workspace(n, id_bound) bytes, 256-byte aligned.
  * ------------------------------------------------------------------------ */
 size_t fast_dedup_gather_workspace(int64_t n, int64_t id_bound);
 fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,

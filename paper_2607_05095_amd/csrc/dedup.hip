@@ -311,18 +311,20 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_list(const int64_t* __restric
 
 // Bucketed marking, one workgroup per bucket of 2^wshift words: OR the
 // bucket's list into an LDS bitmap, then write every record of the bucket
-// below W in striped (coalesced) order with its rank inside the bucket (one
-// block-wide scan per 256 words), and leave the bucket's distinct-id count
-// in total[b].
+// below W with its rank inside the bucket -- each thread takes 4 consecutive
+// words per block-wide scan (1024 words per scan) and stores them as two
+// 16-byte records pairs -- and leave the bucket's distinct-id count in
+// total[b].
 __global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict__ list,
                                                         const uint32_t* __restrict__ start, int nblk,
                                                         int B, const int32_t* __restrict__ listed,
                                                         int wshift, int64_t W,
                                                         uint2* __restrict__ words,
                                                         uint32_t* __restrict__ total) {
-  __shared__ uint32_t bm[BK_MAX_WORDS];
+  __shared__ uint4 bm4[BK_MAX_WORDS / 4];
   __shared__ uint32_t lds4[4];
-  const int WB = 1 << wshift;
+  uint32_t* bm = reinterpret_cast<uint32_t*>(bm4);
+  const int WB = 1 << wshift;                     // a multiple of 32
   const int b = blockIdx.x;
   for (int j = threadIdx.x; j < WB; j += DD_THREADS) bm[j] = 0u;
   __syncthreads();
@@ -344,12 +346,23 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict_
   __syncthreads();
   const int64_t w0 = int64_t(b) * WB;
   uint32_t carry = 0;
-  for (int j0 = 0; j0 < WB; j0 += DD_THREADS) {
-    const int j = j0 + threadIdx.x;
-    const uint32_t x = j < WB ? bm[j] : 0u;
+  for (int j0 = 0; j0 < WB; j0 += 4 * DD_THREADS) {
+    const int j = j0 + 4 * threadIdx.x;
+    const uint4 x = j < WB ? bm4[j >> 2] : make_uint4(0u, 0u, 0u, 0u);
+    const uint32_t p0 = __popc(x.x), p1 = __popc(x.y), p2 = __popc(x.z), p3 = __popc(x.w);
     uint32_t tot;
-    const uint32_t pre = carry + block_exclusive_scan(uint32_t(__popc(x)), lds4, tot);
-    if (j < WB && w0 + j < W) words[w0 + j] = make_uint2(x, pre);
+    const uint32_t r0 = carry + block_exclusive_scan(p0 + p1 + p2 + p3, lds4, tot);
+    const uint32_t r1 = r0 + p0, r2 = r1 + p1, r3 = r2 + p2;
+    const int64_t w = w0 + j;
+    if (j < WB && w + 3 < W) {
+      uint4* dst = reinterpret_cast<uint4*>(words + w);   // w is a multiple of 4: 32-byte aligned
+      dst[0] = make_uint4(x.x, r0, x.y, r1);
+      dst[1] = make_uint4(x.z, r2, x.w, r3);
+    } else if (j < WB) {
+      if (w < W) words[w] = make_uint2(x.x, r0);
+      if (w + 1 < W) words[w + 1] = make_uint2(x.y, r1);
+      if (w + 2 < W) words[w + 2] = make_uint2(x.z, r2);
+    }
     carry += tot;
   }
   if (threadIdx.x == 0) total[b] = carry;
@@ -554,6 +567,7 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
   const size_t need = dedup_layout(n, id_bound, nullptr, nullptr);
   if (!ws || ws_bytes < need)
     return fail(FAST_ERR_WORKSPACE, "%s: workspace %zu < %zu bytes", fn, ws_bytes, need);
+  if (!aligned(ws, 256)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 256-byte aligned", fn);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   DedupWs w;

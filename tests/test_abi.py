@@ -140,8 +140,9 @@ def test_dedup_validation_and_workspace_query():
     args = lambda **k: [k.get("ids", FAKE), k.get("n", 1000), k.get("bound", 1 << 20),
                         k.get("table", FAKE), k.get("rows_n", 1 << 20), 100, k.get("dt", 0),
                         k.get("slot", None), FAKE, FAKE, k.get("nu", FAKE), k.get("rows", FAKE),
-                        None, None, FAKE, k.get("ws", ws), None]
+                        None, None, k.get("wsp", FAKE), k.get("ws", ws), None]
     assert L.fast_dedup_gather(*args(ws=ws - 1)) == WORKSPACE
+    assert L.fast_dedup_gather(*args(wsp=FAKE + 16)) == UNSUPPORTED   # misaligned workspace
     assert L.fast_dedup_gather(*args(n=-1)) == INVALID
     assert L.fast_dedup_gather(*args(nu=None)) == INVALID
     assert L.fast_dedup_gather(*args(ids=None)) == INVALID
