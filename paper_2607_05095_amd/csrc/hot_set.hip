@@ -146,6 +146,8 @@ __device__ __forceinline__ int32_t clamp_count(int32_t f, int32_t max_freq) {
   return f < 0 ? 0 : (f > max_freq ? max_freq : f);
 }
 
+constexpr int HS_HIST_U = 4;
+
 // hist[c] = number of ids whose clamped count is c, c in [0, max_freq].
 // Counts below HS_LDS_BINS go through a per-workgroup LDS histogram (almost
 // every id of a large universe has a small count), the rest straight to HBM.
@@ -169,12 +171,23 @@ __global__ void __launch_bounds__(HS_THREADS) k_hs_hist(const int32_t* __restric
       atomicAdd(&hist[c], 1u);
     }
   };
-  // four counts per 16-byte load when the array allows it, then the tail
+  // four counts per 16-byte load when the array allows it (HS_HIST_U loads
+  // in flight per thread before they are binned), then the tail
   const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
   const int64_t n4 = vec ? n / 4 : 0;
   const int4* f4 = reinterpret_cast<const int4*>(f);
-  for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n4;
-       i += int64_t(gridDim.x) * HS_THREADS) {
+  const int64_t stride = int64_t(gridDim.x) * HS_THREADS;
+  int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x;
+  for (; i + (HS_HIST_U - 1) * stride < n4; i += HS_HIST_U * stride) {
+    int4 x[HS_HIST_U];
+#pragma unroll
+    for (int k = 0; k < HS_HIST_U; ++k) x[k] = f4[i + k * stride];
+#pragma unroll
+    for (int k = 0; k < HS_HIST_U; ++k) {
+      bin(x[k].x); bin(x[k].y); bin(x[k].z); bin(x[k].w);
+    }
+  }
+  for (; i < n4; i += stride) {
     const int4 x = f4[i];
     bin(x.x); bin(x.y); bin(x.z); bin(x.w);
   }
