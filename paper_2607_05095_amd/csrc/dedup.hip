@@ -104,8 +104,7 @@ struct DedupWs {
   uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup), then list offsets
   void* bk_scan_c;    // scan workspace over the counts
   uint2* bk_list;     // [<= n] (word inside the bucket, bits), grouped by bucket
-  uint32_t* bk_base;  // [B] distinct ids per bucket, then the bucket's base rank
-  void* bk_scan_b;    // scan workspace over the buckets
+  uint32_t* bk_base;  // [B + 1] distinct ids per bucket, then the bucket's base rank (and u)
   int32_t* bk_listed; // number of list entries
 };
 
@@ -128,8 +127,7 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
   char* bc = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
   char* bs = take(bk ? scan_workspace(p.B * p.nblk) : 0);
   char* bl = take(bk ? size_t(n) * 8 : 0);
-  char* bb = take(bk ? size_t(p.B) * 4 : 0);
-  char* bt = take(bk ? scan_workspace(p.B) : 0);
+  char* bb = take(bk ? size_t(p.B + 1) * 4 : 0);
   char* bn = take(bk ? 4 : 0);
   if (ws) {
     ws->bytemap = reinterpret_cast<uint8_t*>(by);
@@ -141,7 +139,6 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     ws->bk_scan_c = bs;
     ws->bk_list = reinterpret_cast<uint2*>(bl);
     ws->bk_base = reinterpret_cast<uint32_t*>(bb);
-    ws->bk_scan_b = bt;
     ws->bk_listed = reinterpret_cast<int32_t*>(bn);
   }
   return off;
@@ -597,8 +594,9 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
       hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_list, w.bk_count,
                          nblk, B, w.bk_listed, wshift, W, w.words, w.bk_base);
     }
-    e = scan_launch(BkIn{w.bk_base}, BkOutInPlace{w.bk_base}, p.B, w.bk_scan_b, num_unique, nullptr,
-                    st);
+    // at most 4096 bucket totals: one workgroup scans them in place
+    hipLaunchKernelGGL(k_scan_top<uint32_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.bk_base, p.B,
+                       num_unique, static_cast<int32_t*>(nullptr));
     base = w.bk_base;
   } else {
     if (path == MARK_BYTES) {
