@@ -406,13 +406,14 @@ def test_dedup_edge_cases(case):
 
 
 @pytest.mark.parametrize("bound,n", [(2**29, 3000), (2**31, 3000), (2**31 + 1, 3000), (2**33 + 5, 50_000),
-                                     (3 * 10**7 + 13, 300_000), (40_000, 1200)])
+                                     (3 * 10**7 + 13, 300_000), (40_000, 1200), (2**31, 9_000_000)])
 def test_dedup_sparse_universes(bound, n):
     """Universes far larger than the batch, on both sides of the largest one
     that bucketed marking takes (2^31 ids: 4096 buckets of 2^19) and up to
     2^33 ids (hashed marking), with Zipf-like hot ids (a few ids repeated in
     every workgroup's share), ids at both ends of the universe, and many
-    workgroups."""
+    workgroups; 9 M ids over 2^31 give more (bucket, workgroup) counts than
+    the bucketed marking takes (2^24), so they are marked by hashed atomics."""
     _announce(f"dedup sparse universe bound={bound} n={n}")
     r = np.random.default_rng(bound % 1000 + n)
     hot = r.integers(0, bound, 16)
