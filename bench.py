@@ -654,6 +654,24 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     return res
 
 
+def segment_shares(blocks, T):
+    """Cut every layer block into T contiguous destination ranges (equal
+    segment counts): shares[t] holds, per block, range t's counts, times and
+    Q/K/V/dOut rows (a destination's edges are contiguous in CSR order)."""
+    shares = [[] for _ in range(T)]
+    for x in blocks:
+        counts = np.asarray(x["counts"])
+        ns = counts.shape[0]
+        ends = np.concatenate([[0], np.cumsum(counts)])
+        cuts = np.linspace(0, ns, T + 1).astype(np.int64)
+        for t in range(T):
+            a, c = int(cuts[t]), int(cuts[t + 1])
+            ea, ec = int(ends[a]), int(ends[c])
+            shares[t].append(dict(counts=counts[a:c], dst_t=x["dst_t"][a:c], edge_t=x["edge_t"][ea:ec],
+                                  Q=x["Q"][a:c], K=x["K"][ea:ec], V=x["V"][ea:ec], dO=x["dO"][a:c]))
+    return shares
+
+
 def cpu_baseline_threads(blocks, node_ids, edge_ids, node_table, edge_table, slot, om, ph,
                          scale, sample_edges, max_threads=16):
     """The same oracle pass on all the host threads this process may use (at
@@ -671,17 +689,7 @@ def cpu_baseline_threads(blocks, node_ids, edge_ids, node_table, edge_table, slo
     except AttributeError:
         T = min(max_threads, os.cpu_count() or 1)
     oracle.lib()
-    shares = [[] for _ in range(T)]
-    for x in blocks:
-        counts = np.asarray(x["counts"])
-        ns = counts.shape[0]
-        ends = np.concatenate([[0], np.cumsum(counts)])
-        cuts = np.linspace(0, ns, T + 1).astype(np.int64)
-        for t in range(T):
-            a, c = int(cuts[t]), int(cuts[t + 1])
-            ea, ec = int(ends[a]), int(ends[c])
-            shares[t].append(dict(counts=counts[a:c], dst_t=x["dst_t"][a:c], edge_t=x["edge_t"][ea:ec],
-                                  Q=x["Q"][a:c], K=x["K"][ea:ec], V=x["V"][ea:ec], dO=x["dO"][a:c]))
+    shares = segment_shares(blocks, T)
 
     def segments(share):
         offs = [oracle.csr_offsets(x["counts"]) for x in share]

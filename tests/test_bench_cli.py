@@ -40,3 +40,33 @@ def test_counter_records_are_whole_and_checked_against_the_source(tmp_path, monk
         (tmp_path / f"t_{w}.json").write_text(json.dumps(stale))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "t_{workload}.json"))
     assert bench.read_counters("bigdedup") == {} and bench.read_traffic("large") is None
+
+
+def test_segment_shares_recompose_the_whole_block():
+    """The all-cores CPU baseline runs the oracle over contiguous segment
+    ranges; the ranges' results, concatenated, are the whole block's."""
+    import numpy as np
+
+    import bench
+    import oracle
+    from synth import make_batch
+    b = make_batch(2)
+    blk = b.blocks[0]
+    N, E = blk.num_dst, int(blk.counts.sum())
+    r = np.random.default_rng(5)
+    x = dict(counts=blk.counts, dst_t=blk.dst_t, edge_t=blk.edge_t,
+             Q=r.standard_normal((N, 2, 8)), K=r.standard_normal((E, 2, 8)),
+             V=r.standard_normal((E, 2, 8)), dO=r.standard_normal((N, 2, 8)))
+    shares = bench.segment_shares([x], 5)
+    assert sum(int(sh[0]["counts"].sum()) for sh in shares) == E
+    off = oracle.csr_offsets(blk.counts)
+    out, lse, _, _ = oracle.edge_attention_fwd(off, x["Q"], x["K"], x["V"], 0.3, 0.2)
+    dQ, dK, dV = oracle.edge_attention_bwd(off, x["Q"], x["K"], x["V"], x["dO"], 0.3, 0.2)
+    parts = []
+    for sh in shares:
+        y = sh[0]
+        o = oracle.csr_offsets(y["counts"])
+        parts.append(oracle.edge_attention_fwd(o, y["Q"], y["K"], y["V"], 0.3, 0.2)[0:1]
+                     + oracle.edge_attention_bwd(o, y["Q"], y["K"], y["V"], y["dO"], 0.3, 0.2))
+    for k, ref in enumerate((out, dQ, dK, dV)):
+        assert np.array_equal(np.concatenate([p[k] for p in parts]), ref)
