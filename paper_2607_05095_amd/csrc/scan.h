@@ -1,9 +1,10 @@
 // scan.h -- device-wide exclusive scan over uint32 (default) or uint64 items
-// (three launches: per-tile reduce, one-block scan of the tile sums, per-tile
-// down-sweep).  Item producers and prefix consumers are functors, so callers
-// fuse their own load (counts, bitmap popcounts, miss flags) and store
-// (offsets, word ranks, compaction scatter) into the scan's two passes over
-// the data.  A uint64 item can carry two 32-bit counters that are scanned
+// (per-tile reduce, one-block scan of the tile sums, per-tile down-sweep; up
+// to 2048 tiles the down-sweep adds up the preceding tile sums itself and the
+// middle launch is skipped).  Item producers and prefix consumers are
+// functors, so callers fuse their own load (counts, bitmap popcounts, miss
+// flags) and store (offsets, word ranks, compaction scatter) into the scan's
+// two passes over the data.  A uint64 item can carry two 32-bit counters that are scanned
 // together (high and low word), as long as neither total reaches 2^32.
 #pragma once
 
@@ -119,14 +120,26 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* tsum, int64_t nt,
 // replace the items in LDS (plus the running total after the last item), so
 // that `out` is called in striped order too -- neighbouring lanes write
 // neighbouring outputs (offsets, ranks, slot maps) -- with each item's value
-// recovered as the difference of consecutive prefixes.
-template <class In, class Out, typename T = uint32_t>
+// recovered as the difference of consecutive prefixes.  The tile's base is
+// tsum[tile] after the one-block scan of the tile sums, or, with SUM_PREV
+// (few tiles), the sum of the unscanned tile sums before it, added up by the
+// tile's own workgroup; the last tile then also stores the grand total.
+template <class In, class Out, typename T = uint32_t, bool SUM_PREV = false>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
-                                                            const T* tsum, Out out) {
+                                                            const T* tsum, Out out,
+                                                            int64_t* total_i64, int32_t* total_i32) {
   constexpr int PAD_END = SCAN_TILE + SCAN_TILE / 32;
   __shared__ T tile[PAD_END + 1];
   __shared__ T lds4[4];
   const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
+  T tile_base;
+  if constexpr (SUM_PREV) {
+    T part = 0;
+    for (int64_t t = threadIdx.x; t < int64_t(blockIdx.x); t += SCAN_THREADS) part += tsum[t];
+    block_exclusive_scan(part, lds4, tile_base);   // block-wide sum of the parts
+  } else {
+    tile_base = tsum[blockIdx.x];
+  }
   // striped, coalesced load into LDS (padded every 32 words against bank conflicts)
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
@@ -145,7 +158,13 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
   T total;
   // (the block scan's barriers also order every read of tile above before
   // the writes below)
-  T run = block_exclusive_scan(s, lds4, total) + tsum[blockIdx.x];
+  T run = block_exclusive_scan(s, lds4, total) + tile_base;
+  if constexpr (SUM_PREV) {
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+      if (total_i64) *total_i64 = int64_t(tile_base + total);
+      if (total_i32) *total_i32 = int32_t(tile_base + total);
+    }
+  }
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int j = threadIdx.x * SCAN_ITEMS + k;
@@ -165,9 +184,13 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
   }
 }
 
-// Enqueues the three launches.  ws must hold scan_workspace<T>(n) bytes; the
-// grand total is left at ((T*)ws)[scan_tiles(n)].  total_i64 / total_i32
-// (device, optional) receive the sum of all items.
+// Enqueues the launches: per-tile reduce, then either (at most
+// SCAN_FEW_TILES tiles) the down-sweep in which every tile adds up the tile
+// sums before it, or the one-block scan of the tile sums and the down-sweep.
+// ws must hold scan_workspace<T>(n) bytes.  total_i64 / total_i32 (device,
+// optional) receive the sum of all items.
+constexpr int64_t SCAN_FEW_TILES = 2048;
+
 template <class In, class Out, typename T = uint32_t>
 hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
                        int32_t* total_i32, hipStream_t st) {
@@ -177,11 +200,16 @@ hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
     hipLaunchKernelGGL((k_scan_reduce<In, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n,
                        tsum);
   }
+  if (nt > 0 && nt <= SCAN_FEW_TILES) {
+    hipLaunchKernelGGL((k_scan_down<In, Out, T, true>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
+                       in, n, tsum, out, total_i64, total_i32);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_scan_top<T>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, nt, total_i64,
                      total_i32);
   if (nt > 0) {
-    hipLaunchKernelGGL((k_scan_down<In, Out, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
-                       in, n, tsum, out);
+    hipLaunchKernelGGL((k_scan_down<In, Out, T, false>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
+                       in, n, tsum, out, static_cast<int64_t*>(nullptr), static_cast<int32_t*>(nullptr));
   }
   return hipGetLastError();
 }
