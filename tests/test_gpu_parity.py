@@ -217,7 +217,8 @@ def test_fused_equals_unfused_composition():
 
 
 # ------------------------------------------------------------------ offsets (a1)
-@pytest.mark.parametrize("case", ["cfg0", "cfg2", "cfg3", "cfg4", "empty", "zeros", "ragged", "big"])
+@pytest.mark.parametrize("case", ["cfg0", "cfg2", "cfg3", "cfg4", "empty", "zeros", "ragged", "big",
+                                  "one_tile", "tiles_2048", "tiles_2049"])
 def test_csr_offsets_bit_exact(case):
     _announce(f"offsets {case}")
     r = np.random.default_rng(1)
@@ -230,6 +231,11 @@ def test_csr_offsets_bit_exact(case):
         "zeros": lambda: np.zeros(5000, np.int32),
         "ragged": lambda: r.integers(0, 30, 2049 * 3 + 7).astype(np.int32),
         "big": lambda: r.integers(0, 3, 3_000_001).astype(np.int32),
+        # the scan's two launch plans: up to 2048 tiles of 2048 counts each
+        # tile adds up the preceding tile sums, beyond that a one-block scan
+        "one_tile": lambda: r.integers(0, 50, 2048).astype(np.int32),
+        "tiles_2048": lambda: r.integers(0, 5, 2048 * 2048).astype(np.int32),
+        "tiles_2049": lambda: r.integers(0, 5, 2048 * 2048 + 1).astype(np.int32),
     }[case]()
     n = counts.shape[0]
     d_counts = to_dev(counts) if n else torch.zeros(1, dtype=torch.int32, device="cuda")
