@@ -388,11 +388,9 @@ struct OutPrefix {   // rewrites the whole record: contiguous 8-byte stores
 // uni: every set bit of word w is written at its rank.  With bucketed
 // marking the record holds the rank inside the bucket of 2^wshift words and
 // base[] the bucket's base rank; otherwise base is NULL.
-__global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint2* __restrict__ words,
-                                                          int64_t W, const uint32_t* __restrict__ base,
-                                                          int wshift, int64_t* __restrict__ uni) {
-  const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
-  if (w >= W) return;
+__device__ __forceinline__ void dedup_uni_word(const uint2* __restrict__ words, int64_t w,
+                                               const uint32_t* __restrict__ base, int wshift,
+                                               int64_t* __restrict__ uni) {
   const uint2 rec = words[w];
   uint32_t bits = rec.x;
   uint32_t r = rec.y + (base ? base[w >> wshift] : 0u);
@@ -403,13 +401,11 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni(const uint2* __restric
   }
 }
 
-__global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restrict__ ids, int64_t n,
-                                                          int64_t id_bound,
-                                                          const uint2* __restrict__ words,
-                                                          const uint32_t* __restrict__ base,
-                                                          int wshift, int32_t* __restrict__ inv) {
-  const int64_t i = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
-  if (i >= n) return;
+// inv: the rank of the id's bit (-1 for an id outside [0, id_bound)).
+__device__ __forceinline__ void dedup_inv_id(const int64_t* __restrict__ ids, int64_t i,
+                                             int64_t id_bound, const uint2* __restrict__ words,
+                                             const uint32_t* __restrict__ base, int wshift,
+                                             int32_t* __restrict__ inv) {
   const int64_t id = ids[i];
   if (id < 0 || id >= id_bound) {
     inv[i] = -1;
@@ -419,6 +415,25 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_inv(const int64_t* __restr
   const uint2 rec = words[w];
   const uint32_t below = rec.x & ((1u << (id & 31)) - 1u);
   inv[i] = int32_t(rec.y + (base ? base[w >> wshift] : 0u) + __popc(below));
+}
+
+// uni and inv in one launch: workgroups [0, nbw) take 256 words each, the
+// rest 256 ids each.
+__global__ void __launch_bounds__(DD_THREADS) k_dedup_uni_inv(const uint2* __restrict__ words,
+                                                              int64_t W,
+                                                              const uint32_t* __restrict__ base,
+                                                              int wshift, int64_t* __restrict__ uni,
+                                                              const int64_t* __restrict__ ids,
+                                                              int64_t n, int64_t id_bound,
+                                                              int32_t* __restrict__ inv,
+                                                              uint32_t nbw) {
+  if (blockIdx.x < nbw) {
+    const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
+    if (w < W) dedup_uni_word(words, w, base, wshift, uni);
+  } else {
+    const int64_t i = int64_t(blockIdx.x - nbw) * DD_THREADS + threadIdx.x;
+    if (i < n) dedup_inv_id(ids, i, id_bound, words, base, wshift, inv);
+  }
 }
 
 // Row copy: thread t of a block moves vector c of row k; a block covers
@@ -626,15 +641,13 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
     e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique, nullptr, st);
   }
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-  // 3. uni, 4. inv
-  if (W > 0)
-    hipLaunchKernelGGL(k_dedup_uni, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, w.words, W, base, wshift, uni);
-  if (n > 0)
-    hipLaunchKernelGGL(k_dedup_inv, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
-                       dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words, base, wshift, inv);
+  // 3. uni and inv
+  const int64_t nbw = (W + DD_THREADS - 1) / DD_THREADS, nbi = (n + DD_THREADS - 1) / DD_THREADS;
+  if (nbw + nbi > 0)
+    hipLaunchKernelGGL(k_dedup_uni_inv, dim3(uint32_t(nbw + nbi)), dim3(DD_THREADS), 0, st, w.words, W,
+                       base, wshift, uni, ids, n, id_bound, inv, uint32_t(nbw));
 
-  // 5. rows through the slot map, miss flags, 6. ordered miss list.  Without
+  // 4. rows through the slot map, miss flags, 5. ordered miss list.  Without
   // a slot map and with a row for every id (id_bound <= table_rows) nothing
   // can miss: no flags, no scan, and the miss count is 0.
   const bool all_hit = !slot_map && id_bound <= table_rows;
