@@ -169,21 +169,35 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_mark_bytes(const int64_t* 
   if (id >= 0 && id < id_bound) bytemap[id] = 1;
 }
 
-// bitmap word w <- bytes 32w .. 32w+31 of the byte map (each 0 or 1).
-__global__ void __launch_bounds__(DD_THREADS) k_dedup_pack(const uint4* __restrict__ bytemap,
-                                                           int64_t W, uint2* __restrict__ words) {
-  const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
-  if (w >= W) return;
-  const uint4 a = bytemap[2 * w], b = bytemap[2 * w + 1];
-  const uint32_t q[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  uint32_t word = 0;
+// bitmap word w <- bytes 32w .. 32w+31 of the byte map (each 0 or 1).  A
+// workgroup packs one scan tile of words (SCAN_ITEMS per thread, striped)
+// and stores the tile's popcount sum, the reduce step of the rank scan.
+__global__ void __launch_bounds__(SCAN_THREADS) k_dedup_pack(const uint4* __restrict__ bytemap,
+                                                             int64_t W, uint2* __restrict__ words,
+                                                             uint32_t* __restrict__ tsum) {
+  __shared__ uint32_t lds4[4];
+  const int64_t w0 = int64_t(blockIdx.x) * SCAN_TILE;
+  uint32_t c = 0;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    // bytes b0..b3 in {0,1} at bits 0,8,16,24 -> b0 | b1<<1 | b2<<2 | b3<<3 at bit 24
-    const uint32_t nib = ((q[k] & 0x01010101u) * 0x01020408u) >> 24;
-    word |= (nib & 0xfu) << (4 * k);
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int64_t w = w0 + k * SCAN_THREADS + threadIdx.x;
+    if (w < W) {
+      const uint4 a = bytemap[2 * w], b = bytemap[2 * w + 1];
+      const uint32_t q[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      uint32_t word = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        // bytes b0..b3 in {0,1} at bits 0,8,16,24 -> b0 | b1<<1 | b2<<2 | b3<<3 at bit 24
+        const uint32_t nib = ((q[j] & 0x01010101u) * 0x01020408u) >> 24;
+        word |= (nib & 0xfu) << (4 * j);
+      }
+      words[w].x = word;
+      c += __popc(word);
+    }
   }
-  words[w].x = word;
+  uint32_t total;
+  block_exclusive_scan(c, lds4, total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
 }
 
 // Marking: each workgroup takes MARK_ITEMS ids per thread and first merges
@@ -625,9 +639,11 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
         hipLaunchKernelGGL(k_dedup_mark_bytes, dim3(uint32_t((n + DD_THREADS - 1) / DD_THREADS)),
                            dim3(DD_THREADS), 0, st, ids, n, id_bound, w.bytemap);
       if (W > 0)
-        hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t((W + DD_THREADS - 1) / DD_THREADS)),
-                           dim3(DD_THREADS), 0, st, reinterpret_cast<const uint4*>(w.bytemap), W,
-                           w.words);
+        hipLaunchKernelGGL(k_dedup_pack, dim3(uint32_t(scan_tiles(W))), dim3(SCAN_THREADS), 0, st,
+                           reinterpret_cast<const uint4*>(w.bytemap), W, w.words,
+                           static_cast<uint32_t*>(w.scan_w));
+      e = scan_finish_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique, nullptr,
+                             st);
     } else {
       if (W > 0) {
         const int64_t nb = (2 * W + DD_THREADS - 1) / DD_THREADS;
@@ -637,8 +653,8 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
       if (n > 0)
         hipLaunchKernelGGL(k_dedup_mark, dim3(uint32_t((n + MARK_IDS - 1) / MARK_IDS)),
                            dim3(DD_THREADS), 0, st, ids, n, id_bound, w.words);
+      e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique, nullptr, st);
     }
-    e = scan_launch(InPopc{w.words}, OutPrefix{w.words}, W, w.scan_w, num_unique, nullptr, st);
   }
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   // 3. uni and inv

@@ -191,15 +191,14 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
 // optional) receive the sum of all items.
 constexpr int64_t SCAN_FEW_TILES = 2048;
 
+// The launches after the per-tile reduce, for a scan whose tile sums are
+// already in ws (tsum[t] = the sum of items [t SCAN_TILE, (t+1) SCAN_TILE)),
+// written by k_scan_reduce or by a caller's kernel that produces the items.
 template <class In, class Out, typename T = uint32_t>
-hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
-                       int32_t* total_i32, hipStream_t st) {
+hipError_t scan_finish_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
+                              int32_t* total_i32, hipStream_t st) {
   T* tsum = static_cast<T*>(ws);
   const int64_t nt = scan_tiles(n);
-  if (nt > 0) {
-    hipLaunchKernelGGL((k_scan_reduce<In, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n,
-                       tsum);
-  }
   if (nt > 0 && nt <= SCAN_FEW_TILES) {
     hipLaunchKernelGGL((k_scan_down<In, Out, T, true>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st,
                        in, n, tsum, out, total_i64, total_i32);
@@ -212,6 +211,17 @@ hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
                        in, n, tsum, out, static_cast<int64_t*>(nullptr), static_cast<int32_t*>(nullptr));
   }
   return hipGetLastError();
+}
+
+template <class In, class Out, typename T = uint32_t>
+hipError_t scan_launch(In in, Out out, int64_t n, void* ws, int64_t* total_i64,
+                       int32_t* total_i32, hipStream_t st) {
+  const int64_t nt = scan_tiles(n);
+  if (nt > 0) {
+    hipLaunchKernelGGL((k_scan_reduce<In, T>), dim3(uint32_t(nt)), dim3(SCAN_THREADS), 0, st, in, n,
+                       static_cast<T*>(ws));
+  }
+  return scan_finish_launch<In, Out, T>(in, out, n, ws, total_i64, total_i32, st);
 }
 
 }  // namespace fast
