@@ -33,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+VALU_PEAK_LANE_OPS = 256 * 64 * 2.4e9   # 256 CUs x 64 lanes x 2.4 GHz, one instruction per clock
 SLOPE = 0.2
 WORKLOADS = {"bigdedup": 4, "large": 3}
 METRIC = "sampled edges/sec, fused edge-softmax+aggregation fwd+bwd; % HBM roofline"
@@ -45,12 +46,19 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
+TIME_ENCODE_SOURCES = ["paper_2607_05095_amd/csrc/time_encode.hip", "paper_2607_05095_amd/csrc/common.h"]
+
+
+def source_hash(paths):
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in paths:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def kernel_source_hash():
+    return source_hash(KERNEL_SOURCES)
 
 
 def describe(b):
@@ -552,15 +560,27 @@ def greedy_hot_set_bytes(nv, ne, B):
     return 4 * (nv + ne) + 4 * (nv + ne) + 8 * B
 
 
-def time_encode_summary(b, breakdown):
+def time_encode_summary(b, breakdown, counters=None):
     """Time encoding of both layer blocks in the serial step: algorithmic bytes
-    E (4 + d_t b) + 8 N per block against the measured times."""
+    E (4 + d_t b) + 8 N per block against the measured times; with a counter
+    record of the layer-1 launch taken on the current time-encoding source,
+    also its VALU utilisation (VALU wave instructions x 64 lanes over the
+    layer-1 time, against 256 CUs x 64 lanes x 2.4 GHz)."""
     b_out = 4 if b.dtype == "f32" else 2
     ms = sum(breakdown.get(f"time_encode_L{i + 1}", 0.0) for i in range(len(b.blocks)))
     nbytes = sum(x.num_edges * (4 + b.d_t * b_out) + 8 * x.num_dst for x in b.blocks)
-    return {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
-            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ms > 0 else None,
-            "cosines_per_s": sum(x.num_edges for x in b.blocks) * b.d_t / (ms * 1e-3) if ms > 0 else None}
+    res = {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
+           "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ms > 0 else None,
+           "cosines_per_s": sum(x.num_edges for x in b.blocks) * b.d_t / (ms * 1e-3) if ms > 0 else None}
+    v = (counters or {}).get("time_encode_valu")
+    ms1 = breakdown.get("time_encode_L1", 0.0)
+    if v and v.get("source_sha") == source_hash(TIME_ENCODE_SOURCES) and ms1 > 0:
+        lane = v["valu_wave_insts_per_launch"] * 64 / (ms1 * 1e-3)
+        res["valu_L1"] = {"lane_insts_per_s": lane, "frac": round(lane / VALU_PEAK_LANE_OPS, 4),
+                          "hbm_frac": round((b.blocks[0].num_edges * (4 + b.d_t * b_out) + 8 * b.blocks[0].num_dst)
+                                            / (ms1 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "source": v.get("source")}
+    return res
 
 
 def host_cpu_model():
@@ -866,7 +886,7 @@ def main():
             "algorithmic_bytes_without_lse": fused_bytes_no_lse,
             "hbm_frac_without_lse": round(fused_bytes_no_lse / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
-        "time_encode": time_encode_summary(b, breakdown),
+        "time_encode": time_encode_summary(b, breakdown, read_counters(args.workload)),
         "schedule": "serial: prep (offsets, time encoding, dedup+gather) then attention of each "
                     "batch on one stream",
 

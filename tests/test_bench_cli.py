@@ -35,6 +35,8 @@ def test_counter_records_are_whole_and_checked_against_the_source(tmp_path, monk
         assert rec["workload"] == w
         assert 0 < rec["l2_hit_rate"] < 1 and 0 < rec["occupancy_pct"] <= 100
         assert rec["bytes_per_launch"] > 0 and os.path.exists(os.path.join(ROOT, rec["source"]))
+        te = rec["time_encode_valu"]
+        assert te["valu_wave_insts_per_launch"] > 0 and "k_time_encode<" in te["kernel"]
         # a record taken on other kernel sources is not reported
         stale = dict(rec, kernel_source_sha="0" * 16)
         (tmp_path / f"t_{w}.json").write_text(json.dumps(stale))
@@ -70,3 +72,17 @@ def test_segment_shares_recompose_the_whole_block():
                      + oracle.edge_attention_bwd(o, y["Q"], y["K"], y["V"], y["dO"], 0.3, 0.2))
     for k, ref in enumerate((out, dQ, dK, dV)):
         assert np.array_equal(np.concatenate([p[k] for p in parts]), ref)
+
+
+def test_time_encode_valu_only_from_counters_of_the_current_source():
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import make_batch
+    b = make_batch(4)
+    bd = {"time_encode_L1": 0.2, "time_encode_L2": 0.03}
+    rec = {"time_encode_valu": {"valu_wave_insts_per_launch": 5.6e7, "source": "x",
+                                "source_sha": bench.source_hash(bench.TIME_ENCODE_SOURCES)}}
+    v = bench.time_encode_summary(b, bd, rec)["valu_L1"]
+    assert abs(v["lane_insts_per_s"] - 5.6e7 * 64 / 2e-4) < 1 and 0 < v["frac"] < 1
+    rec["time_encode_valu"]["source_sha"] = "0" * 16
+    assert "valu_L1" not in bench.time_encode_summary(b, bd, rec)
