@@ -100,6 +100,7 @@ struct DedupWs {
   uint2* words;       // [W] word records
   void* scan_w;       // scan workspace over W words (byte map, hash)
   uint8_t* flags;     // [n] miss flags
+  int32_t* slots;     // [n] table slot of each unique id (with a slot map)
   void* scan_n;       // scan workspace over n flags
   uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup), then list offsets
   void* bk_scan_c;    // scan workspace over the counts
@@ -123,6 +124,7 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
   char* wr = take(size_t(W) * 8);
   char* sw = take(bk ? 0 : scan_workspace(W));
   char* fl = take(size_t(n));
+  char* sl = take(size_t(n) * 4);
   char* sn = take(scan_workspace(n));
   char* bc = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
   char* bs = take(bk ? scan_workspace(p.B * p.nblk) : 0);
@@ -134,6 +136,7 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     ws->words = reinterpret_cast<uint2*>(wr);
     ws->scan_w = sw;
     ws->flags = reinterpret_cast<uint8_t*>(fl);
+    ws->slots = reinterpret_cast<int32_t*>(sl);
     ws->scan_n = sn;
     ws->bk_count = reinterpret_cast<uint32_t*>(bc);
     ws->bk_scan_c = bs;
@@ -401,16 +404,23 @@ struct OutPrefix {   // rewrites the whole record: contiguous 8-byte stores
 
 // uni: every set bit of word w is written at its rank.  With bucketed
 // marking the record holds the rank inside the bucket of 2^wshift words and
-// base[] the bucket's base rank; otherwise base is NULL.
+// base[] the bucket's base rank; otherwise base is NULL.  With a slot map,
+// the unique id's slot is looked up here too (slots[rank]), where the
+// lookups of all ids are independent, rather than inside the row copy.
 __device__ __forceinline__ void dedup_uni_word(const uint2* __restrict__ words, int64_t w,
                                                const uint32_t* __restrict__ base, int wshift,
-                                               int64_t* __restrict__ uni) {
+                                               int64_t* __restrict__ uni,
+                                               const int32_t* __restrict__ slot_map,
+                                               int32_t* __restrict__ slots) {
   const uint2 rec = words[w];
   uint32_t bits = rec.x;
   uint32_t r = rec.y + (base ? base[w >> wshift] : 0u);
   while (bits) {
     const int b = __ffs(bits) - 1;
-    uni[r++] = (w << 5) + b;
+    const int64_t id = (w << 5) + b;
+    uni[r] = id;
+    if (slots) slots[r] = slot_map[id];
+    ++r;
     bits &= bits - 1;
   }
 }
@@ -440,10 +450,12 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni_inv(const uint2* __res
                                                               const int64_t* __restrict__ ids,
                                                               int64_t n, int64_t id_bound,
                                                               int32_t* __restrict__ inv,
+                                                              const int32_t* __restrict__ slot_map,
+                                                              int32_t* __restrict__ slots,
                                                               uint32_t nbw) {
   if (blockIdx.x < nbw) {
     const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
-    if (w < W) dedup_uni_word(words, w, base, wshift, uni);
+    if (w < W) dedup_uni_word(words, w, base, wshift, uni, slot_map, slots);
   } else {
     const int64_t i = int64_t(blockIdx.x - nbw) * DD_THREADS + threadIdx.x;
     if (i < n) dedup_inv_id(ids, i, id_bound, words, base, wshift, inv);
@@ -484,7 +496,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __res
                                                             const int64_t* __restrict__ num_unique,
                                                             const V* __restrict__ table,
                                                             int64_t table_rows, int cpr, int rpb,
-                                                            const int32_t* __restrict__ slot_map,
+                                                            const int32_t* __restrict__ slots,
                                                             V* __restrict__ rows,
                                                             uint8_t* __restrict__ flags) {
   const int64_t u = *num_unique;
@@ -498,10 +510,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_gather_rows(const int64_t* __res
     for (int j = 0; j < GATHER_U; ++j) {
       const int64_t k = k0 + j * step;
       slot[j] = -1;
-      if (k < u) {
-        const int64_t id = uni[k];
-        slot[j] = slot_map ? int64_t(slot_map[id]) : id;
-      }
+      if (k < u) slot[j] = slots ? int64_t(slots[k]) : uni[k];
     }
     V val[GATHER_U];
 #pragma unroll
@@ -542,7 +551,7 @@ static bool gather_stream_enabled() {
 
 template <typename V>
 static void launch_gather(const int64_t* uni, const int64_t* num_unique, const void* table,
-                          int64_t table_rows, int64_t row_bytes, const int32_t* slot_map,
+                          int64_t table_rows, int64_t row_bytes, const int32_t* slots,
                           void* rows, uint8_t* flags, int64_t cap, hipStream_t st) {
   const int cpr = int(row_bytes / int64_t(sizeof(V)));
   const int rpb = cpr >= DD_THREADS ? 1 : DD_THREADS / cpr;
@@ -552,11 +561,11 @@ static void launch_gather(const int64_t* uni, const int64_t* num_unique, const v
   if (cpr <= DD_THREADS) {
     if (sizeof(V) == 16 && gather_stream_enabled())
       hipLaunchKernelGGL((k_gather_rows<V, true>), dim3(uint32_t(nb)), dim3(DD_THREADS), 0, st, uni,
-                         num_unique, static_cast<const V*>(table), table_rows, cpr, rpb, slot_map,
+                         num_unique, static_cast<const V*>(table), table_rows, cpr, rpb, slots,
                          static_cast<V*>(rows), flags);
     else
       hipLaunchKernelGGL((k_gather_rows<V, false>), dim3(uint32_t(nb)), dim3(DD_THREADS), 0, st, uni,
-                         num_unique, static_cast<const V*>(table), table_rows, cpr, rpb, slot_map,
+                         num_unique, static_cast<const V*>(table), table_rows, cpr, rpb, slots,
                          static_cast<V*>(rows), flags);
   }
 }
@@ -657,17 +666,19 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
     }
   }
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-  // 3. uni and inv
+  // 3. uni and inv (and the slots of the unique ids, when rows or misses
+  // go through a slot map).  Without a slot map and with a row for every id
+  // (id_bound <= table_rows) nothing can miss: no flags, no scan, and the
+  // miss count is 0.
+  const bool all_hit = !slot_map && id_bound <= table_rows;
+  const bool want_miss = (miss || num_miss) && !all_hit;
+  int32_t* slots = slot_map && (rows || want_miss) ? w.slots : nullptr;
   const int64_t nbw = (W + DD_THREADS - 1) / DD_THREADS, nbi = (n + DD_THREADS - 1) / DD_THREADS;
   if (nbw + nbi > 0)
     hipLaunchKernelGGL(k_dedup_uni_inv, dim3(uint32_t(nbw + nbi)), dim3(DD_THREADS), 0, st, w.words, W,
-                       base, wshift, uni, ids, n, id_bound, inv, uint32_t(nbw));
+                       base, wshift, uni, ids, n, id_bound, inv, slot_map, slots, uint32_t(nbw));
 
-  // 4. rows through the slot map, miss flags, 5. ordered miss list.  Without
-  // a slot map and with a row for every id (id_bound <= table_rows) nothing
-  // can miss: no flags, no scan, and the miss count is 0.
-  const bool all_hit = !slot_map && id_bound <= table_rows;
-  const bool want_miss = (miss || num_miss) && !all_hit;
+  // 4. rows from their slots, miss flags, 5. ordered miss list.
   if (all_hit && num_miss)
     hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(64), 0, st, num_miss, int64_t(0));
   if (rows || want_miss) {
@@ -681,16 +692,16 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
       if (row_bytes / vb > DD_THREADS)
         return fail(FAST_ERR_UNSUPPORTED, "%s: row of %lld bytes is too wide", fn, (long long)row_bytes);
       if (vb == 16)
-        launch_gather<uint4>(uni, num_unique, table, table_rows, row_bytes, slot_map, rows, flags, n, st);
+        launch_gather<uint4>(uni, num_unique, table, table_rows, row_bytes, slots, rows, flags, n, st);
       else if (vb == 8)
-        launch_gather<uint2>(uni, num_unique, table, table_rows, row_bytes, slot_map, rows, flags, n, st);
+        launch_gather<uint2>(uni, num_unique, table, table_rows, row_bytes, slots, rows, flags, n, st);
       else if (vb == 4)
-        launch_gather<uint32_t>(uni, num_unique, table, table_rows, row_bytes, slot_map, rows, flags, n, st);
+        launch_gather<uint32_t>(uni, num_unique, table, table_rows, row_bytes, slots, rows, flags, n, st);
       else
-        launch_gather<uint16_t>(uni, num_unique, table, table_rows, row_bytes, slot_map, rows, flags, n, st);
+        launch_gather<uint16_t>(uni, num_unique, table, table_rows, row_bytes, slots, rows, flags, n, st);
     } else {
       // flags only: one 4-byte "row" per id, nothing copied
-      launch_gather<uint32_t>(uni, num_unique, nullptr, table_rows, 4, slot_map, nullptr, flags, n, st);
+      launch_gather<uint32_t>(uni, num_unique, nullptr, table_rows, 4, slots, nullptr, flags, n, st);
     }
     if (want_miss) {
       e = scan_launch(InFlags{w.flags, num_unique}, OutMiss{miss}, n, w.scan_n, num_miss, nullptr, st);
