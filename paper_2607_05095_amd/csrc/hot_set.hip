@@ -146,7 +146,7 @@ __device__ __forceinline__ int32_t clamp_count(int32_t f, int32_t max_freq) {
   return f < 0 ? 0 : (f > max_freq ? max_freq : f);
 }
 
-constexpr int HS_HIST_U = 4;
+constexpr int HS_HIST_U = 8;
 
 // hist[c] = number of ids whose clamped count is c, c in [0, max_freq].
 // Counts below HS_LDS_BINS go through a per-workgroup LDS histogram (almost
