@@ -626,7 +626,8 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
     """The fp64 oracle, single-threaded, on a bounded sample of the same batch:
     the first `frac` of the segments of each layer block and the matching
     share of node and edge ids, through the same sequence of operators,
-    repeated until about `min_seconds` of CPU time (at most 5 passes)."""
+    repeated until about `min_seconds` of CPU time (at most 5 passes); the
+    median pass time gives the rate."""
     import oracle
     from synth import omega_phi
     om, ph = omega_phi(b.d_t)
@@ -668,13 +669,13 @@ def cpu_baseline(b, step, torch, frac, min_seconds=10.0):
         t0 = time.perf_counter()
         one_pass()
         times.append(time.perf_counter() - t0)
-    dt = float(np.mean(times))
+    dt = float(np.median(times))
     res = {
         "value": sample_edges / dt, "unit": "sampled edges/s", "cores": 1, "kind": "oracle",
         "host_threads": os.cpu_count(), "cpu_model": host_cpu_model(),
         "sample": f"{frac:.0%} of the segments of each layer block ({sample_edges} sampled edges) "
                   f"and of the node/edge ids, through offsets, dedup+gather, time encoding and "
-                  f"fused attention fwd+bwd in fp64, single-threaded; mean of {len(times)} "
+                  f"fused attention fwd+bwd in fp64, single-threaded; median of {len(times)} "
                   f"passes, {sum(times):.1f} s in total",
         "seconds_per_pass": round(dt, 3),
     }
@@ -702,7 +703,7 @@ def segment_shares(blocks, T):
 
 
 def cpu_baseline_threads(blocks, node_ids, edge_ids, node_table, edge_table, slot, om, ph,
-                         scale, sample_edges, max_threads=16):
+                         scale, sample_edges, max_threads=16, passes=3):
     """The same oracle pass on all the host threads this process may use (at
     most `max_threads`): the per-destination operators (offsets, time encoding,
     fused attention fwd+bwd) of each layer block run over T disjoint
@@ -733,17 +734,21 @@ def cpu_baseline_threads(blocks, node_ids, edge_ids, node_table, edge_table, slo
         uni, _ = oracle.dedup(ids)
         oracle.gather(uni, table, sm)
 
+    walls = []
     with ThreadPoolExecutor(max_workers=T) as pool:
-        t0 = time.perf_counter()
-        futs = [pool.submit(rows, node_ids, node_table, None), pool.submit(rows, edge_ids, edge_table, slot)]
-        futs += [pool.submit(segments, sh) for sh in shares]
-        for f in futs:
-            f.result()
-        wall = time.perf_counter() - t0
+        for _ in range(passes):
+            t0 = time.perf_counter()
+            futs = [pool.submit(rows, node_ids, node_table, None),
+                    pool.submit(rows, edge_ids, edge_table, slot)]
+            futs += [pool.submit(segments, sh) for sh in shares]
+            for f in futs:
+                f.result()
+            walls.append(time.perf_counter() - t0)
+    wall = float(np.median(walls))
     return {"value": sample_edges / wall, "unit": "sampled edges/s", "cores": T,
             "seconds_per_pass": round(wall, 3),
-            "how": f"one pass of the same sample: {T} threads over disjoint segment ranges "
-                   f"plus the two dedup+gathers, unchanged oracle routines"}
+            "how": f"median of {passes} passes of the same sample: {T} threads over disjoint "
+                   f"segment ranges plus the two dedup+gathers, unchanged oracle routines"}
 
 
 def read_counters(workload):
