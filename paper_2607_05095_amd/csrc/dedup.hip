@@ -20,10 +20,12 @@
 //     records, ranked inside the bucket, and a scan over the bucket totals
 //     gives each bucket's base rank.  Only LDS atomics; every word record is
 //     written once, with no clearing pass;
-//   * hashed atomics (universes too large for buckets): the same LDS merge,
-//     then one global atomicOr per merged word into a cleared bitmap.
+//   * hashed atomics (universes too large for buckets, or batches with more
+//     than 2^24 (bucket, workgroup) counts): the same LDS merge, then one
+//     global atomicOr per merged word into a cleared bitmap.
 // Rows are then copied with 16/8/4-byte vector moves, one thread per vector
-// of a row, from the table slot that the optional cache slot map names.
+// of a row, from the table slot that the optional cache slot map names (the
+// slots are looked up with the unique ids, in the rank pass).
 #include <cstdlib>
 #include <cstring>
 
