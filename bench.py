@@ -532,7 +532,7 @@ def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3, with_oracle=F
                 sec, batches[0].size, "ids/s", f"one pre-sampled batch ({batches[0].size} ids)")
         del ids, ws
     fv, fe = freqs
-    B = fast.hot_set_budget(alpha, nb, eb)
+    B = fast.fast_hot_set_budget(alpha, nb, eb)
     hv = torch.empty(max(min(B, nb), 1), dtype=torch.int64, device="cuda")
     he = torch.empty(max(min(B, eb), 1), dtype=torch.int64, device="cuda")
     nhv = torch.empty(1, dtype=torch.int64, device="cuda")

@@ -216,8 +216,8 @@ fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets
  * freq_v [num_nodes], freq_e [num_edges]: device int32 counts (from
  * fast_access_count); counts outside [0, max_freq] are clamped into it, so
  * pass max_freq >= the largest count (the number of batches counted).
- * budget: number of ids to cache; Alg. 1's fraction alpha of all ids gives
- * budget = ceil(alpha * (num_nodes + num_edges)) evaluated in fp64.
+ * budget: number of ids to cache (fast_hot_set_budget turns Alg. 1's
+ * fraction alpha of all ids into it).
  * hot_v capacity min(budget, num_nodes), hot_e min(budget, num_edges); either
  * hot list and slot map may be NULL.  num_hot_v, num_hot_e: device int64.
  * Limits: num_nodes, num_edges < 2^31; 0 <= max_freq <= 2^24.
@@ -225,6 +225,15 @@ fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets
  * bytes, 256-byte aligned.
  * ------------------------------------------------------------------------ */
 size_t fast_greedy_hot_set_workspace(int64_t num_nodes, int64_t num_edges, int32_t max_freq);
+/* The budget of Alg. 1 (Sec. 4.2): its selection loop runs while
+ * i + j < alpha * (num_nodes + num_edges), the product evaluated in fp64, so
+ * it takes
+ *   *budget = min(num_nodes + num_edges, ceil(fl64(alpha * (num_nodes + num_edges))))
+ * ids, and 0 when that product is not positive.  A host computation (no
+ * device work, no stream); budget is a HOST pointer.  FAST_ERR_INVALID_ARG
+ * for a NULL budget, a NaN alpha, or a count outside [0, 2^52]. */
+fast_status_t fast_hot_set_budget(double alpha, int64_t num_nodes, int64_t num_edges,
+                                  int64_t* budget);
 fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_nodes, const int32_t* freq_e,
                                   int64_t num_edges, int32_t max_freq, int64_t budget,
                                   int64_t* hot_v, int64_t* num_hot_v, int32_t* slot_v,

@@ -19,7 +19,7 @@ __all__ = [
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
     "fast_dedup_gather_workspace", "fast_dedup_gather",
     "fast_access_count_workspace", "fast_access_count",
-    "fast_greedy_hot_set_workspace", "fast_greedy_hot_set", "hot_set_budget",
+    "fast_greedy_hot_set_workspace", "fast_greedy_hot_set", "fast_hot_set_budget",
     "fast_time_encode", "fast_time_encode_bwd_workspace", "fast_time_encode_bwd",
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
     "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
@@ -87,6 +87,7 @@ _SIGS = {
     "fast_access_count_workspace": (_sz, [_i64]),
     "fast_access_count": (_i32, [_p, _p, _i64, _i64, _p, _p, _sz, _p]),
     "fast_greedy_hot_set_workspace": (_sz, [_i64, _i64, _i32]),
+    "fast_hot_set_budget": (_i32, [C.c_double, _i64, _i64, _p]),
     "fast_greedy_hot_set": (_i32, [_p, _i64, _p, _i64, _i32, _i64, _p, _p, _p, _p, _p, _p, _p,
                                    _sz, _p]),
     "fast_time_encode": (_i32, [_G, _p, _p, _i32, _p, _i32, _p]),
@@ -250,12 +251,11 @@ def fast_greedy_hot_set(freq_v, num_nodes, freq_e, num_edges, max_freq, budget, 
                                      ws_bytes, _stream(stream)))
 
 
-def hot_set_budget(alpha: float, num_nodes: int, num_edges: int) -> int:
-    """Ids that Alg. 1's loop `while i + j < alpha * (|V| + |E|)` selects:
-    ceil of the fp64 product, at most |V| + |E|."""
-    import math
-    total = int(num_nodes) + int(num_edges)
-    return max(0, min(total, math.ceil(float(alpha) * float(total))))
+def fast_hot_set_budget(alpha: float, num_nodes: int, num_edges: int) -> int:
+    """Returns the budget the library computes (a host call)."""
+    out = C.c_int64(0)
+    _check(lib().fast_hot_set_budget(float(alpha), num_nodes, num_edges, C.byref(out)))
+    return out.value
 
 
 def fast_time_encode(g: TCSR, omega, phi, d_t, te, te_dtype, stream=None):

@@ -71,6 +71,14 @@ constexpr int ATT_MAX_BLOCK = 512;   // launch bound of every attention kernel
 constexpr int ATT_CH_FWD = FAST_ATT_CH_FWD;
 constexpr int ATT_CH_BWD = FAST_ATT_CH_BWD;
 constexpr int ATT_NSAVE = (FAST_ATT_SAVE_EDGES + ATT_CH_BWD - 1) / ATT_CH_BWD;
+// Every attention kernel is compiled for at most ATT_MAX_BLOCK threads per
+// workgroup (its register budget follows from that bound); a larger launch
+// is refused by the runtime, so the workgroup sizes may not exceed it.
+static_assert(ATT_BLOCK <= ATT_MAX_BLOCK && ATT_BLOCK_BWD <= ATT_MAX_BLOCK,
+              "attention workgroup size above the kernels' launch bound");
+static_assert(ATT_BLOCK % 64 == 0 && ATT_BLOCK_BWD % 64 == 0 && ATT_BLOCK >= 64 &&
+                  ATT_BLOCK_BWD >= 64,
+              "attention workgroup size must be a whole number of waves");
 
 struct AttnLayout {
   int H, dh, F;   // heads, head dim, F = H*dh
@@ -223,10 +231,13 @@ __device__ __forceinline__ float head_dot(const float (&a)[P][VE], const float (
 }
 
 __device__ __forceinline__ float lrelu(float x, float slope) { return x > 0.f ? x : slope * x; }
+// LeakyReLU' taken at the PRE-activation x (its sign picks the branch).  The
+// activated value cannot stand in for x: a negative slope maps both signs of
+// x to positive values.
 __device__ __forceinline__ float lrelu_grad(float x, float slope) { return x > 0.f ? 1.f : slope; }
 // Softmax in base 2: logits are formed as t = LReLU(pre * log2(e)) (LeakyReLU
-// is positively homogeneous, so t = log2(e) * LReLU(pre) and sign(t) =
-// sign(pre)), and exp(s - m) = exp2(t - m2) is one v_exp_f32.
+// is positively homogeneous, so t = log2(e) * LReLU(pre), and pre * log2(e)
+// has the sign of pre), and exp(s - m) = exp2(t - m2) is one v_exp_f32.
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -317,12 +328,13 @@ struct BwdState {
   float mx, Z, Dn;            // reference point (running max or lse, log2 units), sum w, sum w dalpha
 };
 
-// Edges [base, min(base+CH, e1)): loads K and V, forms t (log2-unit logit)
-// and dalpha = <dOut, V>, and folds them into the running sums.
+// Edges [base, min(base+CH, e1)): loads K and V, forms the pre-activation
+// x = pre * log2(e), the logit t = LReLU(x) and dalpha = <dOut, V>, and folds
+// them into the running sums.  Returns x (not t: LReLU' needs x's sign).
 template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX>
 __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m, int64_t base,
                                           int64_t e1, bool has_lse, float sl2,
-                                          BwdState<VE, P>& S, float (&t)[ATT_CH_BWD],
+                                          BwdState<VE, P>& S, float (&x)[ATT_CH_BWD],
                                           float (&da)[ATT_CH_BWD]) {
   const int F = a.L.F;
   const T* K = static_cast<const T*>(a.K);
@@ -334,15 +346,15 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
     load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kr[i]);
     load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vr[i]);
   }
-  float cm = -INFINITY;
+  float t[ATT_CH_BWD], cm = -INFINITY;
 #pragma unroll
   for (int i = 0; i < ATT_CH_BWD; ++i) {
     float kx[P][VE], vx[P][VE];
     unpack_row<T, VE, P>(kr[i], kx);
     unpack_row<T, VE, P>(vr[i], vx);
-    const float ti = lrelu(head_dot<VE, P, LPH_CT>(S.q, kx, m.lph) * sl2, a.slope);
+    x[i] = head_dot<VE, P, LPH_CT>(S.q, kx, m.lph) * sl2;
     da[i] = head_dot<VE, P, LPH_CT>(S.go, vx, m.lph);
-    t[i] = base + i < e1 ? ti : -INFINITY;
+    t[i] = base + i < e1 ? lrelu(x[i], a.slope) : -INFINITY;
     cm = fmaxf(cm, t[i]);
   }
   if (!has_lse) {
@@ -362,7 +374,7 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
 #pragma unroll
   for (int i = 0; i < ATT_CH_BWD; ++i) {
     const float w = exp2_hw(t[i] - S.mx);       // 0 for masked slots
-    const float wc = w * lrelu_grad(t[i], a.slope);
+    const float wc = w * lrelu_grad(x[i], a.slope);
     const float wcd = wc * da[i];
     S.Z += w;
     S.Dn = fmaf(w, da[i], S.Dn);
@@ -378,11 +390,12 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
   }
 }
 
+// dK, dV of edge e from its pre-activation x (log2 units) and dalpha.
 template <typename T, int VE, int P, bool NT, bool IDX>
-__device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m, int64_t e, float t,
+__device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m, int64_t e, float x,
                                          float da, float invZ, float D, const BwdState<VE, P>& S) {
-  const float al = exp2_hw(t - S.mx) * invZ;
-  const float g = al * (da - D) * lrelu_grad(t, a.slope) * a.scale;
+  const float al = exp2_hw(lrelu(x, a.slope) - S.mx) * invZ;
+  const float g = al * (da - D) * lrelu_grad(x, a.slope) * a.scale;
   if constexpr (IDX) {
     if (a.g_out) {                       // the head's first lane writes its coefficients
       if (m.l == 0) {
@@ -423,7 +436,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
   FAST_ZERO(S.A);
   FAST_ZERO(S.B);
 
-  // pass 1: stream K and V once; keep t and dalpha of the first NSAVE chunks
+  // pass 1: stream K and V once; keep x and dalpha of the first NSAVE chunks
   float st[ATT_NSAVE][ATT_CH_BWD], sda[ATT_NSAVE][ATT_CH_BWD];
 #pragma unroll
   for (int c = 0; c < ATT_NSAVE; ++c) {
@@ -466,9 +479,9 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
     }
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i) {
-      const float t = lrelu(head_dot<VE, P, LPH_CT>(S.q, kx[i], m.lph) * sl2, a.slope);
+      const float x = head_dot<VE, P, LPH_CT>(S.q, kx[i], m.lph) * sl2;
       const float da = head_dot<VE, P, LPH_CT>(S.go, vx[i], m.lph);
-      if (base + i < e1) bwd_emit<T, VE, P, NT, IDX>(a, m, base + i, t, da, invZ, D, S);
+      if (base + i < e1) bwd_emit<T, VE, P, NT, IDX>(a, m, base + i, x, da, invZ, D, S);
     }
   }
 }

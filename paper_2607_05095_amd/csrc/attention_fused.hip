@@ -154,6 +154,9 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
 #ifdef FAST_ATTN_FORCE_NT
   a.L.nt = true;   // tuning build: streaming policy whatever the row alignment
 #endif
+  if (a.L.block > ATT_MAX_BLOCK)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: workgroup of %d threads outside the launch bound %d",
+                fn, a.L.block, ATT_MAX_BLOCK);
   if (g->num_dst == 0) return ok();
   if (!g->dst_offsets) return fail(FAST_ERR_INVALID_ARG, "%s: dst_offsets is NULL", fn);
   a.N = g->num_dst;

@@ -186,7 +186,7 @@ struct RmBwdState {
 template <int H, int G, bool NT, bool IDX>
 __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& m, int64_t base,
                                              int64_t e1, bool has_lse, float sl2,
-                                             RmBwdState<H>& S, float (&t)[RM_CH_BWD][H],
+                                             RmBwdState<H>& S, float (&x)[RM_CH_BWD][H],
                                              float (&da)[RM_CH_BWD][H]) {
   const int F = a.L.F;
   const float* K = static_cast<const float*>(a.K);
@@ -198,7 +198,7 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
     rm_load_row<NT && !IDX, H>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
     rm_load_row<NT && !IDX, H>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
   }
-  float cm[H];
+  float t[RM_CH_BWD][H], cm[H];
 #pragma unroll
   for (int h = 0; h < H; ++h) cm[h] = -INFINITY;
 #pragma unroll
@@ -208,7 +208,8 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
     rm_dots<H, G>(S.go, vx[i], m, da[i]);
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-      t[i][h] = base + i < e1 ? lrelu(d[h] * sl2, a.slope) : -INFINITY;
+      x[i][h] = d[h] * sl2;
+      t[i][h] = base + i < e1 ? lrelu(x[i][h], a.slope) : -INFINITY;
       cm[h] = fmaxf(cm[h], t[i][h]);
     }
   }
@@ -235,7 +236,7 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
 #pragma unroll
     for (int h = 0; h < H; ++h) {
       const float w = exp2_hw(t[i][h] - S.mx[h]);      // 0 for masked slots
-      wc[h] = w * lrelu_grad(t[i][h], a.slope);
+      wc[h] = w * lrelu_grad(x[i][h], a.slope);
       wcd[h] = wc[h] * da[i][h];
       S.Z[h] += w;
       S.Dn[h] = fmaf(w, da[i][h], S.Dn[h]);
@@ -248,16 +249,17 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
   }
 }
 
+// dK, dV of edge e from its pre-activations x (log2 units) and dalpha.
 template <int H, bool NT, bool IDX>
 __device__ __forceinline__ void rm_bwd_emit(const AttnArgs& a, const RmMap<H>& m, int64_t e,
-                                            const float (&t)[H], const float (&da)[H],
+                                            const float (&x)[H], const float (&da)[H],
                                             const float (&invZ)[H], const float (&D)[H],
                                             const RmBwdState<H>& S) {
   float al[H], g[H];
 #pragma unroll
   for (int h = 0; h < H; ++h) {
-    al[h] = exp2_hw(t[h] - S.mx[h]) * invZ[h];
-    g[h] = al[h] * (da[h] - D[h]) * lrelu_grad(t[h], a.slope) * a.scale;
+    al[h] = exp2_hw(lrelu(x[h], a.slope) - S.mx[h]) * invZ[h];
+    g[h] = al[h] * (da[h] - D[h]) * lrelu_grad(x[h], a.slope) * a.scale;
   }
   if constexpr (IDX) {
     if (a.g_out) {                       // every lane holds all heads' values
@@ -303,7 +305,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
 #pragma unroll
   for (int k = 0; k < 4; ++k) S.A[k] = S.B[k] = 0.f;
 
-  // pass 1: stream K and V once; keep t and dalpha of the first chunks
+  // pass 1: stream K and V once; keep x and dalpha of the first chunks
   float st[ATT_RM_NSAVE][RM_CH_BWD][H], sda[ATT_RM_NSAVE][RM_CH_BWD][H];
 #pragma unroll
   for (int c = 0; c < ATT_RM_NSAVE; ++c) {
@@ -348,12 +350,12 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
     }
 #pragma unroll
     for (int i = 0; i < RM_CH_BWD; ++i) {
-      float d[H], da[H], t[H];
+      float d[H], da[H], x[H];
       rm_dots<H, G>(S.q, kx[i], m, d);
       rm_dots<H, G>(S.go, vx[i], m, da);
 #pragma unroll
-      for (int h = 0; h < H; ++h) t[h] = lrelu(d[h] * sl2, a.slope);
-      if (base + i < e1) rm_bwd_emit<H, NT, IDX>(a, m, base + i, t, da, invZ, D, S);
+      for (int h = 0; h < H; ++h) x[h] = d[h] * sl2;
+      if (base + i < e1) rm_bwd_emit<H, NT, IDX>(a, m, base + i, x, da, invZ, D, S);
     }
   }
 }

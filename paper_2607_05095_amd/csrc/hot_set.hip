@@ -21,6 +21,7 @@
 // pair (ids above T, ids at T) then gives every id its position among the
 // selected ids (above-T prefix + min(at-T prefix, R)), which is both the slot
 // in the id-ordered hot list and the value of the slot map.
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 
@@ -465,6 +466,27 @@ extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* ba
                        ids + batch_offsets[k], n, id_bound, int32_t(k + 1), stamp, freq);
   }
   return check_launch(fn);
+}
+
+// Alg. 1's loop runs while i + j < alpha * (|V| + |E|), the product taken in
+// fp64, and stops when both ranked lists are used up: the number of ids it
+// takes is the least integer not below that product, at most |V| + |E|.
+extern "C" fast_status_t fast_hot_set_budget(double alpha, int64_t num_nodes, int64_t num_edges,
+                                             int64_t* budget) {
+  const char* fn = "fast_hot_set_budget";
+  if (!budget) return fail(FAST_ERR_INVALID_ARG, "%s: budget is NULL", fn);
+  if (num_nodes < 0 || num_edges < 0 || num_nodes > (int64_t(1) << 52) ||
+      num_edges > (int64_t(1) << 52))
+    return fail(FAST_ERR_INVALID_ARG, "%s: id counts outside [0, 2^52]", fn);
+  if (alpha != alpha) return fail(FAST_ERR_INVALID_ARG, "%s: alpha is NaN", fn);
+  const int64_t total = num_nodes + num_edges;
+  const double x = alpha * double(total);   // exact integer conversion below 2^53
+  int64_t b;
+  if (!(x > 0.0)) b = 0;
+  else if (x >= double(total)) b = total;
+  else b = int64_t(std::ceil(x));
+  *budget = b;
+  return ok();
 }
 
 extern "C" size_t fast_greedy_hot_set_workspace(int64_t num_nodes, int64_t num_edges,

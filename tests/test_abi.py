@@ -246,10 +246,37 @@ def test_hot_set_validation_and_workspace_queries():
     assert sel(fe=None) == INVALID
     assert sel(wsb=ws - 1) == WORKSPACE
     assert sel(ws=FAKE + 8) == UNSUPPORTED                      # workspace alignment
-    assert fast.hot_set_budget(0.1, 5, 5) == 1                  # fp64 0.1 * 10 == 1.0
-    assert fast.hot_set_budget(0.15, 5, 5) == 2
-    assert fast.hot_set_budget(2.0, 5, 5) == 10
-    assert fast.hot_set_budget(0.0, 5, 5) == 0
+
+
+def test_hot_set_budget():
+    """Alg. 1's budget (Sec. 4.2): the library's count of ids equals the
+    number of ids the oracle's selection loop `while i + j < alpha(|V|+|E|)`
+    takes, with the product in fp64."""
+    import numpy as np
+    import oracle
+    b = fast.fast_hot_set_budget
+    assert b(0.1, 5, 5) == 1            # fl64(0.1 * 10) == 1.0 although 0.1 > 1/10 exactly
+    assert b(0.15, 5, 5) == 2
+    assert b(0.0, 5, 5) == 0
+    assert b(-0.5, 5, 5) == 0
+    assert b(1.0, 5, 5) == 10
+    assert b(1.5, 5, 5) == 10           # capped at |V| + |E|
+    assert b(float("inf"), 3, 4) == 7
+    assert b(0.5, 0, 0) == 0
+    assert b(1e-300, 1, 0) == 1         # any positive product takes one id
+    rng = np.random.default_rng(7)
+    for nv, ne in ((5, 5), (7, 3), (40, 25), (1, 0), (0, 6)):
+        fv = rng.integers(0, 4, nv).astype(np.int32)
+        fe = rng.integers(0, 4, ne).astype(np.int32)
+        for alpha in (0.0, 0.1, 0.15, 0.3, 1 / 3, 0.7, 1.0, 1.5):
+            hv, he = oracle.greedy_hot_set(fv, fe, alpha)
+            assert b(alpha, nv, ne) == hv.size + he.size, (nv, ne, alpha)
+    L = fast.lib()
+    out = ctypes.c_int64(0)
+    assert L.fast_hot_set_budget(0.5, -1, 5, ctypes.byref(out)) == INVALID
+    assert L.fast_hot_set_budget(0.5, 5, -1, ctypes.byref(out)) == INVALID
+    assert L.fast_hot_set_budget(float("nan"), 5, 5, ctypes.byref(out)) == INVALID
+    assert L.fast_hot_set_budget(0.5, 5, 5, None) == INVALID
 
 
 def test_sample_recent_validation():
@@ -343,3 +370,25 @@ def test_coefficient_form_validation():
     assert call(src=FAKE + 2) == UNSUPPORTED
     assert call(scal=FAKE + 2) == UNSUPPORTED
     assert call(rows=0, dst=None, ws=0) == OK    # nothing to write
+
+
+@pytest.mark.parametrize("flag", ["-DFAST_ATT_BLOCK_BWD=1024", "-DFAST_ATT_BLOCK=1024",
+                                  "-DFAST_ATT_BLOCK_BWD=96"])
+def test_attention_workgroup_outside_launch_bound_does_not_build(tmp_path, flag):
+    """Every attention kernel is compiled for at most 512 threads per
+    workgroup; a build whose workgroup size knob exceeds that (or is not a
+    whole number of waves) must fail to compile rather than launch a
+    workgroup the runtime refuses."""
+    hipcc = "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    src = tmp_path / "probe.hip"
+    src.write_text('#include "attention.h"\n')
+    csrc = os.path.join(ROOT, "paper_2607_05095_amd", "csrc")
+    cmd = [hipcc, "--offload-arch=gfx950", "-std=c++17", "-fsyntax-only", "-I",
+           os.path.join(ROOT, "include"), "-I", csrc, str(src)]
+    good = subprocess.run(cmd, capture_output=True, text=True)
+    assert good.returncode == 0, good.stderr
+    bad = subprocess.run(cmd + [flag], capture_output=True, text=True)
+    assert bad.returncode != 0
+    assert "static assertion failed" in bad.stderr

@@ -70,7 +70,7 @@ def test_access_count_and_selection_vs_oracle(cfg, k):
     assert np.array_equal(fv.cpu().numpy(), rv)
     assert np.array_equal(fe.cpu().numpy(), re_)
     for alpha in (0.0, 0.003, 0.01, 0.1, 0.35, 1.0, 1.5):
-        B = fast.hot_set_budget(alpha, nb, eb)
+        B = fast.fast_hot_set_budget(alpha, nb, eb)
         hv, he, sv, se = _select_gpu(fv, fe, k, B)
         ov, oe = oracle.greedy_hot_set(rv, re_, alpha)
         assert hv.size + he.size == B == ov.size + oe.size, alpha
@@ -121,7 +121,7 @@ def test_selection_edge_cases():
     fv_np = r.integers(0, 9000, 20000).astype(np.int32)
     fe_np = r.integers(0, 9000, 30000).astype(np.int32)
     for alpha in (0.001, 0.2, 0.77):
-        B = fast.hot_set_budget(alpha, fv_np.size, fe_np.size)
+        B = fast.fast_hot_set_budget(alpha, fv_np.size, fe_np.size)
         hv, he, _, _ = _select_gpu(dev(fv_np), dev(fe_np), 9000, B, want_slots=False)
         ov, oe = oracle.greedy_hot_set(fv_np, fe_np, alpha)
         assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe))
@@ -138,7 +138,7 @@ def test_bigdedup_universe_properties():
     re_ = oracle.access_count(edges, eb)
     assert np.array_equal(fe.cpu().numpy(), re_)
     del nodes, edges
-    B = fast.hot_set_budget(0.01, nb, eb)           # ~2.1e6 cached rows
+    B = fast.fast_hot_set_budget(0.01, nb, eb)           # ~2.1e6 cached rows
     hv, he, sv, se = _select_gpu(fv, fe, k, B)
     assert hv.size + he.size == B
     # threshold T: every selected count >= T >= every unselected count

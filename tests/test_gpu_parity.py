@@ -58,39 +58,39 @@ def _host(t):
     return t.detach().float().cpu().double().numpy()
 
 
-def _run_fused(d, with_lse=True):
+def _run_fused(d, with_lse=True, slope=SLOPE):
     o = d.ops
     out = d.empty(d.N)
     lse = d.scalars(d.N)
-    fast.fast_edge_attention_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, SLOPE,
+    fast.fast_edge_attention_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, slope,
                                  out, lse)
     dQ, dK, dV = d.empty(d.N), d.empty(d.E), d.empty(d.E)
-    fast.fast_edge_attention_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, SLOPE,
+    fast.fast_edge_attention_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], o["V"], d.scale, slope,
                                  lse if with_lse else None, o["dO"], dQ, dK, dV)
     return out, lse, dQ, dK, dV
 
 
-def _run_unfused(d):
+def _run_unfused(d, slope=SLOPE):
     o = d.ops
     alpha, lse = d.scalars(d.E), d.scalars(d.N)
-    fast.fast_edge_softmax_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, SLOPE, alpha, lse)
+    fast.fast_edge_softmax_fwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, slope, alpha, lse)
     out = d.empty(d.N)
     fast.fast_temporal_aggregate_fwd(d.g, d.H, d.dh, DT[d.dt], alpha, o["V"], out)
     dalpha, dV = d.scalars(d.E), d.empty(d.E)
     fast.fast_temporal_aggregate_bwd(d.g, d.H, d.dh, DT[d.dt], alpha, o["V"], o["dO"], dalpha, dV)
     dQ, dK = d.empty(d.N), d.empty(d.E)
-    fast.fast_edge_softmax_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, SLOPE, alpha,
+    fast.fast_edge_softmax_bwd(d.g, d.H, d.dh, DT[d.dt], o["Q"], o["K"], d.scale, slope, alpha,
                                dalpha, dQ, dK)
     return alpha, lse, out, dalpha, dV, dQ, dK
 
 
-def _check_block(d, segs=None, what=""):
+def _check_block(d, segs=None, what="", slope=SLOPE):
     """Fused and unfused operators vs the oracle on all (segs=None) or the
     sampled segments."""
     torch.cuda.synchronize()
-    fused = _run_fused(d, with_lse=True)
-    fused_nolse = _run_fused(d, with_lse=False)
-    unf = _run_unfused(d)
+    fused = _run_fused(d, with_lse=True, slope=slope)
+    fused_nolse = _run_fused(d, with_lse=False, slope=slope)
+    unf = _run_unfused(d, slope=slope)
     torch.cuda.synchronize()
     if segs is None:
         segs = np.arange(d.N, dtype=np.int64)
@@ -100,9 +100,9 @@ def _check_block(d, segs=None, what=""):
     ei = torch.as_tensor(eidx, device="cuda")
     K = _host(d.ops["K"][ei])
     V = _host(d.ops["V"][ei])
-    out, lse, alpha, _ = oracle.edge_attention_fwd(sub_off, Q, K, V, d.scale, SLOPE)
+    out, lse, alpha, _ = oracle.edge_attention_fwd(sub_off, Q, K, V, d.scale, slope)
     dalpha, _ = oracle.aggregate_bwd(sub_off, alpha, V, dO)
-    dQ, dK, dV, alts = bwd_reference_with_kinks(sub_off, Q, K, V, dO, d.scale, SLOPE)
+    dQ, dK, dV, alts = bwd_reference_with_kinks(sub_off, Q, K, V, dO, d.scale, slope)
     sg = torch.as_tensor(segs, device="cuda")
     nz = np.diff(sub_off) > 0
     # forward
@@ -182,6 +182,24 @@ def test_attention_edge_cases(name, counts, H, dh, dt):
         assert torch.equal(unf[0], torch.ones_like(unf[0]))
     if name == "all_empty":
         assert torch.count_nonzero(fused[0]) == 0 and torch.count_nonzero(fused[2]) == 0
+
+
+@pytest.mark.parametrize("slope", [-0.3, 0.0])
+@pytest.mark.parametrize("name,counts,H,dh,dt", [
+    ("rowmajor_f32", [10, 1, 0, 7, 30, 10, 25, 3, 12], 2, 50, "f32"),
+    ("headmajor_f32", [10, 1, 0, 7, 30, 10, 25, 3, 12], 4, 32, "f32"),
+    ("headmajor_bf16", [20, 1, 0, 7, 41, 20, 25, 3, 12], 4, 32, "bf16"),
+    ("headmajor_f32_dh50", [10, 2, 0, 29, 10], 3, 50, "f32"),
+])
+def test_attention_nonpositive_slope(name, counts, H, dh, dt, slope):
+    """LeakyReLU slopes of 0 and below: the backward's branch is the sign of
+    the pre-activation, which a negative slope hides in the activated logit.
+    Segments longer than the backward's register window re-read their rows,
+    so both of its paths are covered.  fp32 2 x 50 runs the row-major
+    kernels; the other shapes run the head-major ones."""
+    _announce(f"attention slope={slope} {name}")
+    d = _synthetic_block(counts * 8, H, dh, dt, seed=11 + len(counts))
+    _check_block(d, None, f"{name} slope={slope}", slope=slope)
 
 
 def test_attention_empty_graph_and_zero_edges():

@@ -512,7 +512,7 @@ def test_fwd_vs_torch_sdpa():
     np.testing.assert_allclose(out, ref[:, :, 0, :].numpy(), rtol=1e-12, atol=1e-12)
 
 
-@pytest.mark.parametrize("slope", [0.2, 1.0, 0.0])
+@pytest.mark.parametrize("slope", [0.2, 1.0, 0.0, -0.3])
 def test_fwd_vs_dense_masked_attention(slope):
     counts = [5, 0, 1, 3, 8, 2, 0, 6]
     off = _csr(counts)
@@ -608,15 +608,17 @@ def _loss(off, Q, K, V, dO, scale, slope):
     return float((out * dO).sum())
 
 
-def test_bwd_finite_differences_leaky():
+@pytest.mark.parametrize("slope", [SLOPE, 0.0, -0.3])
+def test_bwd_finite_differences_leaky(slope):
     counts = [3, 1, 6, 0, 4]
     off = _csr(counts)
     N, E, H, dh = len(counts), off[-1], 2, 4
     Q, K, V, dO = _rand_qkv(N, E, H, dh, 8)
     scale = 0.9
-    _, _, _, pre = oracle.edge_attention_fwd(off, Q, K, V, scale, SLOPE)
+    _, _, _, pre = oracle.edge_attention_fwd(off, Q, K, V, scale, slope)
     assert np.abs(pre).min() > 1e-3        # away from the LeakyReLU kink
-    dQ, dK, dV = oracle.edge_attention_bwd(off, Q, K, V, dO, scale, SLOPE)
+    assert (pre > 0).any() and (pre < 0).any()
+    dQ, dK, dV = oracle.edge_attention_bwd(off, Q, K, V, dO, scale, slope)
     h = 1e-6
     for name, X, G in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
         fd = np.zeros_like(X)
@@ -626,9 +628,9 @@ def test_bwd_finite_differences_leaky():
             Xm[idx] -= h
             args = {"Q": Q, "K": K, "V": V}
             args[name] = Xp
-            lp = _loss(off, args["Q"], args["K"], args["V"], dO, scale, SLOPE)
+            lp = _loss(off, args["Q"], args["K"], args["V"], dO, scale, slope)
             args[name] = Xm
-            lm = _loss(off, args["Q"], args["K"], args["V"], dO, scale, SLOPE)
+            lm = _loss(off, args["Q"], args["K"], args["V"], dO, scale, slope)
             fd[idx] = (lp - lm) / (2 * h)
         np.testing.assert_allclose(G, fd, rtol=1e-6, atol=1e-7, err_msg=name)
     assert np.all(dQ[3] == 0.0)             # empty segment
