@@ -156,6 +156,35 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
                                 void* ws, size_t ws_bytes, fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
+ * fast_dedup_gather without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and limits as
+ * fast_dedup_gather, minus ws/ws_bytes: its scratch is a fixed array of
+ * FAST_NOALLOC_SCRATCH_BYTES in the library's device code, one per GPU, held
+ * from the library's first use on that GPU until the process ends.  The call
+ * allocates and frees nothing.
+ *   - Size limit: problems whose fast_dedup_gather_workspace(n, id_bound)
+ *     exceeds FAST_NOALLOC_SCRATCH_BYTES return FAST_ERR_UNSUPPORTED before
+ *     anything is enqueued (every dedup of the 1e7-node / 2e8-edge batches
+ *     fits: at most 83 MB).
+ *   - Device: the stream (NULL = the null stream) must belong to the current
+ *     device; the scratch of that device is used (FAST_ERR_INVALID_ARG
+ *     otherwise).
+ *   - Sharing: every call on one GPU uses the same scratch, which keeps the
+ *     last call's contents (each call initialises what it reads).  Calls
+ *     that overlap on one GPU -- concurrent streams, or host threads without
+ *     ordering between their streams -- race on it and give wrong results;
+ *     calls on one stream run in order and are safe.
+ * ------------------------------------------------------------------------ */
+#define FAST_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+fast_status_t fast_dedup_gather_noalloc(const int64_t* ids, int64_t n, int64_t id_bound,
+                                        const void* table, int64_t table_rows, int D,
+                                        fast_dtype_t dtype, const int32_t* slot_map,
+                                        int64_t* uni, int32_t* inv, int64_t* num_unique,
+                                        void* rows, int32_t* miss, int64_t* num_miss,
+                                        fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
  * Most-recent-k temporal neighbour sampling (Sec. 6.1: top-k recent
  * sampling, k = 10 in the paper's experiments).  Root i is node roots[i]
  * queried at time root_t[i]; its candidates are the entries of that node

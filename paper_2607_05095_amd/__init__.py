@@ -17,7 +17,8 @@ __all__ = [
     "dtype_of", "fast_sample_recent_workspace", "fast_sample_recent",
     "fast_version", "fast_last_error",
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
-    "fast_dedup_gather_workspace", "fast_dedup_gather",
+    "fast_dedup_gather_workspace", "fast_dedup_gather", "fast_dedup_gather_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
     "fast_access_count_workspace", "fast_access_count",
     "fast_greedy_hot_set_workspace", "fast_greedy_hot_set", "fast_hot_set_budget",
     "fast_time_encode", "fast_time_encode_bwd_workspace", "fast_time_encode_bwd",
@@ -35,6 +36,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfast.so")
 
 F32, BF16 = 0, 1
+NOALLOC_SCRATCH_BYTES = 128 << 20   # FAST_NOALLOC_SCRATCH_BYTES of include/fast.h
 _STATUS = {0: "FAST_OK", 1: "FAST_ERR_INVALID_ARG", 2: "FAST_ERR_UNSUPPORTED",
            3: "FAST_ERR_WORKSPACE", 4: "FAST_ERR_HIP"}
 
@@ -82,6 +84,8 @@ _SIGS = {
     "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
                                  _p, _p, _p, _p, _sz, _p]),
+    "fast_dedup_gather_noalloc": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
+                                         _p, _p, _p, _p]),
     "fast_sample_recent_workspace": (_sz, [_i64]),
     "fast_sample_recent": (_i32, [_TG, _p, _p, _i64, _i32, _p, _p, _p, _p, _p, _sz, _p]),
     "fast_access_count_workspace": (_sz, [_i64]),
@@ -215,6 +219,14 @@ def fast_dedup_gather(ids, n, id_bound, table, table_rows, D, dtype, slot_map, u
                                    _ptr(slot_map), _ptr(uni), _ptr(inv), _ptr(num_unique),
                                    _ptr(rows), _ptr(miss), _ptr(num_miss), _ptr(ws), ws_bytes,
                                    _stream(stream)))
+
+
+def fast_dedup_gather_noalloc(ids, n, id_bound, table, table_rows, D, dtype, slot_map, uni, inv,
+                              num_unique, rows, miss, num_miss, stream=None):
+    _check(lib().fast_dedup_gather_noalloc(_ptr(ids), n, id_bound, _ptr(table), table_rows, D,
+                                           dtype, _ptr(slot_map), _ptr(uni), _ptr(inv),
+                                           _ptr(num_unique), _ptr(rows), _ptr(miss),
+                                           _ptr(num_miss), _stream(stream)))
 
 
 def fast_sample_recent_workspace(num_roots: int) -> int:

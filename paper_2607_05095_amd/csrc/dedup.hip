@@ -28,6 +28,7 @@
 // slots are looked up with the unique ids, in the rank pass).
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "scan.h"
 
@@ -583,13 +584,13 @@ extern "C" size_t fast_dedup_gather_workspace(int64_t n, int64_t id_bound) {
   return dedup_layout(n, id_bound, nullptr, nullptr);
 }
 
-extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
-                                           const void* table, int64_t table_rows, int D,
-                                           fast_dtype_t dtype, const int32_t* slot_map,
-                                           int64_t* uni, int32_t* inv, int64_t* num_unique,
-                                           void* rows, int32_t* miss, int64_t* num_miss,
-                                           void* ws, size_t ws_bytes, fast_stream_t stream) {
-  const char* fn = "fast_dedup_gather";
+// Both entry points: argument checks, then the launches on workspace ws.
+static fast_status_t dedup_gather_run(const char* fn, const int64_t* ids, int64_t n,
+                                      int64_t id_bound, const void* table, int64_t table_rows,
+                                      int D, fast_dtype_t dtype, const int32_t* slot_map,
+                                      int64_t* uni, int32_t* inv, int64_t* num_unique, void* rows,
+                                      int32_t* miss, int64_t* num_miss, void* ws, size_t ws_bytes,
+                                      fast_stream_t stream) {
   if (n < 0 || id_bound < 0 || table_rows < 0)
     return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
   if (n >= (int64_t(1) << 31)) return fail(FAST_ERR_UNSUPPORTED, "%s: n >= 2^31", fn);
@@ -711,4 +712,82 @@ extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_
     }
   }
   return check_launch(fn);
+}
+
+extern "C" fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
+                                           const void* table, int64_t table_rows, int D,
+                                           fast_dtype_t dtype, const int32_t* slot_map,
+                                           int64_t* uni, int32_t* inv, int64_t* num_unique,
+                                           void* rows, int32_t* miss, int64_t* num_miss,
+                                           void* ws, size_t ws_bytes, fast_stream_t stream) {
+  return dedup_gather_run("fast_dedup_gather", ids, n, id_bound, table, table_rows, D, dtype,
+                          slot_map, uni, inv, num_unique, rows, miss, num_miss, ws, ws_bytes,
+                          stream);
+}
+
+// ---------------------------------------------------------------- no allocation
+// Scratch of fast_dedup_gather_noalloc: a fixed device array in this code
+// object, so the call needs no workspace argument and allocates nothing.
+// Every GPU the library runs on holds its own copy until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: only
+// the per-device address from hipGetSymbolAddress is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[FAST_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+static fast_status_t scratch_for_current_device(const char* fn, hipStream_t st, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: hipGetDevice: %s", fn, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(FAST_ERR_UNSUPPORTED, "%s: device %d beyond the %d this library tracks", fn, dev,
+                kMaxDevices);
+  if (st) {   // the kernels run on the stream's device: it must be the current one
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(st, &sdev);
+    if (e != hipSuccess)
+      return fail(FAST_ERR_HIP, "%s: hipStreamGetDevice: %s", fn, hipGetErrorString(e));
+    if (sdev != dev)
+      return fail(FAST_ERR_INVALID_ARG, "%s: stream of device %d but device %d is current", fn,
+                  int(sdev), dev);
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(FAST_ERR_HIP, "%s: hipGetSymbolAddress(scratch): %s", fn, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FAST_OK;
+}
+
+extern "C" fast_status_t fast_dedup_gather_noalloc(const int64_t* ids, int64_t n, int64_t id_bound,
+                                                   const void* table, int64_t table_rows, int D,
+                                                   fast_dtype_t dtype, const int32_t* slot_map,
+                                                   int64_t* uni, int32_t* inv,
+                                                   int64_t* num_unique, void* rows, int32_t* miss,
+                                                   int64_t* num_miss, fast_stream_t stream) {
+  const char* fn = "fast_dedup_gather_noalloc";
+  if (n < 0 || id_bound < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
+  if (id_bound > kMaxIdBound) return fail(FAST_ERR_UNSUPPORTED, "%s: id_bound > 2^35", fn);
+  const size_t need = dedup_layout(n, id_bound, nullptr, nullptr);
+  if (need > size_t(FAST_NOALLOC_SCRATCH_BYTES))
+    return fail(FAST_ERR_UNSUPPORTED,
+                "%s: n = %lld ids over id_bound = %lld need %zu bytes of scratch, more than the "
+                "%zu this variant holds; call fast_dedup_gather with a workspace",
+                fn, (long long)n, (long long)id_bound, need, size_t(FAST_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  const fast_status_t s = scratch_for_current_device(fn, static_cast<hipStream_t>(stream), &ws);
+  if (s != FAST_OK) return s;
+  return dedup_gather_run(fn, ids, n, id_bound, table, table_rows, D, dtype, slot_map, uni, inv,
+                          num_unique, rows, miss, num_miss, ws, size_t(FAST_NOALLOC_SCRATCH_BYTES),
+                          stream);
 }
