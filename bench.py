@@ -12,11 +12,15 @@ value = sampled edges per step / step time.  The roofline entry covers the
 dominant kernel, the fused backward of the layer-1 block, timed with HIP
 events on the stream it runs on.
 
-    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large] [--no-pipelined]
+    python bench.py [--steps K] [--warmup W] [--workload bigdedup|large] [--also W2,...]
+                    [--no-pipelined]
 
 `value` times the steps serially on one stream (prep, then attention).  The
 line also reports the same steps software-pipelined (unless --no-pipelined):
-prep of batch i+1 on a second stream overlaps attention of batch i.
+prep of batch i+1 on a second stream overlaps attention of batch i.  By
+default the 1e7-node fp32 workload (bigdedup) is the headline and the bf16
+workload with fan-out 20 (large) is measured after it in the same run, under
+the key "large", with its own roofline entry and oracle baseline.
 """
 from __future__ import annotations
 
@@ -771,48 +775,19 @@ def read_traffic(workload):
     return read_counters(workload).get("bytes_per_launch")
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="bigdedup")
-    ap.add_argument("--cpu-frac", type=float, default=1.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-pipelined", dest="pipelined", action="store_false",
-                    help="skip the second timing of the steps software-pipelined over two streams")
-    ap.add_argument("--graph", action="store_true",
-                    help="also time the serial step captured once as a HIP graph and replayed")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device copy (counter calibration)")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "bench.py runs on one GPU only; the multi-GPU sharding "
-                                   "design is described but not built", "n_gpus": args.gpus}))
-        sys.exit(2)
-
-    import torch
-    import paper_2607_05095_amd as fast
-
-    if args.copy_calibration:
-        x = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
-        y = torch.empty_like(x)
-        for _ in range(5):
-            y.copy_(x)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_each_way": x.numel() * 4, "copies": 5}))
-        return
-
+def measure(name, args, torch, fast, headline):
+    """Builds workload `name`, times K serial steps and the fused attention
+    sequence, and returns its result dict.  The headline workload also gets
+    the pipelined and graph timings and the widened operators."""
     from synth import make_batch
-    b = make_batch(WORKLOADS[args.workload])
+    b = make_batch(WORKLOADS[name])
     log(f"workload {b.name}: blocks {[(x.num_dst, x.num_edges) for x in b.blocks]}")
     step = Step(b, torch, fast)
     side = torch.cuda.Stream()
     torch.cuda.synchronize()
     for _ in range(args.warmup):
         step.run_serial()
-    if args.pipelined:
+    if headline and args.pipelined:
         step.run_pipelined(max(args.warmup, 1), side)
     torch.cuda.synchronize()
     log("warmup done")
@@ -836,16 +811,16 @@ def main():
             step.run_serial(rec, dominant)
     ms = timed(serial_steps)
     bwd_ms = float(np.mean([s.elapsed_time(e) for s, e in rec["attn_bwd_L1"]]))
-    log(f"{ms:.3f} ms/step (serial)")
+    log(f"{name}: {ms:.3f} ms/step (serial)")
     # optionally, the same K steps software-pipelined over two streams
     ms_pipe = None
-    if args.pipelined:
+    if headline and args.pipelined:
         ms_pipe = timed(lambda: step.run_pipelined(args.steps, side))
         log(f"{ms_pipe:.3f} ms/step (pipelined)")
 
     # optionally, the serial step captured once as a HIP graph, replayed K times
     ms_graph = None
-    if args.graph:
+    if headline and args.graph:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             step.run_serial()
@@ -861,8 +836,10 @@ def main():
     torch.cuda.synchronize()
     breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec_all.items()}
 
-    widened = widened_ops(b, step, torch, fast, with_oracle=not args.no_cpu_baseline)
-    log(f"widened ops: {widened}")
+    widened = None
+    if headline:
+        widened = widened_ops(b, step, torch, fast, with_oracle=not args.no_cpu_baseline)
+        log(f"widened ops: {widened}")
 
     esz = 4 if b.dtype == "f32" else 2
     F = b.H * b.dh
@@ -873,22 +850,20 @@ def main():
     fused_bytes = sum(attn_fwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) +
                       attn_bwd_bytes(x.num_dst, x.num_edges, F, esz, b.H) for x in b.blocks)
     fused_bytes_no_lse = sum((6 * x.num_edges + 5 * x.num_dst) * F * esz for x in b.blocks)
+    counters = read_counters(name)
     roofline = {
         "kernel": "k_attn_bwd (fused ESM+AGG backward, layer-1 block)",
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(args.workload),
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": counters.get("bytes_per_launch"),
         "algorithmic_bytes_per_launch": bwd_bytes, "avg_launch_ms": round(bwd_ms, 4),
-        "l2_hit_rate": read_counters(args.workload).get("l2_hit_rate"),
-        "occupancy_pct": read_counters(args.workload).get("occupancy_pct"),
+        "l2_hit_rate": counters.get("l2_hit_rate"),
+        "occupancy_pct": counters.get("occupancy_pct"),
     }
     result = {
-        "metric": METRIC,
         "value": b.sampled_edges / (ms * 1e-3),
         "unit": "sampled edges/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": b.dtype, "data": "synthetic",
+        "dtype": b.dtype,
         "config": describe(b),
         "roofline": roofline,
         "fused_attention": {
@@ -900,18 +875,11 @@ def main():
             "algorithmic_bytes_without_lse": fused_bytes_no_lse,
             "hbm_frac_without_lse": round(fused_bytes_no_lse / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
-        "time_encode": time_encode_summary(b, breakdown, read_counters(args.workload)),
-        "schedule": "serial: prep (offsets, time encoding, dedup+gather) then attention of each "
-                    "batch on one stream",
-
+        "time_encode": time_encode_summary(b, breakdown, counters),
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
-        "widened_ops": widened,
-        "widened_note": "operators beyond the timed step, timed alone outside the timed region; "
-                        "with the CPU baseline, each also gives the oracle's rate on a bounded sample",
-        "breakdown_note": "operators timed one by one in 3 extra serial steps outside the timed region",
-        "kernel_source_sha": kernel_source_hash(),
-        "paper_context": PAPER_CONTEXT,
     }
+    if widened is not None:
+        result["widened_ops"] = widened
     if ms_pipe is not None:
         result["pipelined"] = {
             "ms_per_step": round(ms_pipe, 4),
@@ -926,11 +894,92 @@ def main():
             "schedule": "the serial step captured once as a HIP graph, replayed K times",
         }
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle) ...")
-        result["cpu_baseline"] = cpu_baseline(b, step, torch, args.cpu_frac)
-        result["cpu_baseline"]["gpu_over_cpu"] = round(result["value"] / result["cpu_baseline"]["value"], 1)
-        allc = result["cpu_baseline"]["all_cores"]
-        allc["gpu_over_cpu"] = round(result["value"] / allc["value"], 1)
+        log(f"{name}: cpu baseline (oracle) ...")
+        cb = cpu_baseline(b, step, torch, args.cpu_frac)
+        cb["gpu_over_cpu"] = round(result["value"] / cb["value"], 1)
+        cb["all_cores"]["gpu_over_cpu"] = round(result["value"] / cb["all_cores"]["value"], 1)
+        result["cpu_baseline"] = cb
+    del step
+    return result
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="bigdedup",
+                    help="the headline workload of the line")
+    ap.add_argument("--also", default=None,
+                    help="comma-separated workloads measured after the headline one, each under "
+                         "its own key (default: large when the headline is bigdedup; 'none' "
+                         "measures the headline only)")
+    ap.add_argument("--cpu-frac", type=float, default=1.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pipelined", dest="pipelined", action="store_false",
+                    help="skip the second timing of the steps software-pipelined over two streams")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the serial step captured once as a HIP graph and replayed")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "bench.py runs on one GPU only; the multi-GPU sharding "
+                                   "design is described but not built", "n_gpus": args.gpus}))
+        sys.exit(2)
+    if args.also is None:
+        also = ["large"] if args.workload == "bigdedup" else []
+    else:
+        also = [w for w in args.also.split(",") if w and w != "none"]
+    for w in also:
+        if w not in WORKLOADS or w == args.workload:
+            ap.error(f"--also: unknown or repeated workload {w!r}")
+
+    import torch
+    import paper_2607_05095_amd as fast
+
+    if args.copy_calibration:
+        x = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_each_way": x.numel() * 4, "copies": 5}))
+        return
+
+    head = measure(args.workload, args, torch, fast, headline=True)
+    result = {
+        "metric": METRIC,
+        "value": head.pop("value"),
+        "unit": head.pop("unit"),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": head.pop("ms_per_step"),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": head.pop("dtype"), "data": "synthetic",
+        "config": head.pop("config"),
+    }
+    cb = head.pop("cpu_baseline", None)
+    result.update(head)
+    result.update({
+        "schedule": "serial: prep (offsets, time encoding, dedup+gather) then attention of each "
+                    "batch on one stream",
+        "widened_note": "operators beyond the timed step, timed alone outside the timed region; "
+                        "with the CPU baseline, each also gives the oracle's rate on a bounded sample",
+        "breakdown_note": "operators timed one by one in 3 extra serial steps outside the timed region",
+        "kernel_source_sha": kernel_source_hash(),
+        "paper_context": PAPER_CONTEXT,
+    })
+    if cb is not None:
+        result["cpu_baseline"] = cb
+    for w in also:
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        r = measure(w, args, torch, fast, headline=False)
+        r["note"] = ("measured in the same run after the headline workload's buffers were freed: "
+                     "K serial steps, the fused attention sequence, the dominant kernel's roofline "
+                     "and the oracle on the same batch")
+        result[w] = r
     print(json.dumps(result), flush=True)
 
 

@@ -8,6 +8,9 @@ Integer and byte outputs are compared bit-exactly.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import torch
 
@@ -117,3 +120,119 @@ def assert_bwd_close(dQ_gpu, dK_gpu, sub_off, dQ, dK, alts, dt, what):
                  np.all(np.abs(gk - k) <= atol + rtol * np.abs(k)) for q, k in options)
         assert ok, f"{what}: segment {v} with an ambiguous logit matches no branch choice"
     return N
+
+
+# ------------------------------------------------------------------ whole blocks on all host threads
+def host_threads(limit: int = 16) -> int:
+    """Threads for the oracle: the CPUs this process may use, at most `limit`."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(limit, n))
+
+
+def segment_ranges(off: np.ndarray, parts: int):
+    """Cuts the segments of a block into at most `parts` contiguous ranges
+    [a, c) of about equal edge counts (a destination's edges stay together)."""
+    off = np.asarray(off, dtype=np.int64)
+    N, E = off.shape[0] - 1, int(off[-1])
+    if N == 0:
+        return []
+    cuts = np.searchsorted(off, np.linspace(0, E, parts + 1), side="left").astype(np.int64)
+    cuts = np.clip(cuts, 0, N)
+    cuts[0], cuts[-1] = 0, N
+    cuts = np.maximum.accumulate(cuts)
+    return [(int(a), int(c)) for a, c in zip(cuts[:-1], cuts[1:]) if c > a]
+
+
+def over_ranges(fn, ranges, threads=None):
+    """fn(a, c) on every range, on the host threads; the oracle's C routines
+    run outside the interpreter lock.  Re-raises the first failure."""
+    with ThreadPoolExecutor(threads or host_threads()) as ex:
+        return list(ex.map(lambda r: fn(*r), ranges))
+
+
+def _f64(t):
+    if isinstance(t, torch.Tensor):
+        return t.double().numpy()
+    return np.asarray(t, dtype=np.float64)
+
+
+def check_attention_block_full(off, ins, fused, fused_nolse, unfused, scale, slope, dt, what,
+                               parts=None):
+    """Every segment of a layer block against the oracle.  ins: host tensors
+    Q, K, V, dO in the storage dtype.  fused / fused_nolse: host (out, lse,
+    dQ, dK, dV) of the fused pair with and without the saved lse (out and
+    lse of the second are not compared; None skips it); unfused: host (alpha, lse, out,
+    dalpha, dV, dQ, dK) of the operator chain, or None.  The block is cut
+    into contiguous segment ranges, each checked on its own host thread
+    against the oracle run on that range alone."""
+    off = np.asarray(off, dtype=np.int64)
+    T = host_threads()
+    ranges = segment_ranges(off, parts or 4 * T)
+
+    def one(a, c):
+        ea, ec = int(off[a]), int(off[c])
+        sub = (off[a:c + 1] - ea).astype(np.int32)
+        Q, dO = _f64(ins["Q"][a:c]), _f64(ins["dO"][a:c])
+        K, V = _f64(ins["K"][ea:ec]), _f64(ins["V"][ea:ec])
+        tag = f"{what} segments [{a}, {c})"
+        out, lse, alpha, _ = oracle.edge_attention_fwd(sub, Q, K, V, scale, slope)
+        dQ, dK, dV, alts = bwd_reference_with_kinks(sub, Q, K, V, dO, scale, slope)
+        nz = np.diff(sub) > 0
+        g_out, g_lse = fused[0][a:c], _f64(fused[1][a:c])
+        assert_close(g_out, out, dt, tag + " fused out")
+        assert_close(g_lse[nz], lse[nz], "f32", tag + " fused lse")
+        assert np.all(np.isneginf(g_lse[~nz])), tag + ": empty segment lse must be -inf"
+        for name, r in (("lse", fused), ("nolse", fused_nolse)):
+            if r is None:
+                continue
+            assert_close(r[4][ea:ec], dV, dt, f"{tag} fused[{name}] dV")
+            assert_bwd_close(r[2][a:c], r[3][ea:ec], sub, dQ, dK, alts, dt, f"{tag} fused[{name}]")
+        if unfused is not None:
+            dalpha, _ = oracle.aggregate_bwd(sub, alpha, V, dO)
+            u_alpha, u_lse, u_out, u_dalpha, u_dV, u_dQ, u_dK = unfused
+            assert_close(u_alpha[ea:ec], alpha, "f32", tag + " ESM alpha")
+            assert_close(_f64(u_lse[a:c])[nz], lse[nz], "f32", tag + " ESM lse")
+            assert_close(u_out[a:c], out, dt, tag + " AGG out")
+            assert_close(u_dalpha[ea:ec], dalpha, "f32", tag + " AGG dalpha")
+            assert_close(u_dV[ea:ec], dV, dt, tag + " AGG dV")
+            assert_bwd_close(u_dQ[a:c], u_dK[ea:ec], sub, dQ, dK, alts, dt, tag + " ESM-bwd")
+        return c - a
+
+    done = over_ranges(one, ranges, T)
+    assert sum(done) == off.shape[0] - 1
+    return len(ranges)
+
+
+def check_time_encode_full(off, dst_t, edge_t, omega, phi, te, dt, what, parts=None):
+    """Every row of a block's time encoding (te: host tensor [E, d_t]) against
+    the oracle, over contiguous segment ranges on the host threads."""
+    off = np.asarray(off, dtype=np.int64)
+    T = host_threads()
+    ranges = segment_ranges(off, parts or 4 * T)
+
+    def one(a, c):
+        ea, ec = int(off[a]), int(off[c])
+        sub = (off[a:c + 1] - ea).astype(np.int32)
+        ref = oracle.time_encode(sub, dst_t[a:c], edge_t[ea:ec], omega, phi)
+        assert_close(te[ea:ec], ref, dt, f"{what} segments [{a}, {c})")
+        return ec - ea
+
+    assert sum(over_ranges(one, ranges, T)) == int(off[-1])
+
+
+def oracle_sample_chunks(g, roots, rt, k, chunk):
+    """The oracle over consecutive chunks of roots on all host threads (each
+    root's result depends on that root alone), concatenated into one block."""
+    cuts = list(range(0, roots.size, chunk)) + [roots.size]
+    parts = over_ranges(lambda a, c: oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots[a:c],
+                                                          rt[a:c], k),
+                        [(a, c) for a, c in zip(cuts[:-1], cuts[1:]) if c > a])
+    if not parts:
+        return np.zeros(1, np.int32), np.zeros(0, np.int64), np.zeros(0, np.float32), np.zeros(0, np.int64)
+    base = np.cumsum([0] + [int(p[0][-1]) for p in parts[:-1]])
+    off = np.concatenate([[0]] + [p[0][1:].astype(np.int64) + b for p, b in zip(parts, base)])
+    return (off.astype(np.int32), np.concatenate([p[1] for p in parts]),
+            np.concatenate([p[2] for p in parts]), np.concatenate([p[3] for p in parts]))

@@ -13,7 +13,8 @@ import torch
 import oracle
 import paper_2607_05095_amd as fast
 from synth import make_batch, omega_phi
-from tests.parity import SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks
+from tests.parity import (SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks,
+                          check_attention_block_full, check_time_encode_full)
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
@@ -70,6 +71,47 @@ def test_bench_step_matches_the_oracle(cfg):
         got = x["rows"][:u].cpu().numpy() if b.dtype == "f32" else x["rows"][:u].view(torch.int16).cpu().numpy()
         assert np.array_equal(got[hit], rows[hit]), name + " rows"
         assert int(x["nm"].item()) == miss.size, name + " misses"
+
+
+@pytest.mark.parametrize("workload", ["bigdedup", "large"])
+def test_bench_step_full_size_matches_the_oracle(workload):
+    """The step the benchmark times, at its full size: one serial step of
+    bench.Step, then every output of it against the oracle -- offsets and
+    dedup + gather bit-exact, the time encoding row by row and the fused
+    attention segment by segment over ranges on all host threads."""
+    b = make_batch(bench.WORKLOADS[workload])
+    print(f"[parity] bench step {workload} (full size)", flush=True)
+    step = bench.Step(b, torch, fast)
+    step.run_serial()
+    torch.cuda.synchronize()
+    om, ph = omega_phi(b.d_t)
+    for i, (blk, d) in enumerate(zip(b.blocks, step.blocks)):
+        what = f"{workload}/L{i + 1}"
+        print(f"[parity]   {what}: N={blk.num_dst} E={blk.num_edges}", flush=True)
+        off = oracle.csr_offsets(blk.counts)
+        assert np.array_equal(d["off"][0].cpu().numpy(), off), what + " offsets"
+        check_time_encode_full(off, blk.dst_t, blk.edge_t, om, ph, d["te"][0].cpu(), b.dtype,
+                               what + " time encoding")
+        ins = {k: d[k].cpu() for k in ("Q", "K", "V", "dO")}
+        outs = [d[k].cpu() for k in ("out", "lse", "dQ", "dK", "dV")]
+        check_attention_block_full(off, ins, outs, None, None, step.scale, SLOPE, b.dtype,
+                                   what + " attention")
+        del ins, outs
+    for name, ids, x in (("nodes", b.node_ids, step.node[0]), ("edges", b.edge_ids, step.edge[0])):
+        print(f"[parity]   {workload} dedup + gather of {name}: n={ids.size}", flush=True)
+        uni, inv = oracle.dedup(ids)
+        u = int(x["nu"].item())
+        assert u == uni.size and np.array_equal(x["uni"][:u].cpu().numpy(), uni), name
+        assert np.array_equal(x["inv"].cpu().numpy(), inv), name
+        bits = torch.int32 if b.dtype == "f32" else torch.int16
+        slot = None if x["slot"] is None else x["slot"].cpu().numpy()
+        rows, hit, miss = oracle.gather(uni, x["table"].view(bits).cpu().numpy(), slot)
+        got = x["rows"][:u].view(bits).cpu().numpy()
+        assert np.array_equal(got[hit], rows[hit]), name + " rows"
+        m = int(x["nm"].item())
+        assert m == miss.size and np.array_equal(x["miss"][:m].cpu().numpy(), miss), name + " misses"
+    del step
+    torch.cuda.empty_cache()
 
 
 def test_pipelined_schedule_leaves_the_serial_results():

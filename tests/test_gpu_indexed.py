@@ -3,10 +3,11 @@ reading K and V through an index into de-duplicated rows (forward and
 per-edge backward), the occurrence lists of an index (bit-exact), and the
 transposed gather that turns per-edge gradients into row gradients.
 
-Each GPU op is compared with the oracle on the same inputs: the attention
-against the oracle on the gathered rows (sampled segments at the full-size
-workloads), the occurrence lists bit-exactly, and the row sums against the
-oracle's fp64 sums of the same per-edge rows.
+Each GPU op is compared with the oracle on the same inputs, every segment
+and every row at every workload: the attention against the oracle on the
+gathered rows (over segment ranges on all host threads), the occurrence
+lists bit-exactly, and the row sums against the oracle's fp64 sums of the
+same per-edge rows or coefficients.
 """
 import numpy as np
 import pytest
@@ -16,7 +17,7 @@ import oracle
 import paper_2607_05095_amd as fast
 from synth import _randn, make_batch
 from tests.parity import (SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks,
-                          sample_segments, sub_csr, tdtype, to_dev)
+                          check_attention_block_full, over_ranges, segment_ranges, tdtype, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -103,63 +104,60 @@ def _indexed_block(b, i, seed):
     return blk, kidx.astype(np.int32), vidx.astype(np.int32), Uk, Uv, ops
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
-def test_indexed_attention_workloads(cfg):
+BLOCKS = [(0, 0), (1, 0), (2, 0), (2, 1), (3, 0), (3, 1), (4, 0), (4, 1)]
+
+
+def _cpu(t):
+    return t.detach().cpu()
+
+
+def _rows_full(occ_off, occ, idx, U, E, per_edge, H, dh, what):
+    """Occurrence lists bit-exact, then every row's ordered fp64 sum of the
+    per-edge gradients against the oracle's."""
+    w_off, w_occ = oracle.occurrence_csr(idx, U)
+    assert np.array_equal(occ_off.cpu().numpy(), w_off), f"{what} occ_off"
+    assert np.array_equal(occ.cpu().numpy()[:E], w_occ), f"{what} occ"
+    got = _index_add_gpu(occ_off, occ, E, U, per_edge.reshape(E, H * dh)).cpu()
+    want = oracle.index_add_rows(idx, U, _host(per_edge.reshape(E, H * dh)))
+    assert_close(got, want, "f32", f"{what} rows")
+
+
+@pytest.mark.parametrize("cfg,i", BLOCKS)
+def test_indexed_attention_workloads(cfg, i):
+    """Every segment of the block (forward and per-edge backward) and every
+    row gradient against the oracle on the gathered rows."""
     b = make_batch(cfg)
-    for i, blk in enumerate(b.blocks):
-        _announce(f"indexed attention cfg={cfg} block={i}")
-        blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
-        off = oracle.csr_offsets(blk.counts)
-        N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
-        scale = float(np.float32(1 / np.sqrt(dh)))
-        d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
-        g = fast.tcsr(d_off, E)
-        tt = tdtype(dt)
-        out = torch.empty((N, H, dh), dtype=tt, device="cuda")
-        lse = torch.empty((N, H), device="cuda")
-        fast.fast_edge_attention_fwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v, Uv,
-                                             scale, SLOPE, out, lse)
-        dQ = torch.empty((N, H, dh), dtype=tt, device="cuda")
-        dKe = torch.empty((E, H, dh), dtype=tt, device="cuda")
-        dVe = torch.empty((E, H, dh), dtype=tt, device="cuda")
-        fast.fast_edge_attention_bwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v,
-                                             Uv, scale, SLOPE, lse, o["dO"], dQ, dKe, dVe)
-        torch.cuda.synchronize()
-        segs = np.arange(N) if E <= 200_000 else \
-            sample_segments(N, 1500, seed=cfg * 10 + i, include=[0, N - 1])
-        sub_off, eidx = sub_csr(off, segs)
-        sg, ei = torch.as_tensor(segs, device="cuda"), torch.as_tensor(eidx, device="cuda")
-        Q64, dO64 = _host(o["Q"][sg]), _host(o["dO"][sg])
-        K64 = _host(o["K"][torch.as_tensor(kidx[eidx].astype(np.int64), device="cuda")])
-        V64 = _host(o["V"][torch.as_tensor(vidx[eidx].astype(np.int64), device="cuda")])
-        r_out, r_lse, _, _ = oracle.edge_attention_fwd(sub_off, Q64, K64, V64, scale, SLOPE)
-        r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(sub_off, Q64, K64, V64, dO64, scale, SLOPE)
-        what = f"cfg{cfg}/L{i + 1} indexed"
-        assert_close(out[sg], r_out, dt, what + " out")
-        nz = np.diff(sub_off) > 0
-        assert_close(_host(lse[sg])[nz], r_lse[nz], "f32", what + " lse")
-        assert_close(dVe[ei], r_dV, dt, what + " dV_edge")
-        assert_bwd_close(dQ[sg], dKe[ei], sub_off, r_dQ, r_dK, alts, dt, what)
-        # row gradients: occurrence lists bit-exact, then the ordered fp64 sums
-        # of the per-edge gradients (compared on a sample of rows, hubs included)
-        for name, idx, U, per_edge in (("K", kidx, Uk, dKe), ("V", vidx, Uv, dVe)):
-            occ_off, occ = _occ_gpu(idx, U)
-            w_off, w_occ = oracle.occurrence_csr(idx, U)
-            assert np.array_equal(occ_off.cpu().numpy(), w_off), f"{what} occ_off {name}"
-            assert np.array_equal(occ.cpu().numpy()[:E], w_occ), f"{what} occ {name}"
-            rows_grad = _index_add_gpu(occ_off, occ, E, U, per_edge.reshape(E, H * dh))
-            counts = np.diff(w_off)
-            pick = np.unique(np.concatenate([np.argsort(counts)[-20:],
-                                             np.random.default_rng(i).choice(U, min(U, 300), replace=False)]))
-            sub = np.full(U, -1, np.int32)
-            sub[pick] = np.arange(pick.size, dtype=np.int32)
-            sel = np.flatnonzero(sub[idx] >= 0)
-            src = _host(per_edge.reshape(E, H * dh)[torch.as_tensor(sel, device="cuda")])
-            want = oracle.index_add_rows(sub[idx[sel]], pick.size, src)
-            assert_close(rows_grad[torch.as_tensor(pick, device="cuda")], want, "f32",
-                         f"{what} d{name} rows")
-        del o, out, dQ, dKe, dVe
-        torch.cuda.empty_cache()
+    _announce(f"indexed attention cfg={cfg} block={i}")
+    blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
+    off = oracle.csr_offsets(blk.counts)
+    N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
+    scale = float(np.float32(1 / np.sqrt(dh)))
+    d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
+    g = fast.tcsr(d_off, E)
+    tt = tdtype(dt)
+    out = torch.empty((N, H, dh), dtype=tt, device="cuda")
+    lse = torch.empty((N, H), device="cuda")
+    fast.fast_edge_attention_fwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v, Uv,
+                                         scale, SLOPE, out, lse)
+    dQ = torch.empty((N, H, dh), dtype=tt, device="cuda")
+    dKe = torch.empty((E, H, dh), dtype=tt, device="cuda")
+    dVe = torch.empty((E, H, dh), dtype=tt, device="cuda")
+    fast.fast_edge_attention_bwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v,
+                                         Uv, scale, SLOPE, lse, o["dO"], dQ, dKe, dVe)
+    torch.cuda.synchronize()
+    what = f"cfg{cfg}/L{i + 1} indexed"
+    ins = dict(Q=_cpu(o["Q"]), dO=_cpu(o["dO"]),
+               K=_cpu(o["K"][d_k.long()]), V=_cpu(o["V"][d_v.long()]))   # the rows each edge reads
+    check_attention_block_full(off, ins, [_cpu(t) for t in (out, lse, dQ, dKe, dVe)], None, None,
+                               scale, SLOPE, dt, what)
+    del ins
+    # row gradients: occurrence lists bit-exact, then the ordered fp64 sums
+    # of the per-edge gradients, every row
+    for name, idx, U, per_edge in (("K", kidx, Uk, dKe), ("V", vidx, Uv, dVe)):
+        occ_off, occ = _occ_gpu(idx, U)
+        _rows_full(occ_off, occ, idx, U, E, per_edge, H, dh, f"{what} d{name}")
+    del o, out, dQ, dKe, dVe
+    torch.cuda.empty_cache()
 
 
 def test_identity_index_equals_plain_operator():
@@ -242,50 +240,51 @@ def test_index_add_scaled_rows_vs_oracle(H, dh, dt, rows):
     assert torch.all(got[rows:] == 0)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
-def test_indexed_coefficients_and_row_gradients(cfg):
+@pytest.mark.parametrize("cfg,i", BLOCKS)
+def test_indexed_coefficients_and_row_gradients(cfg, i):
+    """Coefficient form: every segment's dQ, and the dK, dV each edge's
+    coefficients form, against the oracle; then every row gradient from the
+    GPU's coefficients against the oracle's fp64 sums of the same ones."""
     b = make_batch(cfg)
-    for i, blk in enumerate(b.blocks):
-        _announce(f"coefficient-form backward cfg={cfg} block={i}")
-        blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
-        off = oracle.csr_offsets(blk.counts)
-        N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
-        scale = float(np.float32(1 / np.sqrt(dh)))
-        d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
-        g = fast.tcsr(d_off, E)
-        dQ = torch.empty((N, H, dh), dtype=tdtype(dt), device="cuda")
-        ge = torch.empty((E, H), device="cuda")
-        ae = torch.empty((E, H), device="cuda")
-        fast.fast_edge_attention_bwd_indexed_coef(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"],
-                                                  d_v, Uv, scale, SLOPE, None, o["dO"], dQ, ge, ae)
-        torch.cuda.synchronize()
-        segs = np.arange(N) if E <= 200_000 else \
-            sample_segments(N, 1500, seed=cfg * 10 + i + 5, include=[0, N - 1])
-        sub_off, eidx = sub_csr(off, segs)
-        sg, ei = torch.as_tensor(segs, device="cuda"), torch.as_tensor(eidx, device="cuda")
-        Q64, dO64 = _host(o["Q"][sg]), _host(o["dO"][sg])
-        K64 = _host(o["K"][torch.as_tensor(kidx[eidx].astype(np.int64), device="cuda")])
-        V64 = _host(o["V"][torch.as_tensor(vidx[eidx].astype(np.int64), device="cuda")])
-        r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(sub_off, Q64, K64, V64, dO64, scale, SLOPE)
-        lseg = np.repeat(np.arange(segs.size), np.diff(sub_off))
-        g64, a64 = ge[ei].double().cpu().numpy(), ae[ei].double().cpu().numpy()
-        dK_formed = torch.from_numpy(g64[:, :, None] * Q64[lseg])
-        dV_formed = torch.from_numpy(a64[:, :, None] * dO64[lseg])
-        what = f"cfg{cfg}/L{i + 1} coefficients"
-        assert_close(dV_formed, r_dV, dt, what + " alpha dO")
-        assert_bwd_close(dQ[sg], dK_formed, sub_off, r_dQ, r_dK, alts, dt, what)
-        # row gradients from the GPU's coefficients against the oracle's fp64
-        # sums of the same coefficients, on a sample of rows (hubs included)
-        for name, idx, U, scal, src in (("K", kidx, Uk, ge, o["Q"]), ("V", vidx, Uv, ae, o["dO"])):
-            occ_off, occ = _occ_gpu(idx, U)
-            rows_grad = _scaled_rows_gpu(occ_off, occ, E, U, d_off, N, H, dh, scal, src)
-            counts_u = np.bincount(idx, minlength=U)
-            pick = np.unique(np.concatenate([np.argsort(counts_u)[-20:],
-                                             np.random.default_rng(i).choice(U, min(U, 300), replace=False)]))
-            sub = np.full(U, -1, np.int32)
-            sub[pick] = np.arange(pick.size, dtype=np.int32)
-            want = oracle.index_add_scaled_rows(sub[idx], off, pick.size, scal.cpu().numpy(), _host(src))
-            assert_close(rows_grad[torch.as_tensor(pick, device="cuda")], want, "f32",
-                         f"{what} d{name} rows")
-        del o, dQ, ge, ae
-        torch.cuda.empty_cache()
+    _announce(f"coefficient-form backward cfg={cfg} block={i}")
+    blk, kidx, vidx, Uk, Uv, o = _indexed_block(b, i, cfg)
+    off = oracle.csr_offsets(blk.counts)
+    N, E, H, dh, dt = blk.num_dst, blk.num_edges, b.H, b.dh, b.dtype
+    scale = float(np.float32(1 / np.sqrt(dh)))
+    d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
+    g = fast.tcsr(d_off, E)
+    dQ = torch.empty((N, H, dh), dtype=tdtype(dt), device="cuda")
+    ge = torch.empty((E, H), device="cuda")
+    ae = torch.empty((E, H), device="cuda")
+    fast.fast_edge_attention_bwd_indexed_coef(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"],
+                                              d_v, Uv, scale, SLOPE, None, o["dO"], dQ, ge, ae)
+    torch.cuda.synchronize()
+    what = f"cfg{cfg}/L{i + 1} coefficients"
+    Qh, dOh = _cpu(o["Q"]), _cpu(o["dO"])
+    Kh, Vh = _cpu(o["K"][d_k.long()]), _cpu(o["V"][d_v.long()])
+    dQh, g64, a64 = _cpu(dQ), ge.double().cpu().numpy(), ae.double().cpu().numpy()
+    off64 = off.astype(np.int64)
+
+    def one(a, c):
+        ea, ec = int(off64[a]), int(off64[c])
+        sub = (off64[a:c + 1] - ea).astype(np.int32)
+        Q64, dO64 = Qh[a:c].double().numpy(), dOh[a:c].double().numpy()
+        K64, V64 = Kh[ea:ec].double().numpy(), Vh[ea:ec].double().numpy()
+        r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(sub, Q64, K64, V64, dO64, scale, SLOPE)
+        lseg = np.repeat(np.arange(c - a), np.diff(sub))
+        dK_formed = torch.from_numpy(g64[ea:ec, :, None] * Q64[lseg])
+        dV_formed = torch.from_numpy(a64[ea:ec, :, None] * dO64[lseg])
+        tag = f"{what} segments [{a}, {c})"
+        assert_close(dV_formed, r_dV, dt, tag + " alpha dO")
+        assert_bwd_close(dQh[a:c], dK_formed, sub, r_dQ, r_dK, alts, dt, tag)
+        return c - a
+
+    assert sum(over_ranges(one, segment_ranges(off64, 64))) == N
+    # row gradients from the GPU's coefficients, every row
+    for name, idx, U, scal, src in (("K", kidx, Uk, ge, o["Q"]), ("V", vidx, Uv, ae, o["dO"])):
+        occ_off, occ = _occ_gpu(idx, U)
+        rows_grad = _scaled_rows_gpu(occ_off, occ, E, U, d_off, N, H, dh, scal, src).cpu()
+        want = oracle.index_add_scaled_rows(idx, off, U, scal.cpu().numpy(), _host(src))
+        assert_close(rows_grad, want, "f32", f"{what} d{name} rows")
+    del o, dQ, ge, ae
+    torch.cuda.empty_cache()

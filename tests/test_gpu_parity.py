@@ -1,8 +1,9 @@
 """GPU parity: every operator through the C ABI against the fp64 CPU oracle.
 
-Workloads 0-2 are compared in full (they span many workgroups and end in a
-ragged tail); workloads 3 and 4 run at their full size in the launch
-configuration the benchmark times and are compared on sampled segments.
+Every workload is compared in full: the small ones span many workgroups and
+end in a ragged tail; the two large ones run at their full size in the
+launch configuration the benchmark times, and the oracle checks every
+segment of them over contiguous segment ranges on all host threads.
 """
 import os
 
@@ -14,7 +15,8 @@ import oracle
 import paper_2607_05095_amd as fast
 from synth import make_batch, make_block_operands, make_slot_map, make_table, omega_phi, tiny_graph
 from tests.parity import (SLOPE, assert_bwd_close, assert_close, bwd_reference_with_kinks,
-                          sample_segments, sub_csr, tdtype, to_dev)
+                          check_attention_block_full, check_time_encode_full, sub_csr, tdtype,
+                          to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -135,16 +137,30 @@ def test_attention_small_workloads_full(cfg):
         _check_block(d, None, f"cfg{cfg}/L{i + 1}")
 
 
-@pytest.mark.parametrize("cfg", [3, 4])
-def test_attention_large_workloads_sampled(cfg):
+def _cpu(t):
+    return t.detach().cpu() if t is not None else None
+
+
+@pytest.mark.parametrize("cfg,block", [(3, 0), (3, 1), (4, 0), (4, 1)])
+def test_attention_large_workloads_full(cfg, block):
+    """The two full-size workloads in the launch configuration the benchmark
+    times: every segment of each layer block, fused forward and backward with
+    and without the saved lse and the unfused chain, against the oracle run
+    over contiguous segment ranges on all host threads."""
     b = make_batch(cfg)
-    for i in range(len(b.blocks)):
-        _announce(f"attention cfg={cfg} block={i} (full size, sampled segments)")
-        d = _block_from_batch(b, i)
-        segs = sample_segments(d.N, 1500, seed=cfg * 10 + i, include=[0, d.N - 1])
-        _check_block(d, segs, f"cfg{cfg}/L{i + 1}")
-        del d
-        torch.cuda.empty_cache()
+    d = _block_from_batch(b, block)
+    _announce(f"attention cfg={cfg} block={block}: N={d.N} E={d.E}, every segment")
+    fused = [_cpu(t) for t in _run_fused(d, with_lse=True)]
+    fused_nolse = [_cpu(t) for t in _run_fused(d, with_lse=False)]
+    unf = [_cpu(t) for t in _run_unfused(d)]
+    ins = {k: _cpu(d.ops[k]) for k in ("Q", "K", "V", "dO")}
+    torch.cuda.synchronize()
+    off = d.off
+    del d
+    torch.cuda.empty_cache()
+    parts = check_attention_block_full(off, ins, fused, fused_nolse, unf, float(np.float32(1.0 / np.sqrt(b.dh))),
+                                       SLOPE, b.dtype, f"cfg{cfg}/L{block + 1}")
+    _announce(f"  {parts} segment ranges equal to the oracle")
 
 
 # ------------------------------------------------------------------ attention: edge cases
@@ -490,20 +506,15 @@ def _te_gpu(blk_off, dst_t, edge_t, omega, phi, dt="f32"):
 
 @pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
 def test_time_encode_workloads(cfg):
+    """Every row of both blocks, the oracle over segment ranges on all host threads."""
     b = make_batch(cfg)
     om, ph = omega_phi(b.d_t)
     for i, blk in enumerate(b.blocks):
         _announce(f"time encode cfg={cfg} block={i} E={blk.num_edges} d_t={b.d_t} {b.dtype}")
         off = oracle.csr_offsets(blk.counts)
-        te = _te_gpu(off, blk.dst_t, blk.edge_t, om, ph, b.dtype)
-        if blk.num_edges <= 200_000:
-            ref = oracle.time_encode(off, blk.dst_t, blk.edge_t, om, ph)
-            assert_close(te, ref, b.dtype, f"te cfg{cfg}/L{i + 1}")
-        else:
-            segs = sample_segments(blk.counts.shape[0], 3000, seed=cfg, include=[0, blk.counts.shape[0] - 1])
-            sub_off, eidx = sub_csr(off, segs)
-            ref = oracle.time_encode(sub_off, blk.dst_t[segs], blk.edge_t[eidx], om, ph)
-            assert_close(te[torch.as_tensor(eidx, device="cuda")], ref, b.dtype, f"te cfg{cfg}/L{i + 1}")
+        te = _te_gpu(off, blk.dst_t, blk.edge_t, om, ph, b.dtype).cpu()
+        check_time_encode_full(off, blk.dst_t, blk.edge_t, om, ph, te, b.dtype, f"te cfg{cfg}/L{i + 1}")
+        del te
 
 
 @pytest.mark.parametrize("d_t,dt", [(1, "f32"), (7, "f32"), (6, "f32"), (100, "bf16"),

@@ -1,9 +1,9 @@
 """GPU parity of the most-recent-k temporal sampler through the C ABI,
 bit-exact against the oracle (offsets, neighbour ids, times, edge ids).
 
-Small and medium graphs are compared root for root in full; on the large
-graph (hub nodes with millions of entries) the oracle's linear scans are
-run on a sample of roots, each root's segment checked one by one.  Two hops
+Every root of every batch is compared, on the large graph (hub nodes with
+millions of entries) too: there the oracle's linear scans run over chunks of
+roots on all host threads, for the whole hop-1 and hop-2 batch.  Two hops
 are chained as in training (hop-2 roots are the hop-1 neighbours at their
 edge times) and the result is fed to the contract check and the time
 encoding.
@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2607_05095_amd as fast
 from synth import make_temporal_graph, omega_phi, sampler_roots
-from tests.parity import assert_close, to_dev
+from tests.parity import assert_close, oracle_sample_chunks, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -137,22 +137,37 @@ def test_sample_recent_edge_cases():
     assert off.cpu().tolist() == [0, 0, 0, 0]
 
 
-def test_sample_recent_large_graph_sampled_roots():
-    # 2e7 events (4e7 entries, hubs with millions of entries); the batch of
-    # 8000 events the benchmark samples, checked on 400 roots
+@pytest.fixture(scope="module")
+def big_graph():
+    # 2e7 events (4e7 entries, hubs with millions of entries): the node
+    # universe of the 1e7-node workload
     g = make_temporal_graph(10_000_000, 20_000_000, seed=9)
     _announce(f"sample recent large graph: V={g.num_nodes} M={g.indptr[-1]}")
-    dg = DevGraph(g)
+    return g, DevGraph(g)
+
+
+def test_sample_recent_large_graph_hop1_every_root(big_graph):
+    """The benchmark's batch of 8000 events (24,000 roots), every root."""
+    g, dg = big_graph
     roots, rt = sampler_roots(g, 8000, seed=9)
     k = 10
-    off, src, et, ei = _sample_gpu(dg, roots, rt, k)
-    off, src, et, ei = _host(off, src, et, ei)
-    pick = np.unique(np.concatenate([np.random.default_rng(0).choice(roots.size, 400, replace=False),
-                                     [0, roots.size - 1]]))
-    w = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots[pick], rt[pick], k)
-    for j, i in enumerate(pick):
-        sl, ws = slice(off[i], off[i + 1]), slice(w[0][j], w[0][j + 1])
-        assert np.array_equal(src[sl], w[1][ws]) and np.array_equal(et[sl], w[2][ws])
-        assert np.array_equal(ei[sl], w[3][ws])
-    counts = np.diff(off)
-    assert counts.min() >= 0 and counts.max() <= k and off[-1] == counts.sum()
+    got = _sample_gpu(dg, roots, rt, k)
+    want = oracle_sample_chunks(g, roots, rt, k, 256)
+    _assert_equal_sample(got, want, "large graph hop 1")
+    counts = np.diff(want[0])
+    assert counts.min() >= 0 and counts.max() <= k and want[0][-1] == counts.sum()
+    _announce(f"  {roots.size} roots, {int(want[0][-1])} sampled edges: equal")
+
+
+def test_sample_recent_large_graph_hop2_every_root(big_graph):
+    """Hop 2 of the same batch: each hop-1 neighbour queried at its edge time,
+    every one of the ~1.5e5 roots (many of them hubs)."""
+    g, dg = big_graph
+    roots, rt = sampler_roots(g, 8000, seed=9)
+    k = 10
+    _, src1, et1, _ = _sample_gpu(dg, roots, rt, k)
+    got = _sample_gpu(dg, src1, et1, k)
+    r2, t2 = src1.cpu().numpy(), et1.cpu().numpy()
+    want = oracle_sample_chunks(g, r2, t2, k, 1024)
+    _assert_equal_sample(got, want, "large graph hop 2")
+    _announce(f"  {r2.size} roots, {int(want[0][-1])} sampled edges: equal")
