@@ -17,7 +17,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# FAST_ORACLE_LIB names another build of oracle.c to load (the sanitizer
+# test's instrumented build); default: liboracle.so beside this file.
+_LIB_PATH = os.environ.get("FAST_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _p = C.c_void_p
