@@ -755,6 +755,33 @@ def cpu_baseline_threads(blocks, node_ids, edge_ids, node_table, edge_table, slo
                    f"segment ranges plus the two dedup+gathers, unchanged oracle routines"}
 
 
+CEILING_EXE = os.path.join(ROOT, "paper_2607_05095_amd", "probe", "stream_ceiling")
+
+
+def stream_ceilings():
+    """The GPU's streaming ceilings (read, write, copy, two-in-two-out) from
+    the probe built beside the library, run as a child process before this
+    process touches the GPU; None when the probe is not built."""
+    import subprocess
+    if not os.path.exists(CEILING_EXE):
+        return None
+    try:
+        r = subprocess.run([CEILING_EXE], capture_output=True, text=True, timeout=180)
+    except subprocess.TimeoutExpired:
+        return {"error": "probe timed out"}
+    if r.returncode != 0:
+        return {"error": (r.stdout + r.stderr)[-300:]}
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def ceiling_fracs(achieved_gbs, ceilings):
+    """The dominant kernel's bandwidth as a fraction of each measured ceiling."""
+    if not ceilings or "copy" not in ceilings:
+        return None
+    return {k: round(achieved_gbs / (ceilings[k]["TB_per_s"] * 1e3), 4)
+            for k in ("copy", "mix22", "read", "write")}
+
+
 def read_counters(workload):
     """rocprofv3 counter record of the dominant kernel on this workload (HBM
     bytes per launch, L2 hit rate, occupancy), from the committed summary, or
@@ -775,7 +802,7 @@ def read_traffic(workload):
     return read_counters(workload).get("bytes_per_launch")
 
 
-def measure(name, args, torch, fast, headline):
+def measure(name, args, torch, fast, headline, ceilings=None):
     """Builds workload `name`, times K serial steps and the fused attention
     sequence, and returns its result dict.  The headline workload also gets
     the pipelined and graph timings and the widened operators."""
@@ -858,6 +885,7 @@ def measure(name, args, torch, fast, headline):
         "algorithmic_bytes_per_launch": bwd_bytes, "avg_launch_ms": round(bwd_ms, 4),
         "l2_hit_rate": counters.get("l2_hit_rate"),
         "occupancy_pct": counters.get("occupancy_pct"),
+        "frac_of_measured_ceiling": ceiling_fracs(achieved, ceilings),
     }
     result = {
         "value": b.sampled_edges / (ms * 1e-3),
@@ -936,6 +964,9 @@ def main():
         if w not in WORKLOADS or w == args.workload:
             ap.error(f"--also: unknown or repeated workload {w!r}")
 
+    # streaming ceilings of this GPU, before this process initialises it
+    ceilings = None if args.copy_calibration else stream_ceilings()
+
     import torch
     import paper_2607_05095_amd as fast
 
@@ -948,7 +979,7 @@ def main():
         print(json.dumps({"copy_bytes_each_way": x.numel() * 4, "copies": 5}))
         return
 
-    head = measure(args.workload, args, torch, fast, headline=True)
+    head = measure(args.workload, args, torch, fast, headline=True, ceilings=ceilings)
     result = {
         "metric": METRIC,
         "value": head.pop("value"),
@@ -972,10 +1003,15 @@ def main():
     })
     if cb is not None:
         result["cpu_baseline"] = cb
+    result["stream_ceilings"] = ceilings
+    result["stream_ceilings_note"] = (
+        "plain read / write / copy / two-in-two-out kernels over 2 GiB buffers on this GPU, one "
+        "16-byte element per thread (paper_2607_05095_amd/probe/stream_ceiling.hip), median of "
+        "15 launches; roofline.frac_of_measured_ceiling divides the dominant kernel's bandwidth by them")
     for w in also:
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        r = measure(w, args, torch, fast, headline=False)
+        r = measure(w, args, torch, fast, headline=False, ceilings=ceilings)
         r["note"] = ("measured in the same run after the headline workload's buffers were freed: "
                      "K serial steps, the fused attention sequence, the dominant kernel's roofline "
                      "and the oracle on the same batch")

@@ -51,6 +51,24 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
+PROBE_SRC = os.path.join(PKG, "probe", "stream_ceiling.hip")
+PROBE_EXE = os.path.join(PKG, "probe", "stream_ceiling")
+
+
+def build_probe(verbose: bool = False) -> str:
+    """The streaming-ceiling probe the benchmark runs beside the operators."""
+    tmp = PROBE_EXE + ".tmp"
+    cmd = [HIPCC] + COMMON[:4] + ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                                  PROBE_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {PROBE_SRC}:\n{r.stdout + r.stderr}")
+    os.replace(tmp, PROBE_EXE)
+    return PROBE_EXE
+
+
 def build(verbose: bool = False, jobs: int | None = None) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     srcs = sources()
@@ -63,6 +81,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    build_probe(verbose)
     return LIB
 
 

@@ -447,7 +447,8 @@ __device__ __forceinline__ void dedup_inv_id(const int64_t* __restrict__ ids, in
 }
 
 // uni and inv in one launch: workgroups [0, nbw) take 256 words each, the
-// rest 256 ids each.
+// rest 256 ids each.  zero_miss, when given, is set to 0 by the first thread
+// (a batch that cannot miss), saving a launch of its own.
 __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni_inv(const uint2* __restrict__ words,
                                                               int64_t W,
                                                               const uint32_t* __restrict__ base,
@@ -457,7 +458,9 @@ __global__ void __launch_bounds__(DD_THREADS) k_dedup_uni_inv(const uint2* __res
                                                               int32_t* __restrict__ inv,
                                                               const int32_t* __restrict__ slot_map,
                                                               int32_t* __restrict__ slots,
-                                                              uint32_t nbw) {
+                                                              uint32_t nbw,
+                                                              int64_t* __restrict__ zero_miss) {
+  if (zero_miss && blockIdx.x == 0 && threadIdx.x == 0) *zero_miss = 0;
   if (blockIdx.x < nbw) {
     const int64_t w = int64_t(blockIdx.x) * DD_THREADS + threadIdx.x;
     if (w < W) dedup_uni_word(words, w, base, wshift, uni, slot_map, slots);
@@ -760,13 +763,15 @@ static fast_status_t dedup_gather_run(const char* fn, const int64_t* ids, int64_
   const bool want_miss = (miss || num_miss) && !all_hit;
   int32_t* slots = slot_map && (rows || want_miss) ? w.slots : nullptr;
   const int64_t nbw = (W + DD_THREADS - 1) / DD_THREADS, nbi = (n + DD_THREADS - 1) / DD_THREADS;
+  int64_t* zero_miss = all_hit ? num_miss : nullptr;
   if (nbw + nbi > 0)
     hipLaunchKernelGGL(k_dedup_uni_inv, dim3(uint32_t(nbw + nbi)), dim3(DD_THREADS), 0, st, w.words, W,
-                       base, wshift, uni, ids, n, id_bound, inv, slot_map, slots, uint32_t(nbw));
+                       base, wshift, uni, ids, n, id_bound, inv, slot_map, slots, uint32_t(nbw),
+                       zero_miss);
+  else if (zero_miss)
+    hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(64), 0, st, zero_miss, int64_t(0));
 
   // 4. rows from their slots, miss flags, 5. ordered miss list.
-  if (all_hit && num_miss)
-    hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(64), 0, st, num_miss, int64_t(0));
   if (rows || want_miss) {
     const int64_t row_bytes = int64_t(D > 0 ? D : 0) * elem_size(dtype);
     uint8_t* flags = want_miss ? w.flags : nullptr;

@@ -1,0 +1,136 @@
+// stream_ceiling.hip -- the HBM streaming ceilings of the GPU it runs on,
+// for comparison with the operators' achieved bandwidth.  Plain kernels over
+// 2 GiB buffers (8x the 256 MB last-level cache): one 16-byte element per
+// thread and one element per thread's lifetime (a grid of n / 256
+// workgroups), the shape that measured fastest for every pattern on MI355X
+// (grid-stride loops with 1k-64k workgroups ran 5-30 % slower).
+//   read   : one stream in            write  : one stream out
+//   copy   : one in, one out           mix22  : two in, two out (the shape of
+//                                               the fused backward's K, V ->
+//                                               dK, dV rows)
+// Prints one JSON object: bytes moved, median time of `reps` launches, TB/s.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+#define CHECK(x)                                                              \
+  do {                                                                        \
+    hipError_t err_ = (x);                                                    \
+    if (err_ != hipSuccess) {                                                 \
+      std::fprintf(stderr, "HIP error %s at line %d\n", hipGetErrorString(err_), __LINE__); \
+      std::exit(1);                                                           \
+    }                                                                         \
+  } while (0)
+
+constexpr int THREADS = 256;
+
+__global__ void __launch_bounds__(THREADS) k_read(const u32x4* __restrict__ a, size_t n,
+                                                  unsigned* __restrict__ sink) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  const u32x4 v = a[i];
+  if ((v.x ^ v.y ^ v.z ^ v.w) == 0x9e3779b9u) sink[0] = 1u;   // keeps the load
+}
+
+__global__ void __launch_bounds__(THREADS) k_write(u32x4* __restrict__ a, size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  a[i] = (u32x4){unsigned(i), 1u, 2u, 3u};
+}
+
+__global__ void __launch_bounds__(THREADS) k_copy(const u32x4* __restrict__ a,
+                                                  u32x4* __restrict__ b, size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  b[i] = a[i];
+}
+
+__global__ void __launch_bounds__(THREADS) k_mix22(const u32x4* __restrict__ a,
+                                                   const u32x4* __restrict__ c,
+                                                   u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                   size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  u32x4 x = a[i], y = c[i];
+  x.x ^= y.y;
+  y.x ^= x.w;
+  b[i] = x;
+  d[i] = y;
+}
+
+struct Buffers {
+  u32x4 *a, *b, *c, *d;
+  unsigned* sink;
+  size_t n;   // 16-byte elements per buffer
+};
+
+template <class Launch>
+static float median_ms(Launch launch, int reps) {
+  hipEvent_t e0, e1;
+  CHECK(hipEventCreate(&e0));
+  CHECK(hipEventCreate(&e1));
+  launch();
+  launch();
+  CHECK(hipDeviceSynchronize());
+  std::vector<float> t;
+  for (int r = 0; r < reps; ++r) {
+    CHECK(hipEventRecord(e0));
+    launch();
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    float ms = 0.f;
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+    t.push_back(ms);
+  }
+  CHECK(hipEventDestroy(e0));
+  CHECK(hipEventDestroy(e1));
+  std::sort(t.begin(), t.end());
+  return t[t.size() / 2];
+}
+
+int main(int argc, char** argv) {
+  const int reps = argc > 1 ? std::atoi(argv[1]) : 15;
+  const size_t bytes = size_t(2) << 30;
+  Buffers B;
+  B.n = bytes / 16;
+  CHECK(hipMalloc(&B.a, bytes));
+  CHECK(hipMalloc(&B.b, bytes));
+  CHECK(hipMalloc(&B.c, bytes));
+  CHECK(hipMalloc(&B.d, bytes));
+  CHECK(hipMalloc(&B.sink, 64));
+  CHECK(hipMemset(B.a, 1, bytes));
+  CHECK(hipMemset(B.c, 2, bytes));
+  CHECK(hipMemset(B.b, 0, bytes));
+  CHECK(hipMemset(B.d, 0, bytes));
+  CHECK(hipDeviceSynchronize());
+  const size_t half = B.n / 2;
+  const dim3 blk(THREADS), g_all(unsigned((B.n + THREADS - 1) / THREADS)),
+      g_half(unsigned((half + THREADS - 1) / THREADS));
+  struct Row { const char* name; double moved; float ms; };
+  std::vector<Row> rows;
+  rows.push_back({"read", double(bytes), median_ms([&] {
+    hipLaunchKernelGGL(k_read, g_all, blk, 0, 0, B.a, B.n, B.sink); }, reps)});
+  rows.push_back({"write", double(bytes), median_ms([&] {
+    hipLaunchKernelGGL(k_write, g_all, blk, 0, 0, B.b, B.n); }, reps)});
+  rows.push_back({"copy", 2.0 * bytes, median_ms([&] {
+    hipLaunchKernelGGL(k_copy, g_all, blk, 0, 0, B.a, B.b, B.n); }, reps)});
+  rows.push_back({"mix22", 2.0 * bytes, median_ms([&] {   // four streams of 1 GiB
+    hipLaunchKernelGGL(k_mix22, g_half, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+  CHECK(hipGetLastError());
+  std::printf("{");
+  for (size_t k = 0; k < rows.size(); ++k)
+    std::printf("%s\"%s\": {\"bytes\": %.0f, \"ms\": %.4f, \"TB_per_s\": %.3f}", k ? ", " : "",
+                rows[k].name, rows[k].moved, rows[k].ms, rows[k].moved / (rows[k].ms * 1e-3) / 1e12);
+  std::printf(", \"reps\": %d, \"buffer_bytes\": %zu}\n", reps, bytes);
+  CHECK(hipFree(B.a));
+  CHECK(hipFree(B.b));
+  CHECK(hipFree(B.c));
+  CHECK(hipFree(B.d));
+  CHECK(hipFree(B.sink));
+  return 0;
+}
