@@ -20,7 +20,10 @@
 // first R_e edges and R_v nodes in id order.  One scan per kind over a packed
 // pair (ids above T, ids at T) then gives every id its position among the
 // selected ids (above-T prefix + min(at-T prefix, R)), which is both the slot
-// in the id-ordered hot list and the value of the slot map.
+// in the id-ordered hot list and the value of the slot map.  When the counts
+// are small (fewer than 64 batches counted), the histogram pass also keeps a
+// histogram per tile of 4096 ids, so the tile sums of the scan come from
+// those few bytes instead of a second read of every count.
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -359,6 +362,99 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_write(
   }
 }
 
+// ------------------------------------------------------------------ tile histograms
+// Counts below HS_TH_BINS (max_freq < HS_TH_BINS): one workgroup per tile of
+// HS_SEL_TILE ids reads the tile's counts once (16 per thread, all loads
+// issued first) and stores the tile's histogram th[tile * nb + c] (nb =
+// max_freq + 1, at most 4096 per bin: uint16).
+constexpr int HS_TH_BINS = 64;
+
+__global__ void __launch_bounds__(HS_THREADS) k_hs_tilehist(const int32_t* __restrict__ f, int64_t n,
+                                                           int32_t max_freq,
+                                                           uint16_t* __restrict__ th) {
+  __shared__ uint32_t s_h[HS_TH_BINS];
+  const int nb = max_freq + 1;
+  if (threadIdx.x < HS_TH_BINS) s_h[threadIdx.x] = 0u;
+  const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
+  const int64_t base = int64_t(blockIdx.x) * HS_SEL_TILE;
+  int32_t c[HS_SEL_ROUNDS][4];
+#pragma unroll
+  for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
+    const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
+    if (vec && i0 + 3 < n) {
+      const int4 v = *reinterpret_cast<const int4*>(f + i0);
+      c[r][0] = v.x; c[r][1] = v.y; c[r][2] = v.z; c[r][3] = v.w;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) c[r][k] = i0 + k < n ? f[i0 + k] : -1;   // -1: past n
+    }
+  }
+  __syncthreads();
+  uint32_t reg[HS_REG_BINS] = {};
+#pragma unroll
+  for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
+    const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (i0 + k >= n) continue;
+      const int32_t b = clamp_count(c[r][k], max_freq);
+      if (b < HS_REG_BINS) {
+#pragma unroll
+        for (int q = 0; q < HS_REG_BINS; ++q) reg[q] += (b == q);
+      } else {
+        atomicAdd(&s_h[b], 1u);
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < HS_REG_BINS; ++q)
+    if (q < nb && reg[q]) atomicAdd(&s_h[q], reg[q]);
+  __syncthreads();
+  if (threadIdx.x < nb) th[int64_t(blockIdx.x) * nb + threadIdx.x] = uint16_t(s_h[threadIdx.x]);
+}
+
+// hist[c] += sum over tiles of th[tile * nb + c]: workgroup k sums tiles k,
+// k + gridDim.x, ... of its kind in LDS (both kinds in one launch: the first
+// half of the grid takes the nodes, the second the edges), then adds its
+// partial histogram with nb global atomics.
+__global__ void __launch_bounds__(HS_THREADS) k_hs_tilesum(const uint16_t* __restrict__ th_v,
+                                                          int64_t tiles_v,
+                                                          const uint16_t* __restrict__ th_e,
+                                                          int64_t tiles_e, int nb,
+                                                          uint32_t* __restrict__ hv,
+                                                          uint32_t* __restrict__ he) {
+  __shared__ uint32_t s_h[HS_TH_BINS];
+  const int half = gridDim.x / 2;
+  const bool edges = int(blockIdx.x) >= half;
+  const uint16_t* th = edges ? th_e : th_v;
+  const int64_t tiles = edges ? tiles_e : tiles_v;
+  const int k = edges ? int(blockIdx.x) - half : int(blockIdx.x);
+  if (threadIdx.x < HS_TH_BINS) s_h[threadIdx.x] = 0u;
+  __syncthreads();
+  // the kind's tiles are split into `half` contiguous ranges; this workgroup
+  // reads its range's nb-bin rows as one flat array
+  const int64_t t0 = tiles * k / half, t1 = tiles * (k + 1) / half;
+  for (int64_t j = t0 * nb + threadIdx.x; j < t1 * nb; j += HS_THREADS)
+    atomicAdd(&s_h[int(j % nb)], uint32_t(th[j]));
+  __syncthreads();
+  if (threadIdx.x < nb && s_h[threadIdx.x]) atomicAdd(&(edges ? he : hv)[threadIdx.x], s_h[threadIdx.x]);
+}
+
+// Scan input of the selection from tile histograms: tile i's packed pair
+// (ids above T, ids at T).
+struct InTilePairs {
+  const uint16_t* th;
+  int nb;
+  const HsParams* prm;
+  __device__ uint64_t operator()(int64_t i) const {
+    const int32_t T = prm->T;
+    uint64_t above = 0;
+    for (int c = T + 1; c < nb; ++c) above += th[i * nb + c];
+    const uint64_t at = T < nb ? th[i * nb + T] : 0u;
+    return (above << 32) | at;
+  }
+};
+
 struct InU64 {
   const uint64_t* p;
   __device__ uint64_t operator()(int64_t i) const { return p[i]; }
@@ -376,7 +472,17 @@ struct HsWs {
   uint64_t* tsum_e;
   void* scan_v;
   void* scan_e;
+  uint16_t* th_v;     // per-tile histograms (max_freq < HS_TH_BINS only)
+  uint16_t* th_e;
 };
+
+static bool use_tile_hist(int32_t max_freq) {
+  static const int mode = [] {   // tuning override: FAST_HS_TILE_HIST=0 turns it off
+    const char* e = std::getenv("FAST_HS_TILE_HIST");
+    return e && e[0] == '0' ? 0 : 1;
+  }();
+  return mode && max_freq + 1 <= HS_TH_BINS;
+}
 
 static int64_t sel_tiles(int64_t n) { return (n + HS_SEL_TILE - 1) / HS_SEL_TILE; }
 
@@ -394,7 +500,12 @@ static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, Hs
   char* te = take(size_t(sel_tiles(ne)) * 8);
   char* sv = take(scan_workspace<uint64_t>(sel_tiles(nv)));
   char* se = take(scan_workspace<uint64_t>(sel_tiles(ne)));
+  const bool tiled = use_tile_hist(max_freq);
+  char* thv = take(tiled ? size_t(sel_tiles(nv)) * size_t(max_freq + 1) * 2 : 0);
+  char* the = take(tiled ? size_t(sel_tiles(ne)) * size_t(max_freq + 1) * 2 : 0);
   if (ws) {
+    ws->th_v = reinterpret_cast<uint16_t*>(thv);
+    ws->th_e = reinterpret_cast<uint16_t*>(the);
     ws->hv = reinterpret_cast<uint32_t*>(hv);
     ws->he = reinterpret_cast<uint32_t*>(he);
     ws->prm = reinterpret_cast<HsParams*>(pr);
@@ -524,30 +635,49 @@ extern "C" fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_
                      reinterpret_cast<int32_t*>(w.hv), nbins, 0);
   hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(nbins, HS_THREADS)), dim3(HS_THREADS), 0, st,
                      reinterpret_cast<int32_t*>(w.he), nbins, 0);
-  if (num_nodes > 0)
-    hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_nodes, HS_THREADS * 16, 4096)), dim3(HS_THREADS),
-                       0, st, freq_v, num_nodes, max_freq, w.hv);
-  if (num_edges > 0)
-    hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_edges, HS_THREADS * 16, 4096)), dim3(HS_THREADS),
-                       0, st, freq_e, num_edges, max_freq, w.he);
+  const bool tiled = use_tile_hist(max_freq);
+  if (tiled) {
+    const int64_t tv = sel_tiles(num_nodes), te = sel_tiles(num_edges);
+    if (tv > 0)
+      hipLaunchKernelGGL(k_hs_tilehist, dim3(uint32_t(tv)), dim3(HS_THREADS), 0, st, freq_v,
+                         num_nodes, max_freq, w.th_v);
+    if (te > 0)
+      hipLaunchKernelGGL(k_hs_tilehist, dim3(uint32_t(te)), dim3(HS_THREADS), 0, st, freq_e,
+                         num_edges, max_freq, w.th_e);
+    hipLaunchKernelGGL(k_hs_tilesum, dim3(2 * 256), dim3(HS_THREADS), 0, st, w.th_v, tv, w.th_e, te,
+                       int(nbins), w.hv, w.he);
+  } else {
+    if (num_nodes > 0)
+      hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_nodes, HS_THREADS * 16, 4096)),
+                         dim3(HS_THREADS), 0, st, freq_v, num_nodes, max_freq, w.hv);
+    if (num_edges > 0)
+      hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_edges, HS_THREADS * 16, 4096)),
+                         dim3(HS_THREADS), 0, st, freq_e, num_edges, max_freq, w.he);
+  }
   hipLaunchKernelGGL(k_hs_threshold, dim3(1), dim3(HS_THREADS), 0, st, w.hv, w.he, max_freq,
                      budget, num_nodes, num_edges, w.prm, num_hot_v, num_hot_e);
   const int64_t B = budget < num_nodes + num_edges ? budget : num_nodes + num_edges;
   hipError_t e = hipSuccess;
   auto select = [&](const int32_t* f, int64_t n, bool edges, uint64_t* tsum, void* scan_ws,
-                    int64_t* hot, int32_t* slot) {
+                    const uint16_t* th, int64_t* hot, int32_t* slot) {
     if (n == 0 || (!hot && !slot) || e != hipSuccess) return;
     const int64_t tiles = sel_tiles(n);
-    hipLaunchKernelGGL(k_sel_tiles, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
-                       w.prm, tsum);
-    e = scan_launch<InU64, OutU64InPlace, uint64_t>(InU64{tsum}, OutU64InPlace{tsum}, tiles, scan_ws,
-                                                   nullptr, nullptr, st);
+    if (tiled) {
+      e = scan_launch<InTilePairs, OutU64InPlace, uint64_t>(InTilePairs{th, int(nbins), w.prm},
+                                                           OutU64InPlace{tsum}, tiles, scan_ws,
+                                                           nullptr, nullptr, st);
+    } else {
+      hipLaunchKernelGGL(k_sel_tiles, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
+                         w.prm, tsum);
+      e = scan_launch<InU64, OutU64InPlace, uint64_t>(InU64{tsum}, OutU64InPlace{tsum}, tiles,
+                                                     scan_ws, nullptr, nullptr, st);
+    }
     if (e != hipSuccess) return;
     hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
                        w.prm, edges, tsum, B < n ? B : n, hot, slot);
   };
-  select(freq_v, num_nodes, false, w.tsum_v, w.scan_v, hot_v, slot_v);
-  select(freq_e, num_edges, true, w.tsum_e, w.scan_e, hot_e, slot_e);
+  select(freq_v, num_nodes, false, w.tsum_v, w.scan_v, w.th_v, hot_v, slot_v);
+  select(freq_e, num_edges, true, w.tsum_e, w.scan_e, w.th_e, hot_e, slot_e);
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   return check_launch(fn);
 }

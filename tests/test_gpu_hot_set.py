@@ -127,6 +127,31 @@ def test_selection_edge_cases():
         assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe))
 
 
+@pytest.mark.parametrize("max_freq", [63, 64])
+def test_selection_both_histogram_paths(max_freq):
+    """Counts below 64 are histogrammed per tile of 4096 ids (the tile sums of
+    the selection come from those histograms); 64 and above take the plain
+    global histogram and a second pass over the counts.  Both against the
+    oracle on ragged sizes (a partial last tile), with counts clamped into
+    [0, max_freq] and a count array that is not 16-byte aligned."""
+    _announce(f"hot set histogram path max_freq={max_freq}")
+    r = np.random.default_rng(max_freq)
+    nv, ne = 4096 * 7 + 1234, 4096 * 11 + 5
+    fv_np = np.minimum(r.zipf(1.3, nv), max_freq + 20).astype(np.int32) - 1
+    fe_np = np.minimum(r.zipf(1.4, ne), max_freq + 20).astype(np.int32) - 1
+    clamp = lambda a: np.clip(a, 0, max_freq)
+    fv_big = torch.tensor(np.concatenate([[7], fv_np]), dtype=torch.int32, device="cuda")
+    fv = fv_big[1:]                                   # 4 bytes off the 16-byte grid
+    fe = torch.tensor(fe_np, dtype=torch.int32, device="cuda")
+    for alpha in (0.0005, 0.02, 0.3, 1.0):
+        B = fast.fast_hot_set_budget(alpha, nv, ne)
+        hv, he, sv, se = _select_gpu(fv, fe, max_freq, B)
+        ov, oe = oracle.greedy_hot_set(clamp(fv_np), clamp(fe_np), alpha)
+        assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe)), alpha
+        _check_slots(sv, hv, nv)
+        _check_slots(se, he, ne)
+
+
 def test_bigdedup_universe_properties():
     k = 4
     nodes, edges, nb, eb = presampled_ids(4, k)
