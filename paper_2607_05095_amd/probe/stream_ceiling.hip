@@ -9,11 +9,13 @@
 //                                               the fused backward's K, V ->
 //                                               dK, dV rows)
 // Prints one JSON object: bytes moved, median time of `reps` launches, TB/s.
+//   stream_ceiling [reps] [--variants]
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 #include <vector>
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -61,6 +63,65 @@ __global__ void __launch_bounds__(THREADS) k_mix22(const u32x4* __restrict__ a,
   y.x ^= x.w;
   b[i] = x;
   d[i] = y;
+}
+
+// Variants of the two-in-two-out traffic (run with --variants): how the two
+// streams are laid over a thread's instructions, a wave's lanes, a
+// workgroup's waves and the grid's workgroups.  Each moves four 1 GiB streams.
+__global__ void __launch_bounds__(THREADS) k_ordered(const u32x4* __restrict__ a,
+                                                     const u32x4* __restrict__ c,
+                                                     u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                     size_t n) {   // load, store, load, store
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  const u32x4 x = a[i];
+  b[i] = x;
+  d[i] = c[i + (x.x & 0u)];   // the second load's address depends on the first load
+}
+
+__global__ void __launch_bounds__(THREADS) k_two_each(const u32x4* __restrict__ a,
+                                                      const u32x4* __restrict__ c,
+                                                      u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                      size_t n) {   // 4 loads, then 4 stores
+  const size_t i = size_t(blockIdx.x) * (2 * THREADS) + threadIdx.x;
+  if (i + THREADS >= n + THREADS) return;
+  const u32x4 x0 = a[i], y0 = c[i], x1 = a[i + THREADS], y1 = c[i + THREADS];
+  b[i] = x0;
+  d[i] = y0;
+  b[i + THREADS] = x1;
+  d[i + THREADS] = y1;
+}
+
+__global__ void __launch_bounds__(THREADS) k_by_lanes(const u32x4* __restrict__ a,
+                                                      const u32x4* __restrict__ c,
+                                                      u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                      size_t n) {   // half a wave per stream pair
+  const int lane = threadIdx.x & 63;
+  const size_t i = (size_t(blockIdx.x) * THREADS + (threadIdx.x & ~63u)) / 2 + (lane & 31);
+  if (i >= n) return;
+  if (lane < 32) b[i] = a[i];
+  else d[i] = c[i];
+}
+
+__global__ void __launch_bounds__(THREADS) k_by_waves(const u32x4* __restrict__ a,
+                                                      const u32x4* __restrict__ c,
+                                                      u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                      size_t n) {   // alternate waves
+  const int w = threadIdx.x >> 6;
+  const size_t i = size_t(blockIdx.x) * (THREADS / 2) + (w >> 1) * 64 + (threadIdx.x & 63);
+  if (i >= n) return;
+  if (w & 1) d[i] = c[i];
+  else b[i] = a[i];
+}
+
+__global__ void __launch_bounds__(THREADS) k_by_groups(const u32x4* __restrict__ a,
+                                                       const u32x4* __restrict__ c,
+                                                       u32x4* __restrict__ b, u32x4* __restrict__ d,
+                                                       size_t n) {   // alternate workgroups
+  const size_t i = size_t(blockIdx.x >> 1) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  if (blockIdx.x & 1) d[i] = c[i];
+  else b[i] = a[i];
 }
 
 struct Buffers {
@@ -121,6 +182,20 @@ int main(int argc, char** argv) {
     hipLaunchKernelGGL(k_copy, g_all, blk, 0, 0, B.a, B.b, B.n); }, reps)});
   rows.push_back({"mix22", 2.0 * bytes, median_ms([&] {   // four streams of 1 GiB
     hipLaunchKernelGGL(k_mix22, g_half, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+  if (argc > 2 && std::strcmp(argv[2], "--variants") == 0) {
+    const dim3 g_two(unsigned((half + 2 * THREADS - 1) / (2 * THREADS)));
+    const dim3 g_dbl(unsigned(2 * ((half + THREADS - 1) / THREADS)));
+    rows.push_back({"mix22_ordered", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_ordered, g_half, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+    rows.push_back({"mix22_two_each", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_two_each, g_two, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+    rows.push_back({"mix22_by_lanes", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_by_lanes, g_dbl, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+    rows.push_back({"mix22_by_waves", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_by_waves, g_dbl, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+    rows.push_back({"mix22_by_groups", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_by_groups, g_dbl, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+  }
   CHECK(hipGetLastError());
   std::printf("{");
   for (size_t k = 0; k < rows.size(); ++k)
