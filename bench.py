@@ -950,6 +950,9 @@ def main():
                     help="also time the serial step captured once as a HIP graph and replayed")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the streaming-ceiling probe (it runs as a child process before this "
+                         "process touches the GPU; profilers that initialise the GPU first need this)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -965,7 +968,7 @@ def main():
             ap.error(f"--also: unknown or repeated workload {w!r}")
 
     # streaming ceilings of this GPU, before this process initialises it
-    ceilings = None if args.copy_calibration else stream_ceilings()
+    ceilings = None if (args.copy_calibration or args.no_ceilings) else stream_ceilings()
 
     import torch
     import paper_2607_05095_amd as fast
