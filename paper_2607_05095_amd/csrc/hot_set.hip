@@ -22,8 +22,10 @@
 // selected ids (above-T prefix + min(at-T prefix, R)), which is both the slot
 // in the id-ordered hot list and the value of the slot map.  When the counts
 // are small (fewer than 64 batches counted), the histogram pass also keeps a
-// histogram per tile of 4096 ids, so the tile sums of the scan come from
-// those few bytes instead of a second read of every count.
+// suffix histogram per tile of 4096 ids, so the tile sums of the scan come
+// from two of those entries instead of a second read of every count, and it
+// stores each id's clamped count as one byte, which the write pass reads in
+// place of the four-byte count; node and edge tiles then share each launch.
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -324,15 +326,15 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_tiles(const int32_t* __restr
 
 __global__ void __launch_bounds__(HS_THREADS) k_sel_write(
     const int32_t* __restrict__ f, int64_t n, int32_t max_freq, const HsParams* __restrict__ prm,
-    bool edges, const uint64_t* __restrict__ tprefix, int64_t cap, int64_t* __restrict__ hot,
-    int32_t* __restrict__ slot) {
+    bool edges, const uint64_t* __restrict__ tprefix, const uint64_t* __restrict__ tbase,
+    int64_t cap, int64_t* __restrict__ hot, int32_t* __restrict__ slot) {
   __shared__ uint64_t lds4[4];
   const int32_t T = prm->T;
   const int64_t R = edges ? prm->R_e : prm->R_v;
   const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
   const bool svec = slot && (reinterpret_cast<uintptr_t>(slot) & 15u) == 0;
   const int64_t base = int64_t(blockIdx.x) * HS_SEL_TILE;
-  uint64_t run = tprefix[blockIdx.x];
+  uint64_t run = tprefix[blockIdx.x] - (tbase ? *tbase : 0u);
   for (int r = 0; r < HS_SEL_ROUNDS; ++r) {     // every thread reaches every block scan
     const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
     uint64_t p[4];
@@ -362,61 +364,219 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_write(
   }
 }
 
+// Write pass over one-byte codes: thread t owns the 16 consecutive ids
+// base + 16t .. base + 16t + 15 of its tile (one 16-byte load).  Byte-wise
+// compares give 16-bit masks of the ids above T and at T, a single 32-bit
+// block scan of the packed per-thread counts (above << 16 | at, each at most
+// 4096 per tile) places them, the selected ids of a thread are consecutive in
+// the hot list, and the tile's slots pass through LDS so that the stores are
+// contiguous across lanes.
+constexpr int HS_SW_IDS = HS_SEL_TILE / HS_THREADS;   // 16 ids per thread
+static_assert(HS_SW_IDS == 16, "one 16-byte load of codes per thread");
+
+// 4-bit mask of the bytes of a whose bit 7 is set (bits 7, 15, 23, 31).
+__device__ __forceinline__ uint32_t byte_msb_nibble(uint32_t a) {
+  return (((a >> 7) & 0x01010101u) * 0x00204081u) >> 21 & 0xfu;
+}
+
+// Masks of the four codes in q (each below 128) above T and equal to T.
+__device__ __forceinline__ void code_masks(uint32_t q, int32_t T, uint32_t& gt, uint32_t& eq) {
+  const uint32_t hi = q | 0x80808080u;
+  const uint32_t g = (hi - uint32_t(T + 1) * 0x01010101u) & 0x80808080u;   // code >= T + 1
+  const uint32_t e = (hi - uint32_t(T) * 0x01010101u) & 0x80808080u;       // code >= T
+  gt = byte_msb_nibble(g);
+  eq = byte_msb_nibble(e & ~g);
+}
+
+// Both kinds in one launch, as in the histogram pass; tprefix holds the
+// exclusive prefixes over the node tiles and then the edge tiles, so an edge
+// tile's prefix is taken relative to tprefix[tiles_v].
+struct SelKind {
+  const uint8_t* codes;
+  int64_t n;
+  int64_t cap;
+  int64_t* hot;
+  int32_t* slot;
+};
+
+__global__ void __launch_bounds__(HS_THREADS) k_sel_write_codes(SelKind kv, SelKind ke, int64_t tiles_v,
+                                                               const HsParams* __restrict__ prm,
+                                                               const uint64_t* __restrict__ tprefix) {
+  __shared__ uint32_t lds4[4];
+  const bool edges = int64_t(blockIdx.x) >= tiles_v;
+  const SelKind& K = edges ? ke : kv;
+  if (!K.hot && !K.slot) return;          // uniform over the workgroup
+  const uint8_t* __restrict__ codes = K.codes;
+  const int64_t n = K.n, cap = K.cap;
+  int64_t* __restrict__ hot = K.hot;
+  int32_t* __restrict__ slot = K.slot;
+  const int64_t tile = edges ? int64_t(blockIdx.x) - tiles_v : int64_t(blockIdx.x);
+  // slots of the tile, 16 bytes per entry; entry j sits at j + j / 8 so that
+  // both the per-thread writes (4 entries 64 bytes apart) and the striped
+  // reads are free of bank conflicts
+  __shared__ int4 s_out[HS_SEL_TILE / 4 + HS_SEL_TILE / 32];
+  const int32_t T = prm->T;
+  const int64_t R = edges ? prm->R_e : prm->R_v;
+  const int64_t base = tile * HS_SEL_TILE;
+  const int64_t i0 = base + int64_t(threadIdx.x) * HS_SW_IDS;
+  const uint4 q = *reinterpret_cast<const uint4*>(codes + i0);   // padded to whole tiles
+  uint32_t gt = 0, eq = 0;
+  {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      uint32_t g, e;
+      code_masks(w[k], T, g, e);
+      gt |= g << (4 * k);
+      eq |= e << (4 * k);
+    }
+  }
+  if (i0 + HS_SW_IDS > n) {                 // ids at or past n are never selected
+    const int64_t valid = n - i0;
+    const uint32_t m = valid <= 0 ? 0u : (1u << valid) - 1u;
+    gt &= m;
+    eq &= m;
+  }
+  uint32_t tot;
+  const uint32_t ex = block_exclusive_scan<uint32_t>((uint32_t(__popc(gt)) << 16) | uint32_t(__popc(eq)),
+                                                     lds4, tot);
+  const uint64_t tp = tprefix[blockIdx.x] - (edges ? tprefix[tiles_v] : 0u);   // no borrow: monotone
+  const int64_t above = int64_t(tp >> 32) + int64_t(ex >> 16);
+  const int64_t at = int64_t(tp & 0xffffffffu) + int64_t(ex & 0xffffu);
+  // ids at T are taken while fewer than R of them come before
+  uint32_t eqsel = 0;
+  if (at + __popc(eq) <= R) {
+    eqsel = eq;
+  } else if (at < R) {
+    uint32_t m = eq;
+    for (int64_t left = R - at; left > 0; --left) {
+      eqsel |= m & (0u - m);
+      m &= m - 1u;
+    }
+  }
+  const uint32_t sel = gt | eqsel;
+  const int32_t pos0 = int32_t(above + (at < R ? at : R));
+  if (hot) {
+    int32_t p = pos0;
+    for (uint32_t m = sel; m; m &= m - 1u, ++p)
+      if (p < cap) hot[p] = i0 + (__ffs(m) - 1);
+  }
+  if (!slot) return;
+  {
+    int32_t p = pos0, o[HS_SW_IDS];
+#pragma unroll
+    for (int k = 0; k < HS_SW_IDS; ++k) {
+      const int32_t b = int32_t((sel >> k) & 1u);
+      o[k] = b ? p : -1;
+      p += b;
+    }
+    const int e0 = 4 * threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = e0 + j;
+      s_out[e + (e >> 3)] = make_int4(o[4 * j], o[4 * j + 1], o[4 * j + 2], o[4 * j + 3]);
+    }
+  }
+  __syncthreads();
+  const bool svec = (reinterpret_cast<uintptr_t>(slot) & 15u) == 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = j * HS_THREADS + threadIdx.x;
+    const int4 v = s_out[e + (e >> 3)];
+    const int64_t i = base + 4 * int64_t(e);
+    if (svec && i + 3 < n) {
+      *reinterpret_cast<int4*>(slot + i) = v;
+    } else {
+      if (i < n) slot[i] = v.x;
+      if (i + 1 < n) slot[i + 1] = v.y;
+      if (i + 2 < n) slot[i + 2] = v.z;
+      if (i + 3 < n) slot[i + 3] = v.w;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ tile histograms
 // Counts below HS_TH_BINS (max_freq < HS_TH_BINS): one workgroup per tile of
 // HS_SEL_TILE ids reads the tile's counts once (16 per thread, all loads
 // issued first) and stores the tile's histogram th[tile * nb + c] (nb =
-// max_freq + 1, at most 4096 per bin: uint16).
+// max_freq + 1, at most 4096 per bin: uint16).  With `codes`, it also stores
+// every id's clamped count as one byte, so the selection's write pass reads
+// one byte per id instead of four.
 constexpr int HS_TH_BINS = 64;
 
-__global__ void __launch_bounds__(HS_THREADS) k_hs_tilehist(const int32_t* __restrict__ f, int64_t n,
-                                                           int32_t max_freq,
+// Bit 7 of each byte of the result is set where that byte of q (a code
+// below 128) is nonzero.
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t q) {
+  return ((q + 0x7f7f7f7fu) | q) & 0x80808080u;
+}
+
+// One launch for both kinds: workgroups [0, tiles_v) take the node tiles,
+// the rest the edge tiles; th holds the node rows, then the edge rows.  A
+// tile's row is its suffix histogram, th[tile * nb + c] = ids of the tile
+// with clamped count >= c, so that the selection reads a tile's (above T,
+// at T) pair as two values.  The counts are read once: streaming loads.
+__global__ void __launch_bounds__(HS_THREADS) k_hs_tilehist(const int32_t* __restrict__ f_v, int64_t n_v,
+                                                           uint8_t* __restrict__ codes_v,
+                                                           const int32_t* __restrict__ f_e, int64_t n_e,
+                                                           uint8_t* __restrict__ codes_e,
+                                                           int64_t tiles_v, int32_t max_freq,
                                                            uint16_t* __restrict__ th) {
   __shared__ uint32_t s_h[HS_TH_BINS];
   const int nb = max_freq + 1;
+  const bool edges = int64_t(blockIdx.x) >= tiles_v;
+  const int32_t* f = edges ? f_e : f_v;
+  const int64_t n = edges ? n_e : n_v;
+  uint8_t* codes = edges ? codes_e : codes_v;
   if (threadIdx.x < HS_TH_BINS) s_h[threadIdx.x] = 0u;
   const bool vec = (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
-  const int64_t base = int64_t(blockIdx.x) * HS_SEL_TILE;
+  const int64_t base = (edges ? int64_t(blockIdx.x) - tiles_v : int64_t(blockIdx.x)) * HS_SEL_TILE;
   int32_t c[HS_SEL_ROUNDS][4];
 #pragma unroll
   for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
     const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
     if (vec && i0 + 3 < n) {
-      const int4 v = *reinterpret_cast<const int4*>(f + i0);
+      const int4 v = __builtin_bit_cast(
+          int4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(f + i0)));
       c[r][0] = v.x; c[r][1] = v.y; c[r][2] = v.z; c[r][3] = v.w;
     } else {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) c[r][k] = i0 + k < n ? f[i0 + k] : -1;   // -1: past n
+      for (int k = 0; k < 4; ++k) c[r][k] = i0 + k < n ? f[i0 + k] : 0;
     }
   }
   __syncthreads();
-  uint32_t reg[HS_REG_BINS] = {};
+  // Each id's clamped count as one byte (0 past n).  Almost every id of a
+  // large universe has count 0: only the nonzero bytes reach the LDS
+  // histogram; bin 0 is implied by the tile's id count.
 #pragma unroll
   for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
     const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
+    if (i0 >= n) continue;
+    uint32_t q = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (i0 + k >= n) continue;
-      const int32_t b = clamp_count(c[r][k], max_freq);
-      if (b < HS_REG_BINS) {
-#pragma unroll
-        for (int q = 0; q < HS_REG_BINS; ++q) reg[q] += (b == q);
-      } else {
-        atomicAdd(&s_h[b], 1u);
-      }
-    }
+    for (int k = 0; k < 4; ++k)
+      q |= uint32_t(i0 + k < n ? clamp_count(c[r][k], max_freq) : 0) << (8 * k);
+    if (codes) *reinterpret_cast<uint32_t*>(codes + i0) = q;
+    for (uint32_t z = nonzero_bytes(q); z; z &= z - 1u)
+      atomicAdd(&s_h[(q >> ((__ffs(z) - 1) & ~7)) & 0xffu], 1u);
   }
-#pragma unroll
-  for (int q = 0; q < HS_REG_BINS; ++q)
-    if (q < nb && reg[q]) atomicAdd(&s_h[q], reg[q]);
   __syncthreads();
-  if (threadIdx.x < nb) th[int64_t(blockIdx.x) * nb + threadIdx.x] = uint16_t(s_h[threadIdx.x]);
+  if (threadIdx.x < nb) {
+    uint32_t v = 0;
+    if (threadIdx.x == 0) {
+      const int64_t left = n - base;
+      v = uint32_t(left < HS_SEL_TILE ? left : HS_SEL_TILE);
+    } else {
+      for (int b = threadIdx.x; b < nb; ++b) v += s_h[b];
+    }
+    th[int64_t(blockIdx.x) * nb + threadIdx.x] = uint16_t(v);
+  }
 }
 
-// hist[c] += sum over tiles of th[tile * nb + c]: workgroup k sums tiles k,
-// k + gridDim.x, ... of its kind in LDS (both kinds in one launch: the first
-// half of the grid takes the nodes, the second the edges), then adds its
-// partial histogram with nb global atomics.
+// hist[c] += sum over tiles of the tile's ids with count c (the difference of
+// adjacent entries of its suffix row): the kind's tiles are split among half
+// of the grid (the first half takes the nodes, the second the edges), each
+// workgroup sums its range in LDS and adds its partial histogram with nb
+// global atomics.
 __global__ void __launch_bounds__(HS_THREADS) k_hs_tilesum(const uint16_t* __restrict__ th_v,
                                                           int64_t tiles_v,
                                                           const uint16_t* __restrict__ th_e,
@@ -434,23 +594,24 @@ __global__ void __launch_bounds__(HS_THREADS) k_hs_tilesum(const uint16_t* __res
   // the kind's tiles are split into `half` contiguous ranges; this workgroup
   // reads its range's nb-bin rows as one flat array
   const int64_t t0 = tiles * k / half, t1 = tiles * (k + 1) / half;
-  for (int64_t j = t0 * nb + threadIdx.x; j < t1 * nb; j += HS_THREADS)
-    atomicAdd(&s_h[int(j % nb)], uint32_t(th[j]));
+  for (int64_t j = t0 * nb + threadIdx.x; j < t1 * nb; j += HS_THREADS) {
+    const int c = int(j % nb);
+    atomicAdd(&s_h[c], uint32_t(th[j]) - (c + 1 < nb ? uint32_t(th[j + 1]) : 0u));
+  }
   __syncthreads();
   if (threadIdx.x < nb && s_h[threadIdx.x]) atomicAdd(&(edges ? he : hv)[threadIdx.x], s_h[threadIdx.x]);
 }
 
-// Scan input of the selection from tile histograms: tile i's packed pair
-// (ids above T, ids at T).
+// Scan input of the selection from the tiles' suffix rows: tile i's packed
+// pair (ids above T, ids at T), over the node tiles and then the edge tiles.
 struct InTilePairs {
   const uint16_t* th;
   int nb;
   const HsParams* prm;
   __device__ uint64_t operator()(int64_t i) const {
     const int32_t T = prm->T;
-    uint64_t above = 0;
-    for (int c = T + 1; c < nb; ++c) above += th[i * nb + c];
-    const uint64_t at = T < nb ? th[i * nb + T] : 0u;
+    const uint64_t above = T + 1 < nb ? th[i * nb + T + 1] : 0u;
+    const uint64_t at = T < nb ? th[i * nb + T] - above : 0u;
     return (above << 32) | at;
   }
 };
@@ -472,8 +633,11 @@ struct HsWs {
   uint64_t* tsum_e;
   void* scan_v;
   void* scan_e;
-  uint16_t* th_v;     // per-tile histograms (max_freq < HS_TH_BINS only)
-  uint16_t* th_e;
+  uint16_t* th;       // per-tile suffix rows, node tiles then edge tiles (tiled path only)
+  uint64_t* tsum;     // exclusive prefixes over the node tiles then the edge tiles (tiled)
+  void* scan;
+  uint8_t* codes_v;   // one-byte clamped counts, padded to whole tiles (tiled path only)
+  uint8_t* codes_e;
 };
 
 static bool use_tile_hist(int32_t max_freq) {
@@ -484,14 +648,22 @@ static bool use_tile_hist(int32_t max_freq) {
   return mode && max_freq + 1 <= HS_TH_BINS;
 }
 
+static bool use_codes(int32_t max_freq) {
+  static const int mode = [] {   // tuning override: FAST_HS_CODES=0 turns it off
+    const char* e = std::getenv("FAST_HS_CODES");
+    return e && e[0] == '0' ? 0 : 1;
+  }();
+  return mode && use_tile_hist(max_freq);
+}
+
 static int64_t sel_tiles(int64_t n) { return (n + HS_SEL_TILE - 1) / HS_SEL_TILE; }
 
 static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, HsWs* ws) {
   size_t off = 0;
-  auto take = [&](size_t bytes) {
+  auto take = [&](size_t bytes) -> char* {   // NULL for a region the layout leaves out
     const size_t o = off;
     off += align_up(bytes, 256);
-    return base ? base + o : nullptr;
+    return base && bytes ? base + o : nullptr;
   };
   char* hv = take(size_t(max_freq + 1) * 4);
   char* he = take(size_t(max_freq + 1) * 4);
@@ -501,11 +673,19 @@ static size_t hs_layout(int64_t nv, int64_t ne, int32_t max_freq, char* base, Hs
   char* sv = take(scan_workspace<uint64_t>(sel_tiles(nv)));
   char* se = take(scan_workspace<uint64_t>(sel_tiles(ne)));
   const bool tiled = use_tile_hist(max_freq);
-  char* thv = take(tiled ? size_t(sel_tiles(nv)) * size_t(max_freq + 1) * 2 : 0);
-  char* the = take(tiled ? size_t(sel_tiles(ne)) * size_t(max_freq + 1) * 2 : 0);
+  const int64_t tiles = sel_tiles(nv) + sel_tiles(ne);
+  char* th = take(tiled ? size_t(tiles) * size_t(max_freq + 1) * 2 : 0);
+  char* ta = take(tiled ? size_t(tiles) * 8 : 0);
+  char* sa = take(tiled ? scan_workspace<uint64_t>(tiles) : 0);
+  const bool cd = use_codes(max_freq);
+  char* cv = take(cd ? size_t(sel_tiles(nv)) * HS_SEL_TILE : 0);
+  char* ce = take(cd ? size_t(sel_tiles(ne)) * HS_SEL_TILE : 0);
   if (ws) {
-    ws->th_v = reinterpret_cast<uint16_t*>(thv);
-    ws->th_e = reinterpret_cast<uint16_t*>(the);
+    ws->codes_v = reinterpret_cast<uint8_t*>(cv);
+    ws->codes_e = reinterpret_cast<uint8_t*>(ce);
+    ws->th = reinterpret_cast<uint16_t*>(th);
+    ws->tsum = reinterpret_cast<uint64_t*>(ta);
+    ws->scan = sa;
     ws->hv = reinterpret_cast<uint32_t*>(hv);
     ws->he = reinterpret_cast<uint32_t*>(he);
     ws->prm = reinterpret_cast<HsParams*>(pr);
@@ -631,21 +811,23 @@ extern "C" fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_
   HsWs w;
   hs_layout(num_nodes, num_edges, max_freq, static_cast<char*>(ws), &w);
   const int64_t nbins = int64_t(max_freq) + 1;
-  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(nbins, HS_THREADS)), dim3(HS_THREADS), 0, st,
-                     reinterpret_cast<int32_t*>(w.hv), nbins, 0);
-  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(nbins, HS_THREADS)), dim3(HS_THREADS), 0, st,
-                     reinterpret_cast<int32_t*>(w.he), nbins, 0);
+  // both count histograms in one fill: he follows hv in the workspace
+  const int64_t span = (w.he - w.hv) + nbins;
+  hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(span, HS_THREADS)), dim3(HS_THREADS), 0, st,
+                     reinterpret_cast<int32_t*>(w.hv), span, 0);
   const bool tiled = use_tile_hist(max_freq);
+  const int64_t tv = sel_tiles(num_nodes), te = sel_tiles(num_edges);
+  // codes are written only where the layout holds them and a write pass will
+  // read them
+  const bool cd = use_codes(max_freq);
+  uint8_t* cv = cd && (hot_v || slot_v) ? w.codes_v : nullptr;
+  uint8_t* ce = cd && (hot_e || slot_e) ? w.codes_e : nullptr;
   if (tiled) {
-    const int64_t tv = sel_tiles(num_nodes), te = sel_tiles(num_edges);
-    if (tv > 0)
-      hipLaunchKernelGGL(k_hs_tilehist, dim3(uint32_t(tv)), dim3(HS_THREADS), 0, st, freq_v,
-                         num_nodes, max_freq, w.th_v);
-    if (te > 0)
-      hipLaunchKernelGGL(k_hs_tilehist, dim3(uint32_t(te)), dim3(HS_THREADS), 0, st, freq_e,
-                         num_edges, max_freq, w.th_e);
-    hipLaunchKernelGGL(k_hs_tilesum, dim3(2 * 256), dim3(HS_THREADS), 0, st, w.th_v, tv, w.th_e, te,
-                       int(nbins), w.hv, w.he);
+    if (tv + te > 0)
+      hipLaunchKernelGGL(k_hs_tilehist, dim3(uint32_t(tv + te)), dim3(HS_THREADS), 0, st, freq_v,
+                         num_nodes, cv, freq_e, num_edges, ce, tv, max_freq, w.th);
+    hipLaunchKernelGGL(k_hs_tilesum, dim3(2 * 256), dim3(HS_THREADS), 0, st, w.th, tv,
+                       w.th + tv * nbins, te, int(nbins), w.hv, w.he);
   } else {
     if (num_nodes > 0)
       hipLaunchKernelGGL(k_hs_hist, dim3(grid_for(num_nodes, HS_THREADS * 16, 4096)),
@@ -657,27 +839,49 @@ extern "C" fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_
   hipLaunchKernelGGL(k_hs_threshold, dim3(1), dim3(HS_THREADS), 0, st, w.hv, w.he, max_freq,
                      budget, num_nodes, num_edges, w.prm, num_hot_v, num_hot_e);
   const int64_t B = budget < num_nodes + num_edges ? budget : num_nodes + num_edges;
+  const bool want_v = num_nodes > 0 && (hot_v || slot_v), want_e = num_edges > 0 && (hot_e || slot_e);
   hipError_t e = hipSuccess;
-  auto select = [&](const int32_t* f, int64_t n, bool edges, uint64_t* tsum, void* scan_ws,
-                    const uint16_t* th, int64_t* hot, int32_t* slot) {
-    if (n == 0 || (!hot && !slot) || e != hipSuccess) return;
-    const int64_t tiles = sel_tiles(n);
-    if (tiled) {
-      e = scan_launch<InTilePairs, OutU64InPlace, uint64_t>(InTilePairs{th, int(nbins), w.prm},
-                                                           OutU64InPlace{tsum}, tiles, scan_ws,
+  if (tiled) {
+    // one scan of the tile pairs over the node tiles then the edge tiles
+    if (want_v || want_e)
+      e = scan_launch<InTilePairs, OutU64InPlace, uint64_t>(InTilePairs{w.th, int(nbins), w.prm},
+                                                           OutU64InPlace{w.tsum}, tv + te, w.scan,
                                                            nullptr, nullptr, st);
-    } else {
+    if (e == hipSuccess && (want_v || want_e)) {
+      if (cd) {
+        const SelKind kv{cv, num_nodes, B < num_nodes ? B : num_nodes, want_v ? hot_v : nullptr,
+                         want_v ? slot_v : nullptr};
+        const SelKind ke{ce, num_edges, B < num_edges ? B : num_edges, want_e ? hot_e : nullptr,
+                         want_e ? slot_e : nullptr};
+        hipLaunchKernelGGL(k_sel_write_codes, dim3(uint32_t(tv + te)), dim3(HS_THREADS), 0, st, kv,
+                           ke, tv, w.prm, w.tsum);
+      } else {
+        if (want_v)
+          hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(tv)), dim3(HS_THREADS), 0, st, freq_v,
+                             num_nodes, max_freq, w.prm, false, w.tsum, nullptr,
+                             B < num_nodes ? B : num_nodes, hot_v, slot_v);
+        if (want_e)
+          hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(te)), dim3(HS_THREADS), 0, st, freq_e,
+                             num_edges, max_freq, w.prm, true, w.tsum + tv, w.tsum + tv,
+                             B < num_edges ? B : num_edges, hot_e, slot_e);
+      }
+    }
+  } else {
+    auto select = [&](const int32_t* f, int64_t n, bool edges, uint64_t* tsum, void* scan_ws,
+                      int64_t* hot, int32_t* slot) {
+      if (n == 0 || (!hot && !slot) || e != hipSuccess) return;
+      const int64_t tiles = sel_tiles(n);
       hipLaunchKernelGGL(k_sel_tiles, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
                          w.prm, tsum);
       e = scan_launch<InU64, OutU64InPlace, uint64_t>(InU64{tsum}, OutU64InPlace{tsum}, tiles,
                                                      scan_ws, nullptr, nullptr, st);
-    }
-    if (e != hipSuccess) return;
-    hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
-                       w.prm, edges, tsum, B < n ? B : n, hot, slot);
-  };
-  select(freq_v, num_nodes, false, w.tsum_v, w.scan_v, w.th_v, hot_v, slot_v);
-  select(freq_e, num_edges, true, w.tsum_e, w.scan_e, w.th_e, hot_e, slot_e);
+      if (e != hipSuccess) return;
+      hipLaunchKernelGGL(k_sel_write, dim3(uint32_t(tiles)), dim3(HS_THREADS), 0, st, f, n, max_freq,
+                         w.prm, edges, tsum, nullptr, B < n ? B : n, hot, slot);
+    };
+    select(freq_v, num_nodes, false, w.tsum_v, w.scan_v, hot_v, slot_v);
+    select(freq_e, num_edges, true, w.tsum_e, w.scan_e, hot_e, slot_e);
+  }
   if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
   return check_launch(fn);
 }
