@@ -124,6 +124,35 @@ __global__ void __launch_bounds__(THREADS) k_by_groups(const u32x4* __restrict__
   else b[i] = a[i];
 }
 
+// Rows of 400 bytes (25 16-byte vectors), one 32-lane group per row and
+// lanes 0..24 one vector each: two rows in (K, V), two rows out (dK, dV), the
+// access shape of the fused attention backward on fp32 rows of 100.  _sep
+// reads and writes four separate arrays; _kv keeps each row's K and V (and
+// dK and dV) side by side in one 800-byte row, so that the traffic is one
+// stream in and one stream out.
+constexpr size_t ROWV = 25;
+__global__ void __launch_bounds__(THREADS) k_rows_sep(const u32x4* __restrict__ k,
+                                                      const u32x4* __restrict__ v,
+                                                      u32x4* __restrict__ dk, u32x4* __restrict__ dv,
+                                                      size_t rows) {
+  const size_t r = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (r >= rows || l >= ROWV) return;
+  const u32x4 x = k[r * ROWV + l], y = v[r * ROWV + l];
+  dk[r * ROWV + l] = x;
+  dv[r * ROWV + l] = y;
+}
+
+__global__ void __launch_bounds__(THREADS) k_rows_kv(const u32x4* __restrict__ kv,
+                                                     u32x4* __restrict__ dkv, size_t rows) {
+  const size_t r = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (r >= rows || l >= ROWV) return;
+  const u32x4 x = kv[r * 2 * ROWV + l], y = kv[r * 2 * ROWV + ROWV + l];
+  dkv[r * 2 * ROWV + l] = x;
+  dkv[r * 2 * ROWV + ROWV + l] = y;
+}
+
 struct Buffers {
   u32x4 *a, *b, *c, *d;
   unsigned* sink;
@@ -195,6 +224,14 @@ int main(int argc, char** argv) {
       hipLaunchKernelGGL(k_by_waves, g_dbl, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
     rows.push_back({"mix22_by_groups", 2.0 * bytes, median_ms([&] {
       hipLaunchKernelGGL(k_by_groups, g_dbl, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
+    // 400-byte rows filling 1 GiB per stream (separate) or 2 GiB of 800-byte rows (interleaved)
+    const size_t nrow = (bytes / 2) / (16 * ROWV);
+    const dim3 g_rows(unsigned((nrow * 32 + THREADS - 1) / THREADS));
+    const double moved = 4.0 * double(nrow) * 16 * ROWV;
+    rows.push_back({"rows400_sep", moved, median_ms([&] {
+      hipLaunchKernelGGL(k_rows_sep, g_rows, blk, 0, 0, B.a, B.c, B.b, B.d, nrow); }, reps)});
+    rows.push_back({"rows400_kv", moved, median_ms([&] {
+      hipLaunchKernelGGL(k_rows_kv, g_rows, blk, 0, 0, B.a, B.b, nrow); }, reps)});
   }
   CHECK(hipGetLastError());
   std::printf("{");
