@@ -13,14 +13,14 @@
 // the 1e-5 target on its own, and the device library's general cosf costs
 // most of the op's time.  cos_rr below first reduces exactly: a Cody-Waite
 // reduction (W. J. Cody and W. Waite, "Software Manual for the Elementary
-// Functions", 1980) x = k*pi/2 + r with pi/2 split into three fp32 parts
-// C1 + C2 + C3 (each the fp32 rounding of what remained of pi/2, derived
-// exactly from Machin's formula for pi), every step one fused multiply-add,
-// so |r| <= pi/4 carries about 1e-7 absolute error for |x| <= 2^16.  The
-// reduced angle r + q*pi/2 (q = k mod 4, taken as the fraction of k/4) is
-// then handed to v_cos_f32 in revolutions, r/(2 pi) + q/4, a value below one
-// revolution, where the hardware cosine measured 3e-7 worst-case absolute
-// error against fp64 on MI355X.  Larger arguments take the library cosf.
+// Functions", 1980) x = k*2pi + r with 2pi split into two fp32 parts D1 + D2
+// (four times the fp32 roundings of pi/2 and of what remained of it, derived
+// exactly from Machin's formula for pi; the third part would change r by
+// less than 1e-10 for |x| <= 2^16), each step one fused multiply-add, so
+// |r| <= pi carries about 2.5e-7 absolute error.  r/(2 pi), a value within
+// half a revolution, goes to v_cos_f32, whose worst-case absolute error
+// measured 3e-7 against fp64 below one revolution on MI355X.  Arguments
+// beyond 2^16 take the library cosf.
 #include "common.h"
 
 namespace fast {
@@ -41,20 +41,23 @@ constexpr int TE_SEGS = FAST_TE_SEGS;    // destination segments per workgroup
 constexpr int TE_TILE_MAX = 256;         // rows staged per tile (at most)
 constexpr int TE_PASSES = FAST_TE_PASSES;  // row passes per tile
 
-// Branch-free: valid (about 3e-7 absolute) for |x| <= 2^16, finite beyond.
+// Branch-free: valid (within 6e-7 absolute) for |x| <= 2^16, finite beyond.
 __device__ __forceinline__ float cos_rr(float x) {
-  const float C1 = 0x1.921fb6p+0f, C2 = -0x1.777a5cp-25f, C3 = -0x1.ee59dap-50f;
-  const float TWO_OVER_PI = 0x1.45f306p-1f, INV_TWO_PI = 0x1.45f306p-3f;
-  const float k = rintf(x * TWO_OVER_PI);
-  float r = fmaf(-k, C1, x);
-  r = fmaf(-k, C2, r);
-  r = fmaf(-k, C3, r);
-  const float q = __builtin_amdgcn_fractf(0.25f * k);   // (k mod 4) / 4, exact
-  return __builtin_amdgcn_cosf(fmaf(r, INV_TWO_PI, q));
+  const float D1 = 0x1.921fb6p+2f, D2 = -0x1.777a5cp-23f;   // 2pi = D1 + D2 + O(2^-47)
+  const float INV_TWO_PI = 0x1.45f306p-3f;
+  const float k = rintf(x * INV_TWO_PI);
+  float r = fmaf(-k, D1, x);
+  r = fmaf(-k, D2, r);
+  return __builtin_amdgcn_cosf(r * INV_TWO_PI);
 }
 
 // Large arguments (|x| > 2^16, or not finite) take the library cosf.
 __device__ __forceinline__ bool cos_cw_ok(float x) { return fabsf(x) <= 65536.f; }
+
+// A bf16 row is checked once: every |fmaf(om, dt, ph)| of its columns is at
+// most fmaf(max |om|, |dt|, max |ph|) up to one rounding, so a bound of 65000
+// keeps them all inside cos_rr's range.
+constexpr float TE_ROW_LIMIT = 65000.f;
 
 // Thread t owns the column chunk t % cpr of rows t / cpr, t / cpr + rpp, ...
 // (rpp = rows per pass), so omega and phi of its columns stay in registers.
@@ -79,12 +82,14 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
   const int rsub = narrow ? int(threadIdx.x) / cpr : 0;
   const int c0 = narrow ? int(threadIdx.x) - rsub * cpr : int(threadIdx.x);
   const int tile = rpp * TE_PASSES < TE_TILE_MAX ? rpp * TE_PASSES : (TE_TILE_MAX / rpp) * rpp;
-  float om[VEC], ph[VEC];
+  float om[VEC], ph[VEC], om_max = 0.f, ph_max = 0.f;
   if (narrow && rsub < rpp) {
 #pragma unroll
     for (int k = 0; k < VEC; ++k) {
       om[k] = omega[c0 * VEC + k];
       ph[k] = phi[c0 * VEC + k];
+      om_max = fmaxf(om_max, fabsf(om[k]));
+      ph_max = fmaxf(ph_max, fabsf(ph[k]));
     }
   }
   for (int64_t t0 = r0; t0 < r1; t0 += tile) {
@@ -103,18 +108,37 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
       if (rsub < rpp) {
         for (int row = rsub; row < nrows; row += rpp) {
           const float dt = s_dt[row];
-          float x[VEC], o[VEC];
-          bool big = false;
+          float o[VEC];
+          if constexpr (sizeof(TO) == 2) {
+            // bf16 rows are ALU-bound (twice the elements per byte written):
+            // one range check per row.  Not-less-than also sends a NaN bound
+            // (a NaN time) to the checked path.
+            if (__builtin_expect(!(fmaf(om_max, fabsf(dt), ph_max) <= TE_ROW_LIMIT), 0)) {
 #pragma unroll
-          for (int k = 0; k < VEC; ++k) {
-            x[k] = fmaf(om[k], dt, ph[k]);
-            o[k] = cos_rr(x[k]);
-            big |= !cos_cw_ok(x[k]);
-          }
-          if (__builtin_expect(big, 0)) {
+              for (int k = 0; k < VEC; ++k) {
+                const float x = fmaf(om[k], dt, ph[k]);
+                o[k] = cos_cw_ok(x) ? cos_rr(x) : cosf(x);
+              }
+            } else {
 #pragma unroll
-            for (int k = 0; k < VEC; ++k)
-              if (!cos_cw_ok(x[k])) o[k] = cosf(x[k]);
+              for (int k = 0; k < VEC; ++k) o[k] = cos_rr(fmaf(om[k], dt, ph[k]));
+            }
+          } else {
+            // fp32 rows are bound by the stores: a compare per element and a
+            // rare fix-up, with no branch in the row loop, measured faster
+            float x[VEC];
+            bool big = false;
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+              x[k] = fmaf(om[k], dt, ph[k]);
+              o[k] = cos_rr(x[k]);
+              big |= !cos_cw_ok(x[k]);
+            }
+            if (__builtin_expect(big, 0)) {
+#pragma unroll
+              for (int k = 0; k < VEC; ++k)
+                if (!cos_cw_ok(x[k])) o[k] = cosf(x[k]);
+            }
           }
           StreamIO<TO, VEC, NT>::store(te + (t0 + row) * d_t + c0 * VEC, o);
         }

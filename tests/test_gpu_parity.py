@@ -539,10 +539,13 @@ def test_time_encode_no_edges():
     assert te.shape[0] == 0
 
 
-def test_time_encode_cosine_accuracy_sweep():
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_time_encode_cosine_accuracy_sweep(out):
     # one destination per edge with dst_t = dt and edge_t = 0, so dt is exact;
-    # omega = 1 makes the argument dt itself (plus a phase-shifted column)
-    _announce("time encode cosine sweep")
+    # omega = 1 makes the argument dt itself (plus a phase-shifted column).
+    # bf16 rows take their range check per row: arguments beyond 2^16 there
+    # must still reach the fallback.
+    _announce(f"time encode cosine sweep {out}")
     r = np.random.default_rng(5)
     n = 400_000
     dt = np.concatenate([r.uniform(0, 1e4, n // 2), r.uniform(1e4, 2e5, n // 4),
@@ -550,7 +553,16 @@ def test_time_encode_cosine_accuracy_sweep():
     off = np.arange(dt.size + 1, dtype=np.int32)
     om = np.array([1.0, 1.0, 0.37], dtype=np.float32)
     ph = np.array([0.0, np.float32(np.pi / 2), -1.25], dtype=np.float32)
-    te = _te_gpu(off, dt, np.zeros(dt.size, np.float32), om, ph)
+    te = _te_gpu(off, dt, np.zeros(dt.size, np.float32), om, ph, out)
     ref = oracle.time_encode(off, dt, np.zeros(dt.size, np.float32), om, ph)
-    err = np.abs(te.cpu().numpy().astype(np.float64) - ref)
-    assert err.max() <= 1e-6, f"max cosine error {err.max():.3g}"
+    if out == "f32":
+        err = np.abs(te.cpu().numpy().astype(np.float64) - ref)
+        assert err.max() <= 1e-6, f"max cosine error {err.max():.3g}"
+    else:
+        # an fp32 cosine within 1e-6, rounded to bf16: rounding is monotone, so
+        # the result lies between the roundings of ref - 1e-6 and ref + 1e-6
+        rnd = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).double().numpy()
+        got = te.cpu().double().numpy()
+        lo, hi = rnd(ref - 1e-6), rnd(ref + 1e-6)
+        bad = (got < lo) | (got > hi)
+        assert not bad.any(), f"{int(bad.sum())} bf16 cosines outside the rounding band"
