@@ -97,9 +97,13 @@ class Step:
     so that prep of the next batch can run while attention of the current
     batch still reads its own offsets (software pipelining on two streams)."""
 
-    def __init__(self, b, torch, fast, slots=2):
+    def __init__(self, b, torch, fast, slots=2, kv="packed"):
         from synth import make_block_operands, make_slot_map, make_table, omega_phi
         self.b, self.torch, self.fast, self.slots = b, torch, fast, slots
+        # "packed": each edge's K and V rows side by side in one [E, 2, H, dh]
+        # array (and dK, dV likewise), the layout a fused K|V projection
+        # writes; "separate": four [E, H, dh] arrays
+        self.kv = kv
         dev = "cuda"
         tdt = torch.float32 if b.dtype == "f32" else torch.bfloat16
         self.DT = fast.F32 if b.dtype == "f32" else fast.BF16
@@ -114,8 +118,18 @@ class Step:
             d["out"] = torch.empty((N, b.H, b.dh), dtype=tdt, device=dev)
             d["lse"] = torch.empty((N, b.H), dtype=torch.float32, device=dev)
             d["dQ"] = torch.empty((N, b.H, b.dh), dtype=tdt, device=dev)
-            d["dK"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
-            d["dV"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
+            if kv == "packed":
+                # the same K and V values, moved into one packed array; K, V,
+                # dK and dV stay addressable as [E, H, dh] views
+                d["KV"] = torch.empty((E, 2, b.H, b.dh), dtype=tdt, device=dev)
+                d["KV"][:, 0] = d.pop("K")
+                d["KV"][:, 1] = d.pop("V")
+                d["K"], d["V"] = d["KV"][:, 0], d["KV"][:, 1]
+                d["dKV"] = torch.empty((E, 2, b.H, b.dh), dtype=tdt, device=dev)
+                d["dK"], d["dV"] = d["dKV"][:, 0], d["dKV"][:, 1]
+            else:
+                d["dK"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
+                d["dV"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
             d["off"], d["ws_off"], d["te"], d["g"] = [], [], [], []
             for _ in range(slots):
                 off = torch.empty(N + 1, dtype=torch.int32, device=dev)
@@ -199,15 +213,28 @@ class Step:
         layer 1, on the offsets of `slot`."""
         f, b = self.fast, self.b
         mark = self._marker(self.torch, rec, names)
+        packed = self.kv == "packed"
         for i, d in enumerate(self.blocks):
-            mark(f"attn_fwd_L{i + 1}", lambda d=d: f.fast_edge_attention_fwd(
-                d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
-                d["out"], d["lse"]))
+            if packed:
+                fn = lambda d=d: f.fast_edge_attention_fwd_packed(
+                    d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["KV"], self.scale, SLOPE,
+                    d["out"], d["lse"])
+            else:
+                fn = lambda d=d: f.fast_edge_attention_fwd(
+                    d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                    d["out"], d["lse"])
+            mark(f"attn_fwd_L{i + 1}", fn)
         for i in reversed(range(len(self.blocks))):
             d = self.blocks[i]
-            mark(f"attn_bwd_L{i + 1}", lambda d=d: f.fast_edge_attention_bwd(
-                d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
-                d["lse"], d["dO"], d["dQ"], d["dK"], d["dV"]))
+            if packed:
+                fn = lambda d=d: f.fast_edge_attention_bwd_packed(
+                    d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["KV"], self.scale, SLOPE,
+                    d["lse"], d["dO"], d["dQ"], d["dKV"])
+            else:
+                fn = lambda d=d: f.fast_edge_attention_bwd(
+                    d["g"][slot], b.H, b.dh, self.DT, d["Q"], d["K"], d["V"], self.scale, SLOPE,
+                    d["lse"], d["dO"], d["dQ"], d["dK"], d["dV"])
+            mark(f"attn_bwd_L{i + 1}", fn)
 
     def run_serial(self, rec=None, names=None):
         self.prep(0, rec, names)
@@ -809,7 +836,7 @@ def measure(name, args, torch, fast, headline, ceilings=None):
     from synth import make_batch
     b = make_batch(WORKLOADS[name])
     log(f"workload {b.name}: blocks {[(x.num_dst, x.num_edges) for x in b.blocks]}")
-    step = Step(b, torch, fast)
+    step = Step(b, torch, fast, kv=args.kv)
     side = torch.cuda.Stream()
     torch.cuda.synchronize()
     for _ in range(args.warmup):
@@ -892,7 +919,7 @@ def measure(name, args, torch, fast, headline, ceilings=None):
         "unit": "sampled edges/s",
         "ms_per_step": round(ms, 4),
         "dtype": b.dtype,
-        "config": describe(b),
+        "config": dict(describe(b), kv_layout=args.kv),
         "roofline": roofline,
         "fused_attention": {
             "edges_per_s": b.sampled_edges / (fused_ms * 1e-3), "ms": round(fused_ms, 4),
@@ -950,6 +977,9 @@ def main():
                     help="also time the serial step captured once as a HIP graph and replayed")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--kv", choices=["packed", "separate"], default="packed",
+                    help="layout of the attention's per-edge K and V rows (and their gradients): "
+                         "one packed [E, 2, H, dh] array, or separate [E, H, dh] arrays")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the streaming-ceiling probe (it runs as a child process before this "
                          "process touches the GPU; profilers that initialise the GPU first need this)")

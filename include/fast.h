@@ -373,6 +373,25 @@ fast_status_t fast_edge_attention_bwd(const fast_tcsr_t* g, int H, int dh, fast_
                                       fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
+ * The fused operator on packed K|V rows (Sec. 4.3 operators; the per-edge key
+ * and value of Eq. 1 side by side, as a fused K|V projection writes them).
+ *   KV: [E, 2, H, dh] of dtype: row e is K[e] (F = H*dh elements) followed by
+ *   V[e]; dKV: the same layout for dK and dV.
+ * Results equal fast_edge_attention_fwd / _bwd on K = KV[:, 0], V = KV[:, 1]
+ * bit for bit (same kernels, rows 2F apart), with the same argument rules and
+ * errors; K, V and their gradients then move as one stream each way.
+ * ------------------------------------------------------------------------ */
+fast_status_t fast_edge_attention_fwd_packed(const fast_tcsr_t* g, int H, int dh,
+                                             fast_dtype_t dtype, const void* Q, const void* KV,
+                                             float scale, float neg_slope, void* out, float* lse,
+                                             fast_stream_t stream);
+fast_status_t fast_edge_attention_bwd_packed(const fast_tcsr_t* g, int H, int dh,
+                                             fast_dtype_t dtype, const void* Q, const void* KV,
+                                             float scale, float neg_slope, const float* lse,
+                                             const void* dout, void* dQ, void* dKV,
+                                             fast_stream_t stream);
+
+/* ------------------------------------------------------------------------
  * Indexed operands (Sec. 4.2: the compressed batch carries each distinct id
  * once plus an inverse index; here the fused operator reads its K and V rows
  * through such an index instead of from a rebuilt per-edge copy).

@@ -25,6 +25,7 @@ __all__ = [
     "fast_edge_softmax_fwd", "fast_edge_softmax_bwd",
     "fast_temporal_aggregate_fwd", "fast_temporal_aggregate_bwd",
     "fast_edge_attention_fwd", "fast_edge_attention_bwd",
+    "fast_edge_attention_fwd_packed", "fast_edge_attention_bwd_packed",
     "fast_edge_attention_fwd_indexed", "fast_edge_attention_bwd_indexed",
     "fast_occurrence_csr_workspace", "fast_occurrence_csr",
     "fast_index_add_rows_workspace", "fast_index_add_rows",
@@ -104,6 +105,9 @@ _SIGS = {
     "fast_edge_attention_fwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p, _p]),
     "fast_edge_attention_bwd": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _f32, _f32, _p, _p,
                                        _p, _p, _p, _p]),
+    "fast_edge_attention_fwd_packed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p]),
+    "fast_edge_attention_bwd_packed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p,
+                                              _p, _p]),
     "fast_edge_attention_fwd_indexed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _p,
                                                _i64, _f32, _f32, _p, _p, _p]),
     "fast_edge_attention_bwd_indexed": (_i32, [_G, _i32, _i32, _i32, _p, _p, _p, _i64, _p, _p,
@@ -319,6 +323,20 @@ def fast_edge_attention_bwd(g: TCSR, H, dh, dtype, Q, K, V, scale, neg_slope, ls
     _check(lib().fast_edge_attention_bwd(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(K), _ptr(V),
                                          scale, neg_slope, _ptr(lse), _ptr(dout), _ptr(dQ),
                                          _ptr(dK), _ptr(dV), _stream(stream)))
+
+
+def fast_edge_attention_fwd_packed(g: TCSR, H, dh, dtype, Q, KV, scale, neg_slope, out, lse,
+                                   stream=None):
+    _check(lib().fast_edge_attention_fwd_packed(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(KV),
+                                                scale, neg_slope, _ptr(out), _ptr(lse),
+                                                _stream(stream)))
+
+
+def fast_edge_attention_bwd_packed(g: TCSR, H, dh, dtype, Q, KV, scale, neg_slope, lse, dout, dQ,
+                                   dKV, stream=None):
+    _check(lib().fast_edge_attention_bwd_packed(C.byref(g), H, dh, dtype, _ptr(Q), _ptr(KV),
+                                                scale, neg_slope, _ptr(lse), _ptr(dout),
+                                                _ptr(dQ), _ptr(dKV), _stream(stream)))
 
 
 def fast_edge_attention_fwd_indexed(g: TCSR, H, dh, dtype, Q, K, k_index, k_rows, V, v_index,

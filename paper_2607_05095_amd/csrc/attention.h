@@ -112,6 +112,9 @@ struct AttnArgs {
   void* dV;
   float* alpha_out;
   float* dalpha_out;
+  // row stride of K, V, dK and dV in elements for the fused operators: F for
+  // separate arrays, 2F for packed K|V rows (0 on entry: F)
+  int64_t ldkv;
   // indexed operands: edge e reads row kidx[e] of K and vidx[e] of V (NULL:
   // row e); an index outside [0, rows) reads the nearest row
   const int32_t* kidx;
@@ -260,7 +263,7 @@ template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX = false>
 __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd(AttnArgs a) {
   LaneMap<P> m;
   if (!lane_setup<VE, P, LPH_CT>(a, m)) return;
-  const int F = a.L.F;
+  const int F = a.L.F, ld = int(a.ldkv);
   const T* K = static_cast<const T*>(a.K);
   const T* V = static_cast<const T*>(a.V);
   const float sl2 = a.scale * LOG2E;
@@ -277,8 +280,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd(AttnArg
     for (int i = 0; i < ATT_CH_FWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
       // indexed rows are shared across segments: keep them cacheable
-      load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kr[i]);
-      load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vr[i]);
+      load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), ld, m, kr[i]);
+      load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), ld, m, vr[i]);
     }
     float t[ATT_CH_FWD];
     float cm = -INFINITY;
@@ -336,15 +339,15 @@ __device__ __forceinline__ void bwd_chunk(const AttnArgs& a, const LaneMap<P>& m
                                           int64_t e1, bool has_lse, float sl2,
                                           BwdState<VE, P>& S, float (&x)[ATT_CH_BWD],
                                           float (&da)[ATT_CH_BWD]) {
-  const int F = a.L.F;
+  const int ld = int(a.ldkv);
   const T* K = static_cast<const T*>(a.K);
   const T* V = static_cast<const T*>(a.V);
   Raw<T, VE> kr[ATT_CH_BWD][P], vr[ATT_CH_BWD][P];
 #pragma unroll
   for (int i = 0; i < ATT_CH_BWD; ++i) {
     const int64_t e = slot_row(base, i, e1);
-    load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kr[i]);
-    load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vr[i]);
+    load_raw<T, VE, P, NT && !IDX>(K, operand_row<IDX>(a.kidx, a.k_rows, e), ld, m, kr[i]);
+    load_raw<T, VE, P, NT && !IDX>(V, operand_row<IDX>(a.vidx, a.v_rows, e), ld, m, vr[i]);
   }
   float t[ATT_CH_BWD], cm = -INFINITY;
 #pragma unroll
@@ -413,8 +416,8 @@ __device__ __forceinline__ void bwd_emit(const AttnArgs& a, const LaneMap<P>& m,
       dk[p][j] = g * S.q[p][j];
       dv[p][j] = al * S.go[p][j];
     }
-  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dK), e, a.L.F, m, dk);
-  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dV), e, a.L.F, m, dv);
+  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dK), e, int(a.ldkv), m, dk);
+  store_row_stream<T, VE, P, NT>(static_cast<T*>(a.dV), e, int(a.ldkv), m, dv);
 }
 
 template <typename T, int VE, int P, int LPH_CT, bool NT, bool IDX = false>
@@ -474,8 +477,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd(AttnArg
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      load_row<T, VE, P>(static_cast<const T*>(a.K), operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
-      load_row<T, VE, P>(static_cast<const T*>(a.V), operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
+      load_row<T, VE, P>(static_cast<const T*>(a.K), operand_row<IDX>(a.kidx, a.k_rows, e), int(a.ldkv), m, kx[i]);
+      load_row<T, VE, P>(static_cast<const T*>(a.V), operand_row<IDX>(a.vidx, a.v_rows, e), int(a.ldkv), m, vx[i]);
     }
 #pragma unroll
     for (int i = 0; i < ATT_CH_BWD; ++i) {

@@ -124,6 +124,15 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
   const int wg = (op == Op::kAttnBwd || op == Op::kAttnBwdIdx) ? ATT_BLOCK_BWD : ATT_BLOCK;
   fast_status_t s = attn_layout(fn, H, dh, dt, rows, nrows, wg, a.L);
   if (s != FAST_OK) return s;
+  // K, V, dK and dV rows: F apart (separate arrays) unless the packed entry
+  // points set 2F; a stride that is a multiple of F keeps every row on the
+  // vector alignment checked above
+  if (a.ldkv == 0) a.ldkv = a.L.F;
+  if (a.ldkv != a.L.F && !(op == Op::kAttnFwd || op == Op::kAttnBwd))
+    return fail(FAST_ERR_UNSUPPORTED, "%s: strided K/V rows only in the fused operators", fn);
+  if (a.ldkv % a.L.F != 0)
+    return fail(FAST_ERR_INVALID_ARG, "%s: K/V row stride %lld is not a multiple of F = %d", fn,
+                (long long)a.ldkv, a.L.F);
   // fp32 rows whose heads break the 16-byte alignment (dh % 4 != 0) but whose
   // width does not (F % 4 == 0): the fused operators use row-major lanes so
   // every row moves as 16-byte accesses (FAST_ATTN_ROWMAJOR=0 turns it off).
@@ -244,6 +253,68 @@ extern "C" fast_status_t fast_edge_attention_bwd(const fast_tcsr_t* g, int H, in
   AttnArgs a = {};
   a.scale = scale; a.slope = neg_slope;
   a.Q = Q; a.K = K; a.V = V; a.dO = dout; a.lse_in = lse; a.dQ = dQ; a.dK = dK; a.dV = dV;
+  const void* rows[] = {Q, K, V, dout, dQ, dK, dV};
+  return attn_run(fn, Op::kAttnBwd, g, H, dh, dtype, a, rows, 7, stream);
+}
+
+// Packed K|V rows: row e of KV holds K_e then V_e (F = H*dh elements each), and
+// dKV the gradients in the same layout; the same kernels with a row stride of
+// 2F, so that K, V (and dK, dV) move as one stream.
+static fast_status_t packed_split(const char* fn, int H, int dh, fast_dtype_t dtype, int64_t* F) {
+  if (H < 1 || dh < 1) return fail(FAST_ERR_INVALID_ARG, "%s: H = %d, dh = %d", fn, H, dh);
+  if (int64_t(H) * dh > 4096) return fail(FAST_ERR_UNSUPPORTED, "%s: H*dh > 4096", fn);
+  if (dtype != FAST_F32 && dtype != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
+  *F = int64_t(H) * dh;
+  return FAST_OK;
+}
+
+extern "C" fast_status_t fast_edge_attention_fwd_packed(const fast_tcsr_t* g, int H, int dh,
+                                                        fast_dtype_t dtype, const void* Q,
+                                                        const void* KV, float scale,
+                                                        float neg_slope, void* out, float* lse,
+                                                        fast_stream_t stream) {
+  const char* fn = "fast_edge_attention_fwd_packed";
+  int64_t F = 0;
+  fast_status_t s = packed_split(fn, H, dh, dtype, &F);
+  if (s != FAST_OK) return s;
+  if (has_work(g)) {
+    FAST_NEED(Q, fn); FAST_NEED(out, fn);
+    if (g->num_edges > 0) FAST_NEED(KV, fn);
+  }
+  const size_t half = size_t(F) * elem_size(dtype);
+  const void* K = KV;
+  const void* V = KV ? static_cast<const char*>(KV) + half : nullptr;
+  AttnArgs a = {};
+  a.scale = scale; a.slope = neg_slope;
+  a.Q = Q; a.K = K; a.V = V; a.out = out; a.lse_out = lse;
+  a.ldkv = 2 * F;
+  const void* rows[] = {Q, K, V, out};
+  return attn_run(fn, Op::kAttnFwd, g, H, dh, dtype, a, rows, 4, stream);
+}
+
+extern "C" fast_status_t fast_edge_attention_bwd_packed(const fast_tcsr_t* g, int H, int dh,
+                                                        fast_dtype_t dtype, const void* Q,
+                                                        const void* KV, float scale,
+                                                        float neg_slope, const float* lse,
+                                                        const void* dout, void* dQ, void* dKV,
+                                                        fast_stream_t stream) {
+  const char* fn = "fast_edge_attention_bwd_packed";
+  int64_t F = 0;
+  fast_status_t s = packed_split(fn, H, dh, dtype, &F);
+  if (s != FAST_OK) return s;
+  if (has_work(g)) {
+    FAST_NEED(Q, fn); FAST_NEED(dout, fn); FAST_NEED(dQ, fn);
+    if (g->num_edges > 0) { FAST_NEED(KV, fn); FAST_NEED(dKV, fn); }
+  }
+  const size_t half = size_t(F) * elem_size(dtype);
+  const void* K = KV;
+  const void* V = KV ? static_cast<const char*>(KV) + half : nullptr;
+  void* dK = dKV;
+  void* dV = dKV ? static_cast<char*>(dKV) + half : nullptr;
+  AttnArgs a = {};
+  a.scale = scale; a.slope = neg_slope;
+  a.Q = Q; a.K = K; a.V = V; a.dO = dout; a.lse_in = lse; a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.ldkv = 2 * F;
   const void* rows[] = {Q, K, V, dout, dQ, dK, dV};
   return attn_run(fn, Op::kAttnBwd, g, H, dh, dtype, a, rows, 7, stream);
 }

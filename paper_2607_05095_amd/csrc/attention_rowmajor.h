@@ -104,7 +104,7 @@ template <int H, int G, bool NT, bool IDX>
 __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd_rm(AttnArgs a) {
   RmMap<H> m;
   if (!rm_setup<H, G>(a, m)) return;
-  const int F = a.L.F;
+  const int F = a.L.F, ld = int(a.ldkv);
   const float* K = static_cast<const float*>(a.K);
   const float* V = static_cast<const float*>(a.V);
   const float sl2 = a.scale * LOG2E;
@@ -124,8 +124,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd_rm(Attn
 #pragma unroll
     for (int i = 0; i < RM_CH_FWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      rm_load_row<NT && !IDX, H>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
-      rm_load_row<NT && !IDX, H>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
+      rm_load_row<NT && !IDX, H>(K, operand_row<IDX>(a.kidx, a.k_rows, e), ld, m, kx[i]);
+      rm_load_row<NT && !IDX, H>(V, operand_row<IDX>(a.vidx, a.v_rows, e), ld, m, vx[i]);
     }
     float t[RM_CH_FWD][H], cm[H];
 #pragma unroll
@@ -188,15 +188,15 @@ __device__ __forceinline__ void rm_bwd_chunk(const AttnArgs& a, const RmMap<H>& 
                                              int64_t e1, bool has_lse, float sl2,
                                              RmBwdState<H>& S, float (&x)[RM_CH_BWD][H],
                                              float (&da)[RM_CH_BWD][H]) {
-  const int F = a.L.F;
+  const int ld = int(a.ldkv);
   const float* K = static_cast<const float*>(a.K);
   const float* V = static_cast<const float*>(a.V);
   float kx[RM_CH_BWD][4], vx[RM_CH_BWD][4];
 #pragma unroll
   for (int i = 0; i < RM_CH_BWD; ++i) {
     const int64_t e = slot_row(base, i, e1);
-    rm_load_row<NT && !IDX, H>(K, operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
-    rm_load_row<NT && !IDX, H>(V, operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
+    rm_load_row<NT && !IDX, H>(K, operand_row<IDX>(a.kidx, a.k_rows, e), ld, m, kx[i]);
+    rm_load_row<NT && !IDX, H>(V, operand_row<IDX>(a.vidx, a.v_rows, e), ld, m, vx[i]);
   }
   float t[RM_CH_BWD][H], cm[H];
 #pragma unroll
@@ -279,8 +279,8 @@ __device__ __forceinline__ void rm_bwd_emit(const AttnArgs& a, const RmMap<H>& m
     dk[k] = pick<H>(g, m.hs[k]) * S.q[k];
     dv[k] = pick<H>(al, m.hs[k]) * S.go[k];
   }
-  rm_store_row<NT, H>(static_cast<float*>(a.dK), e, a.L.F, m, dk);
-  rm_store_row<NT, H>(static_cast<float*>(a.dV), e, a.L.F, m, dv);
+  rm_store_row<NT, H>(static_cast<float*>(a.dK), e, int(a.ldkv), m, dk);
+  rm_store_row<NT, H>(static_cast<float*>(a.dV), e, int(a.ldkv), m, dv);
 }
 
 template <int H, int G, bool NT, bool IDX>
@@ -345,8 +345,8 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
 #pragma unroll
     for (int i = 0; i < RM_CH_BWD; ++i) {
       const int64_t e = slot_row(base, i, e1);
-      rm_load_row<false, H>(static_cast<const float*>(a.K), operand_row<IDX>(a.kidx, a.k_rows, e), F, m, kx[i]);
-      rm_load_row<false, H>(static_cast<const float*>(a.V), operand_row<IDX>(a.vidx, a.v_rows, e), F, m, vx[i]);
+      rm_load_row<false, H>(static_cast<const float*>(a.K), operand_row<IDX>(a.kidx, a.k_rows, e), int(a.ldkv), m, kx[i]);
+      rm_load_row<false, H>(static_cast<const float*>(a.V), operand_row<IDX>(a.vidx, a.v_rows, e), int(a.ldkv), m, vx[i]);
     }
 #pragma unroll
     for (int i = 0; i < RM_CH_BWD; ++i) {

@@ -132,6 +132,33 @@ def test_other_entry_points_validate():
     assert L.fast_check_tcsr(ctypes.byref(gs), 10, -1, FAKE, None) == INVALID  # edge_bound
 
 
+def test_packed_attention_validation():
+    """The packed K|V entry points check their arguments on the host, like
+    the separate-array ones, before anything is enqueued."""
+    L = fast.lib()
+    gp = ctypes.byref(_g())
+    fwd = lambda H=2, dh=50, dt=0, Q=FAKE, KV=FAKE, out=FAKE, g=gp: L.fast_edge_attention_fwd_packed(
+        g, H, dh, dt, Q, KV, 1.0, 0.2, out, None, None)
+    bwd = lambda dt=0, KV=FAKE, dKV=FAKE, dQ=FAKE: L.fast_edge_attention_bwd_packed(
+        gp, 2, 50, dt, FAKE, KV, 1.0, 0.2, None, FAKE, dQ, dKV, None)
+    assert fwd(KV=None) == INVALID            # edges but no K|V rows
+    assert fwd(Q=None) == INVALID
+    assert fwd(out=None) == INVALID
+    assert fwd(H=0) == INVALID and fwd(dh=0) == INVALID
+    assert fwd(dt=5) == INVALID
+    assert fwd(H=64, dh=128) == UNSUPPORTED   # H*dh > 4096
+    assert fwd(KV=FAKE + 2) == UNSUPPORTED    # fp32 rows not 4-byte aligned
+    assert fwd(g=None) == INVALID
+    assert bwd(dKV=None) == INVALID and bwd(KV=None) == INVALID and bwd(dQ=None) == INVALID
+    assert bwd(dt=3) == INVALID
+    # nothing to do: returns before any HIP call
+    g0 = _g(N=0, E=0)
+    assert L.fast_edge_attention_fwd_packed(ctypes.byref(g0), 2, 50, 0, None, None, 1.0, 0.2,
+                                            None, None, None) == OK
+    assert L.fast_edge_attention_bwd_packed(ctypes.byref(g0), 2, 50, 0, None, None, 1.0, 0.2,
+                                            None, None, None, None, None) == OK
+
+
 def test_dedup_validation_and_workspace_query():
     L = fast.lib()
     ws = L.fast_dedup_gather_workspace(1000, 1 << 20)

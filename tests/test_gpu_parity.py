@@ -72,6 +72,25 @@ def _run_fused(d, with_lse=True, slope=SLOPE):
     return out, lse, dQ, dK, dV
 
 
+def _run_fused_packed(d, with_lse=True, slope=SLOPE):
+    """The fused pair on packed K|V rows: KV[e] = (K[e], V[e]); the gradients
+    come back as dKV[e] = (dK[e], dV[e]), poisoned with NaN beforehand."""
+    o = d.ops
+    KV = torch.empty((d.E, 2, d.H, d.dh), dtype=tdtype(d.dt), device="cuda")
+    KV[:, 0] = o["K"]
+    KV[:, 1] = o["V"]
+    out = d.empty(d.N)
+    lse = d.scalars(d.N)
+    fast.fast_edge_attention_fwd_packed(d.g, d.H, d.dh, DT[d.dt], o["Q"], KV if d.E else None,
+                                        d.scale, slope, out, lse)
+    dQ = d.empty(d.N)
+    dKV = torch.full((d.E, 2, d.H, d.dh), float("nan"), dtype=tdtype(d.dt), device="cuda")
+    fast.fast_edge_attention_bwd_packed(d.g, d.H, d.dh, DT[d.dt], o["Q"], KV if d.E else None,
+                                        d.scale, slope, lse if with_lse else None, o["dO"], dQ,
+                                        dKV if d.E else None)
+    return out, lse, dQ, dKV[:, 0], dKV[:, 1]
+
+
 def _run_unfused(d, slope=SLOPE):
     o = d.ops
     alpha, lse = d.scalars(d.E), d.scalars(d.N)
@@ -218,6 +237,72 @@ def test_attention_nonpositive_slope(name, counts, H, dh, dt, slope):
     _check_block(d, None, f"{name} slope={slope}", slope=slope)
 
 
+# ------------------------------------------------------------------ attention: packed K|V rows
+_PACKED_NAMES = ("out", "lse", "dQ", "dK", "dV")
+
+
+def _assert_packed_equals_separate(d, what, slope=SLOPE):
+    for with_lse in (True, False):
+        sep = _run_fused(d, with_lse=with_lse, slope=slope)
+        pk = _run_fused_packed(d, with_lse=with_lse, slope=slope)
+        torch.cuda.synchronize()
+        for n, x, y in zip(_PACKED_NAMES, sep, pk):
+            assert torch.equal(x, y), f"{what} lse={with_lse}: packed {n} differs from separate"
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_attention_packed_kv_equals_separate_workloads(cfg):
+    """Packed K|V rows run the same kernels with rows 2F apart: every output
+    equals the separate-array operator's (itself checked against the oracle in
+    full above) bit for bit, on every block of every workload at full size."""
+    b = make_batch(cfg)
+    for i in range(len(b.blocks)):
+        d = _block_from_batch(b, i)
+        _announce(f"packed K|V cfg={cfg} block={i}: N={d.N} E={d.E}")
+        _assert_packed_equals_separate(d, f"cfg{cfg}/L{i + 1}")
+        del d
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,counts,H,dh,dt,slope", [
+    ("long_segments_rowmajor", [1000, 3, 25, 24, 23, 40, 8, 9, 17], 2, 50, "f32", SLOPE),
+    ("long_bf16", [333, 20, 21, 1, 0, 64], 4, 32, "bf16", SLOPE),
+    ("empties_mixed", [0, 3, 0, 0, 7, 1, 0, 12, 0], 2, 50, "f32", SLOPE),
+    ("odd_dh_vec1", [4, 7, 11, 2], 3, 13, "f32", SLOPE),
+    ("bf16_vec4", [5, 12, 1], 2, 36, "bf16", SLOPE),
+    ("wide_dh_P4", [6, 3, 10], 2, 130, "f32", SLOPE),
+    ("many_heads_bf16", [6, 2, 9], 64, 16, "bf16", SLOPE),
+    ("rowmajor_negative_slope", [10, 1, 0, 7, 30, 10, 25, 3, 12] * 8, 2, 50, "f32", -0.3),
+    ("headmajor_bf16_zero_slope", [20, 1, 0, 7, 41, 20, 25, 3, 12] * 8, 4, 32, "bf16", 0.0),
+])
+def test_attention_packed_kv_edge_cases(name, counts, H, dh, dt, slope):
+    """Both lane layouts, every vector width, segments beyond the backward's
+    register window, empty segments, and slopes of 0 and below."""
+    _announce(f"packed K|V edge case {name}")
+    d = _synthetic_block(counts, H, dh, dt, seed=len(counts) + 3)
+    _assert_packed_equals_separate(d, name, slope=slope)
+
+
+@pytest.mark.parametrize("case", ["cfg1", "long_bf16"])
+def test_attention_packed_kv_vs_oracle(case):
+    """The packed operators against the oracle directly, element by element."""
+    _announce(f"packed K|V vs oracle {case}")
+    if case == "cfg1":
+        d = _block_from_batch(make_batch(1), 0)
+    else:
+        d = _synthetic_block([333, 20, 21, 1, 0, 64], 4, 32, "bf16", seed=9)
+    out, lse, dQ, dK, dV = _run_fused_packed(d)
+    torch.cuda.synchronize()
+    Q, K, V, dO = (_host(d.ops[k]) for k in ("Q", "K", "V", "dO"))
+    r_out, r_lse, _, _ = oracle.edge_attention_fwd(d.off, Q, K, V, d.scale, SLOPE)
+    r_dQ, r_dK, r_dV, alts = bwd_reference_with_kinks(d.off, Q, K, V, dO, d.scale, SLOPE)
+    nz = np.diff(d.off) > 0
+    assert_close(out, r_out, d.dt, case + " packed out")
+    assert_close(_host(lse)[nz], r_lse[nz], "f32", case + " packed lse")
+    assert_close(dV, r_dV, d.dt, case + " packed dV")
+    assert_bwd_close(dQ, dK, d.off, r_dQ, r_dK, alts, d.dt, case + " packed")
+
+
 def test_attention_empty_graph_and_zero_edges():
     _announce("attention N=0")
     d0 = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -225,7 +310,15 @@ def test_attention_empty_graph_and_zero_edges():
     fast.fast_edge_attention_fwd(g, 2, 50, fast.F32, None, None, None, 0.1, SLOPE, None, None)
     fast.fast_edge_attention_bwd(g, 2, 50, fast.F32, None, None, None, 0.1, SLOPE, None, None,
                                  None, None, None)
+    fast.fast_edge_attention_fwd_packed(g, 2, 50, fast.F32, None, None, 0.1, SLOPE, None, None)
+    fast.fast_edge_attention_bwd_packed(g, 2, 50, fast.F32, None, None, 0.1, SLOPE, None, None,
+                                        None, None)
+    # destinations without edges: no K|V rows at all, every output row 0, lse -inf
+    d = _synthetic_block([0, 0, 0], 2, 50, "f32", seed=4)
+    out, lse, dQ, _, _ = _run_fused_packed(d)
     torch.cuda.synchronize()
+    assert torch.count_nonzero(out) == 0 and torch.count_nonzero(dQ) == 0
+    assert torch.all(torch.isneginf(lse))
 
 
 def test_attention_run_to_run_bitwise_determinism():
