@@ -153,6 +153,17 @@ __global__ void __launch_bounds__(THREADS) k_rows_kv(const u32x4* __restrict__ k
   dkv[r * 2 * ROWV + ROWV + l] = y;
 }
 
+// The forward's shape: the same 800-byte K|V rows read, nothing written per
+// row (one 16-byte result per group keeps the loads).
+__global__ void __launch_bounds__(THREADS) k_rows_kv_read(const u32x4* __restrict__ kv,
+                                                          unsigned* __restrict__ sink, size_t rows) {
+  const size_t r = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (r >= rows || l >= ROWV) return;
+  const u32x4 x = kv[r * 2 * ROWV + l], y = kv[r * 2 * ROWV + ROWV + l];
+  if ((x.x ^ y.y ^ x.z ^ y.w) == 0x9e3779b9u) sink[0] = 1u;
+}
+
 struct Buffers {
   u32x4 *a, *b, *c, *d;
   unsigned* sink;
@@ -232,6 +243,8 @@ int main(int argc, char** argv) {
       hipLaunchKernelGGL(k_rows_sep, g_rows, blk, 0, 0, B.a, B.c, B.b, B.d, nrow); }, reps)});
     rows.push_back({"rows400_kv", moved, median_ms([&] {
       hipLaunchKernelGGL(k_rows_kv, g_rows, blk, 0, 0, B.a, B.b, nrow); }, reps)});
+    rows.push_back({"rows400_kv_read", moved / 2, median_ms([&] {
+      hipLaunchKernelGGL(k_rows_kv_read, g_rows, blk, 0, 0, B.a, B.sink, nrow); }, reps)});
   }
   CHECK(hipGetLastError());
   std::printf("{");
