@@ -164,6 +164,27 @@ __global__ void __launch_bounds__(THREADS) k_rows_kv_read(const u32x4* __restric
   if ((x.x ^ y.y ^ x.z ^ y.w) == 0x9e3779b9u) sink[0] = 1u;
 }
 
+// In-place updates: each row (or element) read and written back to the same
+// place, as a backward that overwrites K|V with dK|dV would.
+__global__ void __launch_bounds__(THREADS) k_rows_kv_inplace(u32x4* __restrict__ kv, size_t rows) {
+  const size_t r = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (r >= rows || l >= ROWV) return;
+  u32x4 x = kv[r * 2 * ROWV + l], y = kv[r * 2 * ROWV + ROWV + l];
+  x.x += 1u;
+  y.y += 1u;
+  kv[r * 2 * ROWV + l] = x;
+  kv[r * 2 * ROWV + ROWV + l] = y;
+}
+
+__global__ void __launch_bounds__(THREADS) k_update(u32x4* __restrict__ a, size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  u32x4 x = a[i];
+  x.x += 1u;
+  a[i] = x;
+}
+
 struct Buffers {
   u32x4 *a, *b, *c, *d;
   unsigned* sink;
@@ -243,6 +264,10 @@ int main(int argc, char** argv) {
       hipLaunchKernelGGL(k_rows_sep, g_rows, blk, 0, 0, B.a, B.c, B.b, B.d, nrow); }, reps)});
     rows.push_back({"rows400_kv", moved, median_ms([&] {
       hipLaunchKernelGGL(k_rows_kv, g_rows, blk, 0, 0, B.a, B.b, nrow); }, reps)});
+    rows.push_back({"rows400_kv_inplace", moved, median_ms([&] {
+      hipLaunchKernelGGL(k_rows_kv_inplace, g_rows, blk, 0, 0, B.a, nrow); }, reps)});
+    rows.push_back({"update_inplace", 2.0 * bytes, median_ms([&] {
+      hipLaunchKernelGGL(k_update, g_all, blk, 0, 0, B.a, B.n); }, reps)});
     rows.push_back({"rows400_kv_read", moved / 2, median_ms([&] {
       hipLaunchKernelGGL(k_rows_kv_read, g_rows, blk, 0, 0, B.a, B.sink, nrow); }, reps)});
   }
