@@ -130,15 +130,18 @@ class Step:
             else:
                 d["dK"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
                 d["dV"] = torch.empty((E, b.H, b.dh), dtype=tdt, device=dev)
-            d["off"], d["ws_off"], d["te"], d["g"] = [], [], [], []
+            d["off"], d["te"], d["g"] = [], [], []
             for _ in range(slots):
                 off = torch.empty(N + 1, dtype=torch.int32, device=dev)
                 d["off"].append(off)
-                d["ws_off"].append(torch.empty(fast.fast_csr_offsets_workspace(N), dtype=torch.uint8,
-                                               device=dev))
                 d["te"].append(torch.empty((E, b.d_t), dtype=tdt, device=dev))
                 d["g"].append(fast.tcsr(off, E, edge_t=d["edge_t"], dst_t=d["dst_t"]))
             self.blocks.append(d)
+        # the offsets of all layer blocks: one batched scan per slot
+        self.off_n = [d["N"] for d in self.blocks]
+        self.ws_off_bytes = fast.fast_csr_offsets_batched_workspace(self.off_n)
+        self.ws_off = [torch.empty(self.ws_off_bytes, dtype=torch.uint8, device=dev)
+                       for _ in range(slots)]
         om, ph = omega_phi(b.d_t)
         self.omega = torch.from_numpy(om).to(dev)
         self.phi = torch.from_numpy(ph).to(dev)
@@ -194,17 +197,19 @@ class Step:
         return mark
 
     def prep(self, slot, rec=None, names=None):
-        """Offsets, time encoding, dedup + gather (nodes, edges) into `slot`.
-        The three are independent; the time encoding goes first so that the
-        write-back of its output overlaps the dedups rather than the attention."""
+        """Offsets, time encoding, dedup + gather (nodes, edges) into `slot`;
+        the offsets and the time encoding of all layer blocks in one batched
+        call each.  The three are independent; the time encoding goes first so
+        that the write-back of its output overlaps the dedups rather than the
+        attention."""
         f, b = self.fast, self.b
         mark = self._marker(self.torch, rec, names)
-        for i, d in enumerate(self.blocks):
-            mark(f"offsets_L{i + 1}", lambda d=d: f.fast_csr_offsets(
-                d["counts"], d["N"], d["off"][slot], d["ws_off"][slot], d["ws_off"][slot].numel()))
-        for i, d in enumerate(self.blocks):
-            mark(f"time_encode_L{i + 1}", lambda d=d: f.fast_time_encode(
-                d["g"][slot], self.omega, self.phi, b.d_t, d["te"][slot], self.DT))
+        mark("offsets", lambda: f.fast_csr_offsets_batched(
+            [d["counts"] for d in self.blocks], self.off_n, [d["off"][slot] for d in self.blocks],
+            self.ws_off[slot], self.ws_off_bytes))
+        mark("time_encode", lambda: f.fast_time_encode_batched(
+            [d["g"][slot] for d in self.blocks], self.omega, self.phi, b.d_t,
+            [d["te"][slot] for d in self.blocks], self.DT))
         mark("dedup_gather_nodes", lambda: self._dedup(self.node[slot]))
         mark("dedup_gather_edges", lambda: self._dedup(self.edge[slot]))
 
@@ -601,25 +606,22 @@ def greedy_hot_set_bytes(nv, ne, B):
 
 
 def time_encode_summary(b, breakdown, counters=None):
-    """Time encoding of both layer blocks in the serial step: algorithmic bytes
-    E (4 + d_t b) + 8 N per block against the measured times; with a counter
-    record of the layer-1 launch taken on the current time-encoding source,
-    also its VALU utilisation (VALU wave instructions x 64 lanes over the
-    layer-1 time, against 256 CUs x 64 lanes x 2.4 GHz)."""
+    """Time encoding of all layer blocks (one batched launch) in the serial
+    step: algorithmic bytes E (4 + d_t b) + 8 N per block against the measured
+    time; with a counter record of that launch taken on the current
+    time-encoding source, also its VALU utilisation (VALU wave instructions x
+    64 lanes over the time, against 256 CUs x 64 lanes x 2.4 GHz)."""
     b_out = 4 if b.dtype == "f32" else 2
-    ms = sum(breakdown.get(f"time_encode_L{i + 1}", 0.0) for i in range(len(b.blocks)))
+    ms = breakdown.get("time_encode", 0.0)
     nbytes = sum(x.num_edges * (4 + b.d_t * b_out) + 8 * x.num_dst for x in b.blocks)
     res = {"ms": round(ms, 4), "algorithmic_bytes": nbytes,
            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ms > 0 else None,
            "cosines_per_s": sum(x.num_edges for x in b.blocks) * b.d_t / (ms * 1e-3) if ms > 0 else None}
     v = (counters or {}).get("time_encode_valu")
-    ms1 = breakdown.get("time_encode_L1", 0.0)
-    if v and v.get("source_sha") == source_hash(TIME_ENCODE_SOURCES) and ms1 > 0:
-        lane = v["valu_wave_insts_per_launch"] * 64 / (ms1 * 1e-3)
-        res["valu_L1"] = {"lane_insts_per_s": lane, "frac": round(lane / VALU_PEAK_LANE_OPS, 4),
-                          "hbm_frac": round((b.blocks[0].num_edges * (4 + b.d_t * b_out) + 8 * b.blocks[0].num_dst)
-                                            / (ms1 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                          "source": v.get("source")}
+    if v and v.get("source_sha") == source_hash(TIME_ENCODE_SOURCES) and ms > 0:
+        lane = v["valu_wave_insts_per_launch"] * 64 / (ms * 1e-3)
+        res["valu"] = {"lane_insts_per_s": lane, "frac": round(lane / VALU_PEAK_LANE_OPS, 4),
+                       "source": v.get("source")}
     return res
 
 

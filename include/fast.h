@@ -112,6 +112,19 @@ size_t fast_csr_offsets_workspace(int64_t n);
 fast_status_t fast_csr_offsets(const int32_t* counts, int64_t n, int32_t* offsets,
                                void* ws, size_t ws_bytes, fast_stream_t stream);
 
+/* The offsets of several blocks (the layer blocks of one sampled batch, Sec. 5)
+ * in one pair of launches: for b < nblocks, offsets[b] receives the offsets of
+ * counts[b] ([n[b]]), exactly as fast_csr_offsets would.  counts, n and
+ * offsets are HOST arrays of nblocks device pointers / sizes.  Up to 8 blocks
+ * of at most 2048 * 2048 counts each share the launches; otherwise the blocks
+ * are scanned one after another.  nblocks = 0 does nothing.
+ * Workspace: fast_csr_offsets_batched_workspace(nblocks, n) bytes (0 on a
+ * negative size or a NULL n). */
+size_t fast_csr_offsets_batched_workspace(int nblocks, const int64_t* n);
+fast_status_t fast_csr_offsets_batched(int nblocks, const int32_t* const* counts,
+                                       const int64_t* n, int32_t* const* offsets, void* ws,
+                                       size_t ws_bytes, fast_stream_t stream);
+
 /* ------------------------------------------------------------------------
  * Contract check of a sampled subgraph (the device-data contract above).
  * Counts, into violations[0..5) (device int64, overwritten):
@@ -282,6 +295,17 @@ fast_status_t fast_greedy_hot_set(const int32_t* freq_v, int64_t num_nodes, cons
 fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega, const float* phi,
                                int d_t, void* te, fast_dtype_t te_dtype,
                                fast_stream_t stream);
+
+/* The time features of several blocks (the layer blocks of one batch share
+ * the encoder's omega and phi, Sec. 6.1) in one launch per 8 blocks: te[b]
+ * receives exactly what fast_time_encode(g[b], ...) writes.  g and te are
+ * HOST arrays of nblocks pointers; every block is checked as by
+ * fast_time_encode before anything is launched for its group of 8, and the
+ * widest vector width all te[b] allow is used. */
+fast_status_t fast_time_encode_batched(int nblocks, const fast_tcsr_t* const* g,
+                                       const float* omega, const float* phi, int d_t,
+                                       void* const* te, fast_dtype_t te_dtype,
+                                       fast_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Backward of the time encoding (Sec. 6.1: the encoder's frequencies and

@@ -17,6 +17,7 @@ __all__ = [
     "dtype_of", "fast_sample_recent_workspace", "fast_sample_recent",
     "fast_version", "fast_last_error",
     "fast_csr_offsets_workspace", "fast_csr_offsets", "fast_check_tcsr",
+    "fast_csr_offsets_batched_workspace", "fast_csr_offsets_batched", "fast_time_encode_batched",
     "fast_dedup_gather_workspace", "fast_dedup_gather", "fast_dedup_gather_noalloc",
     "NOALLOC_SCRATCH_BYTES",
     "fast_access_count_workspace", "fast_access_count",
@@ -81,6 +82,9 @@ _SIGS = {
     "fast_version": (C.c_char_p, []),
     "fast_csr_offsets_workspace": (_sz, [_i64]),
     "fast_csr_offsets": (_i32, [_p, _i64, _p, _p, _sz, _p]),
+    "fast_csr_offsets_batched_workspace": (_sz, [_i32, _p]),
+    "fast_csr_offsets_batched": (_i32, [_i32, _p, _p, _p, _p, _sz, _p]),
+    "fast_time_encode_batched": (_i32, [_i32, _p, _p, _p, _i32, _p, _i32, _p]),
     "fast_check_tcsr": (_i32, [_G, _i64, _i64, _p, _p]),
     "fast_dedup_gather_workspace": (_sz, [_i64, _i64]),
     "fast_dedup_gather": (_i32, [_p, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p, _p,
@@ -206,6 +210,37 @@ def fast_csr_offsets_workspace(n: int) -> int:
 def fast_csr_offsets(counts, n, offsets, ws, ws_bytes, stream=None):
     _check(lib().fast_csr_offsets(_ptr(counts), n, _ptr(offsets), _ptr(ws), ws_bytes,
                                   _stream(stream)))
+
+
+def _host_ptrs(xs):
+    """A host array of device pointers (None for a NULL entry)."""
+    return (C.c_void_p * max(len(xs), 1))(*[_ptr(x) for x in xs])
+
+
+def _host_i64(xs):
+    return (C.c_int64 * max(len(xs), 1))(*[int(x) for x in xs])
+
+
+def fast_csr_offsets_batched_workspace(n) -> int:
+    return lib().fast_csr_offsets_batched_workspace(len(n), _host_i64(n))
+
+
+def fast_csr_offsets_batched(counts, n, offsets, ws, ws_bytes, stream=None):
+    """counts, n, offsets: sequences of equal length (one entry per block)."""
+    if not (len(counts) == len(n) == len(offsets)):
+        raise ValueError("counts, n and offsets must have one entry per block")
+    _check(lib().fast_csr_offsets_batched(len(n), _host_ptrs(counts), _host_i64(n),
+                                          _host_ptrs(offsets), _ptr(ws), ws_bytes,
+                                          _stream(stream)))
+
+
+def fast_time_encode_batched(graphs, omega, phi, d_t, te, te_dtype, stream=None):
+    """graphs: TCSR descriptors, te: outputs, one per block."""
+    if len(graphs) != len(te):
+        raise ValueError("graphs and te must have one entry per block")
+    gs = (C.POINTER(TCSR) * max(len(graphs), 1))(*[C.pointer(g) for g in graphs])
+    _check(lib().fast_time_encode_batched(len(graphs), gs, _ptr(omega), _ptr(phi), d_t,
+                                          _host_ptrs(te), te_dtype, _stream(stream)))
 
 
 def fast_check_tcsr(g: TCSR, src_bound, edge_bound, violations, stream=None):

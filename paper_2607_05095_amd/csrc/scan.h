@@ -124,22 +124,14 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* tsum, int64_t nt,
 // tsum[tile] after the one-block scan of the tile sums, or, with SUM_PREV
 // (few tiles), the sum of the unscanned tile sums before it, added up by the
 // tile's own workgroup; the last tile then also stores the grand total.
-template <class In, class Out, typename T = uint32_t, bool SUM_PREV = false>
-__global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
-                                                            const T* tsum, Out out,
-                                                            int64_t* total_i64, int32_t* total_i32) {
+// The down-sweep of one tile: items [base, base + SCAN_TILE) (those below n)
+// from their prefix tile_base; returns the tile's sum in `total`.  Every
+// thread of the workgroup must call it.
+template <class In, class Out, typename T>
+__device__ __forceinline__ void scan_tile_down(In in, int64_t n, int64_t base, T tile_base, Out out,
+                                               T* lds4, T& total_out) {
   constexpr int PAD_END = SCAN_TILE + SCAN_TILE / 32;
   __shared__ T tile[PAD_END + 1];
-  __shared__ T lds4[4];
-  const int64_t base = int64_t(blockIdx.x) * SCAN_TILE;
-  T tile_base;
-  if constexpr (SUM_PREV) {
-    T part = 0;
-    for (int64_t t = threadIdx.x; t < int64_t(blockIdx.x); t += SCAN_THREADS) part += tsum[t];
-    block_exclusive_scan(part, lds4, tile_base);   // block-wide sum of the parts
-  } else {
-    tile_base = tsum[blockIdx.x];
-  }
   // striped, coalesced load into LDS (padded every 32 words against bank conflicts)
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
@@ -159,12 +151,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
   // (the block scan's barriers also order every read of tile above before
   // the writes below)
   T run = block_exclusive_scan(s, lds4, total) + tile_base;
-  if constexpr (SUM_PREV) {
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
-      if (total_i64) *total_i64 = int64_t(tile_base + total);
-      if (total_i32) *total_i32 = int32_t(tile_base + total);
-    }
-  }
+  total_out = total;
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int j = threadIdx.x * SCAN_ITEMS + k;
@@ -181,6 +168,29 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
     const T p0 = tile[j + (j >> 5)];
     const T p1 = j1 < SCAN_TILE ? tile[j1 + (j1 >> 5)] : tile[PAD_END];
     if (i < n) out(i, p0, T(p1 - p0));
+  }
+}
+
+template <class In, class Out, typename T = uint32_t, bool SUM_PREV = false>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(In in, int64_t n,
+                                                            const T* tsum, Out out,
+                                                            int64_t* total_i64, int32_t* total_i32) {
+  __shared__ T lds4[4];
+  T tile_base;
+  if constexpr (SUM_PREV) {
+    T part = 0;
+    for (int64_t t = threadIdx.x; t < int64_t(blockIdx.x); t += SCAN_THREADS) part += tsum[t];
+    block_exclusive_scan(part, lds4, tile_base);   // block-wide sum of the parts
+  } else {
+    tile_base = tsum[blockIdx.x];
+  }
+  T total;
+  scan_tile_down(in, n, int64_t(blockIdx.x) * SCAN_TILE, tile_base, out, lds4, total);
+  if constexpr (SUM_PREV) {
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+      if (total_i64) *total_i64 = int64_t(tile_base + total);
+      if (total_i32) *total_i32 = int32_t(tile_base + total);
+    }
   }
 }
 

@@ -59,17 +59,19 @@ __device__ __forceinline__ bool cos_cw_ok(float x) { return fabsf(x) <= 65536.f;
 // keeps them all inside cos_rr's range.
 constexpr float TE_ROW_LIMIT = 65000.f;
 
+// Workgroup `wg` of one block: segments [wg TE_SEGS, (wg + 1) TE_SEGS).
 // Thread t owns the column chunk t % cpr of rows t / cpr, t / cpr + rpp, ...
 // (rpp = rows per pass), so omega and phi of its columns stay in registers.
 template <typename TO, int VEC, bool NT>
-__global__ void __launch_bounds__(TE_THREADS) k_time_encode(
-    const int32_t* __restrict__ off, int64_t N, int64_t E, const float* __restrict__ dst_t,
-    const float* __restrict__ edge_t, const float* __restrict__ omega,
-    const float* __restrict__ phi, int d_t, TO* __restrict__ te) {
+__device__ __forceinline__ void te_segments(
+    int64_t wg, const int32_t* __restrict__ off, int64_t N, int64_t E,
+    const float* __restrict__ dst_t, const float* __restrict__ edge_t,
+    const float* __restrict__ omega, const float* __restrict__ phi, int d_t,
+    TO* __restrict__ te) {
   __shared__ int64_t s_off[TE_SEGS + 1];
   __shared__ float s_tdst[TE_SEGS];
   __shared__ float s_dt[TE_TILE_MAX];
-  const int64_t s0 = int64_t(blockIdx.x) * TE_SEGS;
+  const int64_t s0 = wg * TE_SEGS;
   const int ns = int(N - s0 < TE_SEGS ? N - s0 : TE_SEGS);
   if (threadIdx.x <= ns) s_off[threadIdx.x] = clamp64(off[s0 + threadIdx.x], 0, E);
   if (threadIdx.x < ns) s_tdst[threadIdx.x] = dst_t[s0 + threadIdx.x];
@@ -161,6 +163,53 @@ __global__ void __launch_bounds__(TE_THREADS) k_time_encode(
   }
 }
 
+template <typename TO, int VEC, bool NT>
+__global__ void __launch_bounds__(TE_THREADS) k_time_encode(
+    const int32_t* __restrict__ off, int64_t N, int64_t E, const float* __restrict__ dst_t,
+    const float* __restrict__ edge_t, const float* __restrict__ omega,
+    const float* __restrict__ phi, int d_t, TO* __restrict__ te) {
+  te_segments<TO, VEC, NT>(blockIdx.x, off, N, E, dst_t, edge_t, omega, phi, d_t, te);
+}
+
+// Several blocks (the layer blocks of one batch) in one launch: workgroups
+// [w0[b], w0[b+1]) encode block b.
+constexpr int TE_MAX_BATCH = 8;
+struct TeBatch {
+  int nb;
+  const int32_t* off[TE_MAX_BATCH];
+  int64_t N[TE_MAX_BATCH], E[TE_MAX_BATCH];
+  const float* dst_t[TE_MAX_BATCH];
+  const float* edge_t[TE_MAX_BATCH];
+  void* te[TE_MAX_BATCH];
+  int64_t w0[TE_MAX_BATCH + 1];
+};
+
+template <typename TO, int VEC, bool NT>
+__global__ void __launch_bounds__(TE_THREADS) k_time_encode_batch(TeBatch B,
+                                                                  const float* __restrict__ omega,
+                                                                  const float* __restrict__ phi,
+                                                                  int d_t) {
+  const int64_t w = blockIdx.x;
+  int b = 0;
+#pragma unroll
+  for (int k = 1; k < TE_MAX_BATCH; ++k)
+    if (k < B.nb && w >= B.w0[k]) b = k;
+  te_segments<TO, VEC, NT>(w - B.w0[b], B.off[b], B.N[b], B.E[b], B.dst_t[b], B.edge_t[b], omega,
+                           phi, d_t, static_cast<TO*>(B.te[b]));
+}
+
+template <typename TO, int VEC>
+static void launch_te_batch(const TeBatch& B, const float* omega, const float* phi, int d_t,
+                            bool nt, hipStream_t st) {
+  const uint32_t grid = uint32_t(B.w0[B.nb]);
+  if (nt)
+    hipLaunchKernelGGL((k_time_encode_batch<TO, VEC, true>), dim3(grid), dim3(TE_THREADS), 0, st, B,
+                       omega, phi, d_t);
+  else
+    hipLaunchKernelGGL((k_time_encode_batch<TO, VEC, false>), dim3(grid), dim3(TE_THREADS), 0, st, B,
+                       omega, phi, d_t);
+}
+
 template <typename TO, int VEC>
 static void launch_te(const fast_tcsr_t* g, const float* omega, const float* phi, int d_t,
                       void* te, hipStream_t st) {
@@ -185,10 +234,11 @@ static void launch_te(const fast_tcsr_t* g, const float* omega, const float* phi
 
 using namespace fast;
 
-extern "C" fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega,
-                                          const float* phi, int d_t, void* te,
-                                          fast_dtype_t te_dtype, fast_stream_t stream) {
-  const char* fn = "fast_time_encode";
+// Argument checks of one block; *work is set when the block has edges.
+static fast_status_t te_check(const char* fn, const fast_tcsr_t* g, const float* omega,
+                              const float* phi, int d_t, const void* te, fast_dtype_t te_dtype,
+                              bool* work) {
+  *work = false;
   if (!g) return fail(FAST_ERR_INVALID_ARG, "%s: graph is NULL", fn);
   if (g->num_dst < 0 || g->num_edges < 0) return fail(FAST_ERR_INVALID_ARG, "%s: negative size", fn);
   if (g->num_edges >= (int64_t(1) << 31)) return fail(FAST_ERR_UNSUPPORTED, "%s: E >= 2^31", fn);
@@ -196,11 +246,97 @@ extern "C" fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* ome
   if (te_dtype != FAST_F32 && te_dtype != FAST_BF16) return fail(FAST_ERR_INVALID_ARG, "%s: bad dtype", fn);
   if (g->num_dst == 0 && g->num_edges > 0)
     return fail(FAST_ERR_INVALID_ARG, "%s: E > 0 edges but no destination", fn);
-  if (g->num_edges == 0) return ok();
+  if (g->num_edges == 0) return FAST_OK;
   if (!g->dst_offsets || !g->dst_t || !g->edge_t || !omega || !phi || !te)
     return fail(FAST_ERR_INVALID_ARG, "%s: NULL dst_offsets/dst_t/edge_t/omega/phi/te", fn);
   if (int64_t(d_t) * g->num_edges >= (int64_t(1) << 40))
     return fail(FAST_ERR_UNSUPPORTED, "%s: output too large", fn);
+  *work = true;
+  return FAST_OK;
+}
+
+// Widest vector (elements per thread access) that every output allows, or 0.
+static int te_vec(fast_dtype_t te_dtype, int d_t, const void* const* te, int n) {
+  auto all = [&](size_t a) {
+    for (int k = 0; k < n; ++k)
+      if (te[k] && !aligned(te[k], a)) return false;
+    return true;
+  };
+  if (te_dtype == FAST_F32) {
+    if (d_t % 4 == 0 && all(16)) return 4;
+    if (d_t % 2 == 0 && all(8)) return 2;
+    return all(4) ? 1 : 0;
+  }
+  if (d_t % 8 == 0 && all(16)) return 8;
+  if (d_t % 4 == 0 && all(8)) return 4;
+  if (d_t % 2 == 0 && all(4)) return 2;
+  return all(2) ? 1 : 0;
+}
+
+extern "C" fast_status_t fast_time_encode_batched(int nblocks, const fast_tcsr_t* const* g,
+                                                  const float* omega, const float* phi, int d_t,
+                                                  void* const* te, fast_dtype_t te_dtype,
+                                                  fast_stream_t stream) {
+  const char* fn = "fast_time_encode_batched";
+  if (nblocks < 0) return fail(FAST_ERR_INVALID_ARG, "%s: nblocks = %d < 0", fn, nblocks);
+  if (nblocks == 0) return ok();
+  if (!g || !te) return fail(FAST_ERR_INVALID_ARG, "%s: NULL host array", fn);
+  TeBatch B = {};
+  const void* outs[TE_MAX_BATCH];
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  bool launched = false;
+  for (int b0 = 0; b0 < nblocks; b0 += TE_MAX_BATCH) {   // at most TE_MAX_BATCH blocks per launch
+    B = {};
+    int64_t w = 0;
+    for (int b = b0; b < nblocks && b < b0 + TE_MAX_BATCH; ++b) {
+      bool work = false;
+      const fast_status_t s = te_check(fn, g[b], omega, phi, d_t, te[b], te_dtype, &work);
+      if (s != FAST_OK) return s;
+      if (!work) continue;
+      const int k = B.nb++;
+      B.off[k] = g[b]->dst_offsets;
+      B.N[k] = g[b]->num_dst;
+      B.E[k] = g[b]->num_edges;
+      B.dst_t[k] = g[b]->dst_t;
+      B.edge_t[k] = g[b]->edge_t;
+      B.te[k] = te[b];
+      B.w0[k] = w;
+      outs[k] = te[b];
+      w += (g[b]->num_dst + TE_SEGS - 1) / TE_SEGS;
+    }
+    if (B.nb == 0) continue;
+    B.w0[B.nb] = w;
+    const int vec = te_vec(te_dtype, d_t, outs, B.nb);
+    if (vec == 0)
+      return fail(FAST_ERR_UNSUPPORTED, "%s: te is not %d-byte aligned", fn,
+                  te_dtype == FAST_F32 ? 4 : 2);
+    // streaming stores only when each output row covers whole cache lines
+    const size_t esz = te_dtype == FAST_F32 ? 4 : 2;
+    bool nt = (size_t(d_t) * esz) % CACHE_LINE == 0;
+    for (int k = 0; k < B.nb; ++k) nt = nt && aligned(B.te[k], CACHE_LINE);
+    launched = true;
+    if (te_dtype == FAST_F32) {
+      if (vec == 4) launch_te_batch<float, 4>(B, omega, phi, d_t, nt, st);
+      else if (vec == 2) launch_te_batch<float, 2>(B, omega, phi, d_t, nt, st);
+      else launch_te_batch<float, 1>(B, omega, phi, d_t, nt, st);
+    } else {
+      if (vec == 8) launch_te_batch<uint16_t, 8>(B, omega, phi, d_t, nt, st);
+      else if (vec == 4) launch_te_batch<uint16_t, 4>(B, omega, phi, d_t, nt, st);
+      else if (vec == 2) launch_te_batch<uint16_t, 2>(B, omega, phi, d_t, nt, st);
+      else launch_te_batch<uint16_t, 1>(B, omega, phi, d_t, nt, st);
+    }
+  }
+  return launched ? check_launch(fn) : ok();   // no block with edges: no HIP call
+}
+
+extern "C" fast_status_t fast_time_encode(const fast_tcsr_t* g, const float* omega,
+                                          const float* phi, int d_t, void* te,
+                                          fast_dtype_t te_dtype, fast_stream_t stream) {
+  const char* fn = "fast_time_encode";
+  bool work = false;
+  const fast_status_t s = te_check(fn, g, omega, phi, d_t, te, te_dtype, &work);
+  if (s != FAST_OK) return s;
+  if (!work) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (te_dtype == FAST_F32) {
     if (d_t % 4 == 0 && aligned(te, 16)) launch_te<float, 4>(g, omega, phi, d_t, te, st);

@@ -159,6 +159,46 @@ def test_packed_attention_validation():
                                             None, None, None, None, None) == OK
 
 
+def test_batched_offsets_and_time_encode_validation():
+    """The batched entry points check every block on the host first; an empty
+    batch and blocks without work return before any HIP call."""
+    L = fast.lib()
+    arr = lambda *v: (ctypes.c_void_p * len(v))(*v)
+    i64 = lambda *v: (ctypes.c_int64 * len(v))(*v)
+    ws = L.fast_csr_offsets_batched_workspace(2, i64(100, 5000))
+    assert ws >= max(L.fast_csr_offsets_workspace(100), L.fast_csr_offsets_workspace(5000))
+    assert L.fast_csr_offsets_batched_workspace(2, i64(100, -1)) == 0
+    assert L.fast_csr_offsets_batched_workspace(1, None) == 0
+    assert L.fast_csr_offsets_batched_workspace(0, None) > 0
+    off = lambda nb, c, n, o, w=ws, wsp=FAKE: L.fast_csr_offsets_batched(nb, c, n, o, wsp, w, None)
+    assert off(0, None, None, None) == OK
+    assert off(-1, None, None, None) == INVALID
+    assert off(2, None, i64(100, 5000), arr(FAKE, FAKE)) == INVALID          # NULL host array
+    assert off(2, arr(FAKE, FAKE), i64(100, -3), arr(FAKE, FAKE)) == INVALID
+    assert off(2, arr(FAKE, FAKE), i64(100, 5000), arr(FAKE, None)) == INVALID
+    assert off(2, arr(FAKE, None), i64(100, 5000), arr(FAKE, FAKE)) == INVALID
+    assert off(2, arr(FAKE, FAKE), i64(100, 1 << 31), arr(FAKE, FAKE)) == UNSUPPORTED
+    assert off(2, arr(FAKE, FAKE), i64(100, 5000), arr(FAKE, FAKE), w=ws - 1) == WORKSPACE
+    assert off(2, arr(FAKE, FAKE), i64(100, 5000), arr(FAKE, FAKE), wsp=None) == WORKSPACE
+
+    gp = lambda g: ctypes.pointer(g)
+    garr = lambda *gs: (ctypes.POINTER(fast.TCSR) * len(gs))(*[gp(g) for g in gs])
+    te = lambda nb, gs, outs, d_t=100, dt=0, om=FAKE: L.fast_time_encode_batched(
+        nb, gs, om, FAKE, d_t, outs, dt, None)
+    gE = fast.TCSR(4, 40, FAKE, None, FAKE, None, FAKE)
+    g0 = fast.TCSR(0, 0, None, None, None, None, None)
+    assert te(0, None, None) == OK
+    assert te(-2, None, None) == INVALID
+    assert te(1, None, arr(FAKE)) == INVALID
+    assert te(2, garr(gE, gE), None) == INVALID
+    assert te(2, garr(g0, g0), arr(None, None)) == OK                   # no edges anywhere
+    assert te(2, garr(gE, gE), arr(FAKE, FAKE), dt=4) == INVALID
+    assert te(2, garr(gE, gE), arr(FAKE, FAKE), d_t=0) == INVALID
+    assert te(2, garr(gE, gE), arr(FAKE, FAKE), om=None) == INVALID
+    assert te(2, garr(gE, fast.TCSR(0, 5, FAKE, None, FAKE, None, FAKE)), arr(FAKE, FAKE)) == INVALID
+    assert te(1, garr(gE), arr(FAKE + 1)) == UNSUPPORTED                   # fp32 rows, odd address
+
+
 def test_dedup_validation_and_workspace_query():
     L = fast.lib()
     ws = L.fast_dedup_gather_workspace(1000, 1 << 20)

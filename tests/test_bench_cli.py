@@ -79,10 +79,10 @@ def test_time_encode_valu_only_from_counters_of_the_current_source():
     import bench
     from synth import make_batch
     b = make_batch(4)
-    bd = {"time_encode_L1": 0.2, "time_encode_L2": 0.03}
+    bd = {"time_encode": 0.2}
     rec = {"time_encode_valu": {"valu_wave_insts_per_launch": 5.6e7, "source": "x",
                                 "source_sha": bench.source_hash(bench.TIME_ENCODE_SOURCES)}}
-    v = bench.time_encode_summary(b, bd, rec)["valu_L1"]
+    v = bench.time_encode_summary(b, bd, rec)["valu"]
     assert abs(v["lane_insts_per_s"] - 5.6e7 * 64 / 2e-4) < 1 and 0 < v["frac"] < 1
     rec["time_encode_valu"]["source_sha"] = "0" * 16
-    assert "valu_L1" not in bench.time_encode_summary(b, bd, rec)
+    assert "valu" not in bench.time_encode_summary(b, bd, rec)

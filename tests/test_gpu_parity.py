@@ -373,6 +373,97 @@ def test_csr_offsets_bit_exact(case):
     assert np.array_equal(off.cpu().numpy(), oracle.csr_offsets(counts))
 
 
+def _offsets_batched(counts_list):
+    d_counts = [to_dev(np.asarray(c, np.int32)) if len(c) else None for c in counts_list]
+    ns = [len(c) for c in counts_list]
+    outs = [torch.full((n + 1,), -7, dtype=torch.int32, device="cuda") for n in ns]
+    wsb = fast.fast_csr_offsets_batched_workspace(ns)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    fast.fast_csr_offsets_batched(d_counts, ns, outs, ws, wsb)
+    torch.cuda.synchronize()
+    return [o.cpu().numpy() for o in outs]
+
+
+@pytest.mark.parametrize("case", ["cfg3", "cfg4", "with_empty", "single", "nine_blocks",
+                                  "big_block", "all_empty"])
+def test_csr_offsets_batched_bit_exact(case):
+    """All layer blocks in one pair of launches (with empty blocks, more than
+    the 8 blocks of one pair, and a block of more than 2048 tiles, which the
+    blocks then take one after another), bit-exact against the oracle."""
+    _announce(f"offsets batched {case}")
+    r = np.random.default_rng(3)
+    ri = lambda hi, n: r.integers(0, hi, n).astype(np.int32)
+    lists = {
+        "cfg3": lambda: [blk.counts for blk in make_batch(3).blocks],
+        "cfg4": lambda: [blk.counts for blk in make_batch(4).blocks],
+        "with_empty": lambda: [ri(30, 5000), np.zeros(0, np.int32), ri(5, 2049), np.zeros(0, np.int32),
+                               ri(7, 2048)],
+        "single": lambda: [ri(30, 777)],
+        "nine_blocks": lambda: [ri(20, int(r.integers(1, 9000))) for _ in range(9)],
+        "big_block": lambda: [ri(3, 2048 * 2048 + 5), ri(9, 100)],
+        "all_empty": lambda: [np.zeros(0, np.int32), np.zeros(0, np.int32)],
+    }[case]()
+    for k, (got, c) in enumerate(zip(_offsets_batched(lists), lists)):
+        assert np.array_equal(got, oracle.csr_offsets(c)), f"block {k}"
+
+
+def _te_block_dev(off, dst_t, edge_t):
+    d_off, d_dst, d_e = to_dev(off), to_dev(dst_t), to_dev(edge_t)
+    return fast.tcsr(d_off, edge_t.shape[0], edge_t=d_e, dst_t=d_dst), (d_off, d_dst, d_e)
+
+
+def _te_batched_vs_single(blocks, om, ph, dt, shift=0):
+    """blocks: (off, dst_t, edge_t) per block; shift: elements by which every
+    output starts past a 256-byte aligned allocation."""
+    graphs, keep, outs, singles = [], [], [], []
+    for off, dst_t, edge_t in blocks:
+        g, k = _te_block_dev(off, dst_t, edge_t)
+        graphs.append(g)
+        keep.append(k)
+        E = edge_t.shape[0]
+        big = torch.full((E * om.shape[0] + shift + 1,), float("nan"), dtype=tdtype(dt), device="cuda")
+        outs.append(big[shift:shift + E * om.shape[0]].view(E, om.shape[0]) if E else None)
+        singles.append(_te_gpu(off, dst_t, edge_t, om, ph, dt) if E else None)
+    fast.fast_time_encode_batched(graphs, to_dev(om), to_dev(ph), om.shape[0], outs, DT[dt])
+    torch.cuda.synchronize()
+    for k, (o, s1) in enumerate(zip(outs, singles)):
+        if o is not None:
+            assert torch.equal(o, s1), f"block {k}: batched differs from the single-block call"
+    return outs
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_time_encode_batched_equals_single_workloads(cfg):
+    """Both layer blocks in one launch write exactly what one call per block
+    writes (itself checked against the oracle on every row above)."""
+    b = make_batch(cfg)
+    _announce(f"time encode batched cfg={cfg}")
+    om, ph = omega_phi(b.d_t)
+    blocks = [(oracle.csr_offsets(x.counts), x.dst_t, x.edge_t) for x in b.blocks]
+    _te_batched_vs_single(blocks, om, ph, b.dtype)
+
+
+@pytest.mark.parametrize("d_t,dt,shift", [(100, "f32", 0), (100, "f32", 1), (6, "bf16", 0),
+                                          (128, "bf16", 3), (7, "f32", 0)])
+def test_time_encode_batched_edge_cases(d_t, dt, shift):
+    """Nine blocks (two launches), blocks without edges or destinations mixed
+    in, outputs off the 16-byte grid (narrower vectors for every block), and
+    the oracle on every block."""
+    _announce(f"time encode batched d_t={d_t} {dt} shift={shift}")
+    r = np.random.default_rng(d_t + shift)
+    blocks = []
+    for k in range(9):
+        counts = [0, 0, 0] if k == 4 else list(r.integers(0, 40, int(r.integers(1, 300))))
+        blk = tiny_graph(counts, seed=k + 7)
+        blocks.append((oracle.csr_offsets(blk.counts), blk.dst_t, blk.edge_t))
+    blocks.insert(2, (np.zeros(1, np.int32), np.zeros(0, np.float32), np.zeros(0, np.float32)))
+    om, ph = omega_phi(d_t)
+    outs = _te_batched_vs_single(blocks, om, ph, dt, shift)
+    for k, (o, (off, dst_t, edge_t)) in enumerate(zip(outs, blocks)):
+        if o is not None:
+            assert_close(o, oracle.time_encode(off, dst_t, edge_t, om, ph), dt, f"te batched block {k}")
+
+
 # ------------------------------------------------------------------ subgraph contract check
 def _check_gpu(off, E, src=None, src_bound=0, eid=None, edge_bound=0, et=None, dt=None):
     d = lambda a, t: None if a is None else to_dev(np.asarray(a, dtype=t))
