@@ -185,6 +185,30 @@ __global__ void __launch_bounds__(THREADS) k_update(u32x4* __restrict__ a, size_
   a[i] = x;
 }
 
+// The packed forward's shape: a 32-lane group per 10-row segment reads the
+// segment's 800-byte K|V rows in two chunks of 5 (10 loads per lane each)
+// and writes one 400-byte row per segment.
+constexpr size_t SEG_ROWS = 10, SEG_CH = 5;
+__global__ void __launch_bounds__(THREADS) k_seg_kv_fwd(const u32x4* __restrict__ kv,
+                                                        u32x4* __restrict__ out, size_t segs) {
+  const size_t g = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (g >= segs || l >= ROWV) return;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (size_t c = 0; c < SEG_ROWS; c += SEG_CH) {
+    u32x4 x[SEG_CH], y[SEG_CH];
+#pragma unroll
+    for (size_t i = 0; i < SEG_CH; ++i) {
+      const size_t r = g * SEG_ROWS + c + i;
+      x[i] = kv[r * 2 * ROWV + l];
+      y[i] = kv[r * 2 * ROWV + ROWV + l];
+    }
+#pragma unroll
+    for (size_t i = 0; i < SEG_CH; ++i) acc ^= x[i] + y[i];
+  }
+  out[g * ROWV + l] = acc;
+}
+
 struct Buffers {
   u32x4 *a, *b, *c, *d;
   unsigned* sink;
@@ -268,6 +292,10 @@ int main(int argc, char** argv) {
       hipLaunchKernelGGL(k_rows_kv_inplace, g_rows, blk, 0, 0, B.a, nrow); }, reps)});
     rows.push_back({"update_inplace", 2.0 * bytes, median_ms([&] {
       hipLaunchKernelGGL(k_update, g_all, blk, 0, 0, B.a, B.n); }, reps)});
+    const size_t nseg = nrow / SEG_ROWS;
+    const dim3 g_segs(unsigned((nseg * 32 + THREADS - 1) / THREADS));
+    rows.push_back({"seg10_kv_fwd", double(nseg) * (SEG_ROWS * 2 + 1) * 16 * ROWV, median_ms([&] {
+      hipLaunchKernelGGL(k_seg_kv_fwd, g_segs, blk, 0, 0, B.a, B.b, nseg); }, reps)});
     rows.push_back({"rows400_kv_read", moved / 2, median_ms([&] {
       hipLaunchKernelGGL(k_rows_kv_read, g_rows, blk, 0, 0, B.a, B.sink, nrow); }, reps)});
   }
