@@ -544,9 +544,11 @@ __global__ void __launch_bounds__(HS_THREADS) k_hs_tilehist(const int32_t* __res
     }
   }
   __syncthreads();
-  // Each id's clamped count as one byte (0 past n).  Almost every id of a
-  // large universe has count 0: only the nonzero bytes reach the LDS
-  // histogram; bin 0 is implied by the tile's id count.
+  // Each id's clamped count as one byte; a 4-byte word that runs past n has
+  // 0 there, and words wholly past n are not written (the write pass masks
+  // every position at or past n).  Almost every id of a large universe has
+  // count 0: only the nonzero bytes reach the LDS histogram; bin 0 is implied
+  // by the tile's id count.
 #pragma unroll
   for (int r = 0; r < HS_SEL_ROUNDS; ++r) {
     const int64_t i0 = base + (int64_t(r) * HS_THREADS + threadIdx.x) * 4;
