@@ -483,8 +483,11 @@ constexpr int GATHER_U = 1;
 // Row moves with an optional streaming (non-temporal) policy: a gathered row
 // is read once and written once per call.  Measured on MI355X, streaming paid
 // for 16-byte moves (bigdedup nodes 0.144 -> 0.125 ms, edges 0.307 -> 0.288
-// ms, large nodes 0.171 -> 0.159 ms) and cost for 8-byte ones (large edges,
-// 344-byte rows: 0.821 -> 0.833 ms), so it is used for 16-byte moves only.
+// ms, large nodes 0.171 -> 0.159 ms).  8-byte moves (344-byte rows) stream
+// their stores whatever NT says: alone the copy runs the same (0.704-0.710
+// ms, large edges), but it leaves no dirty lines for the attention that
+// follows it in the step to write back (large step 2.626 -> 2.557 ms, its
+// layer-1 forward 0.486 -> 0.453 ms).
 template <typename V, bool NT>
 __device__ __forceinline__ V gather_ld(const V* p) {
   if constexpr (NT && sizeof(V) == 16) {
@@ -498,6 +501,8 @@ template <typename V, bool NT>
 __device__ __forceinline__ void gather_st(V* p, const V& v) {
   if constexpr (NT && sizeof(V) == 16)
     __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
+  else if constexpr (sizeof(V) == 8)
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x2, v), reinterpret_cast<u32x2*>(p));
   else
     *p = v;
 }
