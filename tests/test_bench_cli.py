@@ -36,7 +36,8 @@ def test_counter_records_are_whole_and_checked_against_the_source(tmp_path, monk
         assert 0 < rec["l2_hit_rate"] < 1 and 0 < rec["occupancy_pct"] <= 100
         assert rec["bytes_per_launch"] > 0 and os.path.exists(os.path.join(ROOT, rec["source"]))
         te = rec["time_encode_valu"]
-        assert te["valu_wave_insts_per_launch"] > 0 and "k_time_encode<" in te["kernel"]
+        assert te["valu_wave_insts_per_launch"] > 0
+        assert "k_time_encode<" in te["kernel"] or "k_time_encode_batch<" in te["kernel"]
         # a record taken on other kernel sources is not reported
         stale = dict(rec, kernel_source_sha="0" * 16)
         (tmp_path / f"t_{w}.json").write_text(json.dumps(stale))
