@@ -38,14 +38,17 @@ def _count_gpu(batches, bound, freq=None):
     return f
 
 
-def _select_gpu(fv, fe, max_freq, budget, want_slots=True):
+def _select_gpu(fv, fe, max_freq, budget, want_slots=True, slot_offset=0):
+    """slot_offset > 0 places both slot maps that many int32 past a 256-byte
+    boundary (off the 16-byte grid for 1..3: the element-wise stores)."""
     nv, ne = fv.numel(), fe.numel()
     hv = torch.full((max(min(budget, nv), 1),), -7, dtype=torch.int64, device="cuda")
     he = torch.full((max(min(budget, ne), 1),), -7, dtype=torch.int64, device="cuda")
     nhv = torch.empty(1, dtype=torch.int64, device="cuda")
     nhe = torch.empty(1, dtype=torch.int64, device="cuda")
-    sv = torch.empty(nv, dtype=torch.int32, device="cuda") if want_slots else None
-    se = torch.empty(ne, dtype=torch.int32, device="cuda") if want_slots else None
+    o = slot_offset
+    sv = torch.empty(nv + o, dtype=torch.int32, device="cuda")[o:] if want_slots else None
+    se = torch.empty(ne + o, dtype=torch.int32, device="cuda")[o:] if want_slots else None
     wsb = fast.fast_greedy_hot_set_workspace(nv, ne, max_freq)
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
     fast.fast_greedy_hot_set(fv, nv, fe, ne, max_freq, budget, hv, nhv, sv, he, nhe, se, ws, wsb)
@@ -133,7 +136,8 @@ def test_selection_both_histogram_paths(max_freq):
     the selection come from those histograms); 64 and above take the plain
     global histogram and a second pass over the counts.  Both against the
     oracle on ragged sizes (a partial last tile), with counts clamped into
-    [0, max_freq] and a count array that is not 16-byte aligned."""
+    [0, max_freq], a count array that is not 16-byte aligned, and slot maps
+    on and off the 16-byte grid."""
     _announce(f"hot set histogram path max_freq={max_freq}")
     r = np.random.default_rng(max_freq)
     nv, ne = 4096 * 7 + 1234, 4096 * 11 + 5
@@ -143,9 +147,9 @@ def test_selection_both_histogram_paths(max_freq):
     fv_big = torch.tensor(np.concatenate([[7], fv_np]), dtype=torch.int32, device="cuda")
     fv = fv_big[1:]                                   # 4 bytes off the 16-byte grid
     fe = torch.tensor(fe_np, dtype=torch.int32, device="cuda")
-    for alpha in (0.0005, 0.02, 0.3, 1.0):
+    for alpha, off in ((0.0005, 0), (0.02, 1), (0.3, 0), (1.0, 3)):
         B = fast.fast_hot_set_budget(alpha, nv, ne)
-        hv, he, sv, se = _select_gpu(fv, fe, max_freq, B)
+        hv, he, sv, se = _select_gpu(fv, fe, max_freq, B, slot_offset=off)
         ov, oe = oracle.greedy_hot_set(clamp(fv_np), clamp(fe_np), alpha)
         assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe)), alpha
         _check_slots(sv, hv, nv)
