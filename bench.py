@@ -600,6 +600,41 @@ def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3, with_oracle=F
     return res
 
 
+def offsets_bytes(N):
+    """Counts read, offsets written."""
+    return 4 * N + 4 * (N + 1)
+
+
+def dedup_gather_bytes(n, u, hits, row_bytes, slot_map):
+    """Per id 8 + 4 (id read, inverse written); per distinct id 8 (uni) and,
+    through a slot map, 4 (its slot); per cached row 2 x row_bytes (read and
+    written); per miss 4 (its miss-list entry)."""
+    return 12 * n + u * (8 + (4 if slot_map else 0)) + hits * 2 * row_bytes + (u - hits) * 4
+
+
+def step_roofline(b, breakdown, ms, nodes, edges):
+    """Algorithmic bytes of every operator of the step (inputs read once,
+    outputs written once; `nodes`/`edges` = (ids, distinct, cached) of the
+    two dedup + gathers) against the per-operator times and the whole serial
+    step."""
+    esz = 4 if b.dtype == "f32" else 2
+    F = b.H * b.dh
+    ops = {"offsets": sum(offsets_bytes(x.num_dst) for x in b.blocks),
+           "time_encode": sum(x.num_edges * (4 + b.d_t * esz) + 8 * x.num_dst for x in b.blocks),
+           "dedup_gather_nodes": dedup_gather_bytes(*nodes, b.node_D * esz, False),
+           "dedup_gather_edges": dedup_gather_bytes(*edges, b.edge_D * esz, bool(b.edge_cache_rows))}
+    for i, x in enumerate(b.blocks):
+        ops[f"attn_fwd_L{i + 1}"] = attn_fwd_bytes(x.num_dst, x.num_edges, F, esz, b.H)
+        ops[f"attn_bwd_L{i + 1}"] = attn_bwd_bytes(x.num_dst, x.num_edges, F, esz, b.H)
+    frac = lambda nb, t: round(nb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if t and t > 0 else None
+    total = sum(ops.values())
+    return {"algorithmic_bytes": total, "hbm_frac": frac(total, ms),
+            "operators": {k: {"ms": round(breakdown.get(k, 0.0), 4), "bytes": v,
+                              "hbm_frac": frac(v, breakdown.get(k))} for k, v in ops.items()},
+            "note": "each operator's inputs read once and outputs written once, summed over the "
+                    "step, against the serial step time (operators: their breakdown times)"}
+
+
 def greedy_hot_set_bytes(nv, ne, B):
     """Read every count once, write every slot-map entry, write the hot ids."""
     return 4 * (nv + ne) + 4 * (nv + ne) + 8 * B
@@ -891,6 +926,10 @@ def measure(name, args, torch, fast, headline, ceilings=None):
         step.run_serial(rec_all)
     torch.cuda.synchronize()
     breakdown = {k: float(np.mean([s.elapsed_time(e) for s, e in v])) for k, v in rec_all.items()}
+    dd = {}
+    for kind, d in (("nodes", step.node[0]), ("edges", step.edge[0])):
+        u, nm = int(d["nu"].item()), int(d["nm"].item())
+        dd[kind] = (d["n"], u, u - nm)
 
     widened = None
     if headline:
@@ -934,6 +973,7 @@ def measure(name, args, torch, fast, headline, ceilings=None):
         },
         "time_encode": time_encode_summary(b, breakdown, counters),
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
+        "step_roofline": step_roofline(b, breakdown, ms, dd["nodes"], dd["edges"]),
     }
     if widened is not None:
         result["widened_ops"] = widened
@@ -941,6 +981,8 @@ def measure(name, args, torch, fast, headline, ceilings=None):
         result["pipelined"] = {
             "ms_per_step": round(ms_pipe, 4),
             "value": b.sampled_edges / (ms_pipe * 1e-3),
+            "hbm_frac": round(result["step_roofline"]["algorithmic_bytes"] / (ms_pipe * 1e-3) / 1e9
+                              / HBM_PEAK_GBS, 4),
             "schedule": "prep of batch i+1 on a second stream overlaps attention of batch i; "
                         "attention(i) waits for prep(i); double-buffered prep outputs",
         }

@@ -26,6 +26,33 @@ def test_byte_models_match_the_design_figures():
     assert abs(fb - 7_488_000_000) / 7_488_000_000 < 0.001
 
 
+def test_step_byte_models():
+    """The prep operators' byte models on the 1e7-node batch: node ids read
+    their 400-byte rows straight from the table, edge ids through the cache's
+    slot map (291,717 of 541,340 distinct ids cached)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.offsets_bytes(264_000) == 2_112_004
+    assert bench.dedup_gather_bytes(2_664_000, 413_064, 413_064, 400, False) == \
+        12 * 2_664_000 + 413_064 * (8 + 800)
+    assert bench.dedup_gather_bytes(2_640_000, 541_340, 291_717, 688, True) == \
+        12 * 2_640_000 + 541_340 * 12 + 291_717 * 1376 + (541_340 - 291_717) * 4
+    from synth import make_batch
+    b = make_batch(0)
+    n_ids, e_ids = int(b.node_ids.size), int(b.edge_ids.size)
+    rec = bench.step_roofline(b, {"attn_bwd_L1": 0.5}, 2.0, (n_ids, 10, 10), (e_ids, 20, 15))
+    ops = rec["operators"]
+    assert rec["algorithmic_bytes"] == sum(o["bytes"] for o in ops.values())
+    assert set(ops) == {"offsets", "time_encode", "dedup_gather_nodes", "dedup_gather_edges"} | \
+        {f"attn_{d}_L{i + 1}" for d in ("fwd", "bwd") for i in range(len(b.blocks))}
+    F, esz = b.H * b.dh, 4 if b.dtype == "f32" else 2
+    L1 = b.blocks[0]
+    assert ops["attn_bwd_L1"]["bytes"] == bench.attn_bwd_bytes(L1.num_dst, L1.num_edges, F, esz, b.H)
+    assert abs(ops["attn_bwd_L1"]["hbm_frac"] - ops["attn_bwd_L1"]["bytes"] / 0.5e-3 / 8e12) < 1e-4
+    assert ops["offsets"]["hbm_frac"] is None                      # no time recorded
+    assert abs(rec["hbm_frac"] - rec["algorithmic_bytes"] / 2e-3 / 8e12) < 1e-4
+
+
 def test_counter_records_are_whole_and_checked_against_the_source(tmp_path, monkeypatch):
     sys.path.insert(0, ROOT)
     import bench
