@@ -269,6 +269,12 @@ template <> struct VecIO<float, 8> {
 // Products are formed in fp64 (exact for fp32 factors), sums in fp64.
 template <typename T, int VE>
 struct PlainRows {
+  // rows in flight per lane in the pieces of long rows, whose sums are
+  // chains of up to a thousand occurrences: 16 took the hub rows of the
+  // 1e7-node batch's layer-1 block (up to 3.1e5 occurrences) from 0.54 to
+  // 0.45 ms; the scaled source holds two coefficients more per row and
+  // stays at 4 (8 and 16 were slower there)
+  static constexpr int PIECE_UNROLL = 16;
   const T* __restrict__ src;
   int D;
   int64_t n;
@@ -289,6 +295,7 @@ struct PlainRows {
 
 template <typename T, int VE>
 struct ScaledRows {
+  static constexpr int PIECE_UNROLL = IA_UNROLL;
   const T* __restrict__ src;          // [N, H, dh]
   const float* __restrict__ occ_scal; // [n, H], occurrence order
   const int32_t* __restrict__ occ_seg;// [n], occurrence order
@@ -321,16 +328,16 @@ struct ScaledRows {
 
 // acc += the contributions of positions occ[j0 .. j1) in order, chunk c;
 // IA_UNROLL positions are fetched before they are added (in the same order).
-template <int VE, class Src>
+template <int VE, class Src, int U = IA_UNROLL>
 __device__ __forceinline__ void ia_sum(const int32_t* __restrict__ occ, int64_t j0, int64_t j1,
                                        int c, const Src& src, double (&acc)[VE]) {
   int64_t j = j0;
-  for (; j + IA_UNROLL <= j1; j += IA_UNROLL) {
-    typename Src::Item x[IA_UNROLL];
+  for (; j + U <= j1; j += U) {
+    typename Src::Item x[U];
 #pragma unroll
-    for (int r = 0; r < IA_UNROLL; ++r) x[r] = src.fetch(occ, j + r, c);
+    for (int r = 0; r < U; ++r) x[r] = src.fetch(occ, j + r, c);
 #pragma unroll
-    for (int r = 0; r < IA_UNROLL; ++r) src.add(acc, x[r]);
+    for (int r = 0; r < U; ++r) src.add(acc, x[r]);
   }
   for (; j < j1; ++j) src.add(acc, src.fetch(occ, j, c));
 }
@@ -365,7 +372,7 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
-    ia_sum<VE>(occ, j0, j1, c, src, acc);
+    ia_sum<VE, Src, Src::PIECE_UNROLL>(occ, j0, j1, c, src, acc);
 #pragma unroll
     for (int t = 0; t < VE; ++t) partial[q * D + c * VE + t] = acc[t];
   }
