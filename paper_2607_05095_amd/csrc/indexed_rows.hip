@@ -14,10 +14,12 @@
 // fast_index_add_rows: dst[u] = sum of src rows over the occurrences of u,
 // in occurrence order, accumulated in fp64 and rounded once to fp32.  A row
 // with at most IA_PIECE occurrences is summed by one group of lanes; a row
-// read by more positions (a hub id of a skewed batch) is cut into pieces of
-// about sqrt(count) occurrences, each summed by its own group, and the row
-// adds its piece sums in piece order.  The cut depends only on the counts, so the
-// result is the same on every run.
+// read by more positions (a hub id of a skewed batch) is summed as a fixed
+// three-level tree: pieces of consecutive occurrences, each summed by its own
+// group, then (when there are many pieces) groups of consecutive piece sums,
+// then the row adds its group (or piece) sums in order -- each level about
+// cbrt(count) long, so no group walks a long chain of dependent loads.  The
+// tree depends only on the counts, so the result is the same on every run.
 #include "scan.h"
 
 namespace fast {
@@ -218,37 +220,76 @@ constexpr int IA_THREADS = 256;
 constexpr int IA_PIECE = 64;   // occurrences summed by one group
 constexpr int IA_UNROLL = 4;   // rows in flight per lane
 
-// Piece length of a row with c > IA_PIECE occurrences: the smallest power of
-// two >= max(IA_PIECE, sqrt(c)), so the piece sums and the final sum of the
-// pieces take about the same time (a 240k-occurrence hub row: 469 pieces of
-// 512).  A function of c alone, so the cut is the same on every run.
-__device__ __forceinline__ int64_t ia_piece_len(int64_t c) {
-  int64_t p = IA_PIECE;
-  while (p * p < c) p <<= 1;
+constexpr int IA_GROUP_MIN = 16;   // fewest pieces per group of the second level
+
+// The smallest power of two p >= lo with p^3 >= c (c < 2^31: p <= 2048).
+__device__ __forceinline__ int64_t ia_cbrt_pow2(int64_t c, int64_t lo) {
+  int64_t p = lo;
+  while (p * p * p < c) p <<= 1;
   return p;
 }
+// Tree of a row with c > IA_PIECE occurrences: pieces of ia_piece_len(c)
+// occurrences and, when there are more than ia_group_len(c) pieces, groups of
+// that many consecutive pieces.  For c = 3e5 (a hub of the 1e7-node batch):
+// 2344 pieces of 128, 19 groups of 128 pieces.  Functions of c alone.
+__device__ __forceinline__ int64_t ia_piece_len(int64_t c) { return ia_cbrt_pow2(c, IA_PIECE); }
+__device__ __forceinline__ int64_t ia_group_len(int64_t c) { return ia_cbrt_pow2(c, IA_GROUP_MIN); }
 
-// Pieces of a row with more than IA_PIECE occurrences (0 for shorter rows,
-// which one group sums directly); at most 2 c / IA_PIECE.
+// Pieces of a row (0 for c <= IA_PIECE, which one group sums directly); at
+// most 2 c / IA_PIECE.
 __device__ __forceinline__ int64_t ia_multi_pieces(int64_t c) {
   if (c <= IA_PIECE) return 0;
   const int64_t p = ia_piece_len(c);
   return (c + p - 1) / p;
 }
+// Groups of the second level (0 when the row has at most ia_group_len(c)
+// pieces); at most 2 pieces / IA_GROUP_MIN.
+__device__ __forceinline__ int64_t ia_multi_groups(int64_t c) {
+  const int64_t m = ia_multi_pieces(c), g = ia_group_len(c);
+  return m > g ? (m + g - 1) / g : 0;
+}
 
+// Both counts of row u in one 64-bit item (pieces high, groups low) for one
+// scan; item num_rows is 0, so the prefix at num_rows is the pair of totals.
 struct InMulti {
   const int32_t* occ_off;
-  int64_t n;
-  __device__ uint32_t operator()(int64_t u) const {
-    return uint32_t(ia_multi_pieces(clamp64(int64_t(occ_off[u + 1]) - occ_off[u], 0, n)));
+  int64_t n, num_rows;
+  __device__ uint64_t operator()(int64_t u) const {
+    if (u >= num_rows) return 0u;
+    const int64_t c = clamp64(int64_t(occ_off[u + 1]) - occ_off[u], 0, n);
+    return (uint64_t(ia_multi_pieces(c)) << 32) | uint64_t(ia_multi_groups(c));
   }
 };
 struct OutMulti {
   int32_t* multi_off;
-  __device__ void operator()(int64_t u, uint32_t prefix, uint32_t) const {
-    multi_off[u] = int32_t(prefix);
+  int32_t* group_off;
+  __device__ void operator()(int64_t u, uint64_t prefix, uint64_t) const {
+    multi_off[u] = int32_t(prefix >> 32);
+    group_off[u] = int32_t(prefix & 0xffffffffu);
   }
 };
+
+// acc += fp64 rows part[m0 .. m1) (chunk c of VE values, rows of D), in
+// order, U rows loaded before they are added.
+template <int VE, int U>
+__device__ __forceinline__ void ia_sum_partials(const double* __restrict__ part, int64_t m0,
+                                                int64_t m1, int D, int c, double (&acc)[VE]) {
+  int64_t m = m0;
+  for (; m + U <= m1; m += U) {
+    double x[U][VE];
+#pragma unroll
+    for (int r = 0; r < U; ++r)
+#pragma unroll
+      for (int t = 0; t < VE; ++t) x[r][t] = part[(m + r) * D + c * VE + t];
+#pragma unroll
+    for (int r = 0; r < U; ++r)
+#pragma unroll
+      for (int t = 0; t < VE; ++t) acc[t] += x[r][t];
+  }
+  for (; m < m1; ++m)
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] += part[m * D + c * VE + t];
+}
 
 // Eight fp32 values of a row sum (the bf16 sources' widest vector).
 template <> struct VecIO<float, 8> {
@@ -378,48 +419,78 @@ __global__ void __launch_bounds__(IA_THREADS) k_ia_pieces(
   }
 }
 
+// Second level of the long rows: one group of `lanes` lanes per group g in
+// [0, group_off[num_rows]) of ia_group_len(c) consecutive piece sums, added
+// in piece order into partial2[g].
+template <int VE>
+__global__ void __launch_bounds__(IA_THREADS) k_ia_groups(
+    const int32_t* __restrict__ occ_off, const int32_t* __restrict__ multi_off,
+    const int32_t* __restrict__ group_off, int64_t num_rows, int64_t multi_bound,
+    int64_t group_bound, int64_t n, int lanes, int D, const double* __restrict__ partial,
+    double* __restrict__ partial2) {
+  const int64_t g = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
+  const int l = int(threadIdx.x) % lanes;
+  if (g >= group_bound || g >= group_off[num_rows]) return;
+  // the long row u with group_off[u] <= g < group_off[u + 1]
+  int64_t lo = 0, hi = num_rows - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (group_off[mid] <= g) lo = mid; else hi = mid - 1;
+  }
+  const int64_t u = lo, k = g - group_off[u];
+  const int64_t r0 = clamp64(occ_off[u], 0, n);
+  const int64_t r1 = clamp64(occ_off[u + 1], r0, n);
+  const int64_t len = ia_group_len(r1 - r0);
+  const int64_t p0 = clamp64(multi_off[u], 0, multi_bound);
+  const int64_t p1 = clamp64(multi_off[u + 1], p0, multi_bound);
+  const int64_t m0 = clamp64(p0 + k * len, p0, p1);
+  const int64_t m1 = m0 + len < p1 ? m0 + len : p1;
+  const int chunks = D / VE;
+  for (int c = l; c < chunks; c += lanes) {
+    double acc[VE];
+#pragma unroll
+    for (int t = 0; t < VE; ++t) acc[t] = 0.0;
+    ia_sum_partials<VE, 8>(partial, m0, m1, D, c, acc);
+#pragma unroll
+    for (int t = 0; t < VE; ++t) partial2[g * D + c * VE + t] = acc[t];
+  }
+}
+
 // One group per row: a short row sums its occurrences directly (zeros for
-// none), a long row adds its piece sums in piece order.  fp64 sums, rounded
-// once to fp32.
+// none), a long row adds its group sums (or, with few pieces, its piece sums)
+// in order.  fp64 sums, rounded once to fp32.
 template <int VE, class Src>
 __global__ void __launch_bounds__(IA_THREADS) k_ia_rows(
     const int32_t* __restrict__ occ_off, const int32_t* __restrict__ occ,
-    const int32_t* __restrict__ multi_off, int64_t num_rows, int64_t multi_bound, int64_t n,
-    int lanes, int D, Src src, const double* __restrict__ partial, float* __restrict__ dst) {
+    const int32_t* __restrict__ multi_off, const int32_t* __restrict__ group_off,
+    int64_t num_rows, int64_t multi_bound, int64_t group_bound, int64_t n, int lanes, int D,
+    Src src, const double* __restrict__ partial, const double* __restrict__ partial2,
+    float* __restrict__ dst) {
   const int64_t u = (int64_t(blockIdx.x) * IA_THREADS + threadIdx.x) / lanes;
   const int l = int(threadIdx.x) % lanes;
   if (u >= num_rows) return;
   const int64_t j0 = clamp64(occ_off[u], 0, n);
   const int64_t j1 = clamp64(occ_off[u + 1], j0, n);
-  // piece range clamped too: the piece counts of malformed lists may wrap
+  // piece and group ranges clamped too: the counts of malformed lists may wrap
   const int64_t m0 = clamp64(multi_off[u], 0, multi_bound);
   const int64_t m1 = clamp64(multi_off[u + 1], m0, multi_bound);
+  const int64_t g0 = clamp64(group_off[u], 0, group_bound);
+  const int64_t g1 = clamp64(group_off[u + 1], g0, group_bound);
   const bool longrow = ia_multi_pieces(j1 - j0) > 0;
+  // a long row's sums of the level below: its groups, or its pieces
+  const bool grouped = g1 > g0;
+  const double* __restrict__ part = grouped ? partial2 : partial;
+  const int64_t p0 = grouped ? g0 : m0, p1 = grouped ? g1 : m1;
   const int chunks = D / VE;
   for (int c = l; c < chunks; c += lanes) {
     src.chunk(c);
     double acc[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) acc[t] = 0.0;
-    if (!longrow) {
+    if (!longrow)
       ia_sum<VE>(occ, j0, j1, c, src, acc);
-    } else {
-      int64_t m = m0;
-      for (; m + IA_UNROLL <= m1; m += IA_UNROLL) {     // loads ahead, adds in order
-        double x[IA_UNROLL][VE];
-#pragma unroll
-        for (int r = 0; r < IA_UNROLL; ++r)
-#pragma unroll
-          for (int t = 0; t < VE; ++t) x[r][t] = partial[(m + r) * D + c * VE + t];
-#pragma unroll
-        for (int r = 0; r < IA_UNROLL; ++r)
-#pragma unroll
-          for (int t = 0; t < VE; ++t) acc[t] += x[r][t];
-      }
-      for (; m < m1; ++m)
-#pragma unroll
-        for (int t = 0; t < VE; ++t) acc[t] += partial[m * D + c * VE + t];
-    }
+    else
+      ia_sum_partials<VE, IA_UNROLL>(part, p0, p1, D, c, acc);
     float o[VE];
 #pragma unroll
     for (int t = 0; t < VE; ++t) o[t] = float(acc[t]);
@@ -459,11 +530,15 @@ __global__ void __launch_bounds__(IA_THREADS) k_coef_permute(
 
 struct IaWs {
   int32_t* multi_off;
+  int32_t* group_off;
   void* scan;
   double* partial;
+  double* partial2;
 };
 
 static int64_t ia_multi_bound(int64_t n) { return (2 * n) / IA_PIECE + 1; }
+// pieces of rows with groups, over IA_GROUP_MIN / 2
+static int64_t ia_group_bound(int64_t n) { return ia_multi_bound(n) * 2 / IA_GROUP_MIN + 1; }
 
 static size_t ia_layout(int64_t n, int64_t num_rows, int D, char* base, IaWs* ws) {
   size_t off = 0;
@@ -473,12 +548,16 @@ static size_t ia_layout(int64_t n, int64_t num_rows, int D, char* base, IaWs* ws
     return base ? base + o : nullptr;
   };
   char* mo = take(size_t(num_rows + 1) * 4);
-  char* sc = take(scan_workspace(num_rows));
+  char* go = take(size_t(num_rows + 1) * 4);
+  char* sc = take(scan_workspace<uint64_t>(num_rows + 1));
   char* pa = take(size_t(ia_multi_bound(n)) * size_t(D) * 8);
+  char* pb = take(size_t(ia_group_bound(n)) * size_t(D) * 8);
   if (ws) {
     ws->multi_off = reinterpret_cast<int32_t*>(mo);
+    ws->group_off = reinterpret_cast<int32_t*>(go);
     ws->scan = sc;
     ws->partial = reinterpret_cast<double*>(pa);
+    ws->partial2 = reinterpret_cast<double*>(pb);
   }
   return off;
 }
@@ -543,25 +622,33 @@ extern "C" fast_status_t fast_occurrence_csr(const int32_t* index, int64_t n, in
   return check_launch(fn);
 }
 
-// Launches the row sums over occurrence lists for a row source: the piece
-// count scan, the long rows' pieces, then one group per row.
+// Launches the row sums over occurrence lists for a row source: one scan of
+// the (piece, group) counts, the long rows' pieces, their groups, then one
+// group of lanes per row.
 template <int VE, class Src>
 static hipError_t ia_launch(const int32_t* occ_off, const int32_t* occ, int64_t n,
                             int64_t num_rows, int D, const Src& src, const IaWs& w, float* dst,
                             hipStream_t st) {
-  hipError_t e = scan_launch(InMulti{occ_off, n}, OutMulti{w.multi_off}, num_rows, w.scan, nullptr,
-                             w.multi_off + num_rows, st);
+  hipError_t e = scan_launch<InMulti, OutMulti, uint64_t>(
+      InMulti{occ_off, n, num_rows}, OutMulti{w.multi_off, w.group_off}, num_rows + 1, w.scan,
+      nullptr, nullptr, st);
   if (e != hipSuccess) return e;
   const int lanes = pow2_at_least(D / VE, 64);
   const int64_t groups_per_block = IA_THREADS / lanes;
-  const int64_t mb = ia_multi_bound(n);
+  const int64_t mb = ia_multi_bound(n), gb = ia_group_bound(n);
   const int64_t np_blocks = (mb + groups_per_block - 1) / groups_per_block;
+  const int64_t ng_blocks = (gb + groups_per_block - 1) / groups_per_block;
   const int64_t nr_blocks = (num_rows + groups_per_block - 1) / groups_per_block;
-  if (n > 0)
+  if (n > 0) {
     hipLaunchKernelGGL((k_ia_pieces<VE, Src>), dim3(uint32_t(np_blocks)), dim3(IA_THREADS), 0, st,
                        occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, src, w.partial);
+    hipLaunchKernelGGL((k_ia_groups<VE>), dim3(uint32_t(ng_blocks)), dim3(IA_THREADS), 0, st,
+                       occ_off, w.multi_off, w.group_off, num_rows, mb, gb, n, lanes, D, w.partial,
+                       w.partial2);
+  }
   hipLaunchKernelGGL((k_ia_rows<VE, Src>), dim3(uint32_t(nr_blocks)), dim3(IA_THREADS), 0, st,
-                     occ_off, occ, w.multi_off, num_rows, mb, n, lanes, D, src, w.partial, dst);
+                     occ_off, occ, w.multi_off, w.group_off, num_rows, mb, gb, n, lanes, D, src,
+                     w.partial, w.partial2, dst);
   return hipGetLastError();
 }
 
