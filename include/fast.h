@@ -62,7 +62,11 @@ typedef enum {
   FAST_ERR_HIP = 4           /* a HIP launch or runtime call failed */
 } fast_status_t;
 
-typedef enum { FAST_F32 = 0, FAST_BF16 = 1 } fast_dtype_t;
+/* FAST_DTYPE_MAX_ENUM widens the enum's range to every non-negative 32-bit
+ * value, so that a C caller's out-of-range value reaches the library as a
+ * defined value of the type (and is rejected with FAST_ERR_INVALID_ARG) also
+ * in C++, where an enum without it could only hold 0 and 1. */
+typedef enum { FAST_F32 = 0, FAST_BF16 = 1, FAST_DTYPE_MAX_ENUM = 0x7fffffff } fast_dtype_t;
 
 typedef void* fast_stream_t; /* hipStream_t */
 

@@ -35,7 +35,9 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfast.so")
+# the in-tree build; FAST_LIB names another build of the same sources (the
+# sanitizer build of the host code)
+LIB_PATH = os.environ.get("FAST_LIB") or os.path.join(_HERE, "libfast.so")
 
 F32, BF16 = 0, 1
 NOALLOC_SCRATCH_BYTES = 128 << 20   # FAST_NOALLOC_SCRATCH_BYTES of include/fast.h

@@ -33,12 +33,20 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    extra = os.environ.get("FAST_HIPCC_FLAGS", "").split()   # e.g. -DFAST_ATT_CH=10
+# Host-side instrumentation for the sanitizer build of the library (the host
+# code: argument checks, workspace layouts, launches); device code is built
+# as usual.  Each flag is marked for the host compilation only.
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+
+
+def _compile(src: str, verbose: bool, objdir: str = OBJDIR, extra_flags=()) -> str:
+    obj = os.path.join(objdir, os.path.basename(src) + ".o")
+    extra = os.environ.get("FAST_HIPCC_FLAGS", "").split() + list(extra_flags)   # e.g. -DFAST_ATT_CH=10
     cmd = [HIPCC] + COMMON + extra + ["-c", src, "-o", obj]
     if src.endswith(".cpp"):
-        cmd = [HIPCC, "-O2", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC, "-c", src, "-o", obj]
+        cmd = [HIPCC, "-O2", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC] + list(extra_flags) + \
+            ["-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -83,6 +91,35 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     os.replace(tmp, LIB)
     build_probe(verbose)
     return LIB
+
+
+def build_host_sanitized(out: str, verbose: bool = False, jobs: int | None = None) -> str:
+    """libfast.so with ASan + UBSan on its host code, written to `out` (objects
+    beside it).  Load it with clang's ASan runtime preloaded
+    (sanitizer_runtime()); the in-tree library is left untouched."""
+    objdir = os.path.join(os.path.dirname(os.path.abspath(out)), "_build_san")
+    os.makedirs(objdir, exist_ok=True)
+    srcs = sources()
+    jobs = jobs or min(len(srcs), max(1, os.cpu_count() or 4), 8)
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose, objdir, HOST_SANITIZE), srcs))
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-shared-libsan"] + HOST_SANITIZE[:4] + \
+        ["-o", out] + objs
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def sanitizer_runtime() -> str | None:
+    """clang's shared ASan runtime (it carries the UBSan handlers), or None."""
+    r = subprocess.run([HIPCC, "--print-file-name=libclang_rt.asan-x86_64.so"],
+                       capture_output=True, text=True)
+    path = r.stdout.strip()
+    if r.returncode == 0 and os.path.isabs(path) and os.path.exists(path):
+        return path
+    hits = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    return hits[-1] if hits else None
 
 
 if __name__ == "__main__":
