@@ -250,6 +250,36 @@ def _assert_packed_equals_separate(d, what, slope=SLOPE):
             assert torch.equal(x, y), f"{what} lse={with_lse}: packed {n} differs from separate"
 
 
+def _random_attention_case(seed):
+    """A seeded random shape: H in {1..8}, dh in [1, 128], fp32 or bf16, a
+    slope of 0.2, 0, -0.3 or 1, and 20-60 segments of mixed degree (empty,
+    1-30, and now and then 100-400 edges)."""
+    r = np.random.default_rng(4000 + seed)
+    H = int(r.choice([1, 2, 3, 4, 5, 8]))
+    dh = int(r.integers(1, 129))
+    dt = "bf16" if r.random() < 0.4 else "f32"
+    slope = float(r.choice([0.2, 0.0, -0.3, 1.0]))
+    N = int(r.integers(20, 61))
+    counts = r.integers(1, 31, N)
+    counts[r.random(N) < 0.1] = 0
+    counts[r.random(N) < 0.05] = r.integers(100, 401)
+    return [int(c) for c in counts], H, dh, dt, slope
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_attention_random_shapes(seed):
+    """Seeded random head counts, head widths (every vector width and lane
+    layout those reach), storage types, slopes and degree mixes: the fused
+    operators (with and without the saved lse) and the unfused chain against
+    the oracle, and packed K|V rows equal to separate arrays bit for bit."""
+    counts, H, dh, dt, slope = _random_attention_case(seed)
+    _announce(f"attention random shape seed={seed}: H={H} dh={dh} {dt} slope={slope} "
+              f"N={len(counts)} E={sum(counts)}")
+    d = _synthetic_block(counts, H, dh, dt, seed=100 + seed)
+    _check_block(d, None, f"random seed={seed}", slope=slope)
+    _assert_packed_equals_separate(d, f"random seed={seed}", slope=slope)
+
+
 @pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
 def test_attention_packed_kv_equals_separate_workloads(cfg):
     """Packed K|V rows run the same kernels with rows 2F apart: every output
