@@ -161,7 +161,10 @@ fast_status_t fast_check_tcsr(const fast_tcsr_t* g, int64_t src_bound, int64_t e
  * Outputs: uni cap n, inv [n], rows cap n*D (or NULL: dedup only, then
  *   table may be NULL), miss cap n (or NULL; *num_miss is still written
  *   when num_miss != NULL).
- * Limits: n < 2^31, id_bound <= 2^35.
+ * Limits: n < 2^31, id_bound <= 2^35; a row at most 256 vectors of the
+ *   widest access (16, 8, 4 or 2 bytes) that D * element size and the table
+ *   and rows pointers' alignment allow -- every D <= 256 qualifies; a wider
+ *   row returns FAST_ERR_UNSUPPORTED.
  * Workspace: fast_dedup_gather_workspace(n, id_bound) bytes, 256-byte aligned.
  * ------------------------------------------------------------------------ */
 size_t fast_dedup_gather_workspace(int64_t n, int64_t id_bound);

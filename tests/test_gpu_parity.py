@@ -707,6 +707,57 @@ def test_gather_rows_of_odd_eight_byte_width(D, dt):
     assert np.all(_bits(rows)[~hit] == 0), "a miss row must be left untouched"
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_dedup_gather_random(seed):
+    """Seeded random batches: universes from 16 ids to 2^31, 0 to 120 k ids
+    (uniform, or Zipf-hot with a few ids in every workgroup's share), some
+    ids outside the universe, and rows of random width and storage gathered
+    straight from a table or through a slot map into a cache with misses --
+    every marking path and row-copy shape, against the oracle."""
+    r = np.random.default_rng(5000 + seed)
+    bound = int(2 ** r.uniform(4, 31))
+    n = int(r.choice([0, 1, int(r.integers(2, 3000)), int(r.integers(3000, 120_001))],
+                     p=[0.08, 0.08, 0.42, 0.42]))
+    if r.random() < 0.5:
+        ids = r.integers(0, bound, n)
+    else:
+        hot = r.integers(0, bound, 8)
+        ids = np.where(r.random(n) < 0.5, hot[r.integers(0, 8, n)], r.integers(0, bound, n))
+    ids = ids.astype(np.int64)
+    bad = r.random(n) < 0.02
+    ids[bad] = r.choice([-1, -7, bound, bound + 5], int(bad.sum()))
+    valid = (ids >= 0) & (ids < bound)
+    D = int(r.integers(1, 257))          # any width whose row is at most 256 vectors
+    dt = "bf16" if r.random() < 0.5 else "f32"
+    mode = str(r.choice(["none", "table", "slot"], p=[0.2, 0.4, 0.4]))
+    if mode == "table" and bound > 200_000:          # the oracle copies the whole table
+        mode = "slot" if bound <= 50_000_000 else "none"
+    if mode == "slot" and bound > 50_000_000:
+        mode = "none"
+    _announce(f"dedup random seed={seed}: n={n} bound={bound} {mode} D={D} {dt}")
+    table = sm_np = None
+    if mode == "table":
+        table = make_table(bound, D, dt, device="cuda", seed=seed, stream=7)
+    elif mode == "slot":
+        rows = int(r.integers(1, 20_000))
+        table = make_table(rows, D, dt, device="cuda", seed=seed, stream=8)
+        sm_np = r.integers(0, rows, bound).astype(np.int32)
+        sm_np[r.random(bound) < 0.3] = -1
+    uni, inv, u, got_rows, miss, nm = _dedup(ids, bound, table,
+                                             slot_map=to_dev(sm_np) if sm_np is not None else None)
+    ref_uni, ref_inv = oracle.dedup(ids[valid])
+    assert u == ref_uni.size and np.array_equal(uni, ref_uni)
+    assert np.array_equal(inv[valid], ref_inv) and np.all(inv[~valid] == -1)
+    if table is not None:
+        ref_rows, hit, ref_miss = oracle.gather(ref_uni, _bits(table), sm_np)
+        assert np.array_equal(_bits(got_rows)[hit], ref_rows[hit]), "gathered rows differ"
+        assert nm == ref_miss.size and np.array_equal(miss[:nm].cpu().numpy(), ref_miss)
+    else:
+        assert nm == u and np.array_equal(miss[:nm].cpu().numpy(), np.arange(u))
+    del table
+    torch.cuda.empty_cache()
+
+
 # ------------------------------------------------------------------ time encoding (a4)
 def _te_gpu(blk_off, dst_t, edge_t, omega, phi, dt="f32"):
     E = edge_t.shape[0]
@@ -751,6 +802,39 @@ def test_time_encode_no_edges():
     off = np.zeros(6, np.int32)
     te = _te_gpu(off, np.ones(5, np.float32), np.zeros(0, np.float32), *omega_phi(10))
     assert te.shape[0] == 0
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_time_encode_random(seed):
+    """Seeded random blocks: time widths 1-256, fp32 or bf16 output, 1-3000
+    segments of degree 0-60, time scales from 1 to 1e4 and phases drawn at
+    random; every row against the oracle, and the batched launch over a
+    random split of the same segments equal to the single-block calls bit
+    for bit."""
+    r = np.random.default_rng(6000 + seed)
+    d_t = int(r.integers(1, 257))
+    dt = "bf16" if r.random() < 0.5 else "f32"
+    N = int(r.integers(1, 3001))
+    counts = r.integers(0, 61, N)
+    counts[r.random(N) < 0.1] = 0
+    scale = float(10 ** r.uniform(0, 4))
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    E = int(off[-1])
+    dst_t = (r.random(N) * scale + 1.0).astype(np.float32)
+    seg = np.repeat(np.arange(N), counts)
+    edge_t = (dst_t[seg] * r.random(E)).astype(np.float32)
+    om, ph = omega_phi(d_t)
+    ph = (r.uniform(-3.0, 3.0, d_t) if r.random() < 0.5 else ph).astype(np.float32)
+    _announce(f"time encode random seed={seed}: d_t={d_t} {dt} N={N} E={E} scale={scale:.0f}")
+    te = _te_gpu(off, dst_t, edge_t, om, ph, dt)
+    check_time_encode_full(off, dst_t, edge_t, om, ph, te.cpu(), dt, f"te random seed={seed}")
+    cuts = np.sort(r.choice(np.arange(1, N), min(int(r.integers(0, 4)), N - 1), replace=False)) if N > 1 else []
+    bounds = [0] + [int(c) for c in cuts] + [N]
+    blocks = []
+    for a, c in zip(bounds[:-1], bounds[1:]):
+        sub = (off[a:c + 1] - off[a]).astype(np.int32)
+        blocks.append((sub, dst_t[a:c], edge_t[off[a]:off[c]]))
+    _te_batched_vs_single(blocks, om, ph, dt)
 
 
 @pytest.mark.parametrize("out", ["f32", "bf16"])
