@@ -192,3 +192,35 @@ def test_bigdedup_universe_properties():
     assert np.all(np.diff(hv) > 0) and np.all(np.diff(he) > 0)
     _check_slots(sv, hv, nb)
     _check_slots(se, he, eb)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_selection_random(seed):
+    """Seeded random universes (0 to 300 k nodes and edges), count laws
+    (uniform or Zipf-like, clamped at max_freq from 1 to 5000, both sides of
+    the one-byte code path at 64) and budgets from 0 to beyond every id,
+    with slot maps on and off the 16-byte grid: sets and slot maps equal to
+    the oracle's selection."""
+    r = np.random.default_rng(8000 + seed)
+    max_freq = int(r.choice([1, 2, 7, 63, 64, 300, 5000]))
+    nv = int(r.choice([0, int(r.integers(1, 5000)), int(r.integers(5000, 300_001))], p=[0.1, 0.4, 0.5]))
+    ne = int(r.choice([0, int(r.integers(1, 5000)), int(r.integers(5000, 300_001))], p=[0.1, 0.4, 0.5]))
+
+    def law(n):
+        if r.random() < 0.5:
+            return r.integers(0, max_freq + 1, n)
+        return np.minimum(r.zipf(float(r.uniform(1.1, 2.5)), n) - 1, max_freq + 3)
+
+    fv_np, fe_np = law(nv).astype(np.int32), law(ne).astype(np.int32)
+    alpha = float(r.choice([0.0, float(r.uniform(0, 0.05)), float(r.uniform(0.05, 1.0)), 1.0, 1.7]))
+    off = int(r.integers(0, 4))
+    _announce(f"hot set random seed={seed}: |V|={nv} |E|={ne} max_freq={max_freq} alpha={alpha:.4f}")
+    clamp = lambda a: np.clip(a, 0, max_freq)
+    dev = lambda a: torch.tensor(a, dtype=torch.int32, device="cuda")
+    B = fast.fast_hot_set_budget(alpha, nv, ne)
+    hv, he, sv, se = _select_gpu(dev(fv_np), dev(fe_np), max_freq, B, slot_offset=off)
+    ov, oe = oracle.greedy_hot_set(clamp(fv_np), clamp(fe_np), alpha)
+    assert hv.size + he.size == B == ov.size + oe.size
+    assert np.array_equal(hv, np.sort(ov)) and np.array_equal(he, np.sort(oe))
+    _check_slots(sv, hv, nv)
+    _check_slots(se, he, ne)

@@ -89,6 +89,38 @@ def test_index_add_rows_vs_oracle(D, dt, rows):
     assert torch.all(got[rows:] == 0)
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_occurrence_lists_and_row_sums_random(seed):
+    """Seeded random indices: 0 to 400 k positions over 1 to 300 k rows,
+    uniform or Zipf with exponents from 1.05 (hub rows of 10^5 reads, the
+    three-level sums) to 3, some positions outside the row range; source
+    rows of random width and storage.  Occurrence lists bit-exact, row sums
+    against the oracle's fp64 sums, and a second call bitwise equal."""
+    r = np.random.default_rng(7000 + seed)
+    n = int(r.choice([0, int(r.integers(1, 5000)), int(r.integers(5000, 400_001))], p=[0.05, 0.35, 0.6]))
+    rows = int(r.choice([1, int(r.integers(2, 1000)), int(r.integers(1000, 300_001))], p=[0.1, 0.45, 0.45]))
+    if r.random() < 0.3:
+        idx = r.integers(0, rows, n)
+    else:
+        idx = (r.zipf(float(r.uniform(1.05, 3.0)), n) - 1) % rows
+    idx = idx.astype(np.int32)
+    idx[r.random(n) < 0.01] = -1
+    D = int(r.integers(1, 200))
+    dt = "bf16" if r.random() < 0.5 else "f32"
+    _announce(f"index add random seed={seed}: n={n} rows={rows} D={D} {dt}")
+    off, occ = _occ_gpu(idx, rows)
+    w_off, w_occ = oracle.occurrence_csr(idx, rows)
+    assert np.array_equal(off.cpu().numpy(), w_off)
+    assert np.array_equal(occ.cpu().numpy()[:int(w_off[-1])], w_occ)
+    if n == 0:
+        return
+    src = _randn((n, D), dt, "cuda", 7100 + seed)
+    got = _index_add_gpu(off, occ, n, rows, src)
+    want = oracle.index_add_rows(idx, rows, _host(src))
+    assert_close(got, want, "f32", f"index add random seed={seed}")
+    assert torch.equal(got, _index_add_gpu(off, occ, n, rows, src)), "row sums must be reproducible"
+
+
 def _indexed_block(b, i, seed):
     """Operands of block i with K read through the de-duplication inverse of
     the block's source node ids and V through that of its edge ids."""
