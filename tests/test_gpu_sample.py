@@ -73,6 +73,30 @@ def test_sample_recent_vs_oracle(nodes, events, k):
     _assert_equal_sample(got, want, f"V={nodes} k={k}")
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_sample_recent_random(seed):
+    """Seeded random graphs (100 to 2e5 nodes, 1e3 to 2e6 events, Zipf
+    exponents from 1.02 to 1.6 -- hub nodes with up to a million entries),
+    k from 1 to 40, roots at random times (before, between and after the
+    events, some exactly on event times) and some invalid roots: bit-exact
+    against the oracle."""
+    r = np.random.default_rng(9500 + seed)
+    nodes = int(10 ** r.uniform(2, 5.3))
+    events = int(10 ** r.uniform(3, 6.3))
+    k = int(r.integers(1, 41))
+    g = make_temporal_graph(nodes, events, seed=9600 + seed, zipf_s=float(r.uniform(1.02, 1.6)))
+    dg = DevGraph(g)
+    R = int(r.integers(1, 3000))
+    roots = r.integers(-2, nodes + 2, R).astype(np.int64)
+    rt = (r.uniform(-0.1, 1.1, R) * float(g.ev_t.max() if g.ev_t.size else 1.0)).astype(np.float32)
+    on = r.random(R) < 0.2
+    rt[on] = g.ev_t[r.integers(0, g.ev_t.size, int(on.sum()))]
+    _announce(f"sample recent random seed={seed}: V={nodes} events={events} k={k} roots={R}")
+    got = _sample_gpu(dg, roots, rt, k)
+    want = oracle.sample_recent(g.indptr, g.nbr, g.ts, g.eid, roots, rt, k)
+    _assert_equal_sample(got, want, f"random seed={seed}")
+
+
 def test_two_hops_feed_the_block_operators():
     _announce("sample two hops -> contract check -> time encoding")
     g = make_temporal_graph(50000, 500000, seed=4)

@@ -134,3 +134,33 @@ def test_time_encode_bwd_cancelling_column_and_huge_arguments():
     ref = oracle.time_encode_bwd(off, dt, np.zeros(E, np.float32), om, ph, dte)
     assert_close(got[0], ref[0], "f32", "domega (cancelling)")
     assert_close(got[1], ref[1], "f32", "dphi (cancelling)")
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_time_encode_bwd_random(seed):
+    """Seeded random blocks: time widths 1-256 (every vector width the
+    kernel picks), fp32 or bf16 upstream gradients, 1-6000 segments of degree
+    0-60 (a partial last group of segments, more groups than workgroups at
+    the top of the range), time scales 1-1e4 and random phases; both outputs
+    against the oracle's fp64 sums, and a second call bitwise equal."""
+    r = np.random.default_rng(9000 + seed)
+    d_t = int(r.integers(1, 257))
+    dt = "bf16" if r.random() < 0.5 else "f32"
+    N = int(r.integers(1, 6001))
+    counts = r.integers(0, 61, N)
+    counts[r.random(N) < 0.1] = 0
+    scale = float(10 ** r.uniform(0, 4))
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    E = int(off[-1])
+    dst_t = (r.random(N) * scale + 1.0).astype(np.float32)
+    edge_t = (dst_t[np.repeat(np.arange(N), counts)] * r.random(E)).astype(np.float32)
+    om, ph = omega_phi(d_t)
+    ph = (r.uniform(-3.0, 3.0, d_t) if r.random() < 0.5 else ph).astype(np.float32)
+    _announce(f"time encode bwd random seed={seed}: d_t={d_t} {dt} N={N} E={E} scale={scale:.0f}")
+    dte = _randn((max(E, 1), d_t), dt, "cuda", 9100 + seed)[:E]
+    got = _tb_gpu(off, dst_t, edge_t, om, ph, dte)
+    ref = _oracle_chunked(off, dst_t, edge_t, om, ph, dte)
+    assert_close(got[0], ref[0], "f32", f"domega random seed={seed}")
+    assert_close(got[1], ref[1], "f32", f"dphi random seed={seed}")
+    again = _tb_gpu(off, dst_t, edge_t, om, ph, dte)
+    assert np.array_equal(got[0], again[0]) and np.array_equal(got[1], again[1])
