@@ -192,6 +192,62 @@ def test_indexed_attention_workloads(cfg, i):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_indexed_attention_random(seed):
+    """Seeded random shapes (H 1-8, dh 1-96, fp32 or bf16, slopes 0.2 / 0 /
+    -0.3 / 1) and random indices into fewer compact K and V rows than edges
+    (hub rows included): the indexed forward and per-edge backward against
+    the oracle on the rows each edge reads, the coefficient form's dQ equal
+    to the per-edge backward's, and the row gradients against the oracle's
+    sums."""
+    r = np.random.default_rng(9800 + seed)
+    H = int(r.choice([1, 2, 3, 4, 8]))
+    dh = int(r.integers(1, 97))
+    dt = "bf16" if r.random() < 0.4 else "f32"
+    slope = float(r.choice([0.2, 0.0, -0.3, 1.0]))
+    N = int(r.integers(10, 80))
+    counts = r.integers(0, 40, N)
+    counts[r.random(N) < 0.05] = r.integers(100, 300)
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    E = int(off[-1])
+    Uk, Uv = max(1, int(r.integers(1, E + 2) // 2)), max(1, int(r.integers(1, E + 2)))
+    kidx = ((r.zipf(1.5, E) - 1) % Uk).astype(np.int32)
+    vidx = r.integers(0, Uv, E).astype(np.int32)
+    _announce(f"indexed attention random seed={seed}: H={H} dh={dh} {dt} slope={slope} "
+              f"N={N} E={E} Uk={Uk} Uv={Uv}")
+    base = 9900 + 8 * seed
+    o = dict(Q=_randn((N, H, dh), dt, "cuda", base), K=_randn((Uk, H, dh), dt, "cuda", base + 1),
+             V=_randn((Uv, H, dh), dt, "cuda", base + 2), dO=_randn((N, H, dh), dt, "cuda", base + 3))
+    scale = float(np.float32(1 / np.sqrt(dh)))
+    d_off, d_k, d_v = to_dev(off), to_dev(kidx), to_dev(vidx)
+    g = fast.tcsr(d_off, E)
+    tt = tdtype(dt)
+    out = torch.empty((N, H, dh), dtype=tt, device="cuda")
+    lse = torch.empty((N, H), device="cuda")
+    fast.fast_edge_attention_fwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v, Uv,
+                                         scale, slope, out, lse)
+    dQ = torch.empty((N, H, dh), dtype=tt, device="cuda")
+    dKe = torch.empty((max(E, 1), H, dh), dtype=tt, device="cuda")
+    dVe = torch.empty((max(E, 1), H, dh), dtype=tt, device="cuda")
+    fast.fast_edge_attention_bwd_indexed(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"], d_v,
+                                         Uv, scale, slope, lse, o["dO"], dQ, dKe, dVe)
+    dQc = torch.empty((N, H, dh), dtype=tt, device="cuda")
+    ge = torch.empty((max(E, 1), H), device="cuda")
+    ae = torch.empty((max(E, 1), H), device="cuda")
+    fast.fast_edge_attention_bwd_indexed_coef(g, H, dh, DT[dt], o["Q"], o["K"], d_k, Uk, o["V"],
+                                              d_v, Uv, scale, slope, lse, o["dO"], dQc, ge, ae)
+    torch.cuda.synchronize()
+    what = f"indexed random seed={seed}"
+    ins = dict(Q=_cpu(o["Q"]), dO=_cpu(o["dO"]),
+               K=_cpu(o["K"][d_k.long()]), V=_cpu(o["V"][d_v.long()]))
+    check_attention_block_full(off, ins, [_cpu(t) for t in (out, lse, dQ, dKe[:E], dVe[:E])], None,
+                               None, scale, slope, dt, what)
+    assert torch.equal(dQ, dQc), "coefficient-form dQ differs from the per-edge backward's"
+    for name, idx, U, per_edge in (("K", kidx, Uk, dKe[:E]), ("V", vidx, Uv, dVe[:E])):
+        occ_off, occ = _occ_gpu(idx, U)
+        _rows_full(occ_off, occ, idx, U, E, per_edge, H, dh, f"{what} d{name}")
+
+
 def test_identity_index_equals_plain_operator():
     _announce("indexed attention with identity index vs plain")
     b = make_batch(1)
