@@ -155,6 +155,21 @@ fast_status_t attn_run(const char* fn, Op op, const fast_tcsr_t* g, int H, int d
       a.L.SPB = wg / a.L.G;
     }
   }
+  // Backward workgroups: ATT_BLOCK_BWD (512) threads for the row-major lanes
+  // on large grids, ATT_BLOCK (256) otherwise.  Measured on MI355X: the fp32
+  // row-major layer-1 backward of the 1e7-node batch 0.80 ms at 512 against
+  // 0.83 at 256; the bf16 head-major one of the large batch 0.92 at 256
+  // against 0.93; layer-2 blocks (fewer than 4096 workgroups of 512) 0.079
+  // against 0.084 ms at 256, whose last round of workgroups ends sooner.  A
+  // segment's lanes and arithmetic do not depend on the workgroup size.
+  const bool bwd_op = op == Op::kAttnBwd || op == Op::kAttnBwdIdx;
+  if (bwd_op && a.L.block == ATT_BLOCK_BWD && a.L.G <= ATT_BLOCK) {
+    const int64_t wgs_large = (g->num_dst + ATT_BLOCK_BWD / a.L.G - 1) / (ATT_BLOCK_BWD / a.L.G);
+    if (!(a.L.rm && wgs_large >= 4096)) {
+      a.L.block = ATT_BLOCK;
+      a.L.SPB = ATT_BLOCK / a.L.G;
+    }
+  }
   // Non-temporal streaming only when every per-edge row starts and ends on a
   // cache line, so no two rows share a line.
   a.L.nt = (size_t(a.L.F) * elem_size(dt)) % CACHE_LINE == 0;
