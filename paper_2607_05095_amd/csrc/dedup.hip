@@ -483,15 +483,19 @@ constexpr int GATHER_U = 1;
 // Row moves with an optional streaming (non-temporal) policy: a gathered row
 // is read once and written once per call.  Measured on MI355X, streaming paid
 // for 16-byte moves (bigdedup nodes 0.144 -> 0.125 ms, edges 0.307 -> 0.288
-// ms, large nodes 0.171 -> 0.159 ms).  8-byte moves (344-byte rows) stream
-// their stores whatever NT says: alone the copy runs the same (0.704-0.710
-// ms, large edges), but it leaves no dirty lines for the attention that
-// follows it in the step to write back (large step 2.626 -> 2.557 ms, its
-// layer-1 forward 0.486 -> 0.453 ms).
+// ms, large nodes 0.171 -> 0.159 ms) and for 8-byte moves (344-byte rows of
+// the large batch's edges: the whole call 0.688 -> 0.661 ms with streaming
+// loads, step 2.548 -> 2.530 ms).  8-byte moves stream their stores whatever
+// NT says: alone the copy runs the same, but it leaves no dirty lines for the
+// attention that follows it in the step to write back (large step 2.626 ->
+// 2.557 ms, its layer-1 forward 0.486 -> 0.453 ms).
 template <typename V, bool NT>
 __device__ __forceinline__ V gather_ld(const V* p) {
   if constexpr (NT && sizeof(V) == 16) {
     const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return __builtin_bit_cast(V, x);
+  } else if constexpr (NT && sizeof(V) == 8) {
+    const u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
     return __builtin_bit_cast(V, x);
   } else {
     return *p;
@@ -642,7 +646,7 @@ static void launch_gather(const int64_t* uni, const int64_t* num_unique, const v
   if (DD_THREADS % cpr != 0) {
     int64_t nbc = (cap + GATHER_CHUNK - 1) / GATHER_CHUNK;
     if (nbc > FAST_GATHER_MAX_WG) nbc = FAST_GATHER_MAX_WG;
-    if (sizeof(V) == 16 && gather_stream_enabled())
+    if ((sizeof(V) == 16 || sizeof(V) == 8) && gather_stream_enabled())
       hipLaunchKernelGGL((k_gather_chunk<V, true, GATHER_CHUNK>), dim3(uint32_t(nbc)),
                          dim3(DD_THREADS), 0, st, uni, num_unique, static_cast<const V*>(table),
                          table_rows, cpr, slots, static_cast<V*>(rows), flags);
