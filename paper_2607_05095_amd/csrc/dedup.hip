@@ -14,12 +14,12 @@
 //     no atomics at all;
 //   * buckets (sparse universes): each workgroup merges its 2048 ids per
 //     bitmap word in an LDS hash table, counts its merged words per universe
-//     bucket (at most 4096 buckets of at most 2^19 ids), and after a scan of
-//     those counts lists them grouped by bucket; one workgroup per bucket
-//     then ORs its list into an LDS bitmap and writes the bucket's word
-//     records, ranked inside the bucket, and a scan over the bucket totals
-//     gives each bucket's base rank.  Only LDS atomics; every word record is
-//     written once, with no clearing pass;
+//     bucket (at most 4096 buckets of at most 2^19 ids) and writes them to
+//     its own stage region grouped by bucket; one workgroup per bucket then
+//     ORs the bucket's runs of every workgroup into an LDS bitmap and writes
+//     the bucket's word records, ranked inside the bucket, and a scan over
+//     the bucket totals gives each bucket's base rank.  Only LDS atomics;
+//     every word record is written once, with no clearing pass;
 //   * hashed atomics (universes too large for buckets, or batches with more
 //     than 2^24 (bucket, workgroup) counts): the same LDS merge, then one
 //     global atomicOr per merged word into a cleared bitmap.
@@ -107,11 +107,10 @@ struct DedupWs {
   uint8_t* flags;     // [n] miss flags
   int32_t* slots;     // [n] table slot of each unique id (with a slot map)
   void* scan_n;       // scan workspace over n flags
-  uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup), then list offsets
-  void* bk_scan_c;    // scan workspace over the counts
-  uint2* bk_list;     // [<= n] (word inside the bucket, bits), grouped by bucket
+  uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup)
+  uint32_t* bk_loff;  // [B x nblk] start of the (bucket, workgroup) run in its workgroup's stage
+  uint2* bk_stage;    // [nblk x MARK_IDS] each workgroup's (word in bucket, bits), grouped by bucket
   uint32_t* bk_base;  // [B + 1] distinct ids per bucket, then the bucket's base rank (and u)
-  int32_t* bk_listed; // number of list entries
 };
 
 static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws) {
@@ -132,11 +131,12 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
   char* sl = take(size_t(n) * 4);
   char* sn = take(scan_workspace(n));
   char* bc = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
-  char* bs = take(bk ? scan_workspace(p.B * p.nblk) : 0);
-  char* bl = take(bk ? size_t(n) * 8 : 0);
+  char* lo = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
+  char* sg = take(bk ? size_t(p.nblk) * MARK_IDS * 8 : 0);
   char* bb = take(bk ? size_t(p.B + 1) * 4 : 0);
-  char* bn = take(bk ? 4 : 0);
   if (ws) {
+    ws->bk_loff = reinterpret_cast<uint32_t*>(lo);
+    ws->bk_stage = reinterpret_cast<uint2*>(sg);
     ws->bytemap = reinterpret_cast<uint8_t*>(by);
     ws->words = reinterpret_cast<uint2*>(wr);
     ws->scan_w = sw;
@@ -144,10 +144,7 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     ws->slots = reinterpret_cast<int32_t*>(sl);
     ws->scan_n = sn;
     ws->bk_count = reinterpret_cast<uint32_t*>(bc);
-    ws->bk_scan_c = bs;
-    ws->bk_list = reinterpret_cast<uint2*>(bl);
     ws->bk_base = reinterpret_cast<uint32_t*>(bb);
-    ws->bk_listed = reinterpret_cast<int32_t*>(bn);
   }
   return off;
 }
@@ -286,16 +283,20 @@ __device__ __forceinline__ void merge_words(const int64_t* __restrict__ ids, int
   __syncthreads();
 }
 
-// Bucketed marking, counting pass: workgroup g merges its ids by word and
-// counts its merged words per bucket (bucket = word >> wshift) into
-// count[b * nblk + g], so that an exclusive scan of `count` in index order
-// gives every (bucket, workgroup) pair the start of its run in the list.
-__global__ void __launch_bounds__(DD_THREADS) k_bk_count(const int64_t* __restrict__ ids, int64_t n,
+// Bucketed marking, staged form: workgroup g merges its ids by word once,
+// counts the merged words per bucket, and writes them to its own stage
+// region grouped by bucket (run of bucket b at loff[b * nblk + g], count[b *
+// nblk + g] entries), so that no scan of the counts and no second merge are
+// needed before the buckets are marked.
+__global__ void __launch_bounds__(DD_THREADS) k_bk_stage(const int64_t* __restrict__ ids, int64_t n,
                                                          int64_t id_bound, int wshift, int B,
-                                                         int nblk, uint32_t* __restrict__ count) {
+                                                         int nblk, uint32_t* __restrict__ count,
+                                                         uint32_t* __restrict__ loff,
+                                                         uint2* __restrict__ stage) {
   __shared__ uint32_t keys[MARK_SLOTS];
   __shared__ uint32_t bits[MARK_SLOTS];
   __shared__ uint32_t h[BK_MAX_BUCKETS];
+  __shared__ uint32_t lds4[4];
   for (int b = threadIdx.x; b < B; b += DD_THREADS) h[b] = 0u;
   merge_words(ids, n, id_bound, keys, bits);
   for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
@@ -303,40 +304,50 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_count(const int64_t* __restri
     if (w != MARK_EMPTY) atomicAdd(&h[w >> wshift], 1u);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < B; b += DD_THREADS) count[int64_t(b) * nblk + blockIdx.x] = h[b];
-}
-
-// Bucketed marking, listing pass: the same merge, and each merged word goes
-// to its (bucket, workgroup) run as (word inside the bucket, bits); the order
-// inside a run is whatever the LDS atomics give (marking does not use it).
-__global__ void __launch_bounds__(DD_THREADS) k_bk_list(const int64_t* __restrict__ ids, int64_t n,
-                                                        int64_t id_bound, int wshift, int B,
-                                                        int nblk, const uint32_t* __restrict__ start,
-                                                        uint2* __restrict__ list) {
-  __shared__ uint32_t keys[MARK_SLOTS];
-  __shared__ uint32_t bits[MARK_SLOTS];
-  __shared__ uint32_t cur[BK_MAX_BUCKETS];
-  for (int b = threadIdx.x; b < B; b += DD_THREADS) cur[b] = start[int64_t(b) * nblk + blockIdx.x];
-  merge_words(ids, n, id_bound, keys, bits);
+  // exclusive prefix of h over the buckets: thread t owns buckets
+  // [t PER, (t + 1) PER); h becomes the run cursors
+  constexpr int PER = BK_MAX_BUCKETS / DD_THREADS;
+  const int b0 = threadIdx.x * PER;
+  uint32_t c[PER], sum = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    c[k] = b0 + k < B ? h[b0 + k] : 0u;
+    sum += c[k];
+  }
+  uint32_t tot;
+  uint32_t run = block_exclusive_scan(sum, lds4, tot);
+  __syncthreads();                                   // every h read before it is rewritten
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (b0 + k < B) {
+      count[int64_t(b0 + k) * nblk + blockIdx.x] = c[k];
+      loff[int64_t(b0 + k) * nblk + blockIdx.x] = run;
+      h[b0 + k] = run;
+    }
+    run += c[k];
+  }
+  __syncthreads();
   const uint32_t low = (1u << wshift) - 1u;
+  uint2* __restrict__ mine = stage + int64_t(blockIdx.x) * MARK_IDS;
   for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
     const uint32_t w = keys[s];
     if (w != MARK_EMPTY) {
-      const uint32_t pos = atomicAdd(&cur[w >> wshift], 1u);
-      list[pos] = make_uint2(w & low, bits[s]);
+      const uint32_t pos = atomicAdd(&h[w >> wshift], 1u);
+      mine[pos] = make_uint2(w & low, bits[s]);
     }
   }
 }
 
 // Bucketed marking, one workgroup per bucket of 2^wshift words: OR the
-// bucket's list into an LDS bitmap, then write every record of the bucket
+// bucket's run of every workgroup's stage into an LDS bitmap, then write
+// every record of the bucket
 // below W with its rank inside the bucket -- each thread takes 4 consecutive
 // words per block-wide scan (1024 words per scan) and stores them as two
 // 16-byte records pairs -- and leave the bucket's distinct-id count in
 // total[b].
-__global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict__ list,
-                                                        const uint32_t* __restrict__ start, int nblk,
-                                                        int B, const int32_t* __restrict__ listed,
+__global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint32_t* __restrict__ count,
+                                                        const uint32_t* __restrict__ loff,
+                                                        const uint2* __restrict__ stage, int nblk,
                                                         int wshift, int64_t W,
                                                         uint2* __restrict__ words,
                                                         uint32_t* __restrict__ total) {
@@ -347,19 +358,38 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict_
   const int b = blockIdx.x;
   for (int j = threadIdx.x; j < WB; j += DD_THREADS) bm[j] = 0u;
   __syncthreads();
-  const uint32_t s = nblk ? start[int64_t(b) * nblk] : 0u;
-  const uint32_t e = b + 1 < B ? (nblk ? start[int64_t(b + 1) * nblk] : 0u) : uint32_t(*listed);
-  constexpr int U = 8;   // list entries per thread in flight before the ORs
-  for (uint32_t i0 = s; i0 < e; i0 += U * DD_THREADS) {
-    uint2 x[U];
+  {
+    // thread t ORs the runs of workgroups t, t + 256, ...; the
+    // heads of 4 runs are loaded together, then the first 8 entries of all
+    // 4 runs, then the ORs (runs hold about 4 entries: n / (nblk B))
+    constexpr int G = 4, J = 8;
+    for (int g0 = threadIdx.x; g0 < nblk; g0 += G * DD_THREADS) {
+      uint32_t cnt[G], at[G];
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const uint32_t i = i0 + k * DD_THREADS + threadIdx.x;
-      x[k] = i < e ? list[i] : make_uint2(0u, 0u);
-    }
+      for (int k = 0; k < G; ++k) {
+        const int g = g0 + k * DD_THREADS;
+        cnt[k] = g < nblk ? count[int64_t(b) * nblk + g] : 0u;
+        at[k] = g < nblk ? loff[int64_t(b) * nblk + g] : 0u;
+      }
+      uint2 x[G][J];
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      if (x[k].y) atomicOr(&bm[x[k].x], x[k].y);
+      for (int k = 0; k < G; ++k)
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          x[k][j] = uint32_t(j) < cnt[k]
+                        ? stage[int64_t(g0 + k * DD_THREADS) * MARK_IDS + at[k] + j]
+                        : make_uint2(0u, 0u);
+#pragma unroll
+      for (int k = 0; k < G; ++k)
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          if (x[k][j].y) atomicOr(&bm[x[k][j].x], x[k][j].y);
+#pragma unroll
+      for (int k = 0; k < G; ++k)
+        for (uint32_t i = J; i < cnt[k]; ++i) {
+          const uint2 y = stage[int64_t(g0 + k * DD_THREADS) * MARK_IDS + at[k] + i];
+          atomicOr(&bm[y.x], y.y);
+        }
     }
   }
   __syncthreads();
@@ -386,15 +416,6 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint2* __restrict_
   }
   if (threadIdx.x == 0) total[b] = carry;
 }
-
-struct BkIn {
-  const uint32_t* p;
-  __device__ uint32_t operator()(int64_t i) const { return p[i]; }
-};
-struct BkOutInPlace {
-  uint32_t* p;
-  __device__ void operator()(int64_t i, uint32_t prefix, uint32_t) const { p[i] = prefix; }
-};
 
 struct InPopc {
   const uint2* wr;
@@ -716,19 +737,12 @@ static fast_status_t dedup_gather_run(const char* fn, const int64_t* ids, int64_
   if (path == MARK_BUCKETS) {
     const int B = int(p.B), nblk = int(p.nblk);
     if (nblk > 0) {
-      hipLaunchKernelGGL(k_bk_count, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
-                         wshift, B, nblk, w.bk_count);
-    }
-    e = scan_launch(BkIn{w.bk_count}, BkOutInPlace{w.bk_count}, p.B * p.nblk, w.bk_scan_c, nullptr,
-                    w.bk_listed, st);
-    if (e != hipSuccess) return fail(FAST_ERR_HIP, "%s: %s", fn, hipGetErrorString(e));
-    if (nblk > 0) {
-      hipLaunchKernelGGL(k_bk_list, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
-                         wshift, B, nblk, w.bk_count, w.bk_list);
+      hipLaunchKernelGGL(k_bk_stage, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
+                         wshift, B, nblk, w.bk_count, w.bk_loff, w.bk_stage);
     }
     if (B > 0) {
-      hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_list, w.bk_count,
-                         nblk, B, w.bk_listed, wshift, W, w.words, w.bk_base);
+      hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_count, w.bk_loff,
+                         w.bk_stage, nblk, wshift, W, w.words, w.bk_base);
     }
     // at most 4096 bucket totals: one workgroup scans them in place
     hipLaunchKernelGGL(k_scan_top<uint32_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.bk_base, p.B,
