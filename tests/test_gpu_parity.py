@@ -437,6 +437,36 @@ def test_csr_offsets_batched_bit_exact(case):
         assert np.array_equal(got, oracle.csr_offsets(c)), f"block {k}"
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_csr_offsets_random(seed):
+    """Seeded random layer-block sets: 1 to 12 blocks of 0 to 5e6 segments
+    (one, two or three scan launches; blocks beyond the 8 of one batched
+    launch pair and beyond 2048 tiles), degrees up to 60 with empty
+    segments; the batched and the single-block scans bit-exact against the
+    oracle."""
+    r = np.random.default_rng(9700 + seed)
+    k = int(r.integers(1, 13))
+    lists = []
+    for _ in range(k):
+        n = int(r.choice([0, int(r.integers(1, 3000)), int(r.integers(3000, 300_000)),
+                          int(r.integers(4_200_000, 5_000_000))], p=[0.1, 0.4, 0.4, 0.1]))
+        c = r.integers(0, 61, n).astype(np.int32)
+        c[r.random(n) < 0.1] = 0
+        lists.append(c)
+    _announce(f"offsets random seed={seed}: blocks {[x.size for x in lists]}")
+    for i, (got, c) in enumerate(zip(_offsets_batched(lists), lists)):
+        assert np.array_equal(got, oracle.csr_offsets(c)), f"batched block {i}"
+    for i, c in enumerate(lists[:3]):
+        n = c.size
+        d_c = to_dev(c) if n else torch.zeros(1, dtype=torch.int32, device="cuda")
+        out = torch.full((n + 1,), -7, dtype=torch.int32, device="cuda")
+        wsb = fast.fast_csr_offsets_workspace(n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        fast.fast_csr_offsets(d_c, n, out, ws, wsb)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), oracle.csr_offsets(c)), f"single block {i}"
+
+
 def _te_block_dev(off, dst_t, edge_t):
     d_off, d_dst, d_e = to_dev(off), to_dev(dst_t), to_dev(edge_t)
     return fast.tcsr(d_off, edge_t.shape[0], edge_t=d_e, dst_t=d_dst), (d_off, d_dst, d_e)
