@@ -558,7 +558,7 @@ def hot_set_ops(b, torch, fast, num_batches=8, alpha=0.01, reps=3, with_oracle=F
         n = int(ids.numel())
         res[f"access_count_{kind}"] = {
             "ms": round(ms, 4), "ids": n, "id_bound": bound, "batches": num_batches,
-            "bound": "random 4-byte atomics (one exchange per id, one add per distinct id)",
+            "bound": "random 4-byte atomics (one mask OR per id, one add per distinct id and batch)",
             "ids_per_s": round(n / (ms * 1e-3), 1),
         }
         if with_oracle:

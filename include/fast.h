@@ -243,8 +243,9 @@ fast_status_t fast_sample_recent(const fast_temporal_graph_t* g, const int64_t* 
  * non-decreasing; freq: device int32 [id_bound].  A few launches per batch.
  * Limits: id_bound < 2^32, num_batches < 2^31 - 1.
  * Workspace: fast_access_count_workspace(id_bound) bytes, 16-byte aligned
- *   (a batch stamp per id; for dense universes, id_bound at most 32 times the
- *   mean batch size, the same space holds a byte map per batch instead).
+ *   (a byte of batch bits per id for up to 32 batches, else a batch stamp
+ *   per id; for dense universes, id_bound at most 32 times the mean batch
+ *   size, the same space holds a byte map per batch instead).
  * ------------------------------------------------------------------------ */
 size_t fast_access_count_workspace(int64_t id_bound);
 fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets,

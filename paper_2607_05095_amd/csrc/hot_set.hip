@@ -4,11 +4,13 @@
 // row reconstruction reads.
 //
 // Counting.  Every batch adds one to the counter of each distinct id it
-// touches.  One launch per batch; each id stamps its slot with the batch tag
-// (atomicExch), and only the access that replaces an older tag increments
-// the counter, so repeats inside a batch count once.  Integer atomics make
-// the counts exact whatever the interleaving; an LDS hash per workgroup
-// drops most repeats before they reach HBM.
+// touches.  One launch per batch; each id sets its batch's bit in a byte per
+// id (atomicOr; up to 32 batches, in groups of 8 with a clear per group) or
+// stamps its slot with the batch tag (atomicExch; more batches), and only the
+// access that finds the bit clear or replaces an older tag increments the
+// counter, so repeats inside a batch count once.  Integer atomics make the
+// counts exact whatever the interleaving; an LDS hash per workgroup drops
+// most repeats before they reach HBM.
 //
 // Selection.  Alg. 1 ranks each kind by descending count and merges the two
 // lists, a node winning only with a strictly higher count.  The ids it takes
@@ -57,13 +59,34 @@ constexpr int HS_PROBES = 32;
 constexpr uint32_t HS_EMPTY = 0xffffffffu;  // never an id: id_bound < 2^32
 
 // Marks id x for batch `tag`; counts it if the batch had not marked it yet.
-__device__ __forceinline__ void stamp_and_count(int64_t x, int32_t tag, int32_t* stamp,
-                                                int32_t* freq) {
-  // read the stamp in L2 first; a stale read falls through to the exchange,
-  // which decides exactly
-  if (__hip_atomic_load(&stamp[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == tag) return;
-  if (atomicExch(&stamp[x], tag) != tag) atomicAdd(&freq[x], 1);
-}
+struct StampCount {
+  int32_t tag;
+  int32_t* stamp;
+  int32_t* freq;
+  __device__ void operator()(int64_t x) const {
+    // read the stamp in L2 first; a stale read falls through to the exchange,
+    // which decides exactly
+    if (__hip_atomic_load(&stamp[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == tag) return;
+    if (atomicExch(&stamp[x], tag) != tag) atomicAdd(&freq[x], 1);
+  }
+};
+
+// The same with one bit per id and batch of a group of up to 8 batches (a
+// byte per id, four ids to a 32-bit word): the batch's bit is set by an
+// atomic OR, and the access that finds it clear counts the id.  The mask map
+// is a quarter of the stamps, so clearing it once per group costs less.
+constexpr int AC_GROUP = 8;
+struct MaskCount {
+  uint32_t bit;        // 1 << (batch index within its group)
+  uint32_t* mask32;
+  int32_t* freq;
+  __device__ void operator()(int64_t x) const {
+    uint32_t* w = &mask32[x >> 2];
+    const uint32_t b = bit << (8 * (x & 3));
+    if (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & b) return;
+    if (!(atomicOr(w, b) & b)) atomicAdd(&freq[x], 1);
+  }
+};
 
 // A hot id repeats thousands of times in a batch.  Each workgroup takes
 // HS_CHUNK ids at a time and drops repeats inside the chunk through an LDS
@@ -71,10 +94,9 @@ __device__ __forceinline__ void stamp_and_count(int64_t x, int32_t tag, int32_t*
 // empty slot), so only an id's first occurrence in the chunk touches HBM.
 // A probe sequence that finds no room also goes to HBM: the stamp there
 // decides exactly, the hash is only a filter.
+template <typename Act>
 __global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __restrict__ ids,
-                                                            int64_t n, int64_t id_bound,
-                                                            int32_t tag, int32_t* stamp,
-                                                            int32_t* freq) {
+                                                            int64_t n, int64_t id_bound, Act act) {
   __shared__ uint32_t s_key[HS_HASH];
   for (int64_t c0 = int64_t(blockIdx.x) * HS_CHUNK; c0 < n; c0 += int64_t(gridDim.x) * HS_CHUNK) {
     for (int j = threadIdx.x; j < HS_HASH; j += HS_THREADS) s_key[j] = HS_EMPTY;
@@ -96,7 +118,7 @@ __global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __re
         }
         h = (h + 1) & (HS_HASH - 1);
       }
-      if (first) stamp_and_count(x, tag, stamp, freq);
+      if (first) act(x);
     }
     __syncthreads();
   }
@@ -145,6 +167,17 @@ static bool use_count_bytemap(int64_t total_ids, int64_t num_batches, int64_t id
   if (mode) return mode == 1;
   const int64_t mean = num_batches > 0 ? total_ids / num_batches : 0;
   return id_bound <= AC_BYTEMAP_RATIO * (mean > 0 ? mean : 1);
+}
+
+// Masks for up to 32 batches (at most four clears of a byte per id, no
+// more than the one clear of a 4-byte stamp per id); stamps beyond.
+static bool count_masks(int64_t num_batches) {
+  static const int mode = [] {
+    const char* e = std::getenv("FAST_COUNT_MASKS");   // tuning override: 0 stamps, 1 masks
+    return e ? (std::strcmp(e, "0") == 0 ? 0 : 1) : -1;
+  }();
+  if (mode >= 0) return mode == 1;
+  return num_batches <= 4 * AC_GROUP;
 }
 
 // ------------------------------------------------------------------ selection
@@ -754,14 +787,33 @@ extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* ba
     }
     return check_launch(fn);
   }
+  if (count_masks(num_batches)) {
+    if (!aligned(ws, 16)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 16-byte aligned", fn);
+    uint32_t* mask32 = static_cast<uint32_t*>(ws);
+    const int64_t n16 = (id_bound + 15) / 16;          // within the id_bound * 4 + 256 bytes
+    for (int64_t g0 = 0; g0 < num_batches; g0 += AC_GROUP) {
+      const int64_t g1 = g0 + AC_GROUP < num_batches ? g0 + AC_GROUP : num_batches;
+      if (batch_offsets[g1] == batch_offsets[g0]) continue;
+      hipLaunchKernelGGL(k_ac_clear, dim3(grid_for(n16, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
+                         reinterpret_cast<uint4*>(mask32), n16);
+      for (int64_t k = g0; k < g1; ++k) {
+        const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
+        if (n == 0) continue;
+        hipLaunchKernelGGL((k_access_count<MaskCount>), dim3(grid_for(n, HS_CHUNK)), dim3(HS_THREADS),
+                           0, st, ids + batch_offsets[k], n, id_bound,
+                           MaskCount{1u << uint32_t(k - g0), mask32, freq});
+      }
+    }
+    return check_launch(fn);
+  }
   int32_t* stamp = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(k_hs_fill_i32, dim3(grid_for(id_bound, HS_THREADS * 8)), dim3(HS_THREADS), 0,
                      st, stamp, id_bound, 0);
   for (int64_t k = 0; k < num_batches; ++k) {
     const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
     if (n == 0) continue;
-    hipLaunchKernelGGL(k_access_count, dim3(grid_for(n, HS_CHUNK)), dim3(HS_THREADS), 0, st,
-                       ids + batch_offsets[k], n, id_bound, int32_t(k + 1), stamp, freq);
+    hipLaunchKernelGGL((k_access_count<StampCount>), dim3(grid_for(n, HS_CHUNK)), dim3(HS_THREADS), 0,
+                       st, ids + batch_offsets[k], n, id_bound, StampCount{int32_t(k + 1), stamp, freq});
   }
   return check_launch(fn);
 }
