@@ -63,8 +63,11 @@ def _check_slots(slot, hot, n):
     assert np.array_equal(slot.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("cfg,k", [(2, 12), (3, 4), (1, 6)])
+@pytest.mark.parametrize("cfg,k", [(2, 12), (3, 4), (1, 6), (2, 40)])
 def test_access_count_and_selection_vs_oracle(cfg, k):
+    """cfg 2's edge ids are counted in the sparse form: 12 batches with batch
+    bits in two groups, 40 batches with stamps; the other universes are dense
+    (a byte map per batch)."""
     nodes, edges, nb, eb = presampled_ids(cfg, k)
     _announce(f"hot set cfg={cfg} batches={k} |V|={nb} |E|={eb}")
     fv = _count_gpu(nodes, nb)
