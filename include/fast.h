@@ -245,7 +245,7 @@ fast_status_t fast_sample_recent(const fast_temporal_graph_t* g, const int64_t* 
  * Workspace: fast_access_count_workspace(id_bound) bytes, 16-byte aligned
  *   (a byte of batch bits per id for up to 32 batches, else a batch stamp
  *   per id; for dense universes, id_bound at most 32 times the mean batch
- *   size, the same space holds a byte map per batch instead).
+ *   size, the same space holds up to four byte maps, one per batch).
  * ------------------------------------------------------------------------ */
 size_t fast_access_count_workspace(int64_t id_bound);
 fast_status_t fast_access_count(const int64_t* ids, const int64_t* batch_offsets,

@@ -126,10 +126,13 @@ __global__ void __launch_bounds__(HS_THREADS) k_access_count(const int64_t* __re
 
 // Dense universes (id_bound at most AC_BYTEMAP_RATIO times the mean batch
 // size): each batch marks its ids in a byte map with plain stores (repeats
-// store the same 1), then one streaming pass adds the map into freq -- no
-// atomics at all.  The map lives in the stamp workspace (1 byte per id of the
-// 4 there) and is cleared before every batch.
+// store the same 1), then a streaming pass adds the maps into freq -- no
+// atomics at all.  The workspace (4 bytes per id) holds AC_PLANES such maps:
+// a group of up to 4 batches is cleared once, marks one map each, and one
+// pass adds all of them (bytes of 0 or 1, so the 32-bit sum of the maps'
+// words holds each id's count in its byte).
 constexpr int64_t AC_BYTEMAP_RATIO = 32;
+constexpr int AC_PLANES = 4;
 
 __global__ void __launch_bounds__(HS_THREADS) k_ac_clear(uint4* p, int64_t n16) {
   for (int64_t i = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; i < n16;
@@ -145,16 +148,20 @@ __global__ void __launch_bounds__(HS_THREADS) k_ac_mark(const int64_t* __restric
   if (x >= 0 && x < id_bound) map[x] = 1;
 }
 
-// freq[x] += map[x], four ids per thread; bytes past id_bound are never set.
+// freq[x] += sum over the np maps of map_p[x], four ids per thread (maps
+// n4 words apart); bytes past id_bound are never set.
 __global__ void __launch_bounds__(HS_THREADS) k_ac_accumulate(const uint32_t* __restrict__ map4,
-                                                             int64_t n4, int32_t* freq) {
+                                                             int64_t n4, int np, int32_t* freq) {
   for (int64_t t = int64_t(blockIdx.x) * HS_THREADS + threadIdx.x; t < n4;
        t += int64_t(gridDim.x) * HS_THREADS) {
-    const uint32_t m = map4[t];
+    uint32_t m = 0u;
+    for (int p = 0; p < np; ++p) m += map4[int64_t(p) * n4 + t];
     if (m == 0u) continue;
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if ((m >> (8 * k)) & 0xffu) freq[4 * t + k] += 1;
+    for (int k = 0; k < 4; ++k) {
+      const int c = int((m >> (8 * k)) & 0xffu);
+      if (c) freq[4 * t + k] += c;
+    }
   }
 }
 
@@ -774,16 +781,23 @@ extern "C" fast_status_t fast_access_count(const int64_t* ids, const int64_t* ba
   if (use_count_bytemap(batch_offsets[num_batches] - batch_offsets[0], num_batches, id_bound)) {
     if (!aligned(ws, 16)) return fail(FAST_ERR_UNSUPPORTED, "%s: workspace not 16-byte aligned", fn);
     uint8_t* map = static_cast<uint8_t*>(ws);
-    const int64_t n16 = (id_bound + 15) / 16;          // within the id_bound * 4 + 256 bytes
-    for (int64_t k = 0; k < num_batches; ++k) {
-      const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
-      if (n == 0) continue;
-      hipLaunchKernelGGL(k_ac_clear, dim3(grid_for(n16, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
-                         reinterpret_cast<uint4*>(map), n16);
-      hipLaunchKernelGGL(k_ac_mark, dim3(uint32_t((n + HS_THREADS - 1) / HS_THREADS)), dim3(HS_THREADS),
-                         0, st, ids + batch_offsets[k], n, id_bound, map);
+    // AC_PLANES maps of n16 16-byte vectors: within the id_bound * 4 + 256 bytes
+    const int64_t n16 = (id_bound + 15) / 16;
+    for (int64_t g0 = 0; g0 < num_batches; g0 += AC_PLANES) {
+      const int64_t g1 = g0 + AC_PLANES < num_batches ? g0 + AC_PLANES : num_batches;
+      if (batch_offsets[g1] == batch_offsets[g0]) continue;
+      const int np = int(g1 - g0);
+      hipLaunchKernelGGL(k_ac_clear, dim3(grid_for(n16 * np, HS_THREADS * 4)), dim3(HS_THREADS), 0, st,
+                         reinterpret_cast<uint4*>(map), n16 * np);
+      for (int64_t k = g0; k < g1; ++k) {
+        const int64_t n = batch_offsets[k + 1] - batch_offsets[k];
+        if (n == 0) continue;
+        hipLaunchKernelGGL(k_ac_mark, dim3(uint32_t((n + HS_THREADS - 1) / HS_THREADS)),
+                           dim3(HS_THREADS), 0, st, ids + batch_offsets[k], n, id_bound,
+                           map + (k - g0) * n16 * 16);
+      }
       hipLaunchKernelGGL(k_ac_accumulate, dim3(grid_for(n16 * 4, HS_THREADS * 4)), dim3(HS_THREADS), 0,
-                         st, reinterpret_cast<const uint32_t*>(map), n16 * 4, freq);
+                         st, reinterpret_cast<const uint32_t*>(map), n16 * 4, np, freq);
     }
     return check_launch(fn);
   }
