@@ -186,7 +186,7 @@ fast_status_t fast_dedup_gather(const int64_t* ids, int64_t n, int64_t id_bound,
  *   - Size limit: problems whose fast_dedup_gather_workspace(n, id_bound)
  *     exceeds FAST_NOALLOC_SCRATCH_BYTES return FAST_ERR_UNSUPPORTED before
  *     anything is enqueued (every dedup of the 1e7-node / 2e8-edge batches
- *     fits: at most 89 MB).
+ *     fits: at most 86 MB).
  *   - Device: the stream (NULL = the null stream) must belong to the current
  *     device; the scratch of that device is used (FAST_ERR_INVALID_ARG
  *     otherwise).

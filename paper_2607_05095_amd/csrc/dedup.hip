@@ -107,8 +107,7 @@ struct DedupWs {
   uint8_t* flags;     // [n] miss flags
   int32_t* slots;     // [n] table slot of each unique id (with a slot map)
   void* scan_n;       // scan workspace over n flags
-  uint32_t* bk_count; // [B x nblk] merged words per (bucket, workgroup)
-  uint32_t* bk_loff;  // [B x nblk] start of the (bucket, workgroup) run in its workgroup's stage
+  uint16_t* bk_loff;  // [nblk x (B + 1)] start of each bucket's run in workgroup g's stage, then its total
   uint2* bk_stage;    // [nblk x MARK_IDS] each workgroup's (word in bucket, bits), grouped by bucket
   uint32_t* bk_base;  // [B + 1] distinct ids per bucket, then the bucket's base rank (and u)
 };
@@ -130,12 +129,11 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
   char* fl = take(size_t(n));
   char* sl = take(size_t(n) * 4);
   char* sn = take(scan_workspace(n));
-  char* bc = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
-  char* lo = take(bk ? size_t(p.B * p.nblk) * 4 : 0);
+  char* lo = take(bk ? size_t((p.B + 1) * p.nblk) * 2 : 0);
   char* sg = take(bk ? size_t(p.nblk) * MARK_IDS * 8 : 0);
   char* bb = take(bk ? size_t(p.B + 1) * 4 : 0);
   if (ws) {
-    ws->bk_loff = reinterpret_cast<uint32_t*>(lo);
+    ws->bk_loff = reinterpret_cast<uint16_t*>(lo);
     ws->bk_stage = reinterpret_cast<uint2*>(sg);
     ws->bytemap = reinterpret_cast<uint8_t*>(by);
     ws->words = reinterpret_cast<uint2*>(wr);
@@ -143,7 +141,6 @@ static size_t dedup_layout(int64_t n, int64_t id_bound, char* base, DedupWs* ws)
     ws->flags = reinterpret_cast<uint8_t*>(fl);
     ws->slots = reinterpret_cast<int32_t*>(sl);
     ws->scan_n = sn;
-    ws->bk_count = reinterpret_cast<uint32_t*>(bc);
     ws->bk_base = reinterpret_cast<uint32_t*>(bb);
   }
   return off;
@@ -285,17 +282,20 @@ __device__ __forceinline__ void merge_words(const int64_t* __restrict__ ids, int
 
 // Bucketed marking, staged form: workgroup g merges its ids by word once,
 // counts the merged words per bucket, and writes them to its own stage
-// region grouped by bucket (run of bucket b at loff[b * nblk + g], count[b *
-// nblk + g] entries), so that no scan of the counts and no second merge are
-// needed before the buckets are marked.
+// region grouped by bucket, with the start of every bucket's run (and, at
+// index B, the total) in its own row loff[g (B + 1) ...] -- one contiguous
+// row per workgroup, so the table is written in whole cache lines; a run's
+// length is the difference of two neighbouring starts (at most MARK_IDS, so
+// 16 bits hold them).  No scan of the counts and no second merge are needed
+// before the buckets are marked.
 __global__ void __launch_bounds__(DD_THREADS) k_bk_stage(const int64_t* __restrict__ ids, int64_t n,
                                                          int64_t id_bound, int wshift, int B,
-                                                         int nblk, uint32_t* __restrict__ count,
-                                                         uint32_t* __restrict__ loff,
+                                                         uint16_t* __restrict__ loff,
                                                          uint2* __restrict__ stage) {
+  static_assert(MARK_IDS < 65536, "run starts are 16-bit");
   __shared__ uint32_t keys[MARK_SLOTS];
   __shared__ uint32_t bits[MARK_SLOTS];
-  __shared__ uint32_t h[BK_MAX_BUCKETS];
+  __shared__ uint32_t h[BK_MAX_BUCKETS + 1];
   __shared__ uint32_t lds4[4];
   for (int b = threadIdx.x; b < B; b += DD_THREADS) h[b] = 0u;
   merge_words(ids, n, id_bound, keys, bits);
@@ -305,7 +305,7 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_stage(const int64_t* __restri
   }
   __syncthreads();
   // exclusive prefix of h over the buckets: thread t owns buckets
-  // [t PER, (t + 1) PER); h becomes the run cursors
+  // [t PER, (t + 1) PER); h becomes the run starts, h[B] the total
   constexpr int PER = BK_MAX_BUCKETS / DD_THREADS;
   const int b0 = threadIdx.x * PER;
   uint32_t c[PER], sum = 0;
@@ -319,14 +319,14 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_stage(const int64_t* __restri
   __syncthreads();                                   // every h read before it is rewritten
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
-    if (b0 + k < B) {
-      count[int64_t(b0 + k) * nblk + blockIdx.x] = c[k];
-      loff[int64_t(b0 + k) * nblk + blockIdx.x] = run;
-      h[b0 + k] = run;
-    }
+    if (b0 + k < B) h[b0 + k] = run;
     run += c[k];
   }
+  if (threadIdx.x == 0) h[B] = tot;
   __syncthreads();
+  uint16_t* __restrict__ row = loff + int64_t(blockIdx.x) * (B + 1);
+  for (int b = threadIdx.x; b <= B; b += DD_THREADS) row[b] = uint16_t(h[b]);
+  __syncthreads();                                   // starts stored before h turns into cursors
   const uint32_t low = (1u << wshift) - 1u;
   uint2* __restrict__ mine = stage + int64_t(blockIdx.x) * MARK_IDS;
   for (int s = threadIdx.x; s < MARK_SLOTS; s += DD_THREADS) {
@@ -340,22 +340,23 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_stage(const int64_t* __restri
 
 // Bucketed marking, one workgroup per bucket of 2^wshift words: OR the
 // bucket's run of every workgroup's stage into an LDS bitmap, then write
-// every record of the bucket
-// below W with its rank inside the bucket -- each thread takes 4 consecutive
-// words per block-wide scan (1024 words per scan) and stores them as two
-// 16-byte records pairs -- and leave the bucket's distinct-id count in
-// total[b].
-__global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint32_t* __restrict__ count,
-                                                        const uint32_t* __restrict__ loff,
+// every record of the bucket below W with its rank inside the bucket --
+// each thread takes 4 consecutive words per block-wide scan (1024 words per
+// scan) and stores them as two 16-byte record pairs -- and leave the
+// bucket's distinct-id count in total[b].  Buckets are spread over the XCDs
+// in contiguous ranges (xcd_tile), so the neighbouring buckets that share
+// the cache lines of the run-start rows and of the stage runs read them
+// through the same L2.
+__global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint16_t* __restrict__ loff,
                                                         const uint2* __restrict__ stage, int nblk,
-                                                        int wshift, int64_t W,
+                                                        int B, int wshift, int64_t W,
                                                         uint2* __restrict__ words,
                                                         uint32_t* __restrict__ total) {
   __shared__ uint4 bm4[BK_MAX_WORDS / 4];
   __shared__ uint32_t lds4[4];
   uint32_t* bm = reinterpret_cast<uint32_t*>(bm4);
   const int WB = 1 << wshift;                     // a multiple of 32
-  const int b = blockIdx.x;
+  const int b = int(xcd_tile(blockIdx.x, gridDim.x));
   for (int j = threadIdx.x; j < WB; j += DD_THREADS) bm[j] = 0u;
   __syncthreads();
   {
@@ -368,8 +369,9 @@ __global__ void __launch_bounds__(DD_THREADS) k_bk_mark(const uint32_t* __restri
 #pragma unroll
       for (int k = 0; k < G; ++k) {
         const int g = g0 + k * DD_THREADS;
-        cnt[k] = g < nblk ? count[int64_t(b) * nblk + g] : 0u;
-        at[k] = g < nblk ? loff[int64_t(b) * nblk + g] : 0u;
+        const uint16_t* r = loff + int64_t(g) * (B + 1) + b;
+        at[k] = g < nblk ? r[0] : 0u;
+        cnt[k] = g < nblk ? uint32_t(r[1]) - at[k] : 0u;
       }
       uint2 x[G][J];
 #pragma unroll
@@ -738,11 +740,11 @@ static fast_status_t dedup_gather_run(const char* fn, const int64_t* ids, int64_
     const int B = int(p.B), nblk = int(p.nblk);
     if (nblk > 0) {
       hipLaunchKernelGGL(k_bk_stage, dim3(uint32_t(nblk)), dim3(DD_THREADS), 0, st, ids, n, id_bound,
-                         wshift, B, nblk, w.bk_count, w.bk_loff, w.bk_stage);
+                         wshift, B, w.bk_loff, w.bk_stage);
     }
     if (B > 0) {
-      hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_count, w.bk_loff,
-                         w.bk_stage, nblk, wshift, W, w.words, w.bk_base);
+      hipLaunchKernelGGL(k_bk_mark, dim3(uint32_t(B)), dim3(DD_THREADS), 0, st, w.bk_loff,
+                         w.bk_stage, nblk, B, wshift, W, w.words, w.bk_base);
     }
     // at most 4096 bucket totals: one workgroup scans them in place
     hipLaunchKernelGGL(k_scan_top<uint32_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.bk_base, p.B,
