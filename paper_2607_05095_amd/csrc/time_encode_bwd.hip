@@ -8,12 +8,17 @@
 // both signs).  An fp32 sine (a few ulp per term) leaves the sum of a column
 // that nearly cancels with a relative error far above 1e-5, so the sine is
 // evaluated in fp64 on the exact fp32 argument and every product and sum is
-// fp64: a two-part Cody-Waite reduction by pi (x = k*pi + r, |r| <= pi/2; pi
-// split into its fp64 rounding and the fp64 rounding of the remainder, each
-// step one fused multiply-add) and the Taylor series of sin(r)/r in r^2
-// through r^14, whose truncation error is below 6e-12 for |r| <= pi/2.
-// Arguments beyond 2^30 rad (or not finite) take the library sine in a cold
-// second pass of the workgroups that met one.
+// fp64: a one-step Cody-Waite reduction by pi (x = k*pi + r, |r| <= pi/2,
+// one fused multiply-add with the fp64 rounding of pi) and an odd polynomial
+// of degree 11 for sin(r), whose coefficients were fitted near-minimax
+// (Lawson's iteratively reweighted least squares on Chebyshev nodes of
+// [0, (pi/2)^2] in r^2, on the relative error of sin): its relative error is
+// below 2.4e-11 on |r| <= pi/2, and the one-step reduction adds at most
+// 4e-11 absolute for |x| <= 1e6.  Terms of a cancelling column need about
+// 1e-8 (the 1e-5 target on a sum 1e-3 of the sum of its magnitudes).
+// The range is checked once per row: a row whose bound
+// fmaf(max|omega|, |dt|, max|phi|) exceeds 1e6 (or is not finite) is left
+// to the library sine in a cold second pass of the workgroups that met one.
 //
 // Determinism: the reduction order depends only on N and d_t.  A workgroup
 // owns the segment groups b, b + nblk, b + 2*nblk, ... (TB_SEGS segments
@@ -37,36 +42,37 @@ __host__ __device__ inline int64_t tb_blocks(int64_t N) {
   return g < TB_MAX_BLOCKS ? g : TB_MAX_BLOCKS;
 }
 
-// sin(x) for an fp32 x with |x| <= 2^30, in fp64, returned as (-1)^k sin r
-// where x = k*pi + r: the value is sin(r), and bit 31 of `flip` is set when
-// k is odd (sin x = -sin r).  k comes from the magic-number rounding
-// fma(x, 1/pi, 1.5*2^52), whose low word holds k in two's complement.  For
-// |x| <= 2^30, k <= 2^29: k * PI_HI is exact inside the first fma and
-// k * (pi - PI_HI - PI_LO) stays below 1e-24, so r carries an absolute error
-// of about 1e-16.
-__device__ __forceinline__ double sin_reduced(float xf, uint32_t& flip) {
+// sin(x) in fp64 for an fp32 x with |x| <= 1e6.  k = round(x / pi) comes
+// from the magic-number rounding fma(x, 1/pi, 1.5*2^52), whose low word
+// holds k in two's complement; r = x - k*pi in one fused multiply-add
+// (k <= 3.2e5, so the neglected k*(pi - PI_HI) stays below 4e-11), and the
+// parity of k flips the sign of r, since sin x = (-1)^k sin r = sin((-1)^k r).
+__device__ __forceinline__ double sin_reduced(float xf) {
   const double x = double(xf);
-  const double PI_HI = 0x1.921fb54442d18p+1, PI_LO = 0x1.1a62633145c07p-53;
+  const double PI_HI = 0x1.921fb54442d18p+1;
   const double INV_PI = 0x1.45f306dc9c883p-2, MAGIC = 0x1.8p52;
   const double t = fma(x, INV_PI, MAGIC);
   const double k = t - MAGIC;
-  flip = uint32_t(__double2loint(t)) << 31;
   double r = fma(-k, PI_HI, x);
-  r = fma(-k, PI_LO, r);
+  const uint32_t flip = uint32_t(__double2loint(t)) << 31;
+  r = __hiloint2double(int(uint32_t(__double2hiint(r)) ^ flip), __double2loint(r));
   const double r2 = r * r;
-  double p = -0x1.ae7f3e733b81fp-41;          // -1/15!
-  p = fma(p, r2, 0x1.6124613a86d09p-33);      //  1/13!
-  p = fma(p, r2, -0x1.ae64567f544e4p-26);     // -1/11!
-  p = fma(p, r2, 0x1.71de3a556c734p-19);      //  1/9!
-  p = fma(p, r2, -0x1.a01a01a01a01ap-13);     // -1/7!
-  p = fma(p, r2, 0x1.1111111111111p-7);       //  1/5!
-  p = fma(p, r2, -0x1.5555555555555p-3);      // -1/3!
-  return fma(r * r2, p, r);                   // r + r^3 * (...)
+  double p = -0x1.9a6887b9bb2dbp-26;
+  p = fma(p, r2, 0x1.71708023de99ap-19);
+  p = fma(p, r2, -0x1.a017d9a03cff9p-13);
+  p = fma(p, r2, 0x1.11110c4a00de9p-7);
+  p = fma(p, r2, -0x1.555555476965fp-3);
+  return fma(r * r2, p, r);                   // r + r^3 p(r^2)
 }
 
-// Arguments beyond this (or not finite) are left to the library sine, called
-// out of line so that its registers do not weigh on the streaming loop.
-__device__ __forceinline__ bool sin_reduced_ok(float x) { return fabsf(x) <= 0x1p30f; }
+// A row is reduced in-line when every |fmaf(omega[j], dt, phi[j])| of its
+// columns is at most 1e6 * (1 + 2^-22) < 2^20: fmaf(max|omega|, |dt|,
+// max|phi|) bounds them up to two roundings.  Not-less-than sends a NaN
+// bound (a NaN time) to the library path too.
+constexpr float TB_ROW_LIMIT = 1.0e6f;
+__device__ __forceinline__ bool tb_row_ok(float om_max, float ph_max, float dt) {
+  return fmaf(om_max, fabsf(dt), ph_max) <= TB_ROW_LIMIT;
+}
 __device__ __attribute__((noinline)) double sin_library(double x) { return sin(x); }
 
 // Grid: tb_blocks(N) workgroups.  Thread t owns the column chunk t % cpr of
@@ -91,13 +97,15 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
   const bool active = rsub < rpp;
   const int tile = (TB_TILE_MAX / rpp) * rpp;
 
-  float om[VEC], ph[VEC];
+  float om[VEC], ph[VEC], om_max = 0.f, ph_max = 0.f;
   double acc_w[VEC], acc_p[VEC];
-  bool big = false;                        // an argument beyond the reduction's range
+  bool big = false;                        // a row beyond the reduction's range
 #pragma unroll
   for (int k = 0; k < VEC; ++k) {
     om[k] = active ? omega[c0 * VEC + k] : 0.f;
     ph[k] = active ? phi[c0 * VEC + k] : 0.f;
+    om_max = fmaxf(om_max, fabsf(om[k]));
+    ph_max = fmaxf(ph_max, fabsf(ph[k]));
     acc_w[k] = 0.0;
     acc_p[k] = 0.0;
   }
@@ -124,23 +132,21 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
       if (active) {
         for (int row = rsub; row < nrows; row += rpp) {
           const float dt = s_dt[row];
+          if (__builtin_expect(!tb_row_ok(om_max, ph_max, dt), 0)) {
+            big = true;                    // left to the cold pass
+            continue;
+          }
           Raw<TG, VEC> raw;
           raw.template load<NT>(dte + (t0 + row) * d_t + c0 * VEC);
           float g[VEC];
           raw.unpack(g);
+          const double dtd = double(dt);
 #pragma unroll
           for (int k = 0; k < VEC; ++k) {
-            const float x = fmaf(om[k], dt, ph[k]);
-            uint32_t flip;
-            const double s = sin_reduced(x, flip);
-            const bool ok = sin_reduced_ok(x);
-            big |= !ok;
-            // -g * sin x, the sign folded into g; 0 for an argument left to
-            // the cold pass
-            const float gn = ok ? __uint_as_float(__float_as_uint(g[k]) ^ flip ^ 0x80000000u) : 0.f;
-            const double gs = double(gn) * s;
-            acc_p[k] += gs;
-            acc_w[k] = fma(gs, double(dt), acc_w[k]);
+            // the term is -g sin x
+            const double q = double(g[k]) * sin_reduced(fmaf(om[k], dt, ph[k]));
+            acc_p[k] -= q;
+            acc_w[k] = fma(-q, dtd, acc_w[k]);
           }
         }
       }
@@ -148,9 +154,9 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
     }
   }
 
-  // Cold pass, only in a workgroup that met an argument beyond 2^30 rad (or
-  // not finite): the same rows again, adding just those elements with the
-  // library sine.  The order stays a fixed function of the inputs.
+  // Cold pass, only in a workgroup that met a row beyond the reduction's
+  // range (or not finite): the same rows again, adding just those rows with
+  // the library sine.  The order stays a fixed function of the inputs.
   if (__syncthreads_or(big)) {
     for (int64_t grp = blockIdx.x; grp < ngroups; grp += nblk) {
       const int64_t s0 = grp * TB_SEGS;
@@ -174,17 +180,16 @@ __global__ void __launch_bounds__(TB_THREADS) k_time_encode_bwd(
         if (active && big) {
           for (int row = rsub; row < nrows; row += rpp) {
             const float dt = s_dt[row];
+            if (tb_row_ok(om_max, ph_max, dt)) continue;
             Raw<TG, VEC> raw;
             raw.template load<false>(dte + (t0 + row) * d_t + c0 * VEC);
             float g[VEC];
             raw.unpack(g);
             for (int k = 0; k < VEC; ++k) {
               const float x = fmaf(om[k], dt, ph[k]);
-              if (!sin_reduced_ok(x)) {
-                const double gs = -double(g[k]) * sin_library(double(x));
-                acc_p[k] += gs;
-                acc_w[k] = fma(gs, double(dt), acc_w[k]);
-              }
+              const double gs = -double(g[k]) * sin_library(double(x));
+              acc_p[k] += gs;
+              acc_w[k] = fma(gs, double(dt), acc_w[k]);
             }
           }
         }

@@ -136,6 +136,34 @@ def test_time_encode_bwd_cancelling_column_and_huge_arguments():
     assert_close(got[1], ref[1], "f32", "dphi (cancelling)")
 
 
+def test_time_encode_bwd_reduction_range():
+    # Rows on both sides of the in-line reduction's range (a row is reduced
+    # in-line when fmaf(max|omega|, |dt|, max|phi|) <= 1e6, else it takes the
+    # library sine): dt log-uniform over [1e5, 1e8], so that the in-line rows
+    # reach the top of the range, where the one-step reduction is least
+    # accurate, and the cold rows span 1e6 .. 1e8 rad.  Pairs of equal dt and
+    # opposite gradients cancel, so each sum is a small remainder of its terms
+    # and an error of the sine shows at full weight.
+    _announce("time encode bwd around the reduction's range")
+    r = np.random.default_rng(11)
+    n_pair, n_rest = 100_000, 300
+    dt = np.concatenate([np.repeat(10 ** r.uniform(5, 8, n_pair), 2),
+                         10 ** r.uniform(5, 8, n_rest)]).astype(np.float32)
+    E = dt.size
+    off = np.arange(E + 1, dtype=np.int32)                 # one edge per destination
+    om = np.array([1.0, 0.37, 0.05, 1e-3], dtype=np.float32)
+    ph = np.array([0.0, -2.5, 3.0, 0.25], dtype=np.float32)
+    g = r.standard_normal((n_pair, om.size))
+    dte = np.concatenate([np.stack([g, -g], 1).reshape(2 * n_pair, om.size),
+                          1e-3 * r.standard_normal((n_rest, om.size))]).astype(np.float32)
+    inline = np.abs(dt) * 1.0 + 3.0 <= 1e6
+    assert 0.2 < inline.mean() < 0.5                        # both paths well populated
+    got = _tb_gpu(off, dt, np.zeros(E, np.float32), om, ph, to_dev(dte))
+    ref = oracle.time_encode_bwd(off, dt, np.zeros(E, np.float32), om, ph, dte)
+    assert_close(got[0], ref[0], "f32", "domega (reduction range)")
+    assert_close(got[1], ref[1], "f32", "dphi (reduction range)")
+
+
 @pytest.mark.parametrize("seed", range(16))
 def test_time_encode_bwd_random(seed):
     """Seeded random blocks: time widths 1-256 (every vector width the
