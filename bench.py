@@ -839,11 +839,13 @@ def stream_ceilings():
 
 
 def ceiling_fracs(achieved_gbs, ceilings):
-    """The dominant kernel's bandwidth as a fraction of each measured ceiling."""
+    """The dominant kernel's bandwidth as a fraction of each measured ceiling
+    (plain and streaming loads/stores alike)."""
     if not ceilings or "copy" not in ceilings:
         return None
     return {k: round(achieved_gbs / (ceilings[k]["TB_per_s"] * 1e3), 4)
-            for k in ("copy", "mix22", "read", "write")}
+            for k in ("copy", "copy_nt", "mix22", "read", "read_nt", "write", "write_nt")
+            if k in ceilings}
 
 
 def read_counters(workload):
@@ -1083,7 +1085,8 @@ def main():
     result["stream_ceilings"] = ceilings
     result["stream_ceilings_note"] = (
         "plain read / write / copy / two-in-two-out kernels over 2 GiB buffers on this GPU, one "
-        "16-byte element per thread (paper_2607_05095_amd/probe/stream_ceiling.hip), median of "
+        "16-byte element per thread, and read / write / copy with streaming (non-temporal) loads "
+        "and stores (_nt) (paper_2607_05095_amd/probe/stream_ceiling.hip), median of "
         "15 launches; roofline.frac_of_measured_ceiling divides the dominant kernel's bandwidth by them")
     for w in also:
         torch.cuda.synchronize()

@@ -8,7 +8,11 @@
 //   copy   : one in, one out           mix22  : two in, two out (the shape of
 //                                               the fused backward's K, V ->
 //                                               dK, dV rows)
+//   read_nt, write_nt, copy_nt: the first three with streaming
+//                               (non-temporal) loads and stores
 // Prints one JSON object: bytes moved, median time of `reps` launches, TB/s.
+// (The seg10 variants show what the packed forward pays for its output
+// rows: its K|V reads alone stream faster than the plain read above.)
 //   stream_ceiling [reps] [--variants]
 #include <hip/hip_runtime.h>
 
@@ -50,6 +54,29 @@ __global__ void __launch_bounds__(THREADS) k_copy(const u32x4* __restrict__ a,
   const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
   if (i >= n) return;
   b[i] = a[i];
+}
+
+// The same three with streaming (non-temporal) loads and stores, the policy
+// the library's kernels use for data they touch once.
+__global__ void __launch_bounds__(THREADS) k_read_nt(const u32x4* __restrict__ a, size_t n,
+                                                     unsigned* __restrict__ sink) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  const u32x4 v = __builtin_nontemporal_load(a + i);
+  if ((v.x ^ v.y ^ v.z ^ v.w) == 0x9e3779b9u) sink[0] = 1u;
+}
+
+__global__ void __launch_bounds__(THREADS) k_write_nt(u32x4* __restrict__ a, size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  __builtin_nontemporal_store((u32x4){unsigned(i), 1u, 2u, 3u}, a + i);
+}
+
+__global__ void __launch_bounds__(THREADS) k_copy_nt(const u32x4* __restrict__ a,
+                                                     u32x4* __restrict__ b, size_t n) {
+  const size_t i = size_t(blockIdx.x) * THREADS + threadIdx.x;
+  if (i >= n) return;
+  __builtin_nontemporal_store(__builtin_nontemporal_load(a + i), b + i);
 }
 
 __global__ void __launch_bounds__(THREADS) k_mix22(const u32x4* __restrict__ a,
@@ -209,6 +236,33 @@ __global__ void __launch_bounds__(THREADS) k_seg_kv_fwd(const u32x4* __restrict_
   out[g * ROWV + l] = acc;
 }
 
+// The same shape with streaming (non-temporal) K|V loads, as the forward
+// issues them, and the output row stored normally (OUT = 1), streamed
+// (OUT = 2) or not at all (OUT = 0: the loads alone).
+template <int OUT>
+__global__ void __launch_bounds__(THREADS) k_seg_kv_fwd_nt(const u32x4* __restrict__ kv,
+                                                           u32x4* __restrict__ out,
+                                                           unsigned* __restrict__ sink, size_t segs) {
+  const size_t g = (size_t(blockIdx.x) * THREADS + threadIdx.x) / 32;
+  const unsigned l = threadIdx.x & 31u;
+  if (g >= segs || l >= ROWV) return;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (size_t c = 0; c < SEG_ROWS; c += SEG_CH) {
+    u32x4 x[SEG_CH], y[SEG_CH];
+#pragma unroll
+    for (size_t i = 0; i < SEG_CH; ++i) {
+      const size_t r = g * SEG_ROWS + c + i;
+      x[i] = __builtin_nontemporal_load(kv + r * 2 * ROWV + l);
+      y[i] = __builtin_nontemporal_load(kv + r * 2 * ROWV + ROWV + l);
+    }
+#pragma unroll
+    for (size_t i = 0; i < SEG_CH; ++i) acc ^= x[i] + y[i];
+  }
+  if (OUT == 1) out[g * ROWV + l] = acc;
+  else if (OUT == 2) __builtin_nontemporal_store(acc, out + g * ROWV + l);
+  else if ((acc.x ^ acc.w) == 0x9e3779b9u) sink[0] = 1u;
+}
+
 struct Buffers {
   u32x4 *a, *b, *c, *d;
   unsigned* sink;
@@ -265,6 +319,12 @@ int main(int argc, char** argv) {
     hipLaunchKernelGGL(k_write, g_all, blk, 0, 0, B.b, B.n); }, reps)});
   rows.push_back({"copy", 2.0 * bytes, median_ms([&] {
     hipLaunchKernelGGL(k_copy, g_all, blk, 0, 0, B.a, B.b, B.n); }, reps)});
+  rows.push_back({"read_nt", double(bytes), median_ms([&] {
+    hipLaunchKernelGGL(k_read_nt, g_all, blk, 0, 0, B.a, B.n, B.sink); }, reps)});
+  rows.push_back({"write_nt", double(bytes), median_ms([&] {
+    hipLaunchKernelGGL(k_write_nt, g_all, blk, 0, 0, B.b, B.n); }, reps)});
+  rows.push_back({"copy_nt", 2.0 * bytes, median_ms([&] {
+    hipLaunchKernelGGL(k_copy_nt, g_all, blk, 0, 0, B.a, B.b, B.n); }, reps)});
   rows.push_back({"mix22", 2.0 * bytes, median_ms([&] {   // four streams of 1 GiB
     hipLaunchKernelGGL(k_mix22, g_half, blk, 0, 0, B.a, B.c, B.b, B.d, half); }, reps)});
   if (argc > 2 && std::strcmp(argv[2], "--variants") == 0) {
@@ -298,6 +358,13 @@ int main(int argc, char** argv) {
       hipLaunchKernelGGL(k_seg_kv_fwd, g_segs, blk, 0, 0, B.a, B.b, nseg); }, reps)});
     rows.push_back({"rows400_kv_read", moved / 2, median_ms([&] {
       hipLaunchKernelGGL(k_rows_kv_read, g_rows, blk, 0, 0, B.a, B.sink, nrow); }, reps)});
+    const double seg_in = double(nseg) * SEG_ROWS * 2 * 16 * ROWV, seg_out = double(nseg) * 16 * ROWV;
+    rows.push_back({"seg10_kv_fwd_nt", seg_in + seg_out, median_ms([&] {
+      hipLaunchKernelGGL(k_seg_kv_fwd_nt<1>, g_segs, blk, 0, 0, B.a, B.b, B.sink, nseg); }, reps)});
+    rows.push_back({"seg10_kv_fwd_ntst", seg_in + seg_out, median_ms([&] {
+      hipLaunchKernelGGL(k_seg_kv_fwd_nt<2>, g_segs, blk, 0, 0, B.a, B.b, B.sink, nseg); }, reps)});
+    rows.push_back({"seg10_kv_read_nt", seg_in, median_ms([&] {
+      hipLaunchKernelGGL(k_seg_kv_fwd_nt<0>, g_segs, blk, 0, 0, B.a, B.b, B.sink, nseg); }, reps)});
   }
   CHECK(hipGetLastError());
   std::printf("{");
