@@ -115,7 +115,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_fwd_rm(Attn
   const float sl2 = a.scale * LOG2E;
   float q[4];
   // Q and out stream too (each row is read or written once per call): the
-  // bigdedup step's layer-1 forward 0.430 -> 0.385 ms with both, the step
+  // 1e7-node fp32 batch's layer-1 forward 0.430 -> 0.385 ms with both, its step
   // 1.887 -> 1.845 ms.  The HBM reads of K|V then run without the write-back
   // of out lines interleaved at random; read-only, the same access shape
   // reads at 7.0-7.3 TB/s, with 400-byte output rows stored normally at 5.6.
@@ -295,7 +295,7 @@ __device__ __forceinline__ void rm_bwd_emit(const AttnArgs& a, const RmMap<H>& m
   }
   // with indexed operands the per-edge gradients are written once and read
   // back only through the occurrence lists: streamed, as are Q, dO and dQ
-  // (bigdedup layer-1 indexed backward 1.425 -> 1.297 ms)
+  // (1e7-node batch, layer-1 indexed backward 1.425 -> 1.297 ms)
   rm_store_row<NT || IDX, H>(static_cast<float*>(a.dK), e, int(a.ldkv), m, dk);
   rm_store_row<NT || IDX, H>(static_cast<float*>(a.dV), e, int(a.ldkv), m, dv);
 }
@@ -307,7 +307,7 @@ __global__ void __launch_bounds__(ATT_MAX_BLOCK) FAST_ATT_OCC k_attn_bwd_rm(Attn
   const int F = a.L.F;
   const float sl2 = a.scale * LOG2E;
   RmBwdState<H> S;
-  // Q, dO and dQ stream, as in the forward (bigdedup step 1.845 -> 1.837 ms;
+  // Q, dO and dQ stream, as in the forward (that batch's step 1.845 -> 1.837 ms;
   // with indexed operands too, below)
   rm_load_row<true, H>(static_cast<const float*>(a.Q), m.seg, F, m, S.q);
   rm_load_row<true, H>(static_cast<const float*>(a.dO), m.seg, F, m, S.go);

@@ -505,7 +505,7 @@ constexpr int GATHER_U = 1;
 
 // Row moves with an optional streaming (non-temporal) policy: a gathered row
 // is read once and written once per call.  Measured on MI355X, streaming paid
-// for 16-byte moves (bigdedup nodes 0.144 -> 0.125 ms, edges 0.307 -> 0.288
+// for 16-byte moves (1e7-node fp32 batch: nodes 0.144 -> 0.125 ms, edges 0.307 -> 0.288
 // ms, large nodes 0.171 -> 0.159 ms) and for 8-byte moves (344-byte rows of
 // the large batch's edges: the whole call 0.688 -> 0.661 ms with streaming
 // loads, step 2.548 -> 2.530 ms).  8-byte moves stream their stores whatever
