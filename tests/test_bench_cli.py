@@ -114,3 +114,20 @@ def test_time_encode_valu_only_from_counters_of_the_current_source():
     assert abs(v["lane_insts_per_s"] - 5.6e7 * 64 / 2e-4) < 1 and 0 < v["frac"] < 1
     rec["time_encode_valu"]["source_sha"] = "0" * 16
     assert "valu" not in bench.time_encode_summary(b, bd, rec)
+
+
+def test_ceiling_fractions_cover_plain_and_streaming_probes():
+    """The dominant kernel's bandwidth is set against every ceiling the probe
+    reports, the streaming (non-temporal) ones included, and an older probe
+    output without them still gives the plain fractions."""
+    import bench
+    tb = {"read": 6.7, "write": 6.7, "copy": 6.1, "mix22": 5.7, "read_nt": 7.0, "write_nt": 6.6,
+          "copy_nt": 6.4}
+    full = {k: {"TB_per_s": v} for k, v in tb.items()}
+    fr = bench.ceiling_fracs(5720.0, full)
+    assert set(fr) == set(tb)
+    assert fr["copy_nt"] == round(5720.0 / 6400.0, 4) and fr["copy"] == round(5720.0 / 6100.0, 4)
+    plain = {k: v for k, v in full.items() if not k.endswith("_nt")}
+    assert set(bench.ceiling_fracs(5720.0, plain)) == {"read", "write", "copy", "mix22"}
+    assert bench.ceiling_fracs(5720.0, None) is None
+    assert bench.ceiling_fracs(5720.0, {"error": "probe timed out"}) is None
